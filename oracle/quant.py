@@ -1,0 +1,111 @@
+"""Round-to-nearest min-max quantizer of eq. 1 (Sec. 2) and 4-bit nibble packing.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Eq. 1:  X_Q = alpha * round((X_R - beta) / alpha) + beta, with
+  symmetric:  alpha = max|X_R| / (2^(N-1) - 1),  beta = 0   -> codes in [-(2^(N-1)-1), 2^(N-1)-1]
+  asymmetric: alpha = (max X_R - min X_R) / (2^N - 1), beta = min X_R -> codes in [0, 2^N - 1]
+The paper quantizes activations and the KV cache asymmetrically with no range clipping
+(App. A, "Quantization choice", Table 12) and weights symmetrically.
+
+Readings of points the paper leaves open:
+  * "round" is round-to-nearest with ties to even (np.rint).
+  * beta is the real minimum, kept in fp32 (not an integer zero-point).
+  * A group whose range is zero (or an all-zero symmetric row) gets alpha = 1, which
+    reconstructs it exactly.
+  * The encoding is carried out as this exact fp32 op sequence, one IEEE rounding per
+    step, so that an implementation doing the same steps reproduces the codes bit for
+    bit from the same fp32 inputs:
+      asym: mn, mx = min, max;  r = mx - mn;  alpha = r / L (or 1 if r == 0);
+            inv = 1 / alpha;  q = clamp(rint((v - mn) * inv), 0, L),  L = 2^N - 1
+      sym:  a = max|v|;  alpha = a / L (or 1 if a == 0);  inv = 1 / alpha;
+            q = clamp(rint(v * inv), -L, L),  L = 2^(N-1) - 1
+    (dividing by alpha through its fp32 reciprocal is part of this reading).
+"""
+
+import numpy as np
+
+F32 = np.float32
+
+
+def _groups(v: np.ndarray, group: int) -> np.ndarray:
+    K = v.shape[-1]
+    if group <= 0 or K % group != 0:
+        raise ValueError(f"group {group} does not divide row length {K}")
+    return v.reshape(*v.shape[:-1], K // group, group)
+
+
+def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None):
+    """Asymmetric min-max quantization of eq. 1 over contiguous groups of the last axis.
+
+    v: fp32-representable values [..., K].  Returns (codes int64 [..., K] in [0, 2^N-1],
+    alpha fp32 [..., K/group], beta fp32 [..., K/group]).
+    """
+    v32 = np.asarray(v, dtype=F32)
+    group = v32.shape[-1] if group is None else group
+    g = _groups(v32, group)
+    levels = F32(2 ** bits - 1)
+    mn = g.min(axis=-1)
+    mx = g.max(axis=-1)
+    r = (mx - mn).astype(F32)
+    alpha = np.where(r == 0, F32(1), r / levels).astype(F32)
+    inv = (F32(1) / alpha).astype(F32)
+    t = ((g - mn[..., None]).astype(F32) * inv[..., None]).astype(F32)
+    q = np.clip(np.rint(t), 0, levels).astype(np.int64)
+    return q.reshape(v32.shape), alpha, mn.astype(F32)
+
+
+def quant_sym(v: np.ndarray, bits: int = 4, group: int | None = None):
+    """Symmetric quantization of eq. 1 (beta = 0) over contiguous groups of the last axis.
+
+    Returns (codes int64 in [-(2^(N-1)-1), 2^(N-1)-1], alpha fp32 [..., K/group]).
+    """
+    v32 = np.asarray(v, dtype=F32)
+    group = v32.shape[-1] if group is None else group
+    g = _groups(v32, group)
+    levels = F32(2 ** (bits - 1) - 1)
+    amax = np.abs(g).max(axis=-1)
+    alpha = np.where(amax == 0, F32(1), amax / levels).astype(F32)
+    inv = (F32(1) / alpha).astype(F32)
+    t = (g * inv[..., None]).astype(F32)
+    q = np.clip(np.rint(t), -levels, levels).astype(np.int64)
+    return q.reshape(v32.shape), alpha
+
+
+def dequant(q: np.ndarray, alpha: np.ndarray, beta: np.ndarray | None = None,
+            group: int | None = None) -> np.ndarray:
+    """X_Q = alpha * q + beta (eq. 1), in fp64, broadcasting per group."""
+    q64 = np.asarray(q, dtype=np.float64)
+    group = q64.shape[-1] if group is None else group
+    g = _groups(q64, group)
+    out = g * np.asarray(alpha, dtype=np.float64)[..., None]
+    if beta is not None:
+        out = out + np.asarray(beta, dtype=np.float64)[..., None]
+    return out.reshape(q64.shape)
+
+
+def pack_nibbles(q: np.ndarray) -> np.ndarray:
+    """Two 4-bit codes per byte along the last axis: even index in the low nibble.
+
+    Negative codes are stored as two's-complement nibbles.
+    """
+    qi = np.asarray(q, dtype=np.int64)
+    if qi.shape[-1] % 2:
+        raise ValueError("row length must be even to pack nibbles")
+    lo = qi[..., 0::2] & 0xF
+    hi = qi[..., 1::2] & 0xF
+    return (lo | (hi << 4)).astype(np.uint8)
+
+
+def unpack_nibbles(p: np.ndarray, signed: bool) -> np.ndarray:
+    """Inverse of pack_nibbles: uint8 [..., K/2] -> int64 codes [..., K]."""
+    b = np.asarray(p, dtype=np.int64)
+    lo = b & 0xF
+    hi = (b >> 4) & 0xF
+    if signed:
+        lo = np.where(lo >= 8, lo - 16, lo)
+        hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty((*b.shape[:-1], 2 * b.shape[-1]), dtype=np.int64)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out

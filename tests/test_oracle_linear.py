@@ -1,0 +1,112 @@
+"""Pins of the oracle's rotated W4A4 linear layer (CPU only).
+
+* exact integer GEMM == brute-force triple loop on tiny shapes;
+* epilogue == dequant(qa) dequant(qw)^T, the algebraic expansion of eq. 1 on both
+  operands, to 1e-12 in fp64 (catches a dropped zero-point term or a wrong sign);
+* identity rotation == plain per-token quantization;
+* rotating outlier activations raises the W4A4 signal-to-noise ratio (Sec. 2.1 Fig. 3,
+  App. B.2 Table 19 direction).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import hadamard, linear, quant, rotate
+from paper_2405_16406_amd import workloads
+
+
+def test_gemm_exact_bruteforce():
+    rng = np.random.default_rng(0)
+    qa = rng.integers(0, 16, size=(5, 24))
+    qw = rng.integers(-7, 8, size=(6, 24))
+    acc = linear.gemm_exact(qa, qw)
+    for m in range(5):
+        for n in range(6):
+            s = 0
+            for k in range(24):
+                s += int(qa[m, k]) * int(qw[n, k])
+            assert acc[m, n] == s
+
+
+def test_gemm_exact_extreme_values():
+    K = 28672
+    qa = np.full((2, K), 15)
+    qw = np.full((3, K), -7)
+    acc = linear.gemm_exact(qa, qw)
+    assert np.all(acc == -105 * K)
+
+
+def test_epilogue_is_expanded_dequant_product():
+    rng = np.random.default_rng(1)
+    M, N, K = 7, 9, 64
+    qa = rng.integers(0, 16, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    aa = rng.uniform(0.1, 2.0, M).astype(np.float32)
+    ab = rng.uniform(-5, 0, M).astype(np.float32)
+    wa = rng.uniform(1e-3, 1e-2, N).astype(np.float32)
+    rs = qw.sum(1).astype(np.int32)
+    acc = linear.gemm_exact(qa, qw)
+    y64 = linear.epilogue_f64(acc, aa, ab, wa, rs)
+    ref = quant.dequant(qa, aa[:, None], ab[:, None]) @ quant.dequant(qw, wa[:, None]).T
+    assert np.max(np.abs(y64 - ref)) <= 1e-12 * np.max(np.abs(ref))
+    bias = rng.standard_normal(N).astype(np.float16)
+    y = linear.epilogue(acc, aa, ab, wa, rs, bias)
+    assert y.dtype == np.float16
+    np.testing.assert_array_equal(y, (ref + bias.astype(np.float64)).astype(np.float16))
+
+
+def test_identity_rotation_is_plain_per_token_quant():
+    x, _ = workloads.tiny_inputs()
+    p, a, b, y32, q = linear.had_quant_act(x, None, 1)
+    q2, a2, b2 = quant.quant_asym(x.astype(np.float32))
+    np.testing.assert_array_equal(q, q2)
+    np.testing.assert_array_equal(a, a2)
+    np.testing.assert_array_equal(b, b2)
+    np.testing.assert_array_equal(p, quant.pack_nibbles(q2))
+
+
+def test_pack_w4_rowsum_and_range():
+    _, w = workloads.tiny_inputs()
+    p, a, rs, q = linear.pack_w4(w, None, 256)
+    assert q.min() >= -7 and q.max() <= 7
+    np.testing.assert_array_equal(rs, q.sum(1))
+    np.testing.assert_array_equal(quant.unpack_nibbles(p, signed=True), q)
+    assert a.shape == (256,)
+
+
+def _snr_db(ref, y):
+    return 10 * np.log10(np.sum(ref ** 2) / np.sum((ref - y.astype(np.float64)) ** 2))
+
+
+def test_rotation_improves_w4a4_snr():
+    x, w = workloads.tiny_inputs()
+    ref = linear.reference_fp(x, w)
+    plain = linear.rotated_linear(x, w, None, 1)
+    rot = linear.rotated_linear(x, w, None, 256)
+    assert _snr_db(ref, rot["y"]) > _snr_db(ref, plain["y"]) + 3.0
+
+
+def test_rotated_layer_kronecker_invariance_small():
+    # the rotated layer approximates x W^T; with 8-bit-like fine steps it would be exact
+    rng = np.random.default_rng(5)
+    ha = hadamard.dense_factor(28)
+    K = 28 * 8
+    x = rng.standard_normal((6, K)).astype(np.float16)
+    w = (0.02 * rng.standard_normal((10, K))).astype(np.float16)
+    out = linear.rotated_linear(x, w, ha, 8)
+    ref = linear.reference_fp(x, w)
+    assert _snr_db(ref, out["y"]) > 10.0
+    np.testing.assert_array_equal(out["acc"], linear.gemm_exact(out["qa"], out["qw"]))
+    # the weight really was rotated with the same rotation as the activations
+    wr = rotate.rotate_rows(w, ha, 8).astype(np.float32)
+    q, a = quant.quant_sym(wr)
+    np.testing.assert_array_equal(out["qw"], q)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_had_quant_act_code_range(bits):
+    x, _ = workloads.tiny_inputs()
+    _, a, b, y32, q = linear.had_quant_act(x, None, 256, bits=bits)
+    assert q.min() >= 0 and q.max() <= 2 ** bits - 1
+    err = np.abs(quant.dequant(q, a, b) - y32.astype(np.float64))
+    assert np.all(err <= a.astype(np.float64) * 0.5 * (1 + 1e-5))

@@ -1,0 +1,139 @@
+"""Pins of the oracle's quantizer and packing (CPU only).
+
+Fixed by the paper (Sec. 2, eq. 1): asymmetric min-max maps the minimum to code 0 and
+the maximum to 2^N - 1; symmetric maps +-max|x| to +-(2^(N-1) - 1); round-to-nearest
+keeps every reconstruction within alpha/2; App. A Table 12 prefers asymmetric
+quantization for activations and the KV cache.  Hand-worked cases in
+tests/golden/quant_worked.json pin the tie rule and the scale/offset values.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+from hypothesis import given, settings
+from hypothesis import strategies as st
+from hypothesis.extra.numpy import arrays
+
+from oracle import quant
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "quant_worked.json")
+
+
+def _golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", _golden()["asym"])
+def test_asym_golden(case):
+    q, a, b = quant.quant_asym(np.array(case["v"], dtype=np.float32), bits=case["bits"])
+    assert q.tolist() == case["codes"]
+    assert a == np.float32(case["alpha"])
+    assert b == np.float32(case["beta"])
+
+
+@pytest.mark.parametrize("case", _golden()["sym"])
+def test_sym_golden(case):
+    q, a = quant.quant_sym(np.array(case["v"], dtype=np.float32), bits=case["bits"])
+    assert q.tolist() == case["codes"]
+    assert a == np.float32(case["alpha"])
+
+
+def test_asym_closed_forms_and_bound():
+    rng = np.random.default_rng(0)
+    v = (rng.standard_normal((50, 256)) * 3 + 1).astype(np.float32)
+    q, a, b = quant.quant_asym(v, bits=4)
+    assert q.min() >= 0 and q.max() <= 15
+    assert np.all(q[np.arange(50), v.argmin(1)] == 0)
+    assert np.all(q[np.arange(50), v.argmax(1)] == 15)
+    np.testing.assert_array_equal(b[:, 0], v.min(1))
+    vhat = quant.dequant(q, a, b)
+    err = np.abs(vhat - v.astype(np.float64))
+    assert np.all(err <= a.astype(np.float64) * 0.5 * (1 + 1e-6))
+
+
+def test_asym_groups_are_independent():
+    rng = np.random.default_rng(1)
+    v = rng.standard_normal((4, 512)).astype(np.float32)
+    q, a, b = quant.quant_asym(v, bits=4, group=128)
+    assert a.shape == (4, 4) and b.shape == (4, 4)
+    for g in range(4):
+        qg, ag, bg = quant.quant_asym(v[:, g * 128:(g + 1) * 128], bits=4)
+        np.testing.assert_array_equal(q[:, g * 128:(g + 1) * 128], qg)
+        np.testing.assert_array_equal(a[:, g], ag[:, 0])
+        np.testing.assert_array_equal(b[:, g], bg[:, 0])
+
+
+def test_sym_closed_forms_and_bound():
+    rng = np.random.default_rng(2)
+    w = (rng.standard_normal((40, 300)) * 0.02).astype(np.float32)
+    q, a = quant.quant_sym(w, bits=4)
+    assert q.min() >= -7 and q.max() <= 7
+    i = np.abs(w).argmax(1)
+    np.testing.assert_array_equal(q[np.arange(40), i], np.sign(w[np.arange(40), i]) * 7)
+    err = np.abs(quant.dequant(q, a) - w.astype(np.float64))
+    assert np.all(err <= a.astype(np.float64) * 0.5 * (1 + 1e-6))
+
+
+def test_degenerate_groups():
+    v = np.full((2, 8), -2.5, dtype=np.float32)
+    q, a, b = quant.quant_asym(v)
+    assert np.all(q == 0) and np.all(a == 1) and np.all(b == np.float32(-2.5))
+    np.testing.assert_array_equal(quant.dequant(q, a, b), v)
+    q, a = quant.quant_sym(np.zeros((2, 8), dtype=np.float32))
+    assert np.all(q == 0) and np.all(a == 1)
+
+
+def test_asym_beats_sym_on_rotated_activations():
+    # App. A Table 12: asymmetric activation quantization is the better choice
+    rng = np.random.default_rng(4)
+    v = (rng.standard_normal((256, 512)) + 0.4).astype(np.float32)
+    qa, aa, ba = quant.quant_asym(v)
+    qs, as_ = quant.quant_sym(v)
+    ea = np.mean((quant.dequant(qa, aa, ba) - v) ** 2)
+    es = np.mean((quant.dequant(qs, as_) - v) ** 2)
+    assert ea < es
+
+
+def test_pack_layout_and_roundtrip():
+    q = np.array([[1, 2, 15, 0, 7, 8]])
+    p = quant.pack_nibbles(q)
+    assert p.tolist() == [[0x21, 0x0F, 0x87]]
+    np.testing.assert_array_equal(quant.unpack_nibbles(p, signed=False), q)
+    s = np.array([[-7, 7, -1, 0, 3, -4]])
+    ps = quant.pack_nibbles(s)
+    assert ps.tolist() == [[0x79, 0x0F, 0xC3]]
+    np.testing.assert_array_equal(quant.unpack_nibbles(ps, signed=True), s)
+
+
+@settings(max_examples=200, deadline=None)
+@given(arrays(np.float32, st.integers(2, 64).map(lambda n: (2 * n,)),
+              elements=st.floats(-1e4, 1e4, width=32, allow_nan=False, allow_infinity=False)))
+def test_asym_properties(v):
+    q, a, b = quant.quant_asym(v[None, :], bits=4)
+    assert q.min() >= 0 and q.max() <= 15
+    assert b[0, 0] == v.min()
+    r = np.float32(v.max() - v.min())
+    if r > 0:
+        assert q[0, v.argmin()] == 0 and q[0, v.argmax()] == 15
+        err = np.abs(quant.dequant(q, a, b)[0] - v.astype(np.float64))
+        # alpha/2 plus the fp32 rounding of (v - min) * (1/alpha)
+        assert np.all(err <= np.float64(a[0, 0]) * (0.5 + 4e-6) + 1e-6 * np.abs(v).max())
+    p = quant.pack_nibbles(q)
+    np.testing.assert_array_equal(quant.unpack_nibbles(p, signed=False), q)
+
+
+@settings(max_examples=200, deadline=None)
+@given(arrays(np.float32, st.integers(1, 64).map(lambda n: (2 * n,)),
+              elements=st.floats(-100, 100, width=32, allow_nan=False, allow_infinity=False)))
+def test_sym_properties(v):
+    q, a = quant.quant_sym(v[None, :], bits=4)
+    assert q.min() >= -7 and q.max() <= 7
+    amax = np.abs(v).max()
+    if amax > 0:
+        assert abs(q[0, np.abs(v).argmax()]) == 7
+        err = np.abs(quant.dequant(q, a)[0] - v.astype(np.float64))
+        assert np.all(err <= np.float64(a[0, 0]) * (0.5 + 4e-6))
+    np.testing.assert_array_equal(quant.unpack_nibbles(quant.pack_nibbles(q), signed=True), q)
