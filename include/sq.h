@@ -1,0 +1,173 @@
+/*
+ * sq.h -- C ABI of the MI355X (gfx950) rotated W4A4 inference path of SpinQuant
+ * (arXiv 2405.16406): online Hadamard rotation + 4-bit activation quantization, offline
+ * weight preparation, the int4 x int4 GEMM with its dequantising epilogue, and R3 +
+ * 4-bit KV-cache quantization.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named "device" are HIP device pointers (or memory the device can read
+ *    and write).  The caller allocates and owns every buffer, keeps it alive until
+ *    the enqueued work has finished, and synchronises.  The library never allocates,
+ *    frees or synchronises; it only enqueues kernels on `stream` (a hipStream_t; NULL
+ *    means the default stream).  Calls are asynchronous.
+ *  - Tensors are row-major.  fp16 is IEEE binary16; scales are fp32.
+ *  - 4-bit codes are packed two per byte along the row, the element with the even
+ *    index in the low nibble.  Activation and KV codes are unsigned (0..15); weight
+ *    codes are two's-complement nibbles (-7..7).
+ *  - Quantization follows eq. 1 of the paper (Sec. 2):
+ *        X_Q = alpha * round((X - beta) / alpha) + beta,
+ *    asymmetric (alpha = (max-min)/(2^N-1), beta = min) for activations and the KV
+ *    cache, symmetric (alpha = max|X|/(2^(N-1)-1), beta = 0) for weights, no range
+ *    clipping (App. A, "Quantization choice", Table 12).  Round-to-nearest is ties to
+ *    even; (X-beta)/alpha is evaluated as (X-beta) * fl32(1/alpha); a group whose
+ *    range (or max|X|) is zero gets alpha = 1.
+ *  - Online rotation (R4 on the down-projection input, R3 on Q/K; Sec. 3.1
+ *    "Additional unabsorbed rotations"): each contiguous block of n = a*b elements of
+ *    a row is multiplied on the right by R = (S_b (x) H_a) / sqrt(n), where S_b is the
+ *    natural-order Sylvester matrix of order b = 2^k and H_a a +-1 Hadamard matrix of
+ *    order a (dense factor on the inner, contiguous index: element i = i_b*a + i_a).
+ *    (a, b) = (1, 1) is the identity.
+ *  - Errors: every argument is checked on the host before anything is enqueued.  A
+ *    non-OK status means nothing was enqueued and no output was written; the message
+ *    is available from sq_last_error() (per thread).  Launch failures, including "no
+ *    device", return SQ_ERR_HIP.  Arguments are never dereferenced on the host.
+ */
+#ifndef SQ_H_
+#define SQ_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SQ_ABI_VERSION 1
+
+/* Largest row length K accepted by sq_had_quant_act / sq_pack_w4 (rotated or not). */
+#define SQ_MAX_ROW 32768
+/* Largest dense Hadamard factor order a. */
+#define SQ_MAX_DENSE 256
+
+typedef enum {
+  SQ_OK = 0,
+  SQ_ERR_NULL = 1,        /* a required pointer is NULL */
+  SQ_ERR_SHAPE = 2,       /* sizes inconsistent or out of range */
+  SQ_ERR_UNSUPPORTED = 3, /* a valid request this build does not implement (e.g. bits != 4) */
+  SQ_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
+  SQ_ERR_ALIAS = 5,       /* an output overlaps an input or another output */
+  SQ_ERR_HIP = 6          /* the HIP runtime reported an error (no device, launch failure) */
+} sq_status;
+
+/* SQ_ABI_VERSION of the built library. */
+int32_t sq_abi_version(void);
+
+/* Message for the last non-OK status returned on the calling thread ("" if none). */
+const char* sq_last_error(void);
+
+/*
+ * sq_hadamard_factor -- host helper: writes the library's +-1 Hadamard matrix of order
+ * n into out_host[n*n] (row-major int8, HOST memory), for use as `had_dense`.
+ *   n = 1    : [1]
+ *   n = 28   : Paley type II construction from q = 13
+ *   n = 172  : Williamson construction from four symmetric circulants of order 43
+ * Any Hadamard matrix is a valid rotation factor (Sec. 3.1 only asks for "a Hadamard
+ * matrix"); these are the ones the library provides.  Errors: SQ_ERR_NULL,
+ * SQ_ERR_UNSUPPORTED (other n).
+ */
+sq_status sq_hadamard_factor(int32_t n, int8_t* out_host);
+
+/*
+ * sq_had_quant_act -- online Hadamard rotation of every activation row (R4, Sec. 3.1) fused with asymmetric 4-bit quantization of
+ * eq. 1 (Sec. 2) and nibble packing.
+ *
+ *   x          device fp16 [M, ldx], row stride ldx elements; row m is x[m*ldx .. +K)
+ *   M, K       rows (tokens) and row length; M >= 0 (M == 0 is a no-op), 0 < K <= SQ_MAX_ROW,
+ *              K % 8 == 0
+ *   ldx        >= K, ldx % 8 == 0; x must be 16-byte aligned
+ *   had_dense_n  a, order of the dense factor, 1 <= a <= SQ_MAX_DENSE
+ *   had_dense  device int8 +-1 [a, a] row-major (must be a Hadamard matrix); NULL iff a == 1
+ *   had_pow2_n b, power of two, 1 <= b <= 32768; n = a*b must divide K
+ *   bits       4 (others: SQ_ERR_UNSUPPORTED)
+ *   group      quantization group length along the row: group | K, group % 2 == 0;
+ *              group == K is per-token quantization (what sq_w4a4_linear consumes)
+ *   q_out      device uint8 [M, K/2] (contiguous), 16-byte aligned: packed codes 0..15
+ *   alpha, beta device fp32 [M, K/group] (contiguous): scale and offset of each group
+ *   dbg_rot    optional device fp32 [M, K]: the rotated rows (quantizer input); NULL to skip
+ *   stream     hipStream_t
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.
+ */
+sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
+                           int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                           int32_t bits, int32_t group,
+                           uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
+                           void* stream);
+
+/*
+ * sq_pack_w4 -- offline weight preparation: optionally absorb the online
+ * rotation into the weight, W' = W R (Sec. 3.1: rotations merge into the adjacent
+ * weights, so (x R)(W R)^T = x W^T), then symmetric 4-bit quantization of eq. 1 per
+ * output channel (row), nibble packing, and the per-row sum of codes used by the
+ * epilogue's zero-point term.
+ *
+ *   w          device fp16 [N, ldw], 16-byte aligned, ldw >= K, ldw % 8 == 0
+ *   N, K       output channels and row length; N >= 0, 0 < K <= SQ_MAX_ROW, K % 8 == 0
+ *   had_dense_n, had_dense, had_pow2_n   rotation as in sq_had_quant_act ((1, NULL, 1) = none)
+ *   wq         device uint8 [N, K/2], 16-byte aligned: two's-complement nibbles -7..7
+ *   w_alpha    device fp32 [N]: per-channel scale
+ *   w_rowsum   device int32 [N]: sum over k of the codes of row n
+ * Errors: as sq_had_quant_act.
+ */
+sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
+                     int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                     uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream);
+
+/*
+ * sq_w4a4_linear -- the quantized linear layer y = x W^T on 4-bit codes.  The int4 x int4 products
+ * accumulate exactly in int32, acc[m,n] = sum_k qa[m,k] qw[n,k]; the epilogue expands
+ * eq. 1 on both operands:
+ *     y[m,n] = fp16( w_alpha[n] * (x_alpha[m] * acc[m,n] + x_beta[m] * w_rowsum[n]) + bias[n] )
+ *
+ *   xq         device uint8 [M, K/2], 16-byte aligned: per-token activation codes
+ *              (from sq_had_quant_act with group == K)
+ *   x_alpha, x_beta  device fp32 [M]
+ *   M          >= 0 (0 is a no-op)
+ *   wq, w_alpha, w_rowsum   device, from sq_pack_w4: uint8 [N, K/2] (16-byte aligned), fp32 [N], int32 [N]
+ *   N          >= 1
+ *   K          > 0, K % 64 == 0
+ *   bias       optional device fp16 [N]; NULL for none
+ *   y          device fp16 [M, ldy], ldy >= N, 2-byte aligned
+ *   dbg_acc    optional device int32 [M, N] (contiguous): the raw accumulators; NULL to skip
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.
+ */
+sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                         const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                         int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
+                         int32_t* dbg_acc, void* stream);
+
+/*
+ * sq_qk_had_kvquant -- R3 (Sec. 3.1) on post-RoPE queries and keys, per head,
+ * R = S_D / sqrt(D); then asymmetric 4-bit quantization of eq. 1 of the rotated keys
+ * and of the (unrotated) values, one group per `group` contiguous elements of a head
+ * vector (group == D: one (alpha, beta) per batch, token and head).
+ *
+ *   q, k, v    device fp16 [B, S, H, D] contiguous, 16-byte aligned
+ *   B, S, H    >= 0 (any zero: no-op); D = 128
+ *   bits       4; group = 128 (= D)
+ *   q_rot      device fp16 [B, S, H, D]: Q R, rounded to nearest fp16
+ *   k_q, v_q   device uint8 [B, S, H, D/2], 16-byte aligned: packed codes 0..15
+ *   k_alpha, k_beta, v_alpha, v_beta   device fp32 [B, S, H, D/group]
+ *   dbg_k_rot  optional device fp32 [B, S, H, D]: K R before quantization; NULL to skip
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.
+ */
+sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
+                            int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
+                            void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
+                            uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                            void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SQ_H_ */

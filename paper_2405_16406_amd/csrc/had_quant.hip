@@ -1,0 +1,203 @@
+// Online Hadamard rotation of rows fused with 4-bit quantization (eq. 1, Sec. 2).
+//
+// Generic kernel: one workgroup of 256 threads per row.  The rotated row lives in LDS
+// as fp32.  Each contiguous block of n = a*b elements is multiplied by
+// (S_b (x) H_a) / sqrt(n) with element i = i_b*a + i_a:
+//   1. dense stage  Y[i_b][j_a] = sum_{i_a} x[i_b*a + i_a] H[i_a][j_a]   (fp32, from L1/L2)
+//   2. Walsh-Hadamard butterflies over i_b (stride a), one LDS pass per stage
+//   3. scale by fl32(1/sqrt(n))
+// then the quantizer: asymmetric per group (activations) or symmetric per row with the
+// code row sum (weights).
+#include "sq_device.h"
+#include "sq_internal.h"
+
+namespace sq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+
+__device__ float block_min(float v, float* red) {
+  v = wave_min(v);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = fminf(r, red[i]);
+  return r;
+}
+__device__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = fmaxf(r, red[i]);
+  return r;
+}
+__device__ int block_sum(int v, int* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+  __syncthreads();
+  int r = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) r += red[i];
+  return r;
+}
+
+// Fills buf[0..K) with the rotated row (fp32).  Ends with a barrier.
+__device__ void rotate_row_to_lds(const uint16_t* __restrict__ xr, int K, int a,
+                                  const int8_t* __restrict__ H, int b, float inv_sqrt_n,
+                                  float* __restrict__ buf) {
+  const int n = a * b;
+  if (a == 1) {
+    for (int i = threadIdx.x; i < K; i += kThreads) buf[i] = h2f(xr[i]);
+  } else {
+    for (int i = threadIdx.x; i < K; i += kThreads) {
+      const int ja = i % a;
+      const int base = i - ja;
+      float acc = 0.0f;
+      for (int ia = 0; ia < a; ++ia) {
+        const float h = static_cast<float>(H[ia * a + ja]);
+        acc = __fadd_rn(acc, __fmul_rn(h2f(xr[base + ia]), h));
+      }
+      buf[i] = acc;
+    }
+  }
+  __syncthreads();
+  const int half = K / 2;
+  const int npair = n / 2;
+  for (int h = 1; h < b; h <<= 1) {
+    for (int p = threadIdx.x; p < half; p += kThreads) {
+      const int blk = p / npair;
+      const int pin = p - blk * npair;
+      const int ja = pin % a;
+      const int qq = pin / a;
+      const int lo_b = (qq / h) * (2 * h) + (qq % h);
+      const int lo = blk * n + lo_b * a + ja;
+      const int hi = lo + h * a;
+      const float u = buf[lo];
+      const float w = buf[hi];
+      buf[lo] = __fadd_rn(u, w);
+      buf[hi] = __fsub_rn(u, w);
+    }
+    __syncthreads();
+  }
+  if (n > 1) {
+    for (int i = threadIdx.x; i < K; i += kThreads) buf[i] = __fmul_rn(buf[i], inv_sqrt_n);
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+had_quant_act_generic(RotQuantArgs args) {
+  extern __shared__ float buf[];
+  __shared__ float red_f[kWaves];
+  const int64_t row = blockIdx.x;
+  const int K = static_cast<int>(args.K);
+  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, buf);
+  if (args.dbg) {
+    for (int i = threadIdx.x; i < K; i += kThreads) args.dbg[row * K + i] = buf[i];
+  }
+  uint8_t* qrow = args.q + row * (K / 2);
+  const int G = K / args.group;
+  if (G == 1) {
+    float mn = INFINITY, mx = -INFINITY;
+    for (int i = threadIdx.x; i < K; i += kThreads) {
+      mn = fminf(mn, buf[i]);
+      mx = fmaxf(mx, buf[i]);
+    }
+    mn = block_min(mn, red_f);
+    mx = block_max(mx, red_f);
+    const AsymParams p = asym_params(mn, mx);
+    if (threadIdx.x == 0) {
+      args.alpha[row] = p.alpha;
+      args.beta[row] = p.mn;
+    }
+    for (int j = threadIdx.x; j < K / 2; j += kThreads) {
+      const uint32_t c0 = asym_code(buf[2 * j], p);
+      const uint32_t c1 = asym_code(buf[2 * j + 1], p);
+      qrow[j] = static_cast<uint8_t>(c0 | (c1 << 4));
+    }
+    return;
+  }
+  // one wave per group
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int gs = args.group;
+  for (int g = wave; g < G; g += kWaves) {
+    const float* v = buf + g * gs;
+    float mn = INFINITY, mx = -INFINITY;
+    for (int i = lane; i < gs; i += kWave) {
+      mn = fminf(mn, v[i]);
+      mx = fmaxf(mx, v[i]);
+    }
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    const AsymParams p = asym_params(mn, mx);
+    if (lane == 0) {
+      args.alpha[row * G + g] = p.alpha;
+      args.beta[row * G + g] = p.mn;
+    }
+    for (int j = lane; j < gs / 2; j += kWave) {
+      const uint32_t c0 = asym_code(v[2 * j], p);
+      const uint32_t c1 = asym_code(v[2 * j + 1], p);
+      qrow[g * (gs / 2) + j] = static_cast<uint8_t>(c0 | (c1 << 4));
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+pack_w4_generic(RotQuantArgs args) {
+  extern __shared__ float buf[];
+  __shared__ float red_f[kWaves];
+  __shared__ int red_i[kWaves];
+  const int64_t row = blockIdx.x;
+  const int K = static_cast<int>(args.K);
+  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, buf);
+  float amax = 0.0f;
+  for (int i = threadIdx.x; i < K; i += kThreads) amax = fmaxf(amax, fabsf(buf[i]));
+  amax = block_max(amax, red_f);
+  const float alpha = sym_alpha(amax);
+  const float inv = __fdiv_rn(1.0f, alpha);
+  uint8_t* qrow = args.q + row * (K / 2);
+  int sum = 0;
+  for (int j = threadIdx.x; j < K / 2; j += kThreads) {
+    const int c0 = sym_code(buf[2 * j], inv);
+    const int c1 = sym_code(buf[2 * j + 1], inv);
+    sum += c0 + c1;
+    qrow[j] = static_cast<uint8_t>((c0 & 0xF) | ((c1 & 0xF) << 4));
+  }
+  sum = block_sum(sum, red_i);
+  if (threadIdx.x == 0) {
+    args.alpha[row] = alpha;
+    args.rowsum[row] = sum;
+  }
+}
+
+hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hipStream_t stream) {
+  const size_t lds = static_cast<size_t>(a.K) * sizeof(float);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(a.rows)), dim3(kThreads), lds, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream) {
+  return launch_generic(had_quant_act_generic, a, stream);
+}
+
+hipError_t launch_pack_w4(const RotQuantArgs& a, hipStream_t stream) {
+  return launch_generic(pack_w4_generic, a, stream);
+}
+
+}  // namespace sq

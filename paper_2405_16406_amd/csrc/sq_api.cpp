@@ -1,0 +1,256 @@
+// Host side of the C ABI declared in include/sq.h: argument validation, error state
+// and kernel launches.  Every check runs before anything is enqueued; on a non-OK
+// status nothing is written.
+#include "sq.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sq_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+sq_status fail(sq_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+sq_status ok() {
+  g_last_error.clear();
+  return SQ_OK;
+}
+
+sq_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(SQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+struct Range {
+  const void* p;
+  uint64_t bytes;
+  const char* name;
+};
+
+bool overlap(const Range& a, const Range& b) {
+  if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// Outputs must not overlap any input or each other.
+sq_status check_alias(const std::vector<Range>& ins, const std::vector<Range>& outs) {
+  for (size_t i = 0; i < outs.size(); ++i) {
+    for (const Range& in : ins)
+      if (overlap(outs[i], in)) return fail(SQ_ERR_ALIAS, "output %s overlaps input %s", outs[i].name, in.name);
+    for (size_t j = i + 1; j < outs.size(); ++j)
+      if (overlap(outs[i], outs[j]))
+        return fail(SQ_ERR_ALIAS, "output %s overlaps output %s", outs[i].name, outs[j].name);
+  }
+  return SQ_OK;
+}
+
+// Shared checks of the row-rotation arguments.
+sq_status check_rotation(int64_t K, int32_t a, const int8_t* H, int32_t b) {
+  if (a < 1 || a > SQ_MAX_DENSE) return fail(SQ_ERR_SHAPE, "had_dense_n=%d outside [1, %d]", a, SQ_MAX_DENSE);
+  if ((a == 1) != (H == nullptr))
+    return fail(a == 1 ? SQ_ERR_SHAPE : SQ_ERR_NULL, "had_dense must be NULL iff had_dense_n == 1 (n=%d)", a);
+  if (!is_pow2(b) || b > 32768) return fail(SQ_ERR_SHAPE, "had_pow2_n=%d is not a power of two in [1, 32768]", b);
+  const int64_t n = static_cast<int64_t>(a) * b;
+  if (K % n != 0) return fail(SQ_ERR_SHAPE, "rotation width %lld does not divide K=%lld", (long long)n, (long long)K);
+  return SQ_OK;
+}
+
+sq_status check_rows(int64_t M, int64_t K, int64_t ld, const char* mname) {
+  if (M < 0) return fail(SQ_ERR_SHAPE, "%s=%lld < 0", mname, (long long)M);
+  if (M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "%s=%lld too large", mname, (long long)M);
+  if (K <= 0 || K > SQ_MAX_ROW) return fail(SQ_ERR_SHAPE, "K=%lld outside (0, %d]", (long long)K, SQ_MAX_ROW);
+  if (K % 8 != 0) return fail(SQ_ERR_SHAPE, "K=%lld is not a multiple of 8", (long long)K);
+  if (ld < K) return fail(SQ_ERR_SHAPE, "leading dimension %lld < K=%lld", (long long)ld, (long long)K);
+  if (ld % 8 != 0) return fail(SQ_ERR_ALIGN, "leading dimension %lld is not a multiple of 8", (long long)ld);
+  return SQ_OK;
+}
+
+float inv_sqrt(int64_t n) { return static_cast<float>(1.0 / std::sqrt(static_cast<double>(n))); }
+
+}  // namespace
+
+extern "C" {
+
+int32_t sq_abi_version(void) { return SQ_ABI_VERSION; }
+
+const char* sq_last_error(void) { return g_last_error.c_str(); }
+
+sq_status sq_hadamard_factor(int32_t n, int8_t* out_host) {
+  if (!out_host) return fail(SQ_ERR_NULL, "out_host is NULL");
+  std::vector<int8_t> h;
+  if (!sq::hadamard_factor(n, &h)) return fail(SQ_ERR_UNSUPPORTED, "no Hadamard factor of order %d", n);
+  std::memcpy(out_host, h.data(), h.size());
+  return ok();
+}
+
+sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
+                           int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                           int32_t bits, int32_t group,
+                           uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
+                           void* stream) {
+  if (!x || !q_out || !alpha || !beta) return fail(SQ_ERR_NULL, "x, q_out, alpha and beta are required");
+  sq_status s = check_rows(M, K, ldx, "M");
+  if (s != SQ_OK) return s;
+  if ((s = check_rotation(K, had_dense_n, had_dense, had_pow2_n)) != SQ_OK) return s;
+  if (bits != 4) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: only 4-bit activations are implemented", bits);
+  if (group <= 0 || group % 2 != 0 || K % group != 0)
+    return fail(SQ_ERR_SHAPE, "group=%d must be even and divide K=%lld", group, (long long)K);
+  if (!aligned(x, 16) || !aligned(q_out, 16) || !aligned(alpha, 4) || !aligned(beta, 4) ||
+      (dbg_rot && !aligned(dbg_rot, 4)))
+    return fail(SQ_ERR_ALIGN, "x and q_out must be 16-byte aligned, scales 4-byte aligned");
+  const uint64_t G = static_cast<uint64_t>(K / group);
+  const uint64_t um = static_cast<uint64_t>(M);
+  const uint64_t xbytes = um ? ((um - 1) * ldx + K) * 2 : 0;
+  s = check_alias({{x, xbytes, "x"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"}},
+                  {{q_out, um * K / 2, "q_out"}, {alpha, um * G * 4, "alpha"}, {beta, um * G * 4, "beta"},
+                   {dbg_rot, dbg_rot ? um * K * 4 : 0, "dbg_rot"}});
+  if (s != SQ_OK) return s;
+  if (M == 0) return ok();
+  sq::RotQuantArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.rows = M;
+  a.K = K;
+  a.ldx = ldx;
+  a.a = had_dense_n;
+  a.H = had_dense;
+  a.b = had_pow2_n;
+  a.group = group;
+  a.inv_sqrt_n = inv_sqrt(static_cast<int64_t>(had_dense_n) * had_pow2_n);
+  a.q = q_out;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.dbg = dbg_rot;
+  return hip_status(sq::launch_had_quant_act(a, static_cast<hipStream_t>(stream)), "had_quant_act launch");
+}
+
+sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
+                     int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                     uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream) {
+  if (!w || !wq || !w_alpha || !w_rowsum) return fail(SQ_ERR_NULL, "w, wq, w_alpha and w_rowsum are required");
+  sq_status s = check_rows(N, K, ldw, "N");
+  if (s != SQ_OK) return s;
+  if ((s = check_rotation(K, had_dense_n, had_dense, had_pow2_n)) != SQ_OK) return s;
+  if (!aligned(w, 16) || !aligned(wq, 16) || !aligned(w_alpha, 4) || !aligned(w_rowsum, 4))
+    return fail(SQ_ERR_ALIGN, "w and wq must be 16-byte aligned, w_alpha and w_rowsum 4-byte aligned");
+  const uint64_t un = static_cast<uint64_t>(N);
+  const uint64_t wbytes = un ? ((un - 1) * ldw + K) * 2 : 0;
+  s = check_alias({{w, wbytes, "w"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"}},
+                  {{wq, un * K / 2, "wq"}, {w_alpha, un * 4, "w_alpha"}, {w_rowsum, un * 4, "w_rowsum"}});
+  if (s != SQ_OK) return s;
+  if (N == 0) return ok();
+  sq::RotQuantArgs a{};
+  a.x = static_cast<const uint16_t*>(w);
+  a.rows = N;
+  a.K = K;
+  a.ldx = ldw;
+  a.a = had_dense_n;
+  a.H = had_dense;
+  a.b = had_pow2_n;
+  a.group = static_cast<int>(K);
+  a.inv_sqrt_n = inv_sqrt(static_cast<int64_t>(had_dense_n) * had_pow2_n);
+  a.q = wq;
+  a.alpha = w_alpha;
+  a.rowsum = w_rowsum;
+  return hip_status(sq::launch_pack_w4(a, static_cast<hipStream_t>(stream)), "pack_w4 launch");
+}
+
+sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                         const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                         int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
+                         int32_t* dbg_acc, void* stream) {
+  if (!xq || !x_alpha || !x_beta || !wq || !w_alpha || !w_rowsum || !y)
+    return fail(SQ_ERR_NULL, "xq, x_alpha, x_beta, wq, w_alpha, w_rowsum and y are required");
+  if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
+  if (N <= 0 || N > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "N=%lld out of range", (long long)N);
+  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 24))
+    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^24)", (long long)K);
+  if (ldy < N) return fail(SQ_ERR_SHAPE, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+  if (!aligned(xq, 16) || !aligned(wq, 16) || !aligned(y, 2) || !aligned(x_alpha, 4) || !aligned(x_beta, 4) ||
+      !aligned(w_alpha, 4) || !aligned(w_rowsum, 4) || (bias && !aligned(bias, 2)) || (dbg_acc && !aligned(dbg_acc, 4)))
+    return fail(SQ_ERR_ALIGN, "xq/wq need 16-byte, scales 4-byte and y 2-byte alignment");
+  const uint64_t um = static_cast<uint64_t>(M), un = static_cast<uint64_t>(N), uk = static_cast<uint64_t>(K);
+  const uint64_t ybytes = um ? ((um - 1) * ldy + un) * 2 : 0;
+  sq_status s = check_alias({{xq, um * uk / 2, "xq"}, {x_alpha, um * 4, "x_alpha"}, {x_beta, um * 4, "x_beta"},
+                             {wq, un * uk / 2, "wq"}, {w_alpha, un * 4, "w_alpha"}, {w_rowsum, un * 4, "w_rowsum"},
+                             {bias, bias ? un * 2 : 0, "bias"}},
+                            {{y, ybytes, "y"}, {dbg_acc, dbg_acc ? um * un * 4 : 0, "dbg_acc"}});
+  if (s != SQ_OK) return s;
+  if (M == 0) return ok();
+  sq::GemmArgs g{};
+  g.xq = xq;
+  g.xa = x_alpha;
+  g.xb = x_beta;
+  g.M = M;
+  g.wq = wq;
+  g.wa = w_alpha;
+  g.rs = w_rowsum;
+  g.N = N;
+  g.K = K;
+  g.bias = static_cast<const uint16_t*>(bias);
+  g.y = static_cast<uint16_t*>(y);
+  g.ldy = ldy;
+  g.dbg_acc = dbg_acc;
+  return hip_status(sq::launch_w4a4_gemm(g, static_cast<hipStream_t>(stream)), "w4a4_linear launch");
+}
+
+sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
+                            int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
+                            void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
+                            uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                            void* stream) {
+  if (!q || !k || !v || !q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta)
+    return fail(SQ_ERR_NULL, "q, k, v, q_rot, k_q, k_alpha, k_beta, v_q, v_alpha and v_beta are required");
+  if (B < 0 || S < 0 || H < 0) return fail(SQ_ERR_SHAPE, "negative B, S or H");
+  if (D != 128) return fail(SQ_ERR_UNSUPPORTED, "D=%lld: only head_dim 128 is implemented", (long long)D);
+  if (bits != 4) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: only 4-bit KV is implemented", bits);
+  if (group != 128) return fail(SQ_ERR_UNSUPPORTED, "group=%d: only group 128 (= D) is implemented", group);
+  const uint64_t groups = static_cast<uint64_t>(B) * static_cast<uint64_t>(S) * static_cast<uint64_t>(H);
+  if (groups > (uint64_t{1} << 40)) return fail(SQ_ERR_SHAPE, "B*S*H too large");
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(q_rot, 16) || !aligned(k_q, 16) ||
+      !aligned(v_q, 16) || !aligned(k_alpha, 4) || !aligned(k_beta, 4) || !aligned(v_alpha, 4) ||
+      !aligned(v_beta, 4) || (dbg_k_rot && !aligned(dbg_k_rot, 4)))
+    return fail(SQ_ERR_ALIGN, "tensors need 16-byte, scales 4-byte alignment");
+  const uint64_t E = groups * 128;
+  sq_status s = check_alias({{q, E * 2, "q"}, {k, E * 2, "k"}, {v, E * 2, "v"}},
+                            {{q_rot, E * 2, "q_rot"}, {k_q, E / 2, "k_q"}, {k_alpha, groups * 4, "k_alpha"},
+                             {k_beta, groups * 4, "k_beta"}, {v_q, E / 2, "v_q"}, {v_alpha, groups * 4, "v_alpha"},
+                             {v_beta, groups * 4, "v_beta"}, {dbg_k_rot, dbg_k_rot ? E * 4 : 0, "dbg_k_rot"}});
+  if (s != SQ_OK) return s;
+  if (groups == 0) return ok();
+  sq::KvArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.groups = static_cast<int64_t>(groups);
+  a.inv_sqrt_d = inv_sqrt(128);
+  a.q_rot = static_cast<uint16_t*>(q_rot);
+  a.kq = k_q;
+  a.ka = k_alpha;
+  a.kb = k_beta;
+  a.vq = v_q;
+  a.va = v_alpha;
+  a.vb = v_beta;
+  a.dbg_k = dbg_k_rot;
+  return hip_status(sq::launch_qk_had_kvquant(a, static_cast<hipStream_t>(stream)), "qk_had_kvquant launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+// Device helpers shared by the HIP kernels: the eq. 1 quantizer's exact fp32 op
+// sequence, wave/workgroup reductions, fp16 conversions.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace sq {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float h2f(uint16_t bits) {
+  return __half2float(__ushort_as_half(bits));
+}
+__device__ __forceinline__ uint16_t f2h(float v) {
+  return __half_as_ushort(__float2half_rn(v));
+}
+
+// Asymmetric eq. 1 parameters from a group's min and max (4-bit: L = 15).
+//   r = mx - mn;  alpha = r / L (1 if r == 0);  inv = 1 / alpha  -- each one IEEE rounding.
+struct AsymParams {
+  float mn, alpha, inv;
+};
+__device__ __forceinline__ AsymParams asym_params(float mn, float mx) {
+  const float r = __fsub_rn(mx, mn);
+  const float alpha = (r == 0.0f) ? 1.0f : __fdiv_rn(r, 15.0f);
+  return {mn, alpha, __fdiv_rn(1.0f, alpha)};
+}
+// code = clamp(rint((v - mn) * inv), 0, 15)
+__device__ __forceinline__ uint32_t asym_code(float v, const AsymParams& p) {
+  const float t = __fmul_rn(__fsub_rn(v, p.mn), p.inv);
+  return static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), 15.0f));
+}
+
+// Symmetric eq. 1 (beta = 0, L = 7): alpha = amax / 7 (1 if amax == 0); code in [-7, 7].
+__device__ __forceinline__ float sym_alpha(float amax) {
+  return (amax == 0.0f) ? 1.0f : __fdiv_rn(amax, 7.0f);
+}
+__device__ __forceinline__ int sym_code(float v, float inv) {
+  return static_cast<int>(fminf(fmaxf(rintf(__fmul_rn(v, inv)), -7.0f), 7.0f));
+}
+
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+}  // namespace sq

@@ -1,0 +1,73 @@
+// Internal declarations shared by the host API and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+namespace sq {
+
+// Host: the library's dense Hadamard factor of order n (1, 28, 172); false if none.
+bool hadamard_factor(int n, std::vector<int8_t>* out);
+
+// Arguments of one row-rotation + quantization launch (activations or weights).
+struct RotQuantArgs {
+  const uint16_t* x;     // fp16 bits [rows, ldx]
+  int64_t rows;
+  int64_t K;
+  int64_t ldx;
+  int a;                 // dense factor order
+  const int8_t* H;       // [a, a] +-1 (device), nullptr when a == 1
+  int b;                 // Sylvester order
+  int group;             // quantization group (asym mode)
+  float inv_sqrt_n;      // fl32(1 / sqrt(a * b))
+  uint8_t* q;            // packed codes [rows, K/2]
+  float* alpha;          // [rows, K/group] (asym) or [rows] (sym)
+  float* beta;           // [rows, K/group] (asym only)
+  int32_t* rowsum;       // [rows] (sym only)
+  float* dbg;            // optional fp32 [rows, K]
+};
+
+// Rotation + asymmetric per-group 4-bit quantization of activation rows.
+hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream);
+// Rotation + symmetric per-row 4-bit quantization of weight rows, with code row sums.
+hipError_t launch_pack_w4(const RotQuantArgs& a, hipStream_t stream);
+
+struct GemmArgs {
+  const uint8_t* xq;
+  const float* xa;
+  const float* xb;
+  int64_t M;
+  const uint8_t* wq;
+  const float* wa;
+  const int32_t* rs;
+  int64_t N;
+  int64_t K;
+  const uint16_t* bias;  // fp16 bits [N] or nullptr
+  uint16_t* y;           // fp16 bits [M, ldy]
+  int64_t ldy;
+  int32_t* dbg_acc;      // optional [M, N]
+};
+
+hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
+
+struct KvArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t groups;        // B * S * H (one head vector of D = 128 each)
+  float inv_sqrt_d;
+  uint16_t* q_rot;
+  uint8_t* kq;
+  float* ka;
+  float* kb;
+  uint8_t* vq;
+  float* va;
+  float* vb;
+  float* dbg_k;
+};
+
+hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream);
+
+}  // namespace sq

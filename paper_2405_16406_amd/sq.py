@@ -1,0 +1,189 @@
+"""ctypes binding of libsq.so (include/sq.h).
+
+Argument marshalling only: tensors become device pointers, sizes become int64, the
+current torch HIP stream becomes the `stream` argument.  Every step of the path runs in
+the library's HIP kernels; there is no fallback.  A missing library raises.
+Outputs are allocated with torch (device memory is torch's job here) unless passed in.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsq.so")
+
+SQ_OK, SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP = range(7)
+STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSUPPORTED",
+                4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
+
+EXPORTS = ("sq_abi_version", "sq_last_error", "sq_hadamard_factor", "sq_had_quant_act",
+           "sq_pack_w4", "sq_w4a4_linear", "sq_qk_had_kvquant")
+
+
+class SqError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsq.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2405_16406_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    L.sq_abi_version.restype = _I32
+    L.sq_abi_version.argtypes = []
+    L.sq_last_error.restype = ctypes.c_char_p
+    L.sq_last_error.argtypes = []
+    L.sq_hadamard_factor.restype = _I32
+    L.sq_hadamard_factor.argtypes = [_I32, _P]
+    L.sq_had_quant_act.restype = _I32
+    L.sq_had_quant_act.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]
+    L.sq_pack_w4.restype = _I32
+    L.sq_pack_w4.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _P, _P, _P]
+    L.sq_w4a4_linear.restype = _I32
+    L.sq_w4a4_linear.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P]
+    L.sq_qk_had_kvquant.restype = _I32
+    L.sq_qk_had_kvquant.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32,
+                                    _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str) -> None:
+    if status != SQ_OK:
+        raise SqError(status, where, lib().sq_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _need(t: torch.Tensor, dtype, name: str):
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda:
+        raise TypeError(f"{name} must be a {dtype} tensor on the GPU")
+
+
+def abi_version() -> int:
+    return int(lib().sq_abi_version())
+
+
+def hadamard_factor(n: int) -> np.ndarray:
+    """The library's +-1 Hadamard matrix of order n (1, 28, 172) as int8 [n, n] (host)."""
+    out = np.empty((n, n), dtype=np.int8)
+    _check(lib().sq_hadamard_factor(n, out.ctypes.data_as(ctypes.c_void_p)), "sq_hadamard_factor")
+    return out
+
+
+def had_quant_act(x: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1,
+                  group: int | None = None, bits: int = 4, dbg: bool = False, out=None):
+    """Rotate rows of x (fp16 [M, K], row stride x.stride(0)) and quantize (asym 4-bit).
+
+    had: int8 +-1 [a, a] on the device or None.  Returns (q uint8 [M, K/2],
+    alpha fp32 [M, K/group], beta fp32 [M, K/group], dbg_rot fp32 [M, K] or None).
+    """
+    _need(x, torch.float16, "x")
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be 2-D with unit column stride")
+    M, K = x.shape
+    group = K if group is None else group
+    a = 1 if had is None else had.shape[0]
+    if had is not None:
+        _need(had, torch.int8, "had")
+    dev = x.device
+    if out is None:
+        q = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        al = torch.empty((M, K // group), dtype=torch.float32, device=dev)
+        be = torch.empty((M, K // group), dtype=torch.float32, device=dev)
+    else:
+        q, al, be = out
+    rot = torch.empty((M, K), dtype=torch.float32, device=dev) if dbg else None
+    _check(lib().sq_had_quant_act(_ptr(x), M, K, x.stride(0), a, _ptr(had), pow2, bits, group,
+                                  _ptr(q), _ptr(al), _ptr(be), _ptr(rot), _stream(x)), "sq_had_quant_act")
+    return q, al, be, rot
+
+
+def pack_w4(w: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1):
+    """Offline: W' = W R (optional), symmetric per-row 4-bit quant, pack.
+
+    Returns (wq uint8 [N, K/2], w_alpha fp32 [N], w_rowsum int32 [N]).
+    """
+    _need(w, torch.float16, "w")
+    if w.dim() != 2 or w.stride(1) != 1:
+        raise ValueError("w must be 2-D with unit column stride")
+    N, K = w.shape
+    a = 1 if had is None else had.shape[0]
+    dev = w.device
+    wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    wa = torch.empty((N,), dtype=torch.float32, device=dev)
+    rs = torch.empty((N,), dtype=torch.int32, device=dev)
+    _check(lib().sq_pack_w4(_ptr(w), N, K, w.stride(0), a, _ptr(had), pow2, _ptr(wq), _ptr(wa), _ptr(rs),
+                            _stream(w)), "sq_pack_w4")
+    return wq, wa, rs
+
+
+def w4a4_linear(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None, dbg=False):
+    """y = fp16(s_n (alpha_m acc + beta_m rowsum_n) + bias_n) with acc the exact int GEMM.
+
+    Returns (y fp16 [M, N], acc int32 [M, N] or None).
+    """
+    _need(xq, torch.uint8, "xq")
+    _need(wq, torch.uint8, "wq")
+    M, KB = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != KB:
+        raise ValueError("xq and wq disagree on K")
+    K = 2 * KB
+    dev = xq.device
+    y = torch.empty((M, N), dtype=torch.float16, device=dev) if out is None else out
+    acc = torch.empty((M, N), dtype=torch.int32, device=dev) if dbg else None
+    x_alpha = x_alpha.reshape(-1)
+    x_beta = x_beta.reshape(-1)
+    _check(lib().sq_w4a4_linear(_ptr(xq), _ptr(x_alpha), _ptr(x_beta), M, _ptr(wq), _ptr(w_alpha), _ptr(w_rowsum),
+                                N, K, _ptr(bias), _ptr(y), y.stride(0), _ptr(acc), _stream(xq)), "sq_w4a4_linear")
+    return y, acc
+
+
+def qk_had_kvquant(q, k, v, dbg: bool = False, out=None):
+    """R3 on Q and K per head (D = 128) + 4-bit asymmetric K/V quantization, group 128.
+
+    Returns dict(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, k_rot (or None)).
+    """
+    for t, nme in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.float16, nme)
+        if not t.is_contiguous():
+            raise ValueError(f"{nme} must be contiguous")
+    B, S, H, D = q.shape
+    dev = q.device
+    if out is None:
+        out = dict(q_rot=torch.empty_like(q),
+                   k_q=torch.empty((B, S, H, D // 2), dtype=torch.uint8, device=dev),
+                   k_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
+                   k_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
+                   v_q=torch.empty((B, S, H, D // 2), dtype=torch.uint8, device=dev),
+                   v_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
+                   v_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev))
+    kr = torch.empty((B, S, H, D), dtype=torch.float32, device=dev) if dbg else None
+    _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, 4, 128,
+                                   _ptr(out["q_rot"]), _ptr(out["k_q"]), _ptr(out["k_alpha"]), _ptr(out["k_beta"]),
+                                   _ptr(out["v_q"]), _ptr(out["v_alpha"]), _ptr(out["v_beta"]), _ptr(kr),
+                                   _stream(q)), "sq_qk_had_kvquant")
+    out = dict(out)
+    out["k_rot"] = kr
+    return out

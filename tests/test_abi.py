@@ -1,0 +1,134 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function declared in
+include/sq.h, builds valid Hadamard factors, and rejects bad arguments on the host with
+the documented status before anything is enqueued (fake, never-dereferenced pointers)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import hadamard as ohad
+from paper_2405_16406_amd import sq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sq.h")
+
+P = 0x10000  # fake 16-byte-aligned "device" addresses, never dereferenced by the host
+
+
+def fake(i):
+    return ctypes.c_void_p(P * (i + 1) << 8)
+
+
+@pytest.fixture(scope="module")
+def L():
+    return sq.lib()
+
+
+def test_header_symbols_exported(L):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:sq_status|int32_t|const char\*)\s+(sq_\w+)\s*\(", text, re.M))
+    assert declared == set(sq.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_abi_version(L):
+    assert sq.abi_version() == 1
+
+
+@pytest.mark.parametrize("n", [1, 28, 172])
+def test_library_hadamard_factor(n):
+    h = sq.hadamard_factor(n).astype(np.int64)
+    assert np.array_equal(h @ h.T, n * np.eye(n, dtype=np.int64))
+    # the same published construction and selection rule as the oracle's
+    assert np.array_equal(h, ohad.dense_factor(n).astype(np.int64))
+
+
+def test_hadamard_factor_errors(L):
+    buf = np.empty(64, dtype=np.int8)
+    assert L.sq_hadamard_factor(12, buf.ctypes.data_as(ctypes.c_void_p)) == sq.SQ_ERR_UNSUPPORTED
+    assert L.sq_hadamard_factor(28, None) == sq.SQ_ERR_NULL
+    assert b"NULL" in L.sq_last_error()
+
+
+def hqa(L, x=fake(0), M=4, K=256, ldx=256, a=1, H=None, b=1, bits=4, group=None, q=fake(1), al=fake(2),
+        be=fake(3), dbg=None):
+    group = K if group is None else group
+    return L.sq_had_quant_act(x, M, K, ldx, a, H, b, bits, group, q, al, be, dbg, None)
+
+
+def test_had_quant_act_validation(L):
+    assert hqa(L, x=None) == sq.SQ_ERR_NULL
+    assert hqa(L, K=0) == sq.SQ_ERR_SHAPE
+    assert hqa(L, K=12, ldx=16) == sq.SQ_ERR_SHAPE
+    assert hqa(L, K=65536, ldx=65536) == sq.SQ_ERR_SHAPE
+    assert hqa(L, M=-1) == sq.SQ_ERR_SHAPE
+    assert hqa(L, ldx=128) == sq.SQ_ERR_SHAPE
+    assert hqa(L, ldx=260) == sq.SQ_ERR_ALIGN
+    assert hqa(L, a=28, H=None, b=1, K=28 * 8, ldx=28 * 8) == sq.SQ_ERR_NULL
+    assert hqa(L, a=1, H=fake(9)) == sq.SQ_ERR_SHAPE
+    assert hqa(L, b=3) == sq.SQ_ERR_SHAPE
+    assert hqa(L, a=28, H=fake(9), b=4, K=256) == sq.SQ_ERR_SHAPE  # 112 does not divide 256
+    assert hqa(L, a=300, H=fake(9)) == sq.SQ_ERR_SHAPE
+    assert hqa(L, bits=8) == sq.SQ_ERR_UNSUPPORTED
+    assert hqa(L, group=3) == sq.SQ_ERR_SHAPE
+    assert hqa(L, group=96) == sq.SQ_ERR_SHAPE
+    assert hqa(L, x=ctypes.c_void_p(P * 256 + 8)) == sq.SQ_ERR_ALIGN
+    assert hqa(L, q=ctypes.c_void_p(P * 256 + 4)) == sq.SQ_ERR_ALIGN
+    # q_out inside x
+    assert hqa(L, q=ctypes.c_void_p(fake(0).value + 16)) == sq.SQ_ERR_ALIAS
+    # alpha overlapping beta
+    assert hqa(L, be=ctypes.c_void_p(fake(2).value + 4)) == sq.SQ_ERR_ALIAS
+    assert b"overlaps" in L.sq_last_error()
+    # empty batch is a valid no-op: returns before any HIP call
+    assert hqa(L, M=0) == sq.SQ_OK
+    assert L.sq_last_error() == b""
+
+
+def test_pack_w4_validation(L):
+    def call(w=fake(0), N=8, K=256, ldw=256, a=1, H=None, b=1, wq=fake(1), wa=fake(2), rs=fake(3)):
+        return L.sq_pack_w4(w, N, K, ldw, a, H, b, wq, wa, rs, None)
+    assert call(rs=None) == sq.SQ_ERR_NULL
+    assert call(K=100, ldw=100) == sq.SQ_ERR_SHAPE
+    assert call(b=512) == sq.SQ_ERR_SHAPE
+    assert call(wq=ctypes.c_void_p(fake(0).value)) == sq.SQ_ERR_ALIAS
+    assert call(N=0) == sq.SQ_OK
+
+
+def lin(L, xq=fake(0), xa=fake(1), xb=fake(2), M=4, wq=fake(3), wa=fake(4), rs=fake(5), N=64, K=256,
+        bias=None, y=fake(6), ldy=64, acc=None):
+    return L.sq_w4a4_linear(xq, xa, xb, M, wq, wa, rs, N, K, bias, y, ldy, acc, None)
+
+
+def test_w4a4_linear_validation(L):
+    assert lin(L, y=None) == sq.SQ_ERR_NULL
+    assert lin(L, K=96) == sq.SQ_ERR_SHAPE
+    assert lin(L, N=0) == sq.SQ_ERR_SHAPE
+    assert lin(L, ldy=32) == sq.SQ_ERR_SHAPE
+    assert lin(L, y=ctypes.c_void_p(P * 256 + 1)) == sq.SQ_ERR_ALIGN
+    assert lin(L, xq=ctypes.c_void_p(P * 256 + 8)) == sq.SQ_ERR_ALIGN
+    assert lin(L, y=ctypes.c_void_p(fake(0).value)) == sq.SQ_ERR_ALIAS
+    assert lin(L, acc=ctypes.c_void_p(fake(6).value + 64)) == sq.SQ_ERR_ALIAS
+    assert lin(L, M=0) == sq.SQ_OK
+
+
+def kvq(L, B=1, S=2, H=2, D=128, bits=4, group=128, **kw):
+    ptrs = [fake(i) for i in range(10)]
+    for i, nm in enumerate(("q", "k", "v", "qr", "kq", "ka", "kb", "vq", "va", "vb")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_qk_had_kvquant(ptrs[0], ptrs[1], ptrs[2], B, S, H, D, bits, group, *ptrs[3:], None, None)
+
+
+def test_kv_validation(L):
+    assert kvq(L, q=None) == sq.SQ_ERR_NULL
+    assert kvq(L, D=64) == sq.SQ_ERR_UNSUPPORTED
+    assert kvq(L, bits=8) == sq.SQ_ERR_UNSUPPORTED
+    assert kvq(L, group=64) == sq.SQ_ERR_UNSUPPORTED
+    assert kvq(L, B=-1) == sq.SQ_ERR_SHAPE
+    assert kvq(L, qr=fake(0)) == sq.SQ_ERR_ALIAS
+    assert kvq(L, kq=ctypes.c_void_p(fake(4).value + 4)) == sq.SQ_ERR_ALIGN
+    assert kvq(L, B=0) == sq.SQ_OK

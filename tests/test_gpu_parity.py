@@ -1,0 +1,310 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle, element by
+element on the same seeded inputs.  Tolerances are documented in tests/parity.py."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hadamard as ohad
+from oracle import kv as okv
+from oracle import linear as olin
+from oracle import quant as oq
+from oracle import rotate as orot
+from paper_2405_16406_amd import sq, workloads
+
+import parity
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def say(msg):
+    print(f"[gpu case] {msg}", flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def had_table(a):
+    """Oracle's dense factor (the paper allows any Hadamard matrix), uploaded."""
+    return None if a == 1 else dev(ohad.dense_factor(a))
+
+
+def check_act(x, a, b, group=None, sample_rows=None):
+    """GPU sq_had_quant_act vs oracle.had_quant_act on fp16 rows x."""
+    K = x.shape[1]
+    group = K if group is None else group
+    ha = None if a == 1 else ohad.dense_factor(a)
+    q, al, be, rot = sq.had_quant_act(dev(x), had_table(a), b, group=group, dbg=True)
+    gq, gal, gbe, grot = host(q), host(al), host(be), host(rot)
+    rows = np.arange(x.shape[0]) if sample_rows is None else sample_rows
+    xs = x[rows]
+    op, oal, obe, oy, oc = olin.had_quant_act(xs, ha, b, group=group)
+    gc = parity.unpack(gq[rows], signed=False)
+    if a * b == 1:
+        np.testing.assert_array_equal(grot[rows], oy)
+        np.testing.assert_array_equal(gq[rows], op)
+        np.testing.assert_array_equal(gal[rows], oal)
+        np.testing.assert_array_equal(gbe[rows], obe)
+        return 0
+    parity.assert_rot_close(grot[rows], oy)
+    parity.assert_params_close(gal[rows], oal, gbe[rows], obe)
+    return parity.code_flips(gc, oc, oy, oal, obe, group)
+
+
+# ---------------------------------------------------------------- activations
+
+def test_tiny_identity_quant_bit_exact():
+    say("had_quant_act tiny identity")
+    x, _ = workloads.tiny_inputs()
+    assert check_act(x, 1, 1) == 0
+
+
+def test_tiny_sylvester256():
+    say("had_quant_act tiny Sylvester 256")
+    x, _ = workloads.tiny_inputs()
+    check_act(x, 1, 256)
+
+
+@pytest.mark.parametrize("a,b,M", [(28, 4, 37), (172, 2, 5), (28, 16, 64), (1, 64, 3), (1, 1024, 2),
+                                   (172, 64, 9), (28, 512, 4), (28, 1024, 3)])
+def test_kronecker_shapes_small(a, b, M):
+    say(f"had_quant_act a={a} b={b} M={M}")
+    rng = workloads.rng_for(100 + a + b + M)
+    x = workloads.outlier_acts(rng, M, a * b, max(1, a * b // 100), 50.0)
+    check_act(x, a, b)
+
+
+def test_blockwise_rotation_and_groups():
+    say("had_quant_act block rotation n<K with group 128")
+    rng = workloads.rng_for(7)
+    x = workloads.outlier_acts(rng, 19, 28 * 8 * 4, 6, 50.0)
+    check_act(x, 28, 8, group=224)
+    check_act(x, 1, 1, group=128)
+
+
+def test_edge_rows():
+    say("had_quant_act edge rows")
+    K = 28 * 64
+    x = np.zeros((6, K), dtype=np.float16)
+    x[1, :] = 0.5                     # constant row
+    x[2, 17] = 300.0                  # single outlier
+    x[3, :] = np.float16(-65504.0)    # fp16 extreme, constant
+    x[4, ::2] = 1.0
+    x[5] = workloads.outlier_acts(workloads.rng_for(3), 1, K, 3, 50.0)[0]
+    check_act(x, 28, 64)
+    check_act(x, 1, 1)
+
+
+def test_llama2_7b_act_full():
+    say("had_quant_act LLaMA-2-7B M=2048: identity [2048,4096] and R4 H172xH64 [2048,11008]")
+    inp = workloads.mlp_inputs(workloads.LLAMA2_7B_MLP)
+    assert check_act(inp["x_in"], 1, 1) == 0
+    check_act(inp["x_down"], 172, 64)
+
+
+def test_llama3_8b_act_full():
+    say("had_quant_act LLaMA-3-8B M=4096: R4 H28xH512 [4096,14336]")
+    inp = workloads.mlp_inputs(workloads.LLAMA3_8B_MLP)
+    check_act(inp["x_down"], 28, 512)
+
+
+def test_llama2_70b_decode_act():
+    for shape in workloads.LLAMA2_70B_DECODE:
+        say(f"had_quant_act {shape.name}: R4 H28xH1024 [M,28672]")
+        inp = workloads.mlp_inputs(shape)
+        assert check_act(inp["x_in"], 1, 1) == 0
+        check_act(inp["x_down"], 28, 1024)
+
+
+def test_deterministic():
+    say("had_quant_act determinism")
+    x = workloads.mlp_inputs(workloads.LLAMA2_7B_MLP, rows=64)["x_down"]
+    t = dev(x)
+    h = had_table(172)
+    r1 = [host(v) for v in sq.had_quant_act(t, h, 64)[:3]]
+    r2 = [host(v) for v in sq.had_quant_act(t, h, 64)[:3]]
+    for u, v in zip(r1, r2):
+        assert np.array_equal(u, v)
+
+
+# ---------------------------------------------------------------- weights
+
+def check_w(w, a, b):
+    ha = None if a == 1 else ohad.dense_factor(a)
+    wq, wa, rs = sq.pack_w4(dev(w), had_table(a), b)
+    gq, gwa, grs = host(wq), host(wa), host(rs)
+    op, owa, ors, oc = olin.pack_w4(w, ha, b)
+    gc = parity.unpack(gq, signed=True)
+    np.testing.assert_array_equal(grs, gc.sum(1))
+    if a * b == 1:
+        np.testing.assert_array_equal(gq, op)
+        np.testing.assert_array_equal(gwa, owa)
+        np.testing.assert_array_equal(grs, ors)
+        return 0
+    parity.assert_params_close(gwa, owa)
+    w32 = orot.rotate_rows(w, ha, b).astype(np.float32)
+    n = parity.code_flips(gc, oc)
+    if n:
+        # every flipped weight code sits on a rounding boundary of the oracle's own arithmetic
+        t = w32.astype(np.float64) / owa.astype(np.float64)[:, None]
+        frac = np.abs(t - np.floor(t) - 0.5)
+        assert np.all(frac[np.nonzero(gc - oc)] <= 1e-3)
+    return n
+
+
+def test_pack_w4_tiny_and_kronecker():
+    say("pack_w4 tiny (none / Sylvester 256) and small Kronecker")
+    _, w = workloads.tiny_inputs()
+    assert check_w(w, 1, 1) == 0
+    check_w(w, 1, 256)
+    rng = workloads.rng_for(11)
+    check_w(workloads.weights(rng, 37, 28 * 32), 28, 32)
+    check_w(workloads.weights(rng, 20, 172 * 4), 172, 4)
+    z = np.zeros((3, 256), dtype=np.float16)
+    assert check_w(z, 1, 1) == 0
+
+
+def test_pack_w4_llama2_7b_down_full():
+    say("pack_w4 LLaMA-2-7B down [4096,11008] folded with H172xH64")
+    w = workloads.mlp_inputs(workloads.LLAMA2_7B_MLP, rows=1)["w_down"]
+    check_w(w, 172, 64)
+
+
+# ---------------------------------------------------------------- GEMM
+
+def gemm_case(M, N, K, seed, bias=True, sample_rows=None):
+    rng = workloads.rng_for(seed)
+    qa = rng.integers(0, 16, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    xa = rng.uniform(0.05, 3.0, M).astype(np.float32)
+    xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+    wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
+    rs = qw.sum(1).astype(np.int32)
+    bi = (rng.standard_normal(N) * 0.1).astype(np.float16) if bias else None
+    y, acc = sq.w4a4_linear(dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa),
+                            dev(rs), dev(bi) if bias else None, dbg=True)
+    gy, gacc = host(y), host(acc)
+    rows = np.arange(M) if sample_rows is None else sample_rows
+    oy, oacc = olin.w4a4_linear(qa[rows], xa[rows], xb[rows], qw, wa, rs, bi)
+    np.testing.assert_array_equal(gacc[rows], oacc)
+    parity.assert_out_close(gy[rows], oy)
+
+
+@pytest.mark.parametrize("M,N,K", [(16, 256, 256), (37, 200, 320), (1, 8, 64), (130, 129, 128),
+                                   (256, 384, 1024), (8, 1000, 512)])
+def test_gemm_small_shapes(M, N, K):
+    say(f"w4a4_linear M={M} N={N} K={K}")
+    gemm_case(M, N, K, seed=M * 7 + N + K)
+
+
+def test_gemm_extreme_codes():
+    say("w4a4_linear extreme codes K=28672")
+    M, N, K = 3, 64, 28672
+    qa = np.full((M, K), 15)
+    qw = np.full((N, K), -7)
+    qw[1] = 7
+    xa = np.ones(M, np.float32) * 1e-4
+    xb = np.zeros(M, np.float32)
+    wa = np.ones(N, np.float32) * 1e-2
+    rs = qw.sum(1).astype(np.int32)
+    y, acc = sq.w4a4_linear(dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa),
+                            dev(rs), None, dbg=True)
+    oy, oacc = olin.w4a4_linear(qa, xa, xb, qw, wa, rs)
+    np.testing.assert_array_equal(host(acc), oacc)
+    parity.assert_out_close(host(y), oy)
+
+
+def test_gemm_llama2_7b_gate_sampled():
+    say("w4a4_linear LLaMA-2-7B gate [2048x4096]x[11008x4096], sampled rows")
+    rows = np.array([0, 1, 127, 128, 1000, 2047])
+    gemm_case(2048, 11008, 4096, seed=21, bias=False, sample_rows=rows)
+
+
+def test_gemm_llama3_8b_down_sampled():
+    say("w4a4_linear LLaMA-3-8B down [4096x14336]x[4096x14336], sampled rows")
+    rows = np.array([0, 255, 256, 4095])
+    gemm_case(4096, 4096, 14336, seed=22, bias=False, sample_rows=rows)
+
+
+@pytest.mark.parametrize("M", [1, 8, 16])
+def test_gemm_llama2_70b_decode(M):
+    say(f"w4a4_linear LLaMA-2-70B decode M={M}: [M,8192]x[28672,8192] and [M,28672]x[8192,28672]")
+    gemm_case(M, 28672, 8192, seed=30 + M, bias=False)
+    gemm_case(M, 8192, 28672, seed=40 + M, bias=False)
+
+
+# ---------------------------------------------------------------- chain
+
+def test_tiny_rotated_linear_chain():
+    say("tiny rotated W4A4 linear chain (had_quant_act -> pack_w4 -> w4a4_linear)")
+    x, w = workloads.tiny_inputs()
+    q, al, be, _ = sq.had_quant_act(dev(x), None, 256)
+    wq, wa, rs = sq.pack_w4(dev(w), None, 256)
+    y, acc = sq.w4a4_linear(q, al, be, wq, wa, rs, dbg=True)
+    gy = host(y)
+    ref = olin.rotated_linear(x, w, None, 256)
+    gqa = parity.unpack(host(q), signed=False)
+    gqw = parity.unpack(host(wq), signed=True)
+    if np.array_equal(gqa, ref["qa"]) and np.array_equal(gqw, ref["qw"]):
+        np.testing.assert_array_equal(host(acc), ref["acc"])
+        parity.assert_out_close(gy, ref["y"])
+    else:
+        # flipped codes move an output by alpha_m * s_n per flip and k
+        dqa = np.abs(gqa - ref["qa"]).astype(np.float64)
+        dqw = np.abs(gqw - ref["qw"]).astype(np.float64)
+        bound = (ref["x_alpha"][:, None] * (dqa @ np.abs(ref["qw"]).T) * ref["w_alpha"][None, :]
+                 + (np.abs(ref["qa"]) * ref["x_alpha"][:, None] + np.abs(ref["x_beta"])[:, None]) @ dqw.T
+                 * ref["w_alpha"][None, :])
+        err = np.abs(gy.astype(np.float64) - ref["y"].astype(np.float64))
+        scale = np.abs(ref["y"].astype(np.float64)).max(1, keepdims=True)
+        assert np.all(err <= 2e-3 * scale + 1.01 * bound)
+
+
+# ---------------------------------------------------------------- KV
+
+def check_kv(q, k, v, sample=None):
+    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True)
+    g = {n: host(t) for n, t in out.items() if t is not None}
+    B, S, H, D = q.shape
+    flat = lambda a: a.reshape(B * S * H, -1)
+    idx = np.arange(B * S * H) if sample is None else sample
+    qs, ks, vs = (flat(t)[idx][None, :, None, :] for t in (q, k, v))
+    o = okv.qk_had_kvquant(qs, ks, vs)
+    sel = lambda a: flat(a)[idx][None, :, None, :]
+    # Q R: fp16 of an fp32 sum vs fp16 of the fp64 value: one fp16 ulp of rounding plus the
+    # 1e-5 x row-max allowance of an fp32-accumulated rotation (matters for values near 0)
+    gq = sel(g["q_rot"]).astype(np.float64)
+    oq_ = o["q_rot"].astype(np.float64)
+    ulp = np.spacing(np.abs(o["q_rot"]).astype(np.float16)).astype(np.float64)
+    rowmax = np.abs(oq_).max(axis=-1, keepdims=True)
+    assert np.all(np.abs(gq - oq_) <= ulp + 1e-5 * rowmax)
+    parity.assert_rot_close(sel(g["k_rot"]).reshape(-1, 128), o["k_rot"].reshape(-1, 128))
+    parity.assert_params_close(sel(g["k_alpha"]), o["k_alpha"], sel(g["k_beta"]), o["k_beta"])
+    parity.code_flips(parity.unpack(sel(g["k_q"]), False).reshape(-1, 128), o["k_codes"].reshape(-1, 128),
+                      o["k_rot"].reshape(-1, 128), o["k_alpha"].reshape(-1, 1), o["k_beta"].reshape(-1, 1))
+    np.testing.assert_array_equal(sel(g["v_q"]), o["v_q"])
+    np.testing.assert_array_equal(sel(g["v_alpha"]), o["v_alpha"])
+    np.testing.assert_array_equal(sel(g["v_beta"]), o["v_beta"])
+
+
+def test_kv_small():
+    say("qk_had_kvquant small [2,16,4,128] and ragged [1,3,5,128]")
+    check_kv(*workloads.kv_inputs(B=2, S=16, H=4, D=128))
+    check_kv(*workloads.kv_inputs(B=1, S=3, H=5, D=128))
+
+
+def test_kv_full_sampled():
+    say("qk_had_kvquant R3 KV [8,2048,32,128], sampled groups")
+    q, k, v = workloads.kv_inputs()
+    rng = np.random.default_rng(0)
+    sample = np.unique(np.concatenate([rng.choice(8 * 2048 * 32, 20000, replace=False),
+                                       [0, 8 * 2048 * 32 - 1]]))
+    check_kv(q, k, v, sample)
