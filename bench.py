@@ -1,0 +1,303 @@
+"""Benchmark of the rotated W4A4 hot path on one MI355X.
+
+One step = one pass of the whole path over one LLaMA-2-7B transformer layer's worth of
+tokens (M = 2048):
+  1. R3 + 4-bit KV quantization of Q, K, V [1, 2048, 32, 128]          sq_qk_had_kvquant
+  2. per-token 4-bit quantization of the MLP input [2048, 4096]          sq_had_quant_act (identity)
+  3. gate and up projections [2048x4096] x [11008x4096]^T                sq_w4a4_linear x2
+  4. online R4 (S_64 (x) H_172) + 4-bit quantization of the down-projection
+     input [2048, 11008]                                                 sq_had_quant_act
+  5. down projection [2048x11008] x [4096x11008]^T                       sq_w4a4_linear
+Weights are packed once beforehand (sq_pack_w4, R4 folded into W_down), as in
+deployment.  Inputs are synthetic (seeded, LLaMA-shaped, with outlier channels) and
+already resident in HBM; three input/weight sets are rotated so that consecutive steps
+do not hit the 256 MB Infinity Cache.
+
+value = W4A4 linear ops of the step (3 x 2*M*N*K) / step time, in TOPS.  Per-kernel
+durations come from HIP events recorded around every launch on the stream the library
+runs on.  The CPU baseline times the oracle on a bounded slice of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--no-cpu] [--report PATH]
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W4A4 rotated-linear TOPS + Hadamard/quant GB/s at LLaMA-2-7B/3-8B shapes"
+HBM_PEAK_GBS = 8000.0
+INT8_PEAK_TOPS = 5000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--sets", type=int, default=3, help="input/weight sets rotated between steps")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
+    p.add_argument("--report", default=None, help="write per-config kernel timings (JSON) here")
+    return p.parse_args()
+
+
+def gemm_bytes(M, N, K):
+    return M * K // 2 + N * K // 2 + 2 * M * N + 8 * (M + N)
+
+
+def had_bytes(M, K, groups_per_row=1):
+    return 2 * M * K + M * K // 2 + 8 * M * groups_per_row
+
+
+def kv_bytes(E):
+    return 3 * 2 * E + 2 * E + 2 * (E // 2) + 2 * 8 * (E // 128)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the path is not sharded "
+                                   "(see DESIGN.md for how it would shard)", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2405_16406_amd import sq, workloads
+
+    dev = torch.device("cuda:0")
+    shape = workloads.LLAMA2_7B_MLP
+    M, HID, INTER = shape.M, shape.hidden, shape.inter
+    A, B = shape.had_dense, shape.had_pow2
+    NH, HD = 32, 128
+
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    had = up(sq.hadamard_factor(A))
+
+    # ---- resident inputs: `sets` independent sets of activations and packed weights
+    sets = []
+    for s in range(args.sets):
+        sh = workloads.MLPShape(shape.name, shape.seed + 100 * s, M, HID, INTER, A, B)
+        inp = workloads.mlp_inputs(sh)
+        rng = workloads.rng_for(500 + s)
+        qkv = [up(workloads.head_acts(rng, 1, M, NH, HD, 2, 30.0)) for _ in range(3)]
+        wg = sq.pack_w4(up(inp["w_gate"]))
+        wu = sq.pack_w4(up(inp["w_up"]))
+        wd = sq.pack_w4(up(inp["w_down"]), had, B)
+        sets.append(dict(x_in=up(inp["x_in"]), x_down=up(inp["x_down"]), qkv=qkv, wg=wg, wu=wu, wd=wd))
+    torch.cuda.synchronize()
+
+    # ---- outputs (shared by all sets)
+    kv_out = dict(q_rot=torch.empty((1, M, NH, HD), dtype=torch.float16, device=dev),
+                  k_q=torch.empty((1, M, NH, HD // 2), dtype=torch.uint8, device=dev),
+                  k_alpha=torch.empty((1, M, NH, 1), dtype=torch.float32, device=dev),
+                  k_beta=torch.empty((1, M, NH, 1), dtype=torch.float32, device=dev),
+                  v_q=torch.empty((1, M, NH, HD // 2), dtype=torch.uint8, device=dev),
+                  v_alpha=torch.empty((1, M, NH, 1), dtype=torch.float32, device=dev),
+                  v_beta=torch.empty((1, M, NH, 1), dtype=torch.float32, device=dev))
+    xq_in = (torch.empty((M, HID // 2), dtype=torch.uint8, device=dev),
+             torch.empty((M, 1), dtype=torch.float32, device=dev),
+             torch.empty((M, 1), dtype=torch.float32, device=dev))
+    xq_dn = (torch.empty((M, INTER // 2), dtype=torch.uint8, device=dev),
+             torch.empty((M, 1), dtype=torch.float32, device=dev),
+             torch.empty((M, 1), dtype=torch.float32, device=dev))
+    y_gate = torch.empty((M, INTER), dtype=torch.float16, device=dev)
+    y_up = torch.empty((M, INTER), dtype=torch.float16, device=dev)
+    y_dn = torch.empty((M, HID), dtype=torch.float16, device=dev)
+
+    names = ["kv_quant", "act_quant", "gate_gemm", "up_gemm", "r4_had_quant", "down_gemm"]
+
+    def step(s, ev=None):
+        d = sets[s]
+        calls = [
+            lambda: sq.qk_had_kvquant(*d["qkv"], out=kv_out),
+            lambda: sq.had_quant_act(d["x_in"], out=xq_in),
+            lambda: sq.w4a4_linear(*xq_in, *d["wg"], out=y_gate),
+            lambda: sq.w4a4_linear(*xq_in, *d["wu"], out=y_up),
+            lambda: sq.had_quant_act(d["x_down"], had, B, out=xq_dn),
+            lambda: sq.w4a4_linear(*xq_dn, *d["wd"], out=y_dn),
+        ]
+        for i, c in enumerate(calls):
+            if ev is not None:
+                ev[i][0].record()
+            c()
+            if ev is not None:
+                ev[i][1].record()
+
+    for w in range(args.warmup):
+        step(w % args.sets)
+    torch.cuda.synchronize()
+
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in names]
+          for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for k in range(args.steps):
+        step(k % args.sets, ev[k])
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    per = {n: float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+           for i, n in enumerate(names)}
+
+    gemm_ops = 2 * M * INTER * HID
+    step_ops = 3 * gemm_ops
+    value = step_ops / (ms_step * 1e-3) / 1e12
+    gemm_ms = np.mean([per["gate_gemm"], per["up_gemm"], per["down_gemm"]])
+    gemm_tops = gemm_ops / (gemm_ms * 1e-3) / 1e12
+    E = M * NH * HD
+    kernels = {
+        "kv_quant": dict(ms=per["kv_quant"], GBps=kv_bytes(E) / (per["kv_quant"] * 1e-3) / 1e9),
+        "act_quant": dict(ms=per["act_quant"], GBps=had_bytes(M, HID) / (per["act_quant"] * 1e-3) / 1e9),
+        "r4_had_quant": dict(ms=per["r4_had_quant"], GBps=had_bytes(M, INTER) / (per["r4_had_quant"] * 1e-3) / 1e9),
+    }
+    for n in ("gate_gemm", "up_gemm", "down_gemm"):
+        kernels[n] = dict(ms=per[n], TOPS=gemm_ops / (per[n] * 1e-3) / 1e12)
+    for k_ in kernels.values():
+        for f in list(k_):
+            k_[f] = round(k_[f], 4)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8",
+        "data": "synthetic",
+        "config": {"workload": "LLaMA-2-7B layer, M=2048 tokens: R3+KV4 quant [1,2048,32,128]; "
+                               "act quant [2048,4096]; gate/up W4A4 [2048x4096]x[11008x4096]; "
+                               "R4 S_64(x)H_172 + quant [2048,11008]; down W4A4 [2048x11008]x[4096x11008]",
+                   "tokens": M, "hidden": HID, "intermediate": INTER, "heads": NH, "head_dim": HD,
+                   "r4": f"S_{B} (x) H_{A}", "buffer_sets": args.sets},
+        "roofline": {"kernel": "w4a4_gemm", "bound": "mfma", "achieved": round(gemm_tops, 2),
+                     "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": None},
+        "kernels": kernels,
+        "wall_s": round(wall, 3),
+    }
+
+    if args.report:
+        out["report"] = args.report
+        report = kernel_report(torch, sq, workloads, dev)
+        with open(args.report, "w") as f:
+            json.dump(report, f, indent=1)
+
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(shape, target_s):
+    """The oracle, as it stands, on a row slice of the same workload (rows are independent)."""
+    import threadpoolctl
+
+    from oracle import hadamard as ohad
+    from oracle import kv as okv
+    from oracle import linear as olin
+    from paper_2405_16406_amd import workloads
+
+    cores = len(os.sched_getaffinity(0))
+    with threadpoolctl.threadpool_limits(cores):
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        full = workloads.mlp_inputs(shape, rows=1)
+        ha = ohad.dense_factor(shape.had_dense)
+        # offline weight preparation (not timed)
+        wg = olin.pack_w4(full["w_gate"])
+        wu = olin.pack_w4(full["w_up"])
+        wd = olin.pack_w4(full["w_down"], ha, shape.had_pow2)
+
+        def run(rows):
+            inp = workloads.mlp_inputs(shape, rows=rows)
+            q, k, v = (workloads.head_acts(workloads.rng_for(900), 1, rows, 32, 128, 2, 30.0) for _ in range(3))
+            t0 = time.perf_counter()
+            okv.qk_had_kvquant(q, k, v)
+            _, a1, b1, _, qa1 = olin.had_quant_act(inp["x_in"], None, 1)
+            olin.w4a4_linear(qa1, a1[:, 0], b1[:, 0], wg[3], wg[1], wg[2])
+            olin.w4a4_linear(qa1, a1[:, 0], b1[:, 0], wu[3], wu[1], wu[2])
+            _, a2, b2, _, qa2 = olin.had_quant_act(inp["x_down"], ha, shape.had_pow2)
+            olin.w4a4_linear(qa2, a2[:, 0], b2[:, 0], wd[3], wd[1], wd[2])
+            return time.perf_counter() - t0
+
+        rows = 64
+        dt = run(rows)
+        while dt < target_s / 3 and rows < shape.M:
+            rows = min(shape.M, rows * 4)
+            dt = run(rows)
+    ops = 3 * 2 * rows * shape.inter * shape.hidden
+    return {"value": round(ops / dt / 1e12, 5), "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {rows} of {shape.M} token rows of the same layer (KV quant, act quant, gate/up, "
+                      f"R4 + quant, down; exact fp64-BLAS integer GEMM), {dt:.2f} s"}
+
+
+def kernel_report(torch, sq, workloads, dev):
+    """Per-config kernel timings (HIP events, median of repeated launches) for the docs."""
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    def timed(fn, reps=20):
+        for _ in range(3):
+            fn()
+        ts = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    rep = []
+    cfgs = [workloads.LLAMA2_7B_MLP, workloads.LLAMA3_8B_MLP] + workloads.LLAMA2_70B_DECODE
+    for sh in cfgs:
+        inp = workloads.mlp_inputs(sh)
+        had = up(sq.hadamard_factor(sh.had_dense))
+        xin, xdn = up(inp["x_in"]), up(inp["x_down"])
+        wg = sq.pack_w4(up(inp["w_gate"]))
+        wd = sq.pack_w4(up(inp["w_down"]), had, sh.had_pow2)
+        qi = sq.had_quant_act(xin)[:3]
+        qd = sq.had_quant_act(xdn, had, sh.had_pow2)[:3]
+        M = sh.M
+        t_aq = timed(lambda: sq.had_quant_act(xin, out=qi))
+        t_hq = timed(lambda: sq.had_quant_act(xdn, had, sh.had_pow2, out=qd))
+        t_g = timed(lambda: sq.w4a4_linear(*qi, *wg))
+        t_d = timed(lambda: sq.w4a4_linear(*qd, *wd))
+        rep.append(dict(config=sh.name,
+                        act_quant=dict(ms=t_aq, GBps=had_bytes(M, sh.hidden) / t_aq / 1e6),
+                        r4_had_quant=dict(ms=t_hq, GBps=had_bytes(M, sh.inter) / t_hq / 1e6),
+                        gate_gemm=dict(ms=t_g, TOPS=2 * M * sh.inter * sh.hidden / t_g / 1e9,
+                                       GBps=gemm_bytes(M, sh.inter, sh.hidden) / t_g / 1e6),
+                        down_gemm=dict(ms=t_d, TOPS=2 * M * sh.inter * sh.hidden / t_d / 1e9,
+                                       GBps=gemm_bytes(M, sh.hidden, sh.inter) / t_d / 1e6)))
+        del inp, xin, xdn, wg, wd, qi, qd
+        torch.cuda.empty_cache()
+    q, k, v = (up(t) for t in workloads.kv_inputs())
+    o = sq.qk_had_kvquant(q, k, v)
+    o.pop("k_rot")
+    t_kv = timed(lambda: sq.qk_had_kvquant(q, k, v, out=o))
+    E = q.numel()
+    rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6)))
+    return rep
+
+
+if __name__ == "__main__":
+    main()

@@ -181,6 +181,73 @@ pack_w4_generic(RotQuantArgs args) {
   }
 }
 
+// Unrotated rows, per-token quantization: the row stays in registers.  Each thread owns
+// chunks of 8 consecutive elements (one 16-byte load, one 4-byte code store).
+template <int W, int CHMAX>
+__global__ void __launch_bounds__(64 * W)
+quant_rows_identity(RotQuantArgs args) {
+  constexpr int T = 64 * W;
+  __shared__ float red[2 * W];
+  const int64_t row = blockIdx.x;
+  const int nchunk = static_cast<int>(args.K / 8);
+  const uint16_t* __restrict__ xr = args.x + row * args.ldx;
+  float v[CHMAX][8];
+  float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < CHMAX; ++j) {
+    const int ch = threadIdx.x + j * T;
+    if (ch < nchunk) {
+      const uint4 d = reinterpret_cast<const uint4*>(xr)[ch];
+      const uint32_t w[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[j][2 * i] = h2f(static_cast<uint16_t>(w[i] & 0xFFFFu));
+        v[j][2 * i + 1] = h2f(static_cast<uint16_t>(w[i] >> 16));
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        mn = fminf(mn, v[j][i]);
+        mx = fmaxf(mx, v[j][i]);
+      }
+    }
+  }
+  mn = wave_min(mn);
+  mx = wave_max(mx);
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    red[wave] = mn;
+    red[W + wave] = mx;
+  }
+  __syncthreads();
+  mn = red[0];
+  mx = red[W];
+#pragma unroll
+  for (int i = 1; i < W; ++i) {
+    mn = fminf(mn, red[i]);
+    mx = fmaxf(mx, red[W + i]);
+  }
+  const AsymParams p = asym_params(mn, mx);
+  if (threadIdx.x == 0) {
+    args.alpha[row] = p.alpha;
+    args.beta[row] = p.mn;
+  }
+  uint32_t* qrow = reinterpret_cast<uint32_t*>(args.q + row * (args.K / 2));
+#pragma unroll
+  for (int j = 0; j < CHMAX; ++j) {
+    const int ch = threadIdx.x + j * T;
+    if (ch < nchunk) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) word |= asym_code(v[j][i], p) << (4 * i);
+      qrow[ch] = word;
+      if (args.dbg) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) args.dbg[row * args.K + ch * 8 + i] = v[j][i];
+      }
+    }
+  }
+}
+
 hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hipStream_t stream) {
   const size_t lds = static_cast<size_t>(a.K) * sizeof(float);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -193,6 +260,16 @@ hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hip
 }  // namespace
 
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream) {
+  if (a.a == 1 && a.b == 1 && a.group == a.K) {
+    if (a.K <= 4 * 64 * 8 * 8) {
+      hipLaunchKernelGGL((quant_rows_identity<4, 8>), dim3(static_cast<unsigned>(a.rows)), dim3(256), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL((quant_rows_identity<8, 8>), dim3(static_cast<unsigned>(a.rows)), dim3(512), 0, stream, a);
+    }
+    return hipGetLastError();
+  }
+  const hipError_t e = launch_had_quant_kron(a, stream);
+  if (e != hipErrorNotSupported) return e;
   return launch_generic(had_quant_act_generic, a, stream);
 }
 

@@ -1,0 +1,422 @@
+// Fast path of the online rotation + per-token 4-bit quantization for rows of length
+// K = a * b rotated by (S_b (x) H_a) / sqrt(K), element i = i_b * a + i_a.
+//
+// View a row as X2[i_b][i_a] (b x a).  Then Y2 = S_b^T X2 H_a:
+//   * dense stage X2 H_a on the fp16 matrix cores (v_mfma_f32_32x32x16_f16): the inputs
+//     are exact fp16 and H_a is +-1, so every product is exact and only the fp32
+//     accumulation rounds.  MFMA tile: M = 32 consecutive i_b, N = 32 j_a, K = 16 i_a;
+//     H_a is zero-padded to APAD x (NT*32).
+//   * Sylvester stage over i_b.  A 32x32 fp32 MFMA result gives lane l, register r the
+//     element m = 8*(r/4) + 4*(l/32) + r%4 of column l%32: i_b bits 0, 1, 3, 4 are
+//     register bits, bit 2 is the lane half, the next bits index the M tiles of a wave,
+//     and the top bits the waves of the workgroup (MW of them).
+//       MW == 1: bit 2 is one cross-lane exchange per value.
+//       MW  > 1: after the in-register stages every lane writes its values to LDS and
+//                reads back complete groups over (wave, lane half), so the remaining
+//                log2(2*MW) stages are in-register too.
+//   * per-row min/max, then the eq. 1 asymmetric quantizer with the 1/sqrt(K) scale
+//     folded into alpha and beta: code = rint((v - mn) * (1/alpha)) in the unscaled
+//     domain, rounded by adding 2^23 (exact round-half-to-even for 0 <= t < 2^22; the
+//     code is then the low byte of the float), one LDS byte per code, and a final pass
+//     packs nibbles and writes 16 bytes per lane.
+// Persistent: each workgroup (MW*NW waves; waves split i_b by MW and j_a by NW) loads the
+// +-1 fragments once and walks rows blockIdx.x, +gridDim.x, ..., prefetching the next
+// row while it transforms the current one.
+#include "sq_device.h"
+#include "sq_internal.h"
+
+#include <mutex>
+
+namespace sq {
+namespace {
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE>
+struct Kron {
+  static constexpr int W = MW * NW;          // waves per workgroup
+  static constexpr int THREADS = 64 * W;
+  static constexpr int KS = APAD / 16;       // k-steps of the dense stage
+  static constexpr int MT = B / 32 / MW;     // M tiles (32 i_b each) per wave
+  static constexpr int NTW = NT / NW;        // N tiles (32 j_a each) per wave
+  static constexpr int K = A * B;
+  static constexpr int P = MT * 16;          // values per lane before the exchange (NTW == 1)
+  static constexpr int SL = MW > 1 ? P / (2 * MW) : 0;  // positions per lane after the exchange
+  static constexpr int NV = MW > 1 ? SL * 2 * MW : MT * NTW * 16;  // values per lane
+  static constexpr int ROW_CHUNKS = K * 2 / 16;                    // 16-byte chunks of a row
+  static constexpr int PF = STAGE ? (ROW_CHUNKS + THREADS - 1) / THREADS : 0;
+  static_assert(APAD % 16 == 0 && APAD >= A && NT * 32 >= A, "padding");
+  static_assert(A % 4 == 0, "Hadamard orders are multiples of 4");
+  static_assert(B % (32 * MW) == 0 && NT % NW == 0, "tiling");
+  static_assert(MW == 1 || (NTW == 1 && !STAGE), "wave split over i_b: one N tile, direct loads");
+  static_assert(MW == 1 || (P % (2 * MW)) == 0, "exchange slices");
+  static_assert(K % 16 == 0, "16-code packing");
+  // LDS layout (bytes)
+  static constexpr int ROW_BYTES = STAGE ? K * 2 : 0;
+  static constexpr int XCH_BYTES = MW > 1 ? MW * P * 64 * 4 : 0;
+  static constexpr int CODE_BYTES = K;       // one byte per code before packing
+  static constexpr int RED_BYTES = 2 * W * 4;
+  static constexpr int LDS = ROW_BYTES + XCH_BYTES + CODE_BYTES + RED_BYTES;
+};
+
+__device__ __forceinline__ void bfly(float& lo, float& hi) {
+  const float u = lo, w = hi;
+  lo = __fadd_rn(u, w);
+  hi = __fsub_rn(u, w);
+}
+
+// 8 consecutive fp16 of an X2 row starting at column k0 (zero beyond column A).
+template <int A>
+__device__ __forceinline__ v8h load_afrag(const uint16_t* __restrict__ rowp, int k0) {
+  uint2 lo = make_uint2(0, 0), hi = make_uint2(0, 0);
+  if (k0 + 8 <= A) {
+    lo = *reinterpret_cast<const uint2*>(rowp + k0);
+    hi = *reinterpret_cast<const uint2*>(rowp + k0 + 4);
+  } else if (k0 + 4 <= A) {
+    lo = *reinterpret_cast<const uint2*>(rowp + k0);
+  }
+  const uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  return __builtin_bit_cast(v8h, u);
+}
+
+// rint(t) for 0 <= t < 2^22 as the low bits of t + 2^23 (one IEEE round-half-to-even add)
+__device__ __forceinline__ uint32_t rne_bits(float t) {
+  return __float_as_uint(__fadd_rn(t, 8388608.0f));
+}
+
+template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE, bool DBG>
+__global__ void __launch_bounds__(64 * MW * NW)
+had_quant_kron(RotQuantArgs args) {
+  using C = Kron<A, APAD, NT, B, MW, NW, STAGE>;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint16_t* lds_row = reinterpret_cast<uint16_t*>(smem);
+  float* lds_xch = reinterpret_cast<float*>(smem + C::ROW_BYTES);
+  uint8_t* lds_code = smem + C::ROW_BYTES + C::XCH_BYTES;
+  float* lds_red = reinterpret_cast<float*>(smem + C::ROW_BYTES + C::XCH_BYTES + C::CODE_BYTES);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave % MW;
+  const int wn = wave / MW;
+  const int g = lane >> 5;
+  const int c = lane & 31;
+  const int64_t rows = args.rows;
+  const float s_n = args.inv_sqrt_n;
+
+  // +-1 factor as MFMA B fragments: B[k][n] = H[k][n], k = ks*16 + 8g + e, n = tile*32 + c
+  v8h bfrag[C::NTW][C::KS];
+#pragma unroll
+  for (int nt = 0; nt < C::NTW; ++nt) {
+    const int n = (wn * C::NTW + nt) * 32 + c;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = ks * 16 + 8 * g + e;
+        const float h = (k < A && n < A) ? static_cast<float>(args.H[k * A + n]) : 0.0f;
+        bfrag[nt][ks][e] = static_cast<_Float16>(h);
+      }
+    }
+  }
+
+  int64_t row = blockIdx.x;
+  if (row >= rows) return;
+
+  // first row: A fragments in registers (direct) or the row in LDS (staged)
+  v8h af[STAGE ? 1 : C::MT][C::KS];
+  uint4 pf[STAGE ? C::PF : 1];
+  auto load_direct = [&](int64_t r) {
+    const uint16_t* xr = args.x + r * args.ldx;
+#pragma unroll
+    for (int mt = 0; mt < (STAGE ? 1 : C::MT); ++mt) {
+      const int ib = (wm * C::MT + mt) * 32 + c;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) af[mt][ks] = load_afrag<A>(xr + ib * A, ks * 16 + 8 * g);
+    }
+  };
+  auto load_stage = [&](int64_t r) {
+    const uint4* xr = reinterpret_cast<const uint4*>(args.x + r * args.ldx);
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = threadIdx.x + j * C::THREADS;
+      if (i < C::ROW_CHUNKS) pf[j] = xr[i];
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = threadIdx.x + j * C::THREADS;
+      if (i < C::ROW_CHUNKS) reinterpret_cast<uint4*>(lds_row)[i] = pf[j];
+    }
+  };
+  if constexpr (STAGE) {
+    load_stage(row);
+    store_stage();
+    __syncthreads();
+  } else {
+    load_direct(row);
+  }
+
+  for (; row < rows; row += gridDim.x) {
+    const int64_t next = row + gridDim.x;
+    // ---- dense stage
+    v16f acc[C::MT][C::NTW];
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][nt][r] = 0.0f;
+    if constexpr (!STAGE) {
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks)
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+          acc[mt][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[mt][ks], bfrag[0][ks], acc[mt][0], 0, 0, 0);
+      if (next < rows) load_direct(next);  // prefetch: in flight during the rest of this row
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        v8h a_[C::MT];
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) a_[mt] = load_afrag<A>(lds_row + (mt * 32 + c) * A, ks * 16 + 8 * g);
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < C::NTW; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a_[mt], bfrag[nt][ks], acc[mt][nt], 0, 0, 0);
+      }
+      if (next < rows) load_stage(next);
+    }
+
+    // ---- Sylvester stages held in registers: i_b bits 0, 1, 3, 4 (register bits) and the tile bits
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+        for (int rb = 1; rb < 16; rb <<= 1)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if ((r & rb) == 0) {
+              float lo = acc[mt][nt][r], hi = acc[mt][nt][r + rb];
+              bfly(lo, hi);
+              acc[mt][nt][r] = lo;
+              acc[mt][nt][r + rb] = hi;
+            }
+#pragma unroll
+    for (int tb = 1; tb < C::MT; tb <<= 1)
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+        if ((mt & tb) == 0)
+#pragma unroll
+          for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              float lo = acc[mt][nt][r], hi = acc[mt + tb][nt][r];
+              bfly(lo, hi);
+              acc[mt][nt][r] = lo;
+              acc[mt + tb][nt][r] = hi;
+            }
+
+    // ---- remaining bits; val[] = this lane's values, with their (i_b, j_a) given by vpos()
+    float val[C::NV];
+    if constexpr (MW == 1) {
+      // bit 2 across the lane halves: lower half u + w, upper half w' - u' via fma(+-1, v, partner)
+      const float sg = g ? -1.0f : 1.0f;
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float v = acc[mt][nt][r];
+            const float p = __shfl_xor(v, 32, 64);
+            val[(mt * C::NTW + nt) * 16 + r] = __fmaf_rn(sg, v, p);
+          }
+    } else {
+      // write (wave, position, lane half, column); read back whole (wave, half) groups
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) lds_xch[((wm * C::P) + mt * 16 + r) * 64 + lane] = acc[mt][0][r];
+      __syncthreads();
+      const int pbase = (wm * 2 + g) * C::SL;
+#pragma unroll
+      for (int t = 0; t < C::SL; ++t)
+#pragma unroll
+        for (int s = 0; s < MW; ++s)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) val[(t * MW + s) * 2 + h] = lds_xch[((s * C::P) + pbase + t) * 64 + h * 32 + c];
+      // butterflies over (source wave, half): index bit 0 = i_b bit 2, bits 1.. = wave bits
+#pragma unroll
+      for (int t = 0; t < C::SL; ++t)
+#pragma unroll
+        for (int hb = 1; hb < 2 * MW; hb <<= 1)
+#pragma unroll
+          for (int q = 0; q < 2 * MW; ++q)
+            if ((q & hb) == 0) bfly(val[t * 2 * MW + q], val[t * 2 * MW + q + hb]);
+    }
+
+    // ---- per-row min/max over real columns (padded columns hold exact zeros)
+    float mn = INFINITY, mx = -INFINITY;
+    if constexpr (MW == 1) {
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt) {
+        float a = INFINITY, b = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            a = fminf(a, val[(mt * C::NTW + nt) * 16 + r]);
+            b = fmaxf(b, val[(mt * C::NTW + nt) * 16 + r]);
+          }
+        if ((wn * C::NTW + nt) * 32 + c < A) {
+          mn = fminf(mn, a);
+          mx = fmaxf(mx, b);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::NV; ++i) {
+        mn = fminf(mn, val[i]);
+        mx = fmaxf(mx, val[i]);
+      }
+      if (c >= A) {
+        mn = INFINITY;
+        mx = -INFINITY;
+      }
+    }
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    if (lane == 0) {
+      lds_red[wave] = mn;
+      lds_red[C::W + wave] = mx;
+    }
+    __syncthreads();
+    mn = lds_red[0];
+    mx = lds_red[C::W];
+#pragma unroll
+    for (int w = 1; w < C::W; ++w) {
+      mn = fminf(mn, lds_red[w]);
+      mx = fmaxf(mx, lds_red[C::W + w]);
+    }
+    // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
+    const float r_u = __fsub_rn(mx, mn);
+    const float alpha_u = (r_u == 0.0f) ? 1.0f : __fdiv_rn(r_u, 15.0f);
+    const float inv_u = (r_u == 0.0f) ? 0.0f : __fdiv_rn(1.0f, alpha_u);
+    if (threadIdx.x == 0) {
+      args.alpha[row] = (r_u == 0.0f) ? 1.0f : __fmul_rn(alpha_u, s_n);
+      args.beta[row] = __fmul_rn(mn, s_n);
+    }
+
+    // ---- codes: one LDS byte each at output position i_b*A + j_a = lane base + constant
+    int lbase;  // lane-dependent part of i_b*A + j_a
+    if constexpr (MW == 1) {
+      lbase = 4 * g * A + wn * C::NTW * 32 + c;
+    } else {
+      constexpr int TPU = 16 / C::SL;  // exchange slices per 16-register tile
+      static_assert(C::SL >= 4 && 16 % C::SL == 0, "slice layout");
+      const int u = wm * 2 + g;
+      lbase = ((u / TPU) * 32 + 8 * (u % TPU) * (C::SL / 4)) * A + c;
+    }
+    const bool real = (MW == 1) ? true : (c < A);
+#pragma unroll
+    for (int i = 0; i < C::NV; ++i) {
+      int off, ja_hi;  // constant part of the offset; j_a - c for the padding test
+      if constexpr (MW == 1) {
+        const int mt = i / (16 * C::NTW);
+        const int nt = (i / 16) % C::NTW;
+        const int r = i % 16;
+        off = (mt * 32 + 8 * (r >> 2) + (r & 3)) * A + nt * 32;
+        ja_hi = (wn * C::NTW + nt) * 32;
+      } else {
+        const int t = i / (2 * MW);
+        const int s = (i / 2) % MW;
+        const int h = i % 2;
+        off = (s * C::MT * 32 + 8 * (t >> 2) + 4 * h + (t & 3)) * A;
+        ja_hi = 0;
+      }
+      if (real && ja_hi + c < A) {
+        const uint32_t q = rne_bits(__fmul_rn(__fsub_rn(val[i], mn), inv_u));
+        lds_code[lbase + off] = static_cast<uint8_t>(q);
+        if constexpr (DBG) args.dbg[row * C::K + lbase + off] = __fmul_rn(val[i], s_n);
+      }
+    }
+    if constexpr (STAGE) {
+      if (next < rows) store_stage();  // every wave is past its last read of lds_row
+    }
+    __syncthreads();
+
+    // ---- pack 16 codes -> 8 bytes per thread, 8-byte stores
+    uint2* qrow = reinterpret_cast<uint2*>(args.q + row * (C::K / 2));
+    for (int i = threadIdx.x; i < C::K / 16; i += C::THREADS) {
+      const uint4 b = reinterpret_cast<const uint4*>(lds_code)[i];
+      const uint32_t w[4] = {b.x, b.y, b.z, b.w};
+      uint32_t o[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t x0 = w[2 * h], x1 = w[2 * h + 1];
+        const uint32_t p0 = (x0 & 0xFu) | ((x0 >> 4) & 0xF0u) | ((x0 >> 8) & 0xF00u) | ((x0 >> 12) & 0xF000u);
+        const uint32_t p1 = (x1 & 0xFu) | ((x1 >> 4) & 0xF0u) | ((x1 >> 8) & 0xF00u) | ((x1 >> 12) & 0xF000u);
+        o[h] = p0 | (p1 << 16);
+      }
+      qrow[i] = make_uint2(o[0], o[1]);
+    }
+    // the next row's first LDS writes (exchange / reduction / codes) come after at
+    // least one more barrier, so no extra barrier is needed here
+  }
+}
+
+int g_num_cu = 0;
+std::once_flag g_cu_once;
+
+int num_cus() {
+  std::call_once(g_cu_once, [] {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&g_num_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      g_num_cu = 256;
+  });
+  return g_num_cu;
+}
+
+template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE, bool DBG>
+hipError_t launch_kron_t(const RotQuantArgs& a, hipStream_t stream) {
+  using C = Kron<A, APAD, NT, B, MW, NW, STAGE>;
+  auto kern = had_quant_kron<A, APAD, NT, B, MW, NW, STAGE, DBG>;
+  static int blocks_per_cu = 0;
+  static hipError_t init = [&] {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_per_cu, kern, C::THREADS, C::LDS);
+    if (blocks_per_cu < 1) blocks_per_cu = 1;
+    return e;
+  }();
+  if (init != hipSuccess) return init;
+  const int64_t cap = static_cast<int64_t>(num_cus()) * blocks_per_cu;
+  const unsigned grid = static_cast<unsigned>(a.rows < cap ? a.rows : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
+  return hipGetLastError();
+}
+
+template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE>
+hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
+  return a.dbg ? launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, true>(a, stream)
+               : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
+}
+
+}  // namespace
+
+// Returns hipErrorNotSupported when no fast path covers the arguments.
+hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
+  if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
+  if (a.a == 28 && a.b == 512) return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
+  if (a.a == 172 && a.b == 64) return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
+  if (a.a == 28 && a.b == 1024) return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
+  return hipErrorNotSupported;
+}
+
+}  // namespace sq

@@ -31,6 +31,9 @@ struct RotQuantArgs {
 
 // Rotation + asymmetric per-group 4-bit quantization of activation rows.
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream);
+// Fast path for K = a*b rows with a registered dense order, per-token groups;
+// hipErrorNotSupported when it does not apply.
+hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream);
 // Rotation + symmetric per-row 4-bit quantization of weight rows, with code row sums.
 hipError_t launch_pack_w4(const RotQuantArgs& a, hipStream_t stream);
 

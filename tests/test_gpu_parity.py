@@ -124,6 +124,18 @@ def test_llama2_70b_decode_act():
         check_act(inp["x_down"], 28, 1024)
 
 
+@pytest.mark.parametrize("a,b,M", [(28, 512, 33), (172, 64, 21), (28, 1024, 5)])
+def test_debug_output_does_not_change_results(a, b, M):
+    say(f"had_quant_act with and without dbg_rot a={a} b={b} M={M}")
+    rng = workloads.rng_for(500 + a + M)
+    x = dev(workloads.outlier_acts(rng, M, a * b, max(1, a * b // 100), 50.0))
+    h = had_table(a)
+    r1 = [host(v) for v in sq.had_quant_act(x, h, b, dbg=False)[:3]]
+    r2 = [host(v) for v in sq.had_quant_act(x, h, b, dbg=True)[:3]]
+    for u, v in zip(r1, r2):
+        assert np.array_equal(u, v)
+
+
 def test_deterministic():
     say("had_quant_act determinism")
     x = workloads.mlp_inputs(workloads.LLAMA2_7B_MLP, rows=64)["x_down"]
