@@ -45,7 +45,32 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
     p.add_argument("--report", default=None, help="write per-config kernel timings (JSON) here")
+    p.add_argument("--calib-copy", action="store_true",
+                   help="only run a plain 512 MiB device-to-device copy (counter calibration) and exit")
     return p.parse_args()
+
+
+GEMM_SRC = os.path.join(ROOT, "paper_2405_16406_amd", "csrc", "w4a4_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a4_gemm_traffic.json")
+
+
+def source_hash(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE runs, if
+    they were taken on the current kernel source; otherwise None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != source_hash(GEMM_SRC):
+        return None
+    return t.get("bytes_per_launch")
 
 
 def gemm_bytes(M, N, K):
@@ -64,8 +89,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the path is not sharded "
-                                   "(see DESIGN.md for how it would shard)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this build runs on one GPU only: the rotated W4A4 path is not "
+                                   "sharded across GPUs", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
@@ -73,6 +98,14 @@ def main():
     from paper_2405_16406_amd import sq, workloads
 
     dev = torch.device("cuda:0")
+    if args.calib_copy:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes": src.numel(), "launches": 4}), flush=True)
+        return
     shape = workloads.LLAMA2_7B_MLP
     M, HID, INTER = shape.M, shape.hidden, shape.inter
     A, B = shape.had_dense, shape.had_pow2
@@ -189,7 +222,8 @@ def main():
                    "r4": f"S_{B} (x) H_{A}", "buffer_sets": args.sets},
         "roofline": {"kernel": "w4a4_gemm", "bound": "mfma", "achieved": round(gemm_tops, 2),
                      "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(),
+                     "ops_per_launch": gemm_ops, "algorithmic_bytes_per_launch": gemm_bytes(M, INTER, HID)},
         "kernels": kernels,
         "wall_s": round(wall, 3),
     }
@@ -253,18 +287,18 @@ def kernel_report(torch, sq, workloads, dev):
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
     def timed(fn, reps=20):
+        """Median-free average over back-to-back launches (no host sync between them)."""
         for _ in range(3):
             fn()
-        ts = []
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
         for _ in range(reps):
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record()
             fn()
-            b.record()
-            torch.cuda.synchronize()
-            ts.append(a.elapsed_time(b))
-        return float(np.median(ts))
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
 
     rep = []
     cfgs = [workloads.LLAMA2_7B_MLP, workloads.LLAMA3_8B_MLP] + workloads.LLAMA2_70B_DECODE

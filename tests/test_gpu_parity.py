@@ -320,3 +320,29 @@ def test_kv_full_sampled():
     sample = np.unique(np.concatenate([rng.choice(8 * 2048 * 32, 20000, replace=False),
                                        [0, 8 * 2048 * 32 - 1]]))
     check_kv(q, k, v, sample)
+
+
+@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "6", "7", "8", "9"])
+def test_gemm_tile_variants(variant, monkeypatch):
+    say(f"w4a4_linear tile variant {variant}: ragged shapes, paired and unpaired stores")
+    monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
+    for (M, N, K) in [(300, 390, 448), (64, 130, 192), (257, 257, 128), (520, 600, 320)]:
+        rng = workloads.rng_for(M + N + K)
+        qa = rng.integers(0, 16, size=(M, K))
+        qw = rng.integers(-7, 8, size=(N, K))
+        xa = rng.uniform(0.05, 3.0, M).astype(np.float32)
+        xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+        wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
+        rs = qw.sum(1).astype(np.int32)
+        bi = (rng.standard_normal(N) * 0.1).astype(np.float16)
+        args = (dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs), dev(bi))
+        oy, oacc = olin.w4a4_linear(qa, xa, xb, qw, wa, rs, bi)
+        y_dbg, acc = sq.w4a4_linear(*args, dbg=True)
+        np.testing.assert_array_equal(host(acc), oacc)
+        parity.assert_out_close(host(y_dbg), oy)
+        y_fast, _ = sq.w4a4_linear(*args)                      # paired 32-bit stores
+        np.testing.assert_array_equal(host(y_fast), host(y_dbg))
+        wide = torch.zeros((M, N + 3), dtype=torch.float16, device=DEV)
+        sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: unpaired stores
+        np.testing.assert_array_equal(host(wide[:, :N]), host(y_dbg))
+        assert not host(wide[:, N:]).any()
