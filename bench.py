@@ -47,11 +47,13 @@ def parse():
     p.add_argument("--report", default=None, help="write per-config kernel timings (JSON) here")
     p.add_argument("--calib-copy", action="store_true",
                    help="only run a plain 512 MiB device-to-device copy (counter calibration) and exit")
+    p.add_argument("--summarize", default=None, metavar="DIR",
+                   help="write the profiles/ summaries from rocprofv3 outputs under DIR and exit (no GPU)")
     return p.parse_args()
 
 
 GEMM_SRC = os.path.join(ROOT, "paper_2405_16406_amd", "csrc", "w4a4_gemm.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a4_gemm_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a4_gemm_llama2_7b_m2048_traffic.json")
 
 
 def source_hash(path):
@@ -73,6 +75,122 @@ def measured_traffic():
     return t.get("bytes_per_launch")
 
 
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+WORKLOAD_TAG = "llama2_7b_m2048"
+# the commands whose outputs --summarize reads (run from /tmp with TMPDIR=/tmp; DIR = rocprofv3 output root)
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d DIR/trace -o bench -- "
+             "python /root/repo/bench.py --no-cpu --steps 20",
+    "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/pmc_fetch -o bench -- "
+             "python /root/repo/bench.py --no-cpu --steps 5 --warmup 2",
+    "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/pmc_write -o bench -- "
+             "python /root/repo/bench.py --no-cpu --steps 5 --warmup 2",
+    "calib_fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/pmc_cfetch -o copy -- "
+                   "python /root/repo/bench.py --calib-copy",
+    "calib_write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/pmc_cwrite -o copy -- "
+                   "python /root/repo/bench.py --calib-copy",
+    "summary": "python bench.py --summarize DIR",
+}
+CALIB_BYTES = 512 << 20  # bytes read and written by each --calib-copy launch
+
+
+def _csv_rows(d, pattern):
+    import csv
+    import glob
+    out = []
+    for f in sorted(glob.glob(os.path.join(d, pattern))):
+        with open(f) as fh:
+            out += list(csv.DictReader(fh))
+    return out
+
+
+def _short(name):
+    name = name.replace("(anonymous namespace)::", "").replace("sq::", "")
+    for cut in ("(sq::", "(RotQuantArgs", "(GemmArgs", "(KvArgs"):
+        if cut in name:
+            name = name[:name.index(cut)]
+    return name.replace("void ", "").strip()
+
+
+def _pmc_per_kernel(rows, counter):
+    """mean over dispatches of the counter summed over its dimensions, per (kernel, grid)"""
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        key = (r["Kernel_Name"], int(r["Grid_Size"]), int(r["Dispatch_Id"]))
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    agg = {}
+    for (name, grid, _), v in per.items():
+        agg.setdefault((name, grid), []).append(v)
+    return {k: (float(np.mean(v)), len(v)) for k, v in agg.items()}
+
+
+def summarize(d):
+    """Turn rocprofv3 outputs (the PROFILE_COMMANDS, DIR = d) into the profiles/ summaries."""
+    cmds = "\n".join(f"    {c.replace('DIR', '<DIR>')}" for c in PROFILE_COMMANDS.values())
+    os.makedirs(PROFILE_DIR, exist_ok=True)
+    # ---- kernel durations
+    trace = _csv_rows(d, "trace/*kernel_trace.csv")
+    dur = {}
+    for r in trace:
+        grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+        key = (r["Kernel_Name"], grid)
+        dur.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    bench_line = ""
+    bl = os.path.join(d, "trace_bench.json")
+    if os.path.exists(bl):
+        with open(bl) as f:
+            bench_line = f.read().strip()
+    lines = [f"# Kernel durations, rotated W4A4 path, LLaMA-2-7B layer (M = 2048 tokens)", "",
+             "rocprofv3 kernel trace of the default bench step (20 timed steps after 10 warm-up",
+             "steps; weight packing runs once before them).  Commands (from /tmp, TMPDIR=/tmp):", "",
+             cmds, "", "| kernel | grid (threads) | calls | avg us | min us | max us |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for (name, grid), v in sorted(dur.items(), key=lambda kv: -np.mean(kv[1]) * len(kv[1])):
+        lines.append(f"| `{_short(name)}` | {grid} | {len(v)} | {np.mean(v):.1f} | {np.min(v):.1f} | {np.max(v):.1f} |")
+    if bench_line:
+        lines += ["", "bench.py line printed by the traced run:", "", "```", bench_line, "```"]
+    with open(os.path.join(PROFILE_DIR, f"rotated_w4a4_{WORKLOAD_TAG}_kernel_stats.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    # ---- HBM traffic from FETCH_SIZE / WRITE_SIZE, scaled by the copy calibration
+    fetch = _pmc_per_kernel(_csv_rows(d, "pmc_fetch/*counter_collection.csv"), "FETCH_SIZE")
+    write = _pmc_per_kernel(_csv_rows(d, "pmc_write/*counter_collection.csv"), "WRITE_SIZE")
+    cf = _pmc_per_kernel(_csv_rows(d, "pmc_cfetch/*counter_collection.csv"), "FETCH_SIZE")
+    cw = _pmc_per_kernel(_csv_rows(d, "pmc_cwrite/*counter_collection.csv"), "WRITE_SIZE")
+    cfk = [v[0] for k, v in cf.items() if "copyBuffer" in k[0]]
+    cwk = [v[0] for k, v in cw.items() if "copyBuffer" in k[0]]
+    f_fetch = CALIB_BYTES / (cfk[0] * 1024.0)
+    f_write = CALIB_BYTES / (cwk[0] * 1024.0)
+    lines = [f"# HBM traffic per launch, rotated W4A4 path, LLaMA-2-7B layer (M = 2048 tokens)", "",
+             "rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch, one counter per run), scaled by",
+             "what the same counters read for a plain 512 MiB device-to-device copy:",
+             f"FETCH_SIZE reads {cfk[0]:.0f} KiB for 524288 KiB read (factor {f_fetch:.4f}),",
+             f"WRITE_SIZE reads {cwk[0]:.0f} KiB for 524288 KiB written (factor {f_write:.4f}).",
+             "Commands (from /tmp, TMPDIR=/tmp):", "", cmds, "",
+             "| kernel | grid (threads) | dispatches | FETCH KiB | WRITE KiB | HBM read MB | HBM write MB |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+    gemm = []
+    for key in sorted(fetch, key=lambda k: -fetch[k][0]):
+        fk, n = fetch[key]
+        wk = write.get(key, (float("nan"), 0))[0]
+        rd, wr = fk * 1024 * f_fetch, wk * 1024 * f_write
+        lines.append(f"| `{_short(key[0])}` | {key[1]} | {n} | {fk:.0f} | {wk:.0f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} |")
+        if "w4a4_gemm" in key[0]:
+            gemm += [(rd, wr)] * n
+    with open(os.path.join(PROFILE_DIR, f"rotated_w4a4_{WORKLOAD_TAG}_hbm_traffic.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    t = {"kernel": "w4a4_gemm", "workload": "LLaMA-2-7B layer, M = 2048: gate, up and down projections",
+         "kernel_source_sha256_16": source_hash(GEMM_SRC),
+         "bytes_per_launch": round(float(np.mean([a + b for a, b in gemm]))),
+         "read_bytes_per_launch": round(float(np.mean([a for a, _ in gemm]))),
+         "write_bytes_per_launch": round(float(np.mean([b for _, b in gemm]))),
+         "fetch_factor": f_fetch, "write_factor": f_write, "commands": PROFILE_COMMANDS}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(t, f, indent=1)
+    print(json.dumps({k: t[k] for k in ("bytes_per_launch", "read_bytes_per_launch", "write_bytes_per_launch")}))
+
+
 def gemm_bytes(M, N, K):
     return M * K // 2 + N * K // 2 + 2 * M * N + 8 * (M + N)
 
@@ -87,6 +205,9 @@ def kv_bytes(E):
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args.summarize)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the rotated W4A4 path is not "
@@ -223,7 +344,8 @@ def main():
         "roofline": {"kernel": "w4a4_gemm", "bound": "mfma", "achieved": round(gemm_tops, 2),
                      "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
                      "traffic": measured_traffic(),
-                     "ops_per_launch": gemm_ops, "algorithmic_bytes_per_launch": gemm_bytes(M, INTER, HID)},
+                     "ops_per_launch": gemm_ops,
+                     "algorithmic_bytes_per_launch": round((2 * gemm_bytes(M, INTER, HID) + gemm_bytes(M, HID, INTER)) / 3)},
         "kernels": kernels,
         "wall_s": round(wall, 3),
     }

@@ -11,14 +11,16 @@ The paper quantizes activations and the KV cache asymmetrically with no range cl
 Readings of points the paper leaves open:
   * "round" is round-to-nearest with ties to even (np.rint).
   * beta is the real minimum, kept in fp32 (not an integer zero-point).
-  * A group whose range is zero (or an all-zero symmetric row) gets alpha = 1, which
-    reconstructs it exactly.
+  * A group whose alpha = range / L would be zero or subnormal in fp32 (range below
+    L * 2^-126, e.g. a constant group or an all-zero symmetric row) is treated as
+    constant: alpha = 1 and every code 0, so it dequantizes to beta (exactly for a
+    constant group, within the range otherwise).  This keeps 1 / alpha finite.
   * The encoding is carried out as this exact fp32 op sequence, one IEEE rounding per
     step, so that an implementation doing the same steps reproduces the codes bit for
     bit from the same fp32 inputs:
-      asym: mn, mx = min, max;  r = mx - mn;  alpha = r / L (or 1 if r == 0);
+      asym: mn, mx = min, max;  r = mx - mn;  alpha = r / L (1 if that is below 2^-126);
             inv = 1 / alpha;  q = clamp(rint((v - mn) * inv), 0, L),  L = 2^N - 1
-      sym:  a = max|v|;  alpha = a / L (or 1 if a == 0);  inv = 1 / alpha;
+      sym:  a = max|v|;  alpha = a / L (1 if that is below 2^-126);  inv = 1 / alpha;
             q = clamp(rint(v * inv), -L, L),  L = 2^(N-1) - 1
     (dividing by alpha through its fp32 reciprocal is part of this reading).
 """
@@ -26,6 +28,7 @@ Readings of points the paper leaves open:
 import numpy as np
 
 F32 = np.float32
+TINY = F32(np.finfo(np.float32).tiny)  # 2^-126, the smallest normal fp32
 
 
 def _groups(v: np.ndarray, group: int) -> np.ndarray:
@@ -48,7 +51,8 @@ def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None):
     mn = g.min(axis=-1)
     mx = g.max(axis=-1)
     r = (mx - mn).astype(F32)
-    alpha = np.where(r == 0, F32(1), r / levels).astype(F32)
+    alpha = (r / levels).astype(F32)
+    alpha = np.where(alpha < TINY, F32(1), alpha).astype(F32)
     inv = (F32(1) / alpha).astype(F32)
     t = ((g - mn[..., None]).astype(F32) * inv[..., None]).astype(F32)
     q = np.clip(np.rint(t), 0, levels).astype(np.int64)
@@ -65,7 +69,8 @@ def quant_sym(v: np.ndarray, bits: int = 4, group: int | None = None):
     g = _groups(v32, group)
     levels = F32(2 ** (bits - 1) - 1)
     amax = np.abs(g).max(axis=-1)
-    alpha = np.where(amax == 0, F32(1), amax / levels).astype(F32)
+    alpha = (amax / levels).astype(F32)
+    alpha = np.where(alpha < TINY, F32(1), alpha).astype(F32)
     inv = (F32(1) / alpha).astype(F32)
     t = (g * inv[..., None]).astype(F32)
     q = np.clip(np.rint(t), -levels, levels).astype(np.int64)

@@ -32,6 +32,7 @@ namespace {
 
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE>
 struct Kron {
@@ -125,7 +126,7 @@ had_quant_kron(RotQuantArgs args) {
 
   // first row: A fragments in registers (direct) or the row in LDS (staged)
   v8h af[STAGE ? 1 : C::MT][C::KS];
-  uint4 pf[STAGE ? C::PF : 1];
+  v4u pf[STAGE ? C::PF : 1];
   auto load_direct = [&](int64_t r) {
     const uint16_t* xr = args.x + r * args.ldx;
 #pragma unroll
@@ -135,19 +136,21 @@ had_quant_kron(RotQuantArgs args) {
       for (int ks = 0; ks < C::KS; ++ks) af[mt][ks] = load_afrag<A>(xr + ib * A, ks * 16 + 8 * g);
     }
   };
+  // staged rows: chunk j of this thread is 16-byte chunk threadIdx.x + j * THREADS of the row;
+  // the load index is clamped so every load is unconditional (the duplicate is not stored)
   auto load_stage = [&](int64_t r) {
-    const uint4* xr = reinterpret_cast<const uint4*>(args.x + r * args.ldx);
+    const v4u* xr = reinterpret_cast<const v4u*>(args.x + r * args.ldx);
 #pragma unroll
     for (int j = 0; j < C::PF; ++j) {
       const int i = threadIdx.x + j * C::THREADS;
-      if (i < C::ROW_CHUNKS) pf[j] = xr[i];
+      pf[j] = xr[i < C::ROW_CHUNKS ? i : C::ROW_CHUNKS - 1];
     }
   };
   auto store_stage = [&]() {
 #pragma unroll
     for (int j = 0; j < C::PF; ++j) {
       const int i = threadIdx.x + j * C::THREADS;
-      if (i < C::ROW_CHUNKS) reinterpret_cast<uint4*>(lds_row)[i] = pf[j];
+      if (i < C::ROW_CHUNKS) reinterpret_cast<v4u*>(lds_row)[i] = pf[j];
     }
   };
   if constexpr (STAGE) {
@@ -303,11 +306,13 @@ had_quant_kron(RotQuantArgs args) {
       mx = fmaxf(mx, lds_red[C::W + w]);
     }
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
+    // (a group whose scaled alpha is below kMinNormal is constant: alpha 1, codes 0)
     const float r_u = __fsub_rn(mx, mn);
-    const float alpha_u = (r_u == 0.0f) ? 1.0f : __fdiv_rn(r_u, 15.0f);
-    const float inv_u = (r_u == 0.0f) ? 0.0f : __fdiv_rn(1.0f, alpha_u);
+    const float a_u = __fdiv_rn(r_u, 15.0f);
+    const bool cst = __fmul_rn(a_u, s_n) < kMinNormal;
+    const float inv_u = cst ? 0.0f : __fdiv_rn(1.0f, a_u);
     if (threadIdx.x == 0) {
-      args.alpha[row] = (r_u == 0.0f) ? 1.0f : __fmul_rn(alpha_u, s_n);
+      args.alpha[row] = cst ? 1.0f : __fmul_rn(a_u, s_n);
       args.beta[row] = __fmul_rn(mn, s_n);
     }
 

@@ -18,14 +18,20 @@ __device__ __forceinline__ uint16_t f2h(float v) {
   return __half_as_ushort(__float2half_rn(v));
 }
 
+// Smallest normal fp32 (2^-126).  A group whose alpha would fall below it (zero or
+// subnormal: a constant group, or a range under L * 2^-126) is quantized as constant with
+// alpha = 1, so 1 / alpha stays finite and every code is 0.
+constexpr float kMinNormal = 1.17549435e-38f;
+
 // Asymmetric eq. 1 parameters from a group's min and max (4-bit: L = 15).
-//   r = mx - mn;  alpha = r / L (1 if r == 0);  inv = 1 / alpha  -- each one IEEE rounding.
+//   r = mx - mn;  alpha = r / L (1 if below kMinNormal);  inv = 1 / alpha  -- each one IEEE rounding.
 struct AsymParams {
   float mn, alpha, inv;
 };
 __device__ __forceinline__ AsymParams asym_params(float mn, float mx) {
   const float r = __fsub_rn(mx, mn);
-  const float alpha = (r == 0.0f) ? 1.0f : __fdiv_rn(r, 15.0f);
+  const float a = __fdiv_rn(r, 15.0f);
+  const float alpha = (a < kMinNormal) ? 1.0f : a;  // zero or subnormal: constant group
   return {mn, alpha, __fdiv_rn(1.0f, alpha)};
 }
 // code = clamp(rint((v - mn) * inv), 0, 15)
@@ -34,9 +40,10 @@ __device__ __forceinline__ uint32_t asym_code(float v, const AsymParams& p) {
   return static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), 15.0f));
 }
 
-// Symmetric eq. 1 (beta = 0, L = 7): alpha = amax / 7 (1 if amax == 0); code in [-7, 7].
+// Symmetric eq. 1 (beta = 0, L = 7): alpha = amax / 7 (1 if below kMinNormal); code in [-7, 7].
 __device__ __forceinline__ float sym_alpha(float amax) {
-  return (amax == 0.0f) ? 1.0f : __fdiv_rn(amax, 7.0f);
+  const float a = __fdiv_rn(amax, 7.0f);
+  return (a < kMinNormal) ? 1.0f : a;
 }
 __device__ __forceinline__ int sym_code(float v, float inv) {
   return static_cast<int>(fminf(fmaxf(rintf(__fmul_rn(v, inv)), -7.0f), 7.0f));

@@ -11,14 +11,14 @@
 // expanded with the same byte order, so the k permutation this introduces cancels in
 // the dot product.  |16 acc| <= 16 * 15 * 7 * K < 2^31 for K < 1.2M.
 //
-// Prefill kernel (w4a4_gemm_tile): 256 threads per 256 x 128 output tile, 4 waves in a
-// 2 x 2 arrangement, each wave a 128 x 64 sub-tile = 4 x 2 MFMA blocks.  K advances in
-// stages of 128 (64 packed bytes per row) through a double-buffered packed LDS tile
-// (row pitch 72 bytes: a 16-lane group of 8-byte fragment reads hits 16 distinct bank
-// pairs); the next stage's global loads are issued before the current stage's MFMAs and
-// written to the other buffer afterwards, one barrier per stage.
-// Small-M kernel (w4a4_gemm_v1): 128 x 128 tiles, 64-k single-buffered stages; used for
-// M < 128.
+// Main kernel (w4a4_gemm_ring): the packed operand tiles stream from global memory into
+// an LDS ring by direct-to-LDS buffer loads, several stages ahead; each wave reads its
+// fragments back with ds_read_b128, expands them with VALU and issues the MFMAs.  Tile
+// shapes: 128 x 128 (4 waves of 64 x 64) for small M, 256 x 128 (4 waves of 128 x 64,
+// two workgroups per CU) and 256 x 256 (8 waves of 128 x 64).
+// Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
+// used where 32-bit buffer offsets do not cover the operands.
+// Small kernel (w4a4_gemm_v1): 128 x 128 tiles, single-buffered; kept as a baseline.
 #include <cstdlib>
 #include <utility>
 
@@ -77,6 +77,82 @@ __device__ __forceinline__ void store_block(const GemmArgs& g, const v16i& acc, 
     if (g.bias) yv = __fadd_rn(yv, bn);
     g.y[m * g.ldy + n] = f2h(yv);
   }
+}
+
+// Tile order.  Consecutive workgroup ids go to different XCDs (round robin over 8), so each
+// XCD is given a contiguous range of tile ids; within it the tile walks M fastest, so the
+// CUs of one XCD share weight (B) tiles in their L2 and each weight tile is read from HBM
+// about once.  Grid: x = tiles along N, y = tiles along M.
+__device__ __forceinline__ void tile_origin(int bm, int bn, int64_t& m0, int64_t& n0) {
+  const int tiles_m = gridDim.y;
+  const int total = gridDim.x * gridDim.y;
+  const int bid = blockIdx.y * gridDim.x + blockIdx.x;
+  const int q8 = total / 8, r8 = total % 8;
+  const int xcd = bid % 8, idx = bid / 8;
+  const int tile = xcd < r8 ? xcd * (q8 + 1) + idx : r8 * (q8 + 1) + (xcd - r8) * q8 + idx;
+  m0 = static_cast<int64_t>(tile % tiles_m) * bm;
+  n0 = static_cast<int64_t>(tile / tiles_m) * bn;
+}
+
+// y = (alpha_m s_n) acc + beta_m (s_n rs_n) [+ bias_n] for the TM x TN blocks of one wave,
+// whose top-left output is (mw, nw); one fma per output.  Neighbouring columns sit in
+// neighbouring lanes; even lanes store both as one 32-bit word when the output rows are
+// 4-byte aligned.  One 32 x 32 block row at a time (sched_barrier keeps the scheduler from
+// hoisting every block's accumulators at once).
+template <int TM, int TN>
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
+                                              int lane) {
+  const bool pair = ((g.ldy & 1) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 3) == 0) && (g.dbg_acc == nullptr);
+  const int c = lane & 31;
+  float csn[TN], cwr[TN], cbn[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int64_t n = nw + j * 32 + c;
+    const int64_t nc = n < g.N ? n : g.N - 1;
+    csn[j] = g.wa[nc];
+    cwr[j] = __fmul_rn(csn[j], static_cast<float>(g.rs[nc]));
+    cbn[j] = g.bias ? h2f(g.bias[nc]) : 0.0f;
+  }
+  static_for<TM>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t mb = mw + i * 32 + 4 * (lane >> 5);
+    float ra_[16], rb_[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t m = mb + 8 * (r >> 2) + (r & 3);
+      const int64_t mc = m < g.M ? m : g.M - 1;
+      ra_[r] = g.xa[mc];
+      rb_[r] = g.xb[mc];
+    }
+    static_for<TN>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      const int64_t n = nw + j * 32 + c;
+      const bool nok = n < g.N;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = mb + 8 * (r >> 2) + (r & 3);
+        const bool mok = m < g.M;
+        const int a = acc[i][j][r] >> 4;
+        float yv = __fmaf_rn(__fmul_rn(ra_[r], csn[j]), static_cast<float>(a), __fmul_rn(rb_[r], cwr[j]));
+        if (g.bias) yv = __fadd_rn(yv, cbn[j]);
+        const uint32_t h = f2h(yv);
+        if (pair) {
+          // quad_perm [1,0,3,2]: each lane receives its neighbour's value
+          const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(h), 0xB1, 0xF, 0xF, false));
+          if ((c & 1) == 0 && mok && nok) {
+            if (n + 1 < g.N)
+              *reinterpret_cast<uint32_t*>(g.y + m * g.ldy + n) = h | (other << 16);
+            else
+              g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
+          }
+        } else if (mok && nok) {
+          if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
+          g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
+        }
+      }
+    });
+  });
 }
 
 // ------------------------------------------------------------------ prefill tile kernel
@@ -139,18 +215,8 @@ w4a4_gemm_tile(GemmArgs g) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  // Tile order.  Consecutive workgroup ids go to different XCDs (round robin over 8), so
-  // each XCD is given a contiguous range of tile ids; within it the tile walks M fastest,
-  // so the CUs of one XCD share weight (B) tiles in their L2 and each weight tile is read
-  // from HBM about once.
-  const int tiles_m = gridDim.y;
-  const int total = gridDim.x * gridDim.y;
-  const int bid = blockIdx.y * gridDim.x + blockIdx.x;
-  const int q8 = total / 8, r8 = total % 8;
-  const int xcd = bid % 8, idx = bid / 8;
-  const int tile = xcd < r8 ? xcd * (q8 + 1) + idx : r8 * (q8 + 1) + (xcd - r8) * q8 + idx;
-  const int64_t m0 = static_cast<int64_t>(tile % tiles_m) * BM;
-  const int64_t n0 = static_cast<int64_t>(tile / tiles_m) * BN;
+  int64_t m0, n0;
+  tile_origin(BM, BN, m0, n0);
   const int wm = (wave / WAVES_N) * (TM * 32);
   const int wn = (wave % WAVES_N) * (TN * 32);
   const int64_t KB = g.K / 2;
@@ -238,310 +304,220 @@ w4a4_gemm_tile(GemmArgs g) {
     mma_step(acc, af1, bf1, af0, bf0, f, more);
   }
 
-  // ---- epilogue: y = (alpha_m s_n) acc + beta_m (s_n rs_n) [+ bias_n], one fma per output.
-  // Neighbouring columns sit in neighbouring lanes; even lanes store both as one 32-bit word
-  // when the output rows are 4-byte aligned.  One 32 x 32 block at a time (sched_barrier
-  // keeps the scheduler from hoisting every block's accumulators at once).
-  const bool pair = ((g.ldy & 1) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 3) == 0) && (g.dbg_acc == nullptr);
-  const int c = lane & 31;
-  float csn[TN], cwr[TN], cbn[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t n = n0 + wn + j * 32 + c;
-    const int64_t nc = n < g.N ? n : g.N - 1;
-    csn[j] = g.wa[nc];
-    cwr[j] = __fmul_rn(csn[j], static_cast<float>(g.rs[nc]));
-    cbn[j] = g.bias ? h2f(g.bias[nc]) : 0.0f;
-  }
-  static_for<TM>([&](auto ic) {
-    constexpr int i = decltype(ic)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    const int64_t mb = m0 + wm + i * 32 + 4 * (lane >> 5);
-    float ra_[16], rb_[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t m = mb + 8 * (r >> 2) + (r & 3);
-      const int64_t mc = m < g.M ? m : g.M - 1;
-      ra_[r] = g.xa[mc];
-      rb_[r] = g.xb[mc];
-    }
-    static_for<TN>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
-      const int64_t n = n0 + wn + j * 32 + c;
-      const bool nok = n < g.N;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = mb + 8 * (r >> 2) + (r & 3);
-        const bool mok = m < g.M;
-        const int a = acc[i][j][r] >> 4;
-        float yv = __fmaf_rn(__fmul_rn(ra_[r], csn[j]), static_cast<float>(a), __fmul_rn(rb_[r], cwr[j]));
-        if (g.bias) yv = __fadd_rn(yv, cbn[j]);
-        const uint32_t h = f2h(yv);
-        if (pair) {
-          // quad_perm [1,0,3,2]: each lane receives its neighbour's value
-          const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(h), 0xB1, 0xF, 0xF, false));
-          if ((c & 1) == 0 && mok && nok) {
-            if (n + 1 < g.N)
-              *reinterpret_cast<uint32_t*>(g.y + m * g.ldy + n) = h | (other << 16);
-            else
-              g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
-          }
-        } else if (mok && nok) {
-          if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
-          g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
-        }
-      }
-    });
-  });
+  tile_epilogue(g, acc, m0 + wm, n0 + wn, lane);
 }
 
-// ------------------------------------------------------------------ int8-LDS tile kernel
-// The packed operands are expanded to int8 once per workgroup while staging (instead of
-// once per wave per fragment) and the MFMA fragments are read with ds_read_b128.  Rows
-// are 128 int8 (one 128-k stage) at a 144-byte LDS pitch, so 16 lanes reading 16 rows hit
-// 16 distinct groups of 4 banks.  Global reads are buffer loads: the k advance is an SGPR
-// offset and reads past the end of A or B (M and N tails) return zeros.
-constexpr int kIPitch = 144;
+// ------------------------------------------------------------------ LDS-ring tile kernel
+// Packed operand tiles go from global memory straight into LDS (buffer_load_dwordx4 ... lds:
+// no registers, no VALU), NS stages deep, so a stage's loads are in flight for NS - 1 stages
+// of MFMA work.  A stage covers 128 k (64 packed bytes per row) and is laid out as 1 KB
+// blocks, one per 32 rows and pair of 16-byte chunks: lane l of the copying wave brings row
+// l % 32, chunk 2p + l / 32 to byte 16 l of the block.  A wave reads a block back with one
+// contiguous ds_read_b128 (no bank conflicts); each lane then holds 32 codes of one row,
+// which expand into the operands of two MFMA k-steps.  Both operands use the same k-slot
+// order, so the dot product is unchanged.  Rows past M or N and chunks past K are out of the
+// buffer range and land as zeros.
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void expand_chunk_act(uint4 d, uint4& lo, uint4& hi) {
-  lo = make_uint4(d.x & 0x0F0F0F0Fu, (d.x >> 4) & 0x0F0F0F0Fu, d.y & 0x0F0F0F0Fu, (d.y >> 4) & 0x0F0F0F0Fu);
-  hi = make_uint4(d.z & 0x0F0F0F0Fu, (d.z >> 4) & 0x0F0F0F0Fu, d.w & 0x0F0F0F0Fu, (d.w >> 4) & 0x0F0F0F0Fu);
-}
-__device__ __forceinline__ void expand_chunk_wgt(uint4 d, uint4& lo, uint4& hi) {
-  lo = make_uint4((d.x << 4) & 0xF0F0F0F0u, d.x & 0xF0F0F0F0u, (d.y << 4) & 0xF0F0F0F0u, d.y & 0xF0F0F0F0u);
-  hi = make_uint4((d.z << 4) & 0xF0F0F0F0u, d.z & 0xF0F0F0F0u, (d.w << 4) & 0xF0F0F0F0u, d.w & 0xF0F0F0F0u);
-}
-
-template <int WAVES_M, int WAVES_N, int TM, int TN>
-struct I8Tile {
-  static constexpr int THREADS = 64 * WAVES_M * WAVES_N;
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS>
+struct Ring {
+  static constexpr int WAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * WAVES;
   static constexpr int BM = WAVES_M * TM * 32;
   static constexpr int BN = WAVES_N * TN * 32;
-  static constexpr int STAGE = (BM + BN) * kIPitch;
-  static constexpr int LDS = 2 * STAGE;
-  static constexpr int ACH = BM * 4 / THREADS;   // packed 16-byte chunks per thread per stage
-  static constexpr int BCH = BN * 4 / THREADS;
-  static_assert(ACH * THREADS == BM * 4 && BCH * THREADS == BN * 4, "staging split");
+  static constexpr int ABLK = BM / 16;  // 1 KB blocks per stage: 32 rows x 2 chunk pairs
+  static constexpr int BBLK = BN / 16;
+  static constexpr int ADPW = ABLK / WAVES;  // block copies per wave per stage
+  static constexpr int DPW = (ABLK + BBLK) / WAVES;
+  static constexpr int STAGE = (ABLK + BBLK) * 1024;
+  static constexpr int LDS = NS * STAGE;
+  static_assert(ADPW * WAVES == ABLK && DPW * WAVES == ABLK + BBLK, "blocks split evenly over waves");
+  static_assert(NS >= 2 && (NS - 1) * DPW <= 63, "outstanding copies fit the vmcnt counter");
 };
 
-template <int WAVES_M, int WAVES_N, int TM, int TN, bool KTAIL>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N)
-w4a4_gemm_i8lds(GemmArgs g) {
-  using T = I8Tile<WAVES_M, WAVES_N, TM, TN>;
-  constexpr int BM = T::BM, BN = T::BN, THREADS = T::THREADS;
+template <int TM, int TN>
+struct RingPacked {  // one chunk pair (two k-steps) of the wave's A and B blocks
+  v4u a[TM];
+  v4u b[TN];
+};
+template <int TM, int TN>
+struct RingOps {  // MFMA operands of one k-step
+  v4i a[TM];
+  v4i b[TN];
+};
+
+// Operands of k-step H (0: dwords 0-1, 1: dwords 2-3) of a packed chunk pair.
+template <int H, int TM, int TN>
+__device__ __forceinline__ void expand_half(const RingPacked<TM, TN>& P, RingOps<TM, TN>& E) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const uint32_t d0 = P.a[i][2 * H], d1 = P.a[i][2 * H + 1];
+    E.a[i] = v4i{static_cast<int>(d0 & 0x0F0F0F0Fu), static_cast<int>((d0 >> 4) & 0x0F0F0F0Fu),
+                 static_cast<int>(d1 & 0x0F0F0F0Fu), static_cast<int>((d1 >> 4) & 0x0F0F0F0Fu)};
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const uint32_t d0 = P.b[j][2 * H], d1 = P.b[j][2 * H + 1];
+    E.b[j] = v4i{static_cast<int>((d0 << 4) & 0xF0F0F0F0u), static_cast<int>(d0 & 0xF0F0F0F0u),
+                 static_cast<int>((d1 << 4) & 0xF0F0F0F0u), static_cast<int>(d1 & 0xF0F0F0F0u)};
+  }
+}
+
+// s_waitcnt with vmcnt = VM (0..63: bits 3:0 and 15:14) and lgkmcnt = 0 (expcnt not waited on)
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(VM >= 0 && VM <= 63, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));
+}
+
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, WPE)
+w4a4_gemm_ring(GemmArgs g) {
+  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int tiles_m = gridDim.y;
-  const int total = gridDim.x * gridDim.y;
-  const int bid = blockIdx.y * gridDim.x + blockIdx.x;
-  const int q8 = total / 8, r8 = total % 8;
-  const int xcd = bid % 8, idx = bid / 8;
-  const int tile = xcd < r8 ? xcd * (q8 + 1) + idx : r8 * (q8 + 1) + (xcd - r8) * q8 + idx;
-  const int m0 = (tile % tiles_m) * BM;
-  const int n0 = (tile / tiles_m) * BN;
-  const int wm = (wave / WAVES_N) * (TM * 32);
-  const int wn = (wave % WAVES_N) * (TN * 32);
-  const int KB = static_cast<int>(g.K / 2);
-  const int nstage = (KB + kBKB - 1) / kBKB;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int64_t m0, n0;
+  tile_origin(R::BM, R::BN, m0, n0);
+  const int wm = (wave / WAVES_N) * TM;  // first 32-row group of this wave in the tile
+  const int wn = (wave % WAVES_N) * TN;
+  const uint32_t KB = static_cast<uint32_t>(g.K / 2);
+  const int nstage = static_cast<int>((KB + 63) / 64);
 
-  const __amdgpu_buffer_rsrc_t ra_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc((void*)g.xq, (short)0, static_cast<int>(g.M * KB), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc((void*)g.wq, (short)0, static_cast<int>(g.N * KB), 0x00020000);
-
-  // staging: chunk c = tid + q*THREADS covers tile row (c % 16) + 16 (c / 64), packed column (c / 16) % 4
-  const int srow = (tid & 15) + 16 * (tid >> 6);
-  const int scol = (tid >> 4) & 3;
-  const int aoff0 = (m0 + srow) * KB + scol * 16;  // byte offsets of chunk 0; chunk q adds q*THREADS/4 rows
-  const int boff0 = (n0 + srow) * KB + scol * 16;
-  uint4 pa[T::ACH], pb[T::BCH];
-  auto gload = [&](int st) {
-    const int kb = st * kBKB;
+  // Buffer ranges: offsets are 32-bit and (M + BM) * K/2 < 2^31 is checked on the host.
+  const __amdgpu_buffer_rsrc_t rsa =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.xq), 0, static_cast<int>(g.M * KB), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsb =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.wq), 0, static_cast<int>(g.N * KB), 0x00020000);
+  // Copy d of this wave is block b = wave + WAVES d of a stage: A blocks first, then B.
+  uint32_t rowoff[R::DPW], colofs[R::DPW];
+  static_for<R::DPW>([&](auto dc) {
+    constexpr int d = decltype(dc)::value;
+    const int b = wave + R::WAVES * d;
+    const int bl = d < R::ADPW ? b : b - R::ABLK;
+    const int64_t row = (d < R::ADPW ? m0 : n0) + (bl >> 1) * 32 + (lane & 31);
+    rowoff[d] = static_cast<uint32_t>(row) * KB;
+    colofs[d] = (bl & 1) * 32 + (lane >> 5) * 16;
+  });
+  auto issue = [&](int st) {
+    uint8_t* sb = lds + (st % NS) * R::STAGE;
+    const uint32_t k0 = static_cast<uint32_t>(st) * 64;
+    static_for<R::DPW>([&](auto dc) {
+      constexpr int d = decltype(dc)::value;
+      const uint32_t col = k0 + colofs[d];
+      // past K (or a stage past the end, issued only to keep the copy count uniform): out of range
+      const uint32_t off = (col < KB) ? rowoff[d] + col : 0x80000000u;
+      auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<uintptr_t>(sb + (wave + R::WAVES * d) * 1024));
+      if constexpr (d < R::ADPW)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, dst, 16, static_cast<int>(off), 0, 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, dst, 16, static_cast<int>(off), 0, 0, 0);
+    });
+  };
+  auto read = [&](RingPacked<TM, TN>& P, int st, int p) {
+    const uint8_t* sb = lds + (st % NS) * R::STAGE + lane * 16 + p * 1024;
 #pragma unroll
-    for (int q = 0; q < T::ACH; ++q)
-      pa[q] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            ra_rsrc, aoff0 + q * (THREADS / 4) * KB, kb, 0));
+    for (int i = 0; i < TM; ++i) P.a[i] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 2048);
 #pragma unroll
-    for (int q = 0; q < T::BCH; ++q)
-      pb[q] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                            rb_rsrc, boff0 + q * (THREADS / 4) * KB, kb, 0));
-    if constexpr (KTAIL) {
-      // a half stage (K % 128 == 64): columns past K belong to the next row; zero A
-      const bool z = kb + scol * 16 >= KB;
+    for (int j = 0; j < TN; ++j) P.b[j] = *reinterpret_cast<const v4u*>(sb + (R::ABLK + 2 * (wn + j)) * 1024);
+  };
+  // MFMAs of one k-step from E, with the next k-step's operands expanded into F in between
+  constexpr int NM = TM * TN;
+  constexpr int NV = 6 * (TM + TN);
+  constexpr int PER = (NV + NM - 2) / (NM - 1);
+  auto mma = [&](v16i (&acc)[TM][TN], const RingOps<TM, TN>& E) {
 #pragma unroll
-      for (int q = 0; q < T::ACH; ++q) pa[q] = z ? make_uint4(0, 0, 0, 0) : pa[q];
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(E.a[i], E.b[j], acc[i][j], 0, 0, 0);
+  };
+  // ds_reads (NR of them) first, then one MFMA per PER expansion ops
+  auto interleave = [&](auto nr) {
+    constexpr int NR = decltype(nr)::value;
+    if constexpr (NR > 0) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+#pragma unroll
+    for (int k = 0; k < NM - 1; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x002, PER, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
   };
-  auto lstore = [&](int buf) {
-    uint8_t* base = lds + buf * T::STAGE + srow * kIPitch + scol * 32;
-#pragma unroll
-    for (int q = 0; q < T::ACH; ++q) {
-      uint4 lo, hi;
-      expand_chunk_act(pa[q], lo, hi);
-      uint8_t* p = base + q * (THREADS / 4) * kIPitch;
-      *reinterpret_cast<uint4*>(p) = lo;
-      *reinterpret_cast<uint4*>(p + 16) = hi;
-    }
-#pragma unroll
-    for (int q = 0; q < T::BCH; ++q) {
-      uint4 lo, hi;
-      expand_chunk_wgt(pb[q], lo, hi);
-      uint8_t* p = base + (BM + q * (THREADS / 4)) * kIPitch;
-      *reinterpret_cast<uint4*>(p) = lo;
-      *reinterpret_cast<uint4*>(p + 16) = hi;
-    }
-  };
-  auto read_frags = [&](v4i (&af)[TM], v4i (&bf)[TN], int buf, int ks) {
-    const uint8_t* As = lds + buf * T::STAGE + (lane & 31) * kIPitch + ks * 32 + (lane >> 5) * 16;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const v4i*>(As + (wm + i * 32) * kIPitch);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bf[j] = *reinterpret_cast<const v4i*>(As + (BM + wn + j * 32) * kIPitch);
+  auto sync = [&]() {
+    wait_vm_lgkm0<(NS - 2) * R::DPW>();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
 
   v16i acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v16i{};
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  v4i af0[TM], bf0[TN], af1[TM], bf1[TN];
-  read_frags(af0, bf0, 0, 0);
-  auto mfmas = [&](const v4i (&af)[TM], const v4i (&bf)[TN]) {
-    static_for<TM>([&](auto ic) {
-      static_for<TN>([&](auto jc) {
-        constexpr int i = decltype(ic)::value, j = decltype(jc)::value;
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
-      });
-    });
-  };
-  constexpr int NM = TM * TN;
-  constexpr int NV = 12 * (T::ACH + T::BCH);  // expansion VALU per thread per stage
-  constexpr int NW = 2 * (T::ACH + T::BCH);   // 16-byte LDS stores per thread per stage
-  // Every stage is one scheduling region (no branches): the last stage re-reads its own
-  // data and stores it into the unused buffer.
+  // Pipeline over k-steps (four per stage).  Packed chunk pairs are read from LDS two
+  // k-steps before their first expansion, operands are expanded one k-step ahead of their
+  // MFMAs, and the stage sync sits in the second k-step, after the last read of the
+  // current stage's slot (which the copy issued right after it refills).
+  for (int s = 0; s < NS - 1; ++s) issue(s);
+  sync();
+  issue(NS - 1);
+  RingPacked<TM, TN> P0, P1;
+  RingOps<TM, TN> E0, E1;
+  read(P0, 0, 0);
+  read(P1, 0, 1);
+  expand_half<0>(P0, E0);
+
+  // Branch-free steady state: the last iteration also syncs, copies (out of range) and
+  // expands the stage after the end; those operands are never used.
   for (int st = 0; st < nstage; ++st) {
-    const int buf = st & 1;
-    gload(st + 1 < nstage ? st + 1 : st);
-    read_frags(af1, bf1, buf, 1);
-    mfmas(af0, bf0);
-    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
-    read_frags(af0, bf0, buf, 2);
-    mfmas(af1, bf1);
-    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
-    read_frags(af1, bf1, buf, 3);
-    mfmas(af0, bf0);
-    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
-    // k-step 3, first half of its MFMAs: interleaved with expanding + storing the next stage
-    static_for<TM / 2>([&](auto ic) {
-      static_for<TN>([&](auto jc) {
-        constexpr int i = decltype(ic)::value, j = decltype(jc)::value;
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af1[i], bf1[j], acc[i][j], 0, 0, 0);
-      });
-    });
-    lstore(buf ^ 1);
-    static_for<NM / 2>([&](auto) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, (2 * NV + NM - 1) / NM, 0);
-      __builtin_amdgcn_sched_group_barrier(0x200, (2 * NW + NM - 1) / NM, 0);
-    });
-    __syncthreads();
-    // next stage's first fragments; the second half of k-step 3 covers their latency
-    read_frags(af0, bf0, buf ^ 1, 0);
-    static_for<TM - TM / 2>([&](auto ic) {
-      static_for<TN>([&](auto jc) {
-        constexpr int i = TM / 2 + decltype(ic)::value, j = decltype(jc)::value;
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af1[i], bf1[j], acc[i][j], 0, 0, 0);
-      });
-    });
-    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - (TM / 2) * TN, 0);
+    constexpr std::integral_constant<int, 0> none{};
+    constexpr std::integral_constant<int, TM + TN> all{};
+    mma(acc, E0);                 // k-step 4 st
+    expand_half<1>(P0, E1);
+    interleave(none);
+    sync();                       // stage st + 1 has landed; slot st is free
+    issue(st + NS);
+    read(P0, st + 1, 0);
+    mma(acc, E1);                 // k-step 4 st + 1
+    expand_half<0>(P1, E0);
+    interleave(all);
+    mma(acc, E0);                 // k-step 4 st + 2
+    expand_half<1>(P1, E1);
+    interleave(none);
+    read(P1, st + 1, 1);
+    mma(acc, E1);                 // k-step 4 st + 3
+    expand_half<0>(P0, E0);
+    interleave(all);
   }
+  // copies of stages past the end may still be landing in LDS
+  wait_vm_lgkm0<0>();
+  asm volatile("" ::: "memory");
 
-  // ---- epilogue (as in the packed-LDS kernel)
-  const bool pair = ((g.ldy & 1) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 3) == 0) && (g.dbg_acc == nullptr);
-  const int c = lane & 31;
-  float csn[TN], cwr[TN], cbn[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t n = n0 + wn + j * 32 + c;
-    const int64_t nc = n < g.N ? n : g.N - 1;
-    csn[j] = g.wa[nc];
-    cwr[j] = __fmul_rn(csn[j], static_cast<float>(g.rs[nc]));
-    cbn[j] = g.bias ? h2f(g.bias[nc]) : 0.0f;
-  }
-  static_for<TM>([&](auto ic) {
-    constexpr int i = decltype(ic)::value;
-    __builtin_amdgcn_sched_barrier(0);
-    const int64_t mb = m0 + wm + i * 32 + 4 * (lane >> 5);
-    float ra_[16], rb_[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t m = mb + 8 * (r >> 2) + (r & 3);
-      const int64_t mc = m < g.M ? m : g.M - 1;
-      ra_[r] = g.xa[mc];
-      rb_[r] = g.xb[mc];
-    }
-    static_for<TN>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
-      const int64_t n = n0 + wn + j * 32 + c;
-      const bool nok = n < g.N;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = mb + 8 * (r >> 2) + (r & 3);
-        const bool mok = m < g.M;
-        const int a = acc[i][j][r] >> 4;
-        float yv = __fmaf_rn(__fmul_rn(ra_[r], csn[j]), static_cast<float>(a), __fmul_rn(rb_[r], cwr[j]));
-        if (g.bias) yv = __fadd_rn(yv, cbn[j]);
-        const uint32_t h = f2h(yv);
-        if (pair) {
-          const uint32_t other = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(h), 0xB1, 0xF, 0xF, false));
-          if ((c & 1) == 0 && mok && nok) {
-            if (n + 1 < g.N)
-              *reinterpret_cast<uint32_t*>(g.y + m * g.ldy + n) = h | (other << 16);
-            else
-              g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
-          }
-        } else if (mok && nok) {
-          if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
-          g.y[m * g.ldy + n] = static_cast<uint16_t>(h);
-        }
-      }
-    });
-  });
+  tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
 }
 
-// Buffer offsets are 32-bit: the int8-LDS kernel needs (M + BM) * K/2 and (N + BN) * K/2 below 2^31.
-template <int WM, int WN, int TM, int TN>
-bool fits_i8(const GemmArgs& g) {
-  using T = I8Tile<WM, WN, TM, TN>;
+template <int WM, int WN, int TM, int TN, int NS>
+bool fits_ring(const GemmArgs& g) {
+  using R = Ring<WM, WN, TM, TN, NS>;
   const int64_t kb = g.K / 2;
-  return (g.M + T::BM) * kb < (int64_t{1} << 31) && (g.N + T::BN) * kb < (int64_t{1} << 31);
+  return (g.M + R::BM) * kb + 64 < (int64_t{1} << 31) && (g.N + R::BN) * kb + 64 < (int64_t{1} << 31);
 }
 
-template <int WM, int WN, int TM, int TN, bool KTAIL>
-hipError_t launch_i8_t(const GemmArgs& g, hipStream_t stream) {
-  using T = I8Tile<WM, WN, TM, TN>;
-  auto kern = w4a4_gemm_i8lds<WM, WN, TM, TN, KTAIL>;
+// WPE: waves per SIMD the registers must allow (2 for two 4-wave workgroups per CU)
+template <int WM, int WN, int TM, int TN, int NS, int WPE = 1>
+hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
+  using R = Ring<WM, WN, TM, TN, NS>;
+  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, R::LDS);
   if (init != hipSuccess) return init;
-  const dim3 grid(static_cast<unsigned>((g.N + T::BN - 1) / T::BN), static_cast<unsigned>((g.M + T::BM - 1) / T::BM));
-  hipLaunchKernelGGL(kern, grid, dim3(T::THREADS), T::LDS, stream, g);
+  const dim3 grid(static_cast<unsigned>((g.N + R::BN - 1) / R::BN), static_cast<unsigned>((g.M + R::BM - 1) / R::BM));
+  hipLaunchKernelGGL(kern, grid, dim3(R::THREADS), R::LDS, stream, g);
   return hipGetLastError();
-}
-
-template <int WM, int WN, int TM, int TN>
-hipError_t launch_i8(const GemmArgs& g, hipStream_t stream) {
-  return (g.K % 128) ? launch_i8_t<WM, WN, TM, TN, true>(g, stream) : launch_i8_t<WM, WN, TM, TN, false>(g, stream);
 }
 
 // ------------------------------------------------------------------ small-M kernel
@@ -634,22 +610,32 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 3: launch_tile<2, 1, 4, 4>(g, stream); break;   // 256 x 128, 2 waves of 128 x 128
     case 4: launch_tile<1, 2, 4, 4>(g, stream); break;   // 128 x 256, 2 waves of 128 x 128
     case 5: launch_tile<2, 4, 4, 2>(g, stream); break;   // 256 x 256, 8 waves of 128 x 64
-    case 6: if (fits_i8<2, 2, 4, 4>(g)) return launch_i8<2, 2, 4, 4>(g, stream); break;  // 256 x 256, int8 LDS
-    case 7: if (fits_i8<2, 2, 4, 2>(g)) return launch_i8<2, 2, 4, 2>(g, stream); break;  // 256 x 128, int8 LDS
-    case 8: if (fits_i8<2, 2, 2, 4>(g)) return launch_i8<2, 2, 2, 4>(g, stream); break;  // 128 x 256, int8 LDS
+    case 10: if (fits_ring<2, 2, 4, 2, 4>(g)) return launch_ring<2, 2, 4, 2, 4>(g, stream); break;  // 256 x 128
+    case 11: if (fits_ring<2, 2, 4, 4, 4>(g)) return launch_ring<2, 2, 4, 4, 4>(g, stream); break;  // 256 x 256
+    case 12: if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream); break;  // 256 x 256, 8 waves
+    case 13: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream); break;  // 128 x 128
+    case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
     case 9: {
       const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
       hipLaunchKernelGGL(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
       break;
     }
     default: {
-      // Measured on MI355X: the 256 x 256 tile (8 waves of 128 x 64) wins once there are
-      // enough tiles to fill the 256 CUs; smaller problems use 128 x 128 tiles.
+      // Measured on MI355X (LLaMA MLP shapes): decode-sized M runs 128 x 128 ring tiles;
+      // otherwise 256 x 128 ring tiles two workgroups per CU, unless the 256 x 256 tiles
+      // fill whole rounds of the 256 CUs (then the 8-wave 256 x 256 ring tile wins).
+      // Problems whose byte offsets do not fit 31 bits use the register-staged kernel.
       const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-      if (g.M >= 128 && tiles256 >= 256)
-        launch_tile<2, 4, 4, 2>(g, stream);
-      else
+      if (g.M <= 128) {
+        if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream);
         launch_tile<2, 2, 2, 2>(g, stream);
+      } else if (tiles256 >= 256 && (tiles256 % 256 == 0 || tiles256 % 256 >= 192)) {
+        if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
+        launch_tile<2, 4, 4, 2>(g, stream);
+      } else {
+        if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
+        launch_tile<2, 4, 4, 2>(g, stream);
+      }
       break;
     }
   }

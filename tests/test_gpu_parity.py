@@ -93,12 +93,14 @@ def test_blockwise_rotation_and_groups():
 def test_edge_rows():
     say("had_quant_act edge rows")
     K = 28 * 64
-    x = np.zeros((6, K), dtype=np.float16)
+    x = np.zeros((8, K), dtype=np.float16)
     x[1, :] = 0.5                     # constant row
     x[2, 17] = 300.0                  # single outlier
     x[3, :] = np.float16(-65504.0)    # fp16 extreme, constant
     x[4, ::2] = 1.0
     x[5] = workloads.outlier_acts(workloads.rng_for(3), 1, K, 3, 50.0)[0]
+    x[6, 40] = np.float16(6e-8)       # smallest fp16 subnormal, alone
+    x[7, ::3] = np.float16(-3e-6)     # subnormal values only
     check_act(x, 28, 64)
     check_act(x, 1, 1)
 
@@ -322,11 +324,11 @@ def test_kv_full_sampled():
     check_kv(q, k, v, sample)
 
 
-@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "6", "7", "8", "9"])
+@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "9", "10", "11", "12", "13", "14"])
 def test_gemm_tile_variants(variant, monkeypatch):
     say(f"w4a4_linear tile variant {variant}: ragged shapes, paired and unpaired stores")
     monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
-    for (M, N, K) in [(300, 390, 448), (64, 130, 192), (257, 257, 128), (520, 600, 320)]:
+    for (M, N, K) in [(300, 390, 448), (64, 130, 192), (257, 257, 128), (520, 600, 320), (384, 264, 2112)]:
         rng = workloads.rng_for(M + N + K)
         qa = rng.integers(0, 16, size=(M, K))
         qw = rng.integers(-7, 8, size=(N, K))

@@ -97,6 +97,24 @@ def test_asym_beats_sym_on_rotated_activations():
     assert ea < es
 
 
+def test_tiny_range_is_constant():
+    # alpha = range / L below the smallest normal fp32 would make 1 / alpha overflow: the
+    # group is quantized as constant (alpha 1, codes 0) and dequantizes to beta, within the range.
+    tiny = np.finfo(np.float32).tiny
+    for top in [np.float32(8.76e-43), np.float32(1e-37), np.float32(15 * tiny * 0.999)]:
+        v = np.array([[top, 0, 0, 0]], dtype=np.float32)
+        q, a, b = quant.quant_asym(v, bits=4)
+        assert a[0, 0] == 1 and b[0, 0] == 0 and not q.any()
+        assert np.abs(quant.dequant(q, a, b) - v).max() <= top
+    for top in [np.float32(8.76e-43), np.float32(5e-38), np.float32(7 * tiny * 0.999)]:
+        qs, as_ = quant.quant_sym(np.array([[top, -top / 2, 0, 0]], dtype=np.float32), bits=4)
+        assert as_[0, 0] == 1 and not qs.any()
+    # just above the threshold the quantizer works normally
+    v = np.array([[np.float32(16 * tiny), 0, 0, 0]], dtype=np.float32)
+    q, a, b = quant.quant_asym(v, bits=4)
+    assert a[0, 0] >= tiny and q.tolist() == [[15, 0, 0, 0]]
+
+
 def test_pack_layout_and_roundtrip():
     q = np.array([[1, 2, 15, 0, 7, 8]])
     p = quant.pack_nibbles(q)
@@ -116,7 +134,7 @@ def test_asym_properties(v):
     assert q.min() >= 0 and q.max() <= 15
     assert b[0, 0] == v.min()
     r = np.float32(v.max() - v.min())
-    if r > 0:
+    if r / np.float32(15) >= np.finfo(np.float32).tiny:
         assert q[0, v.argmin()] == 0 and q[0, v.argmax()] == 15
         err = np.abs(quant.dequant(q, a, b)[0] - v.astype(np.float64))
         # alpha/2 plus the fp32 rounding of (v - min) * (1/alpha)
@@ -132,7 +150,7 @@ def test_sym_properties(v):
     q, a = quant.quant_sym(v[None, :], bits=4)
     assert q.min() >= -7 and q.max() <= 7
     amax = np.abs(v).max()
-    if amax > 0:
+    if amax / np.float32(7) >= np.finfo(np.float32).tiny:
         assert abs(q[0, np.abs(v).argmax()]) == 7
         err = np.abs(quant.dequant(q, a)[0] - v.astype(np.float64))
         assert np.all(err <= np.float64(a[0, 0]) * (0.5 + 4e-6))
