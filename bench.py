@@ -5,7 +5,7 @@ tokens (M = 2048):
   1. R3 + 4-bit KV quantization of Q, K, V [1, 2048, 32, 128]          sq_qk_had_kvquant
   2. per-token 4-bit quantization of the MLP input [2048, 4096]          sq_had_quant_act (identity)
   3. gate and up projections [2048x4096] x [11008x4096]^T                sq_w4a4_linear x2
-  4. online R4 (S_64 (x) H_172) + 4-bit quantization of the down-projection
+  4. online R4 (H_172 (x) S_64) + 4-bit quantization of the down-projection
      input [2048, 11008]                                                 sq_had_quant_act
   5. down projection [2048x11008] x [4096x11008]^T                       sq_w4a4_linear
 Weights are packed once beforehand (sq_pack_w4, R4 folded into W_down), as in
@@ -338,9 +338,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": "LLaMA-2-7B layer, M=2048 tokens: R3+KV4 quant [1,2048,32,128]; "
                                "act quant [2048,4096]; gate/up W4A4 [2048x4096]x[11008x4096]; "
-                               "R4 S_64(x)H_172 + quant [2048,11008]; down W4A4 [2048x11008]x[4096x11008]",
+                               "R4 H_172(x)S_64 + quant [2048,11008]; down W4A4 [2048x11008]x[4096x11008]",
                    "tokens": M, "hidden": HID, "intermediate": INTER, "heads": NH, "head_dim": HD,
-                   "r4": f"S_{B} (x) H_{A}", "buffer_sets": args.sets},
+                   "r4": f"H_{A} (x) S_{B}", "buffer_sets": args.sets},
         "roofline": {"kernel": "w4a4_gemm", "bound": "mfma", "achieved": round(gemm_tops, 2),
                      "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
                      "traffic": measured_traffic(),

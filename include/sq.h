@@ -21,12 +21,12 @@
  *    cache, symmetric (alpha = max|X|/(2^(N-1)-1), beta = 0) for weights, no range
  *    clipping (App. A, "Quantization choice", Table 12).  Round-to-nearest is ties to
  *    even; (X-beta)/alpha is evaluated as (X-beta) * fl32(1/alpha); a group whose
- *    range (or max|X|) is zero gets alpha = 1.
+ *    alpha would be zero or subnormal (e.g. a constant group) gets alpha = 1, codes 0.
  *  - Online rotation (R4 on the down-projection input, R3 on Q/K; Sec. 3.1
  *    "Additional unabsorbed rotations"): each contiguous block of n = a*b elements of
- *    a row is multiplied on the right by R = (S_b (x) H_a) / sqrt(n), where S_b is the
- *    natural-order Sylvester matrix of order b = 2^k and H_a a +-1 Hadamard matrix of
- *    order a (dense factor on the inner, contiguous index: element i = i_b*a + i_a).
+ *    a row is multiplied on the right by R = (H_a (x) S_b) / sqrt(n), where H_a is a
+ *    +-1 Hadamard matrix of order a and S_b the natural-order Sylvester matrix of order
+ *    b = 2^k (dense factor on the outer, strided index: element i = i_a*b + i_b).
  *    (a, b) = (1, 1) is the identity.
  *  - Errors: every argument is checked on the host before anything is enqueued.  A
  *    non-OK status means nothing was enqueued and no output was written; the message

@@ -9,7 +9,7 @@ Table 12) with dense fp64 Hadamard factors and exact integer arithmetic.
 
 Modules
   hadamard  Sylvester, Paley-II and Williamson constructions of +-1 Hadamard matrices
-  rotate    row rotation x -> x (S_b (x) H_a) / sqrt(n)
+  rotate    row rotation x -> x (H_a (x) S_b) / sqrt(n)
   quant     eq. 1 min-max quantizer (asymmetric and symmetric), nibble packing
   linear    the rotated W4A4 linear layer: act quant, weight prep, exact GEMM, epilogue
   kv        R3 on post-RoPE Q/K and 4-bit asymmetric K/V cache quantization

@@ -2,9 +2,9 @@
 //
 // Generic kernel: one workgroup of 256 threads per row.  The rotated row lives in LDS
 // as fp32.  Each contiguous block of n = a*b elements is multiplied by
-// (S_b (x) H_a) / sqrt(n) with element i = i_b*a + i_a:
-//   1. dense stage  Y[i_b][j_a] = sum_{i_a} x[i_b*a + i_a] H[i_a][j_a]   (fp32, from L1/L2)
-//   2. Walsh-Hadamard butterflies over i_b (stride a), one LDS pass per stage
+// (H_a (x) S_b) / sqrt(n) with element i = i_a*b + i_b:
+//   1. dense stage  Y[j_a][i_b] = sum_{i_a} x[i_a*b + i_b] H[i_a][j_a]   (fp32, from L1/L2)
+//   2. Walsh-Hadamard butterflies over i_b (contiguous), one LDS pass per stage
 //   3. scale by fl32(1/sqrt(n))
 // then the quantizer: asymmetric per group (activations) or symmetric per row with the
 // code row sum (weights).
@@ -59,29 +59,31 @@ __device__ void rotate_row_to_lds(const uint16_t* __restrict__ xr, int K, int a,
   if (a == 1) {
     for (int i = threadIdx.x; i < K; i += kThreads) buf[i] = h2f(xr[i]);
   } else {
+    // element i of block blk is (j_a, i_b) with i = blk*n + j_a*b + i_b
     for (int i = threadIdx.x; i < K; i += kThreads) {
-      const int ja = i % a;
-      const int base = i - ja;
+      const int blk = i / n;
+      const int r = i - blk * n;
+      const int ja = r / b;
+      const int ib = r - ja * b;
+      const uint16_t* col = xr + blk * n + ib;
       float acc = 0.0f;
       for (int ia = 0; ia < a; ++ia) {
         const float h = static_cast<float>(H[ia * a + ja]);
-        acc = __fadd_rn(acc, __fmul_rn(h2f(xr[base + ia]), h));
+        acc = __fadd_rn(acc, __fmul_rn(h2f(col[ia * b]), h));
       }
       buf[i] = acc;
     }
   }
   __syncthreads();
+  // Walsh-Hadamard butterflies over i_b inside every contiguous chunk of b elements
   const int half = K / 2;
-  const int npair = n / 2;
+  const int hb = b / 2;
   for (int h = 1; h < b; h <<= 1) {
     for (int p = threadIdx.x; p < half; p += kThreads) {
-      const int blk = p / npair;
-      const int pin = p - blk * npair;
-      const int ja = pin % a;
-      const int qq = pin / a;
-      const int lo_b = (qq / h) * (2 * h) + (qq % h);
-      const int lo = blk * n + lo_b * a + ja;
-      const int hi = lo + h * a;
+      const int chunk = p / hb;
+      const int q = p - chunk * hb;
+      const int lo = chunk * b + (q / h) * (2 * h) + (q % h);
+      const int hi = lo + h;
       const float u = buf[lo];
       const float w = buf[hi];
       buf[lo] = __fadd_rn(u, w);

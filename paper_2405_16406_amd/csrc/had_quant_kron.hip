@@ -1,11 +1,14 @@
 // Fast path of the online rotation + per-token 4-bit quantization for rows of length
-// K = a * b rotated by (S_b (x) H_a) / sqrt(K), element i = i_b * a + i_a.
+// K = a * b rotated by (H_a (x) S_b) / sqrt(K), element i = i_a * b + i_b.
 //
-// View a row as X2[i_b][i_a] (b x a).  Then Y2 = S_b^T X2 H_a:
-//   * dense stage X2 H_a on the fp16 matrix cores (v_mfma_f32_32x32x16_f16): the inputs
+// View a row as X2[i_a][i_b] (a x b, i_b contiguous).  Then Y2 = H_a^T X2 S_b, computed as
+// its transpose T[i_b][j_a] = (S_b^T X2^T H_a)[i_b][j_a] = y[j_a * b + i_b]:
+//   * dense stage X2^T H_a on the fp16 matrix cores (v_mfma_f32_32x32x16_f16): the inputs
 //     are exact fp16 and H_a is +-1, so every product is exact and only the fp32
 //     accumulation rounds.  MFMA tile: M = 32 consecutive i_b, N = 32 j_a, K = 16 i_a;
-//     H_a is zero-padded to APAD x (NT*32).
+//     an A fragment gathers 8 values of one column i_b at stride b (consecutive lanes
+//     read consecutive i_b, so each gather is coalesced).  H_a is zero-padded to
+//     APAD x (NT*32).
 //   * Sylvester stage over i_b.  A 32x32 fp32 MFMA result gives lane l, register r the
 //     element m = 8*(r/4) + 4*(l/32) + r%4 of column l%32: i_b bits 0, 1, 3, 4 are
 //     register bits, bit 2 is the lane half, the next bits index the M tiles of a wave,
@@ -17,8 +20,9 @@
 //   * per-row min/max, then the eq. 1 asymmetric quantizer with the 1/sqrt(K) scale
 //     folded into alpha and beta: code = rint((v - mn) * (1/alpha)) in the unscaled
 //     domain, rounded by adding 2^23 (exact round-half-to-even for 0 <= t < 2^22; the
-//     code is then the low byte of the float), one LDS byte per code, and a final pass
-//     packs nibbles and writes 16 bytes per lane.
+//     code is then the low bits of the float).  Codes of consecutive i_b of one column
+//     are nibble-packed in registers (the two lane halves swap 16-bit halves) and
+//     stored straight to global memory: output position j_a * b + i_b.
 // Persistent: each workgroup (MW*NW waves; waves split i_b by MW and j_a by NW) loads the
 // +-1 fragments once and walks rows blockIdx.x, +gridDim.x, ..., prefetching the next
 // row while it transforms the current one.
@@ -56,9 +60,8 @@ struct Kron {
   // LDS layout (bytes)
   static constexpr int ROW_BYTES = STAGE ? K * 2 : 0;
   static constexpr int XCH_BYTES = MW > 1 ? MW * P * 64 * 4 : 0;
-  static constexpr int CODE_BYTES = K;       // one byte per code before packing
   static constexpr int RED_BYTES = 2 * W * 4;
-  static constexpr int LDS = ROW_BYTES + XCH_BYTES + CODE_BYTES + RED_BYTES;
+  static constexpr int LDS = ROW_BYTES + XCH_BYTES + RED_BYTES;
 };
 
 __device__ __forceinline__ void bfly(float& lo, float& hi) {
@@ -67,18 +70,17 @@ __device__ __forceinline__ void bfly(float& lo, float& hi) {
   hi = __fsub_rn(u, w);
 }
 
-// 8 consecutive fp16 of an X2 row starting at column k0 (zero beyond column A).
-template <int A>
-__device__ __forceinline__ v8h load_afrag(const uint16_t* __restrict__ rowp, int k0) {
-  uint2 lo = make_uint2(0, 0), hi = make_uint2(0, 0);
-  if (k0 + 8 <= A) {
-    lo = *reinterpret_cast<const uint2*>(rowp + k0);
-    hi = *reinterpret_cast<const uint2*>(rowp + k0 + 4);
-  } else if (k0 + 4 <= A) {
-    lo = *reinterpret_cast<const uint2*>(rowp + k0);
+// A fragment of the dense stage: the 8 fp16 X2[i_a][i_b] of one column i_b (colp points
+// at element i_b of the row) for i_a = k0 .. k0+7, at stride B; zero for i_a >= A.
+template <int A, int B>
+__device__ __forceinline__ v8h gather_afrag(const uint16_t* __restrict__ colp, int k0) {
+  uint32_t w[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int k = k0 + 2 * p;  // A is a multiple of 4 and k0 of 8: pairs are all in or all out
+    w[p] = (k < A) ? (static_cast<uint32_t>(colp[k * B]) | (static_cast<uint32_t>(colp[(k + 1) * B]) << 16)) : 0u;
   }
-  const uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-  return __builtin_bit_cast(v8h, u);
+  return __builtin_bit_cast(v8h, make_uint4(w[0], w[1], w[2], w[3]));
 }
 
 // rint(t) for 0 <= t < 2^22 as the low bits of t + 2^23 (one IEEE round-half-to-even add)
@@ -93,8 +95,7 @@ had_quant_kron(RotQuantArgs args) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* lds_row = reinterpret_cast<uint16_t*>(smem);
   float* lds_xch = reinterpret_cast<float*>(smem + C::ROW_BYTES);
-  uint8_t* lds_code = smem + C::ROW_BYTES + C::XCH_BYTES;
-  float* lds_red = reinterpret_cast<float*>(smem + C::ROW_BYTES + C::XCH_BYTES + C::CODE_BYTES);
+  float* lds_red = reinterpret_cast<float*>(smem + C::ROW_BYTES + C::XCH_BYTES);
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -133,7 +134,7 @@ had_quant_kron(RotQuantArgs args) {
     for (int mt = 0; mt < (STAGE ? 1 : C::MT); ++mt) {
       const int ib = (wm * C::MT + mt) * 32 + c;
 #pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) af[mt][ks] = load_afrag<A>(xr + ib * A, ks * 16 + 8 * g);
+      for (int ks = 0; ks < C::KS; ++ks) af[mt][ks] = gather_afrag<A, B>(xr + ib, ks * 16 + 8 * g);
     }
   };
   // staged rows: chunk j of this thread is 16-byte chunk threadIdx.x + j * THREADS of the row;
@@ -183,7 +184,7 @@ had_quant_kron(RotQuantArgs args) {
       for (int ks = 0; ks < C::KS; ++ks) {
         v8h a_[C::MT];
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) a_[mt] = load_afrag<A>(lds_row + (mt * 32 + c) * A, ks * 16 + 8 * g);
+        for (int mt = 0; mt < C::MT; ++mt) a_[mt] = gather_afrag<A, B>(lds_row + mt * 32 + c, ks * 16 + 8 * g);
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -316,61 +317,85 @@ had_quant_kron(RotQuantArgs args) {
       args.beta[row] = __fmul_rn(mn, s_n);
     }
 
-    // ---- codes: one LDS byte each at output position i_b*A + j_a = lane base + constant
-    int lbase;  // lane-dependent part of i_b*A + j_a
+    // ---- codes, nibble-packed in registers, stored at output positions j_a * B + i_b
+    uint8_t* qrow = args.q + row * (C::K / 2);
+    auto code = [&](float v) { return rne_bits(__fmul_rn(__fsub_rn(v, mn), inv_u)) & 0xFu; };
     if constexpr (MW == 1) {
-      lbase = 4 * g * A + wn * C::NTW * 32 + c;
-    } else {
-      constexpr int TPU = 16 / C::SL;  // exchange slices per 16-register tile
-      static_assert(C::SL >= 4 && 16 % C::SL == 0, "slice layout");
-      const int u = wm * 2 + g;
-      lbase = ((u / TPU) * 32 + 8 * (u % TPU) * (C::SL / 4)) * A + c;
-    }
-    const bool real = (MW == 1) ? true : (c < A);
+      // lane (c, g) holds i_b = mt*32 + 8*q + 4*g + e (r = 4q + e) of column j_a: runs of 4
+      // positions; the partner lane half holds the other 4 of every 8, so after swapping
+      // 16-bit halves each lane half owns whole 16-byte runs (32 positions): half g stores
+      // the M tiles of parity g, and a wave's stores cover 1 KB contiguously.
 #pragma unroll
-    for (int i = 0; i < C::NV; ++i) {
-      int off, ja_hi;  // constant part of the offset; j_a - c for the padding test
-      if constexpr (MW == 1) {
-        const int mt = i / (16 * C::NTW);
-        const int nt = (i / 16) % C::NTW;
-        const int r = i % 16;
-        off = (mt * 32 + 8 * (r >> 2) + (r & 3)) * A + nt * 32;
-        ja_hi = (wn * C::NTW + nt) * 32;
-      } else {
-        const int t = i / (2 * MW);
-        const int s = (i / 2) % MW;
-        const int h = i % 2;
-        off = (s * C::MT * 32 + 8 * (t >> 2) + 4 * h + (t & 3)) * A;
-        ja_hi = 0;
+      for (int nt = 0; nt < C::NTW; ++nt) {
+        const int ja = (wn * C::NTW + nt) * 32 + c;
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+          uint32_t h16[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint32_t h = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float v = val[(mt * C::NTW + nt) * 16 + 4 * q + e];
+              h |= code(v) << (4 * e);
+              if constexpr (DBG) {
+                if (ja < A) args.dbg[row * C::K + ja * B + mt * 32 + 8 * q + 4 * g + e] = __fmul_rn(v, s_n);
+              }
+            }
+            h16[q] = h;
+          }
+          const uint32_t p01 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(h16[0] | (h16[1] << 16)), 32, 64));
+          const uint32_t p23 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(h16[2] | (h16[3] << 16)), 32, 64));
+          const uint32_t other[4] = {p01 & 0xFFFFu, p01 >> 16, p23 & 0xFFFFu, p23 >> 16};
+          uint32_t w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) w[q] = g ? (other[q] | (h16[q] << 16)) : (h16[q] | (other[q] << 16));
+          if ((mt & 1) == g && ja < A)
+            *reinterpret_cast<uint4*>(qrow + (ja * B + mt * 32) / 2) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
       }
-      if (real && ja_hi + c < A) {
-        const uint32_t q = rne_bits(__fmul_rn(__fsub_rn(val[i], mn), inv_u));
-        lds_code[lbase + off] = static_cast<uint8_t>(q);
-        if constexpr (DBG) args.dbg[row * C::K + lbase + off] = __fmul_rn(val[i], s_n);
+    } else {
+      // lane (c, u = 2*wm + g) holds, for every exchange slice s, the 2*SL consecutive
+      // positions ibase + s*MT*32 + 8*(t>>2) + 4*h + (t&3) <-> val[(t*MW + s)*2 + h]
+      constexpr int TPU = 16 / C::SL;  // exchange slices per 16-register tile
+      static_assert(C::SL == 4 || C::SL == 8 || C::SL == 16, "slice layout");
+      const int u = wm * 2 + g;
+      const int ibase = (u / TPU) * 32 + 8 * (u % TPU) * (C::SL / 4);
+#pragma unroll
+      for (int s = 0; s < MW; ++s) {
+        uint32_t w[C::SL / 4];
+#pragma unroll
+        for (int wi = 0; wi < C::SL / 4; ++wi) {
+          uint32_t x = 0;
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float v = val[((4 * wi + e) * MW + s) * 2 + h];
+              x |= code(v) << (4 * (4 * h + e));
+              if constexpr (DBG) {
+                if (c < A) args.dbg[row * C::K + c * B + ibase + s * C::MT * 32 + 8 * wi + 4 * h + e] = __fmul_rn(v, s_n);
+              }
+            }
+          w[wi] = x;
+        }
+        if (c < A) {
+          uint8_t* dst = qrow + (c * B + ibase + s * C::MT * 32) / 2;
+          if constexpr (C::SL == 4) {
+            *reinterpret_cast<uint32_t*>(dst) = w[0];
+          } else if constexpr (C::SL == 8) {
+            *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+          } else {
+            *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+          }
+        }
       }
     }
     if constexpr (STAGE) {
       if (next < rows) store_stage();  // every wave is past its last read of lds_row
     }
+    // the next row rewrites lds_red (and lds_row / lds_xch): all waves must be done with them
     __syncthreads();
-
-    // ---- pack 16 codes -> 8 bytes per thread, 8-byte stores
-    uint2* qrow = reinterpret_cast<uint2*>(args.q + row * (C::K / 2));
-    for (int i = threadIdx.x; i < C::K / 16; i += C::THREADS) {
-      const uint4 b = reinterpret_cast<const uint4*>(lds_code)[i];
-      const uint32_t w[4] = {b.x, b.y, b.z, b.w};
-      uint32_t o[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint32_t x0 = w[2 * h], x1 = w[2 * h + 1];
-        const uint32_t p0 = (x0 & 0xFu) | ((x0 >> 4) & 0xF0u) | ((x0 >> 8) & 0xF00u) | ((x0 >> 12) & 0xF000u);
-        const uint32_t p1 = (x1 & 0xFu) | ((x1 >> 4) & 0xF0u) | ((x1 >> 8) & 0xF00u) | ((x1 >> 12) & 0xF000u);
-        o[h] = p0 | (p1 << 16);
-      }
-      qrow[i] = make_uint2(o[0], o[1]);
-    }
-    // the next row's first LDS writes (exchange / reduction / codes) come after at
-    // least one more barrier, so no extra barrier is needed here
   }
 }
 

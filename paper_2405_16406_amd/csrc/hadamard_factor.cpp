@@ -1,7 +1,7 @@
 // Host construction of the library's dense +-1 Hadamard factors (orders 1, 28, 172).
 //
 // The online rotations R3/R4 of Sec. 3.1 are Hadamard matrices; for widths that are
-// not powers of two the rotation is S_b (x) H_a with a small dense factor H_a.  The
+// not powers of two the rotation is H_a (x) S_b with a small dense factor H_a.  The
 // paper does not say which Hadamard matrix of order 28 or 172; any one is valid.
 //   order 28 : Paley type II from the prime q = 13 (q = 1 mod 4):
 //              H = C (x) [[1,1],[1,-1]] + I (x) [[1,-1],[-1,-1]],

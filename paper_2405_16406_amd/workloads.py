@@ -53,7 +53,7 @@ def head_acts(rng: np.random.Generator, B: int, S: int, H: int, D: int, n_outlie
 class MLPShape:
     """One LLaMA MLP layer at M tokens: gate/up [inter, hidden], down [hidden, inter].
 
-    The down-projection input is rotated online by S_b (x) H_a with b = had_pow2,
+    The down-projection input is rotated online by H_a (x) S_b with b = had_pow2,
     a = had_dense (a * b == inter).
     """
     name: str

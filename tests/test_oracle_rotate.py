@@ -22,22 +22,22 @@ def test_reshape_form_equals_explicit_kronecker(a, b, blocks):
     x = rng.standard_normal((4, n * blocks))
     y = rotate.rotate_rows(x, ha, b)
     ha64 = np.ones((1, 1)) if ha is None else ha.astype(np.float64)
-    R = np.kron(hadamard.sylvester(b).astype(np.float64), ha64) / np.sqrt(n)
+    R = np.kron(ha64, hadamard.sylvester(b).astype(np.float64)) / np.sqrt(n)
     expect = np.concatenate([x[:, i * n:(i + 1) * n] @ R for i in range(blocks)], axis=1)
     np.testing.assert_allclose(y, expect, rtol=0, atol=1e-12)
 
 
 def test_reshape_index_convention_unit_vector():
-    # e_{i_b*a + i_a} maps to row (i_b, i_a) of S_b (x) H_a: y[j_b*a + j_a] = S[i_b,j_b] H[i_a,j_a]/sqrt(n)
+    # e_{i_a*b + i_b} maps to row (i_a, i_b) of H_a (x) S_b: y[j_a*b + j_b] = H[i_a,j_a] S[i_b,j_b]/sqrt(n)
     ha = hadamard.dense_factor(28)
     b = 4
     n = 28 * b
-    i_b, i_a = 2, 5
+    i_a, i_b = 5, 2
     x = np.zeros((1, n))
-    x[0, i_b * 28 + i_a] = 1.0
-    y = rotate.rotate_rows(x, ha, b)[0].reshape(b, 28)
+    x[0, i_a * b + i_b] = 1.0
+    y = rotate.rotate_rows(x, ha, b)[0].reshape(28, b)
     S = hadamard.sylvester(b).astype(np.float64)
-    expect = np.outer(S[i_b], ha[i_a].astype(np.float64)) / np.sqrt(n)
+    expect = np.outer(ha[i_a].astype(np.float64), S[i_b]) / np.sqrt(n)
     np.testing.assert_allclose(y, expect, rtol=0, atol=1e-15)
 
 
