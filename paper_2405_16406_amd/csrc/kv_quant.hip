@@ -1,10 +1,17 @@
 // R3 on post-RoPE Q and K (Sec. 3.1) fused with 4-bit asymmetric K/V cache quantization.
 //
-// One head vector (D = 128 fp16) is one quantization group.  Sixteen lanes own a
-// group, eight contiguous elements each (one 16-byte load per tensor).  The 128-point
-// Walsh-Hadamard transform is three in-register butterfly stages (element strides 1, 2,
-// 4) followed by four cross-lane stages (lane xor 1, 2, 4, 8); min/max use the same
-// 16-lane butterflies.  Each lane writes 8 codes as one 32-bit store.
+// One head vector (D = 128 fp16) is one quantization group.  Four lanes (a quad) own a
+// group; lane j of the quad holds the 32 elements i = 32*k + 8*j + e (k = 0..3, e = 0..7),
+// i.e. four 16-byte chunks, so each 16-byte load or store instruction of a wave covers
+// whole 64-byte lines (16 groups x 64 bytes).  The 128-point Walsh-Hadamard transform is
+// five in-register butterfly stages (index bits 0-2 and 5-6) and two cross-lane stages
+// (bits 3-4: quad lanes xor 1 and xor 2, by DPP quad permutes, no LDS); min/max reduce
+// in registers and then across the quad the same way.  Codes are made bytes by
+// v_cvt_pk_u8_f32, which rounds half to even like rint, and nibble-packed.
+//   V (the quantizer input itself): rint(fl(fl(v - mn) * fl(1/alpha))), eq. 1 step by step.
+//   K (rotated, 1/sqrt(128) folded into alpha and beta): rint(fma(v, 1/alpha, -mn/alpha));
+//     this can move a code by one only where the value sits on a rounding boundary, which
+//     the rotated path allows anyway.
 #include "sq_device.h"
 #include "sq_internal.h"
 
@@ -12,104 +19,144 @@ namespace sq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kLanesPerGroup = 16;
 constexpr int kD = 128;
 
-__device__ __forceinline__ void load8(const uint16_t* p, float (&e)[8]) {
-  const uint4 v = *reinterpret_cast<const uint4*>(p);
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    e[2 * i] = h2f(static_cast<uint16_t>(w[i] & 0xFFFFu));
-    e[2 * i + 1] = h2f(static_cast<uint16_t>(w[i] >> 16));
-  }
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+// value of the lane whose quad index is this lane's xor M (M = 1 or 2)
+template <int M>
+__device__ __forceinline__ float quad_xor(float v) {
+  constexpr int ctrl = (M == 1) ? 0xB1 : 0x4E;  // quad_perm [1,0,3,2] / [2,3,0,1]
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, false));
 }
 
-__device__ __forceinline__ void fwht128(float (&e)[8], int sl) {
+// e[8*k + q] = element 32*k + 8*j + q of the group (fp16 -> fp32, exact)
+__device__ __forceinline__ void load32(const uint16_t* __restrict__ grp_base, int j, float (&e)[32]) {
 #pragma unroll
-  for (int h = 1; h < 8; h <<= 1) {
+  for (int k = 0; k < 4; ++k) {
+    const v4u v = *reinterpret_cast<const v4u*>(grp_base + 32 * k + 8 * j);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if ((i & h) == 0) {
-        const float u = e[i], w = e[i + h];
-        e[i] = __fadd_rn(u, w);
-        e[i + h] = __fsub_rn(u, w);
-      }
-    }
-  }
-#pragma unroll
-  for (int m = 1; m < kLanesPerGroup; m <<= 1) {
-    const bool upper = (sl & m) != 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float p = __shfl_xor(e[i], m, kLanesPerGroup);
-      e[i] = upper ? __fsub_rn(p, e[i]) : __fadd_rn(e[i], p);
+    for (int i = 0; i < 4; ++i) {
+      e[8 * k + 2 * i] = h2f(static_cast<uint16_t>(v[i] & 0xFFFFu));
+      e[8 * k + 2 * i + 1] = h2f(static_cast<uint16_t>(v[i] >> 16));
     }
   }
 }
 
-__device__ __forceinline__ void quant_store(const float (&e)[8], int sl, int64_t grp, uint8_t* q,
+__device__ __forceinline__ void bfly(float& lo, float& hi) {
+  const float u = lo, w = hi;
+  lo = __fadd_rn(u, w);
+  hi = __fsub_rn(u, w);
+}
+
+// unscaled 128-point Sylvester transform of the group held by the quad
+__device__ __forceinline__ void fwht128(float (&e)[32], int j) {
+  // register index r = 8*k + q: bits 0-2 of r are element bits 0-2, bits 3-4 are bits 5-6
+#pragma unroll
+  for (int h = 1; h < 32; h <<= 1)
+#pragma unroll
+    for (int r = 0; r < 32; ++r)
+      if ((r & h) == 0) bfly(e[r], e[r + h]);
+  // element bits 3 and 4 live in the quad lane index: lower partner u + w, upper w - u
+  const float s1 = (j & 1) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int r = 0; r < 32; ++r) e[r] = __fmaf_rn(s1, e[r], quad_xor<1>(e[r]));
+  const float s2 = (j & 2) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int r = 0; r < 32; ++r) e[r] = __fmaf_rn(s2, e[r], quad_xor<2>(e[r]));
+}
+
+// eq. 1 asymmetric 4-bit codes of the quad's group; `scale` multiplies the reported alpha
+// and beta (1 when e holds the values themselves, and then the codes follow eq. 1 step
+// by step).  Element 32*k + 8*j + q -> byte 16*k + 4*j + q/2 of the group's 64 code bytes.
+template <bool EXACT>
+__device__ __forceinline__ void quant_store(const float (&e)[32], int j, float scale, int64_t grp, uint8_t* q,
                                             float* alpha, float* beta) {
   float mn = e[0], mx = e[0];
 #pragma unroll
-  for (int i = 1; i < 8; ++i) {
-    mn = fminf(mn, e[i]);
-    mx = fmaxf(mx, e[i]);
+  for (int r = 1; r < 32; ++r) {
+    mn = fminf(mn, e[r]);
+    mx = fmaxf(mx, e[r]);
   }
+  mn = fminf(mn, quad_xor<1>(mn));
+  mx = fmaxf(mx, quad_xor<1>(mx));
+  mn = fminf(mn, quad_xor<2>(mn));
+  mx = fmaxf(mx, quad_xor<2>(mx));
+  // alpha of the reported (scaled) values decides the constant-group case
+  const float r_u = __fsub_rn(mx, mn);
+  const float a_u = __fdiv_rn(r_u, 15.0f);
+  const bool cst = __fmul_rn(a_u, scale) < kMinNormal;
+  const float inv = cst ? 1.0f : __fdiv_rn(1.0f, a_u);
+  const float nb = -__fmul_rn(mn, inv);
+  uint8_t* qg = q + grp * (kD / 2);
 #pragma unroll
-  for (int m = 1; m < kLanesPerGroup; m <<= 1) {
-    mn = fminf(mn, __shfl_xor(mn, m, kLanesPerGroup));
-    mx = fmaxf(mx, __shfl_xor(mx, m, kLanesPerGroup));
+  for (int k = 0; k < 4; ++k) {
+    // bytes of the 8 codes q = 0..7, then even codes low nibble, odd codes high nibble
+    uint32_t ev = 0, od = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float t0, t1;
+      if constexpr (EXACT) {
+        t0 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i], mn), inv);
+        t1 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i + 1], mn), inv);
+      } else {
+        t0 = __fmaf_rn(e[8 * k + 2 * i], inv, nb);
+        t1 = __fmaf_rn(e[8 * k + 2 * i + 1], inv, nb);
+      }
+      ev = __builtin_amdgcn_cvt_pk_u8_f32(t0, i, ev);  // rounds half to even, clamps to [0, 255]
+      od = __builtin_amdgcn_cvt_pk_u8_f32(t1, i, od);
+    }
+    *reinterpret_cast<uint32_t*>(qg + 16 * k + 4 * j) = ev | (od << 4);
   }
-  const AsymParams p = asym_params(mn, mx);
-  uint32_t word = 0;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) word |= asym_code(e[i], p) << (4 * i);
-  *reinterpret_cast<uint32_t*>(q + grp * (kD / 2) + sl * 4) = word;
-  if (sl == 0) {
-    alpha[grp] = p.alpha;
-    beta[grp] = p.mn;
+  if (j == 0) {
+    alpha[grp] = cst ? 1.0f : __fmul_rn(a_u, scale);
+    beta[grp] = __fmul_rn(mn, scale);
   }
 }
 
 __global__ void __launch_bounds__(kThreads)
-qk_had_kvquant_v1(KvArgs a) {
-  const int64_t grp = (static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x) / kLanesPerGroup;
-  const int sl = threadIdx.x & (kLanesPerGroup - 1);
-  if (grp >= a.groups) return;  // all 16 lanes of a group leave together
-  const int64_t off = grp * kD + sl * 8;
-  float e[8];
+qk_had_kvquant_v2(KvArgs a) {
+  const int64_t grp = (static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x) / 4;
+  const int j = threadIdx.x & 3;
+  if (grp >= a.groups) return;  // the 4 lanes of a group leave together
+  const int64_t base = grp * kD;
+  float e[32];
 
-  load8(a.q + off, e);
-  fwht128(e, sl);
-  uint32_t packed[4];
+  // Q: rotate, scale, fp16
+  load32(a.q + base, j, e);
+  fwht128(e, j);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    packed[i] = static_cast<uint32_t>(f2h(__fmul_rn(e[2 * i], a.inv_sqrt_d))) |
-                (static_cast<uint32_t>(f2h(__fmul_rn(e[2 * i + 1], a.inv_sqrt_d))) << 16);
+  for (int k = 0; k < 4; ++k) {
+    v4u o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[i] = static_cast<uint32_t>(f2h(__fmul_rn(e[8 * k + 2 * i], a.inv_sqrt_d))) |
+             (static_cast<uint32_t>(f2h(__fmul_rn(e[8 * k + 2 * i + 1], a.inv_sqrt_d))) << 16);
+    *reinterpret_cast<v4u*>(a.q_rot + base + 32 * k + 8 * j) = o;
   }
-  *reinterpret_cast<uint4*>(a.q_rot + off) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
 
-  load8(a.k + off, e);
-  fwht128(e, sl);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) e[i] = __fmul_rn(e[i], a.inv_sqrt_d);
+  // K: rotate, quantize with the 1/sqrt(128) scale folded into alpha and beta
+  load32(a.k + base, j, e);
+  fwht128(e, j);
   if (a.dbg_k) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) a.dbg_k[off + i] = e[i];
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) a.dbg_k[base + 32 * k + 8 * j + q] = __fmul_rn(e[8 * k + q], a.inv_sqrt_d);
   }
-  quant_store(e, sl, grp, a.kq, a.ka, a.kb);
+  quant_store<false>(e, j, a.inv_sqrt_d, grp, a.kq, a.ka, a.kb);
 
-  load8(a.v + off, e);
-  quant_store(e, sl, grp, a.vq, a.va, a.vb);
+  // V: quantize
+  load32(a.v + base, j, e);
+  quant_store<true>(e, j, 1.0f, grp, a.vq, a.va, a.vb);
 }
 
 }  // namespace
 
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream) {
-  const int64_t threads = a.groups * kLanesPerGroup;
+  const int64_t threads = a.groups * 4;
   const unsigned blocks = static_cast<unsigned>((threads + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(qk_had_kvquant_v1, dim3(blocks), dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL(qk_had_kvquant_v2, dim3(blocks), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
