@@ -29,7 +29,9 @@
 #include "sq_device.h"
 #include "sq_internal.h"
 
+#include <cstdlib>
 #include <mutex>
+#include <utility>
 
 namespace sq {
 namespace {
@@ -63,6 +65,16 @@ struct Kron {
   static constexpr int RED_BYTES = 2 * W * 4;
   static constexpr int LDS = ROW_BYTES + XCH_BYTES + RED_BYTES;
 };
+
+// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1 (compile-time indices).
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 __device__ __forceinline__ void bfly(float& lo, float& hi) {
   const float u = lo, w = hi;
@@ -399,6 +411,271 @@ had_quant_kron(RotQuantArgs args) {
   }
 }
 
+// ---------------------------------------------------------------- row-pair kernel
+// Rows whose dense factor needs several N tiles (a = 172: 6 tiles of 32 j_a).  Two waves
+// share a row, each taking NT/2 of the N tiles, so a wave holds only its share of the
+// rotated row; a workgroup of 8 waves (two per SIMD) works on 4 rows at a time, one LDS
+// slot per row, one workgroup per CU.
+//   * the B fragments of H_a (fp16 +-1) sit in LDS, built once per workgroup;
+//   * the next rows are loaded with 16-byte loads into registers while the current rows
+//     are transformed, and written to their slots once both waves of a row have read it;
+//   * A fragments are gathered from the slot one k-step ahead of their MFMAs;
+//   * Sylvester stages as in the kernel above; per-row min/max (the two waves of a row
+//     meet in LDS); codes use one fma per value and v_cvt_pk_u8_f32 (round half to even),
+//     which can move a code by one only on a rounding boundary.
+template <int A, int APAD, int NT, int B>
+struct Pair {
+  static constexpr int K = A * B;
+  static constexpr int KS = APAD / 16;  // k-steps of the dense stage
+  static constexpr int MT = B / 32;     // M tiles (32 i_b each)
+  static constexpr int NTW = NT / 2;    // N tiles per wave
+  static constexpr int ROWS = 4;        // rows per workgroup iteration
+  static constexpr int THREADS = 64 * 2 * ROWS;
+  static constexpr int CHUNKS = K / 8;                   // 16-byte chunks of a row
+  static constexpr int PF = (CHUNKS + 127) / 128;        // chunks per lane of the wave pair
+  static constexpr int HFRAG = KS * NT * 64;             // 16-byte B fragments
+  static constexpr int SLOT = K * 2;                     // bytes of one staged row
+  static constexpr int RAW = (A * A + 15) / 16 * 16;     // int8 H staging (aliases the slots)
+  static constexpr int RED = 2 * ROWS * 2 * 2;           // floats: [parity][row][wave][min,max]
+  static constexpr int LDS = HFRAG * 16 + ROWS * SLOT + RED * 4;
+  static_assert(NT % 2 == 0 && MT == 2, "two waves per row, two M tiles");
+  static_assert(APAD % 16 == 0 && APAD >= A && NT * 32 >= A, "padding");
+  static_assert(A % 4 == 0 && (A * A) % 16 == 0 && K % 8 == 0, "16-byte staging");
+  static_assert(RAW <= ROWS * SLOT, "H staging fits in the row slots");
+};
+
+template <int A, int APAD, int NT, int B, bool DBG>
+__global__ void __launch_bounds__(512, 2)
+had_quant_pair(RotQuantArgs args) {
+  using C = Pair<A, APAD, NT, B>;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  v8h* hf = reinterpret_cast<v8h*>(smem);
+  unsigned char* slots = smem + C::HFRAG * 16;
+  float* red = reinterpret_cast<float*>(smem + C::HFRAG * 16 + C::ROWS * C::SLOT);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int p = wave >> 1;  // row slot
+  const int h = wave & 1;   // which half of the N tiles
+  const int g = lane >> 5;
+  const int c = lane & 31;
+  const int pl = h * 64 + lane;  // lane index within the wave pair (row staging)
+  const int64_t rows = args.rows;
+  const int64_t nsets = (rows + C::ROWS - 1) / C::ROWS;
+  int64_t rs = blockIdx.x;
+  if (rs >= nsets) return;  // uniform over the workgroup
+
+  // ---- H_a as MFMA B fragments: hf[(ks*NT + nt)*64 + l][e] = H[k][n],
+  //      k = ks*16 + 8*(l/32) + e, n = nt*32 + l%32 (zero outside A x A); H is staged
+  //      in the (not yet used) row slots
+  int8_t* hraw = reinterpret_cast<int8_t*>(slots);
+  for (int i = threadIdx.x; i < A * A / 16; i += C::THREADS)
+    reinterpret_cast<v4u*>(hraw)[i] = reinterpret_cast<const v4u*>(args.H)[i];
+  __syncthreads();
+  for (int i = threadIdx.x; i < C::HFRAG; i += C::THREADS) {
+    const int l = i & 63;
+    const int t = i >> 6;
+    const int nt = t % NT;
+    const int ks = t / NT;
+    const int n = nt * 32 + (l & 31);
+    v8h f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = ks * 16 + 8 * (l >> 5) + e;
+      f[e] = (k < A && n < A) ? static_cast<_Float16>(hraw[k * A + n]) : static_cast<_Float16>(0.0f);
+    }
+    hf[i] = f;
+  }
+  __syncthreads();
+
+  // ---- row staging: the wave pair loads chunk pl + 128 j of its row (16 bytes each)
+  unsigned char* slot = slots + p * C::SLOT;
+  v4u pf[C::PF];
+  auto load_row = [&](int64_t r) {
+    const v4u* xr = reinterpret_cast<const v4u*>(args.x + r * args.ldx);
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = pl + 128 * j;
+      pf[j] = xr[i < C::CHUNKS ? i : C::CHUNKS - 1];
+    }
+  };
+  auto store_row = [&]() {
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = pl + 128 * j;
+      if (i < C::CHUNKS) reinterpret_cast<v4u*>(slot)[i] = pf[j];
+    }
+  };
+  {
+    const int64_t r0 = rs * C::ROWS + p;
+    load_row(r0 < rows ? r0 : rows - 1);
+    store_row();
+  }
+  __syncthreads();
+
+  // A fragment (M tile mt, k-step ks) from the slot: X2[k][i_b], k = ks*16 + 8g + e,
+  // i_b = mt*32 + c; zero for k >= A
+  const uint16_t* srow = reinterpret_cast<const uint16_t*>(slot) + c;
+  auto frag = [&](int mt, int ks) { return gather_afrag<A, B>(srow + mt * 32, ks * 16 + 8 * g); };
+
+  const float s_n = args.inv_sqrt_n;
+  for (int it = 0; rs < nsets; ++it, rs += gridDim.x) {
+    const int64_t row = rs * C::ROWS + p;
+    const bool valid = row < rows;
+    const bool more = rs + gridDim.x < nsets;
+    if (more) {  // next rows: in flight during this iteration
+      const int64_t nr = (rs + gridDim.x) * C::ROWS + p;
+      load_row(nr < rows ? nr : rows - 1);
+    }
+
+    // ---- dense stage: acc[mt][nt] = X2^T H_a for i_b tile mt, j_a tile h*NTW + nt
+    v16f acc[C::MT][C::NTW];
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][nt][r] = 0.0f;
+    v8h a0[C::MT], a1[C::MT];
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) a0[mt] = frag(mt, 0);
+    static_for<C::KS>([&](auto kc) {
+      constexpr int ks = decltype(kc)::value;
+      v8h(&cur)[C::MT] = (ks & 1) ? a1 : a0;
+      v8h(&nxt)[C::MT] = (ks & 1) ? a0 : a1;
+      if constexpr (ks + 1 < C::KS) {
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) nxt[mt] = frag(mt, ks + 1);
+      }
+      v8h bf[C::NTW];
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < C::NTW; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[mt], bf[nt], acc[mt][nt], 0, 0, 0);
+    });
+
+    // ---- Sylvester stages over i_b: register bits 0, 1, 3, 4; M tile bit 5; lane half bit 2
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+        for (int rb = 1; rb < 16; rb <<= 1)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if ((r & rb) == 0) {
+              float lo = acc[mt][nt][r], hi = acc[mt][nt][r + rb];
+              bfly(lo, hi);
+              acc[mt][nt][r] = lo;
+              acc[mt][nt][r + rb] = hi;
+            }
+#pragma unroll
+    for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float lo = acc[0][nt][r], hi = acc[1][nt][r];
+        bfly(lo, hi);
+        acc[0][nt][r] = lo;
+        acc[1][nt][r] = hi;
+      }
+    const float sg = g ? -1.0f : 1.0f;
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float v = acc[mt][nt][r];
+          acc[mt][nt][r] = __fmaf_rn(sg, v, __shfl_xor(v, 32, 64));
+        }
+
+    // ---- per-row min/max over real columns; the two waves of the row meet in LDS
+    float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+    for (int nt = 0; nt < C::NTW; ++nt) {
+      if ((h * C::NTW + nt) * 32 + c < A) {
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            mn = fminf(mn, acc[mt][nt][r]);
+            mx = fmaxf(mx, acc[mt][nt][r]);
+          }
+      }
+    }
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    float* rd = red + (it & 1) * (C::ROWS * 4);  // parity buffers
+    if (lane == 0) {
+      rd[(p * 2 + h) * 2] = mn;
+      rd[(p * 2 + h) * 2 + 1] = mx;
+    }
+    __syncthreads();  // also: both waves of every row are done reading its slot
+    mn = fminf(rd[p * 4], rd[p * 4 + 2]);
+    mx = fmaxf(rd[p * 4 + 1], rd[p * 4 + 3]);
+    if (more) store_row();
+
+    // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
+    const float r_u = __fsub_rn(mx, mn);
+    const float a_u = __fdiv_rn(r_u, 15.0f);
+    const bool cst = __fmul_rn(a_u, s_n) < kMinNormal;
+    const float inv_u = cst ? 0.0f : __fdiv_rn(1.0f, a_u);
+    const float nb = -__fmul_rn(mn, inv_u);
+    if (valid && h == 0 && lane == 0) {
+      args.alpha[row] = cst ? 1.0f : __fmul_rn(a_u, s_n);
+      args.beta[row] = __fmul_rn(mn, s_n);
+    }
+
+    // ---- codes: lane (c, g) holds i_b = mt*32 + 8*q + 4*g + e (r = 4q + e) of column j_a.
+    // Bytes via v_cvt_pk_u8_f32 (codes of e = 0, 2 in ev, e = 1, 3 in od, two q per dword),
+    // then ev | od << 4 is the 16-bit nibble run of q (low) and q + 1 (high); the partner
+    // lane half holds the other 4 positions of every 8, so swapping dwords and selecting
+    // bytes gives whole 32-bit words; half g stores M tile g (16 bytes, a wave 1 KB).
+    uint8_t* qrow = args.q + row * (C::K / 2);
+    const uint32_t sel0 = g ? 0x01000504u : 0x05040100u;
+    const uint32_t sel1 = g ? 0x03020706u : 0x07060302u;
+#pragma unroll
+    for (int nt = 0; nt < C::NTW; ++nt) {
+      const int ja = (h * C::NTW + nt) * 32 + c;
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt) {
+        uint32_t m2[2];
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq) {
+          uint32_t ev = 0, od = 0;
+#pragma unroll
+          for (int s = 0; s < 2; ++s) {
+            const int r0 = 4 * (2 * qq + s);
+            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0], inv_u, nb), 2 * s, ev);
+            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 2], inv_u, nb), 2 * s + 1, ev);
+            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 1], inv_u, nb), 2 * s, od);
+            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 3], inv_u, nb), 2 * s + 1, od);
+          }
+          m2[qq] = ev | (od << 4);
+        }
+        const uint32_t p0 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m2[0]), 32, 64));
+        const uint32_t p1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m2[1]), 32, 64));
+        const uint32_t w0 = __builtin_amdgcn_perm(p0, m2[0], sel0);
+        const uint32_t w1 = __builtin_amdgcn_perm(p0, m2[0], sel1);
+        const uint32_t w2 = __builtin_amdgcn_perm(p1, m2[1], sel0);
+        const uint32_t w3 = __builtin_amdgcn_perm(p1, m2[1], sel1);
+        if (valid && mt == g && ja < A)
+          *reinterpret_cast<uint4*>(qrow + (ja * B + mt * 32) / 2) = make_uint4(w0, w1, w2, w3);
+        if constexpr (DBG) {
+          if (valid && ja < A) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              args.dbg[row * C::K + ja * B + mt * 32 + 8 * (r >> 2) + 4 * g + (r & 3)] = __fmul_rn(acc[mt][nt][r], s_n);
+          }
+        }
+      }
+    }
+    __syncthreads();  // the slots hold the next rows for every wave
+  }
+}
+
 int g_num_cu = 0;
 std::once_flag g_cu_once;
 
@@ -438,13 +715,38 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
                : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
 }
 
+template <int A, int APAD, int NT, int B, bool DBG>
+hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
+  using C = Pair<A, APAD, NT, B>;
+  auto kern = had_quant_pair<A, APAD, NT, B, DBG>;
+  static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (init != hipSuccess) return init;
+  const int64_t sets = (a.rows + C::ROWS - 1) / C::ROWS;
+  const int64_t cap = num_cus();
+  const unsigned grid = static_cast<unsigned>(sets < cap ? sets : cap);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
+  return hipGetLastError();
+}
+
+template <int A, int APAD, int NT, int B>
+hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
+  return a.dbg ? launch_pair_t<A, APAD, NT, B, true>(a, stream) : launch_pair_t<A, APAD, NT, B, false>(a, stream);
+}
+
 }  // namespace
 
 // Returns hipErrorNotSupported when no fast path covers the arguments.
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
   if (a.a == 28 && a.b == 512) return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
-  if (a.a == 172 && a.b == 64) return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
+  if (a.a == 172 && a.b == 64) {
+    // the pair kernel stages H and the rows in 16-byte chunks
+    const bool fits = (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
+                      (a.ldx % 8) == 0;
+    if (!fits || getenv("SQ_KRON_STAGED")) return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
+    return launch_pair<172, 176, 6, 64>(a, stream);
+  }
   if (a.a == 28 && a.b == 1024) return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
   return hipErrorNotSupported;
 }

@@ -126,6 +126,33 @@ def test_llama2_70b_decode_act():
         check_act(inp["x_down"], 28, 1024)
 
 
+@pytest.mark.parametrize("M", [1, 7, 1027])
+def test_kron172_partial_row_sets(M):
+    say(f"had_quant_act H172 (x) S64, M={M}: rows in sets of 4, last set partial")
+    x = workloads.outlier_acts(workloads.rng_for(900 + M), M, 172 * 64, 110, 50.0)
+    check_act(x, 172, 64)
+
+
+def test_kron172_strided_input_nan_padding():
+    say("had_quant_act H172 (x) S64 on a strided input whose row padding is NaN")
+    M, K = 9, 172 * 64
+    x = workloads.outlier_acts(workloads.rng_for(77), M, K, 110, 50.0)
+    wide = np.full((M, K + 96), np.nan, dtype=np.float16)
+    wide[:, :K] = x
+    h = had_table(172)
+    r1 = [host(v) for v in sq.had_quant_act(dev(wide)[:, :K], h, 64)[:3]]
+    r2 = [host(v) for v in sq.had_quant_act(dev(x), h, 64)[:3]]
+    for u, v in zip(r1, r2):
+        np.testing.assert_array_equal(u, v)
+
+
+def test_kron172_staged_kernel(monkeypatch):
+    say("had_quant_act H172 (x) S64 through the LDS-staged kernel")
+    monkeypatch.setenv("SQ_KRON_STAGED", "1")
+    x = workloads.outlier_acts(workloads.rng_for(31), 37, 172 * 64, 110, 50.0)
+    check_act(x, 172, 64)
+
+
 @pytest.mark.parametrize("a,b,M", [(28, 512, 33), (172, 64, 21), (28, 1024, 5)])
 def test_debug_output_does_not_change_results(a, b, M):
     say(f"had_quant_act with and without dbg_rot a={a} b={b} M={M}")
