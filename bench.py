@@ -4,12 +4,15 @@ One step = one pass of the whole path over one LLaMA-2-7B transformer layer's wo
 tokens (M = 2048):
   1. R3 + 4-bit KV quantization of Q, K, V [1, 2048, 32, 128]          sq_qk_had_kvquant
   2. per-token 4-bit quantization of the MLP input [2048, 4096]          sq_had_quant_act (identity)
-  3. gate and up projections [2048x4096] x [11008x4096]^T                sq_w4a4_linear x2
+  3. gate and up projections as one launch against the two packed weights
+     stacked: [2048x4096] x [22016x4096]^T                               sq_w4a4_linear
   4. online R4 (H_172 (x) S_64) + 4-bit quantization of the down-projection
      input [2048, 11008]                                                 sq_had_quant_act
   5. down projection [2048x11008] x [4096x11008]^T                       sq_w4a4_linear
 Weights are packed once beforehand (sq_pack_w4, R4 folded into W_down), as in
-deployment.  Inputs are synthetic (seeded, LLaMA-shaped, with outlier channels) and
+deployment; gate and up share the input, so their packed weights are stacked into one
+[22016, 4096] matrix (packing is per output row, so this changes no code) and run as one
+GEMM launch.  Inputs are synthetic (seeded, LLaMA-shaped, with outlier channels) and
 already resident in HBM; three input/weight sets are rotated so that consecutive steps
 do not hit the 256 MB Infinity Cache.
 
@@ -242,10 +245,9 @@ def main():
         inp = workloads.mlp_inputs(sh)
         rng = workloads.rng_for(500 + s)
         qkv = [up(workloads.head_acts(rng, 1, M, NH, HD, 2, 30.0)) for _ in range(3)]
-        wg = sq.pack_w4(up(inp["w_gate"]))
-        wu = sq.pack_w4(up(inp["w_up"]))
+        wgu = sq.pack_w4(up(np.concatenate([inp["w_gate"], inp["w_up"]])))  # stacked gate/up rows
         wd = sq.pack_w4(up(inp["w_down"]), had, B)
-        sets.append(dict(x_in=up(inp["x_in"]), x_down=up(inp["x_down"]), qkv=qkv, wg=wg, wu=wu, wd=wd))
+        sets.append(dict(x_in=up(inp["x_in"]), x_down=up(inp["x_down"]), qkv=qkv, wgu=wgu, wd=wd))
     torch.cuda.synchronize()
 
     # ---- outputs (shared by all sets)
@@ -262,19 +264,17 @@ def main():
     xq_dn = (torch.empty((M, INTER // 2), dtype=torch.uint8, device=dev),
              torch.empty((M, 1), dtype=torch.float32, device=dev),
              torch.empty((M, 1), dtype=torch.float32, device=dev))
-    y_gate = torch.empty((M, INTER), dtype=torch.float16, device=dev)
-    y_up = torch.empty((M, INTER), dtype=torch.float16, device=dev)
+    y_gu = torch.empty((M, 2 * INTER), dtype=torch.float16, device=dev)  # [gate | up]
     y_dn = torch.empty((M, HID), dtype=torch.float16, device=dev)
 
-    names = ["kv_quant", "act_quant", "gate_gemm", "up_gemm", "r4_had_quant", "down_gemm"]
+    names = ["kv_quant", "act_quant", "gate_up_gemm", "r4_had_quant", "down_gemm"]
 
     def step(s, ev=None):
         d = sets[s]
         calls = [
             lambda: sq.qk_had_kvquant(*d["qkv"], out=kv_out),
             lambda: sq.had_quant_act(d["x_in"], out=xq_in),
-            lambda: sq.w4a4_linear(*xq_in, *d["wg"], out=y_gate),
-            lambda: sq.w4a4_linear(*xq_in, *d["wu"], out=y_up),
+            lambda: sq.w4a4_linear(*xq_in, *d["wgu"], out=y_gu),
             lambda: sq.had_quant_act(d["x_down"], had, B, out=xq_dn),
             lambda: sq.w4a4_linear(*xq_dn, *d["wd"], out=y_dn),
         ]
@@ -309,16 +309,17 @@ def main():
     gemm_ops = 2 * M * INTER * HID
     step_ops = 3 * gemm_ops
     value = step_ops / (ms_step * 1e-3) / 1e12
-    gemm_ms = np.mean([per["gate_gemm"], per["up_gemm"], per["down_gemm"]])
-    gemm_tops = gemm_ops / (gemm_ms * 1e-3) / 1e12
+    # the two GEMM launches of a step: gate+up (2 x gemm_ops) and down (gemm_ops)
+    gemm_ms = per["gate_up_gemm"] + per["down_gemm"]
+    gemm_tops = step_ops / (gemm_ms * 1e-3) / 1e12
     E = M * NH * HD
     kernels = {
         "kv_quant": dict(ms=per["kv_quant"], GBps=kv_bytes(E) / (per["kv_quant"] * 1e-3) / 1e9),
         "act_quant": dict(ms=per["act_quant"], GBps=had_bytes(M, HID) / (per["act_quant"] * 1e-3) / 1e9),
         "r4_had_quant": dict(ms=per["r4_had_quant"], GBps=had_bytes(M, INTER) / (per["r4_had_quant"] * 1e-3) / 1e9),
     }
-    for n in ("gate_gemm", "up_gemm", "down_gemm"):
-        kernels[n] = dict(ms=per[n], TOPS=gemm_ops / (per[n] * 1e-3) / 1e12)
+    kernels["gate_up_gemm"] = dict(ms=per["gate_up_gemm"], TOPS=2 * gemm_ops / (per["gate_up_gemm"] * 1e-3) / 1e12)
+    kernels["down_gemm"] = dict(ms=per["down_gemm"], TOPS=gemm_ops / (per["down_gemm"] * 1e-3) / 1e12)
     for k_ in kernels.values():
         for f in list(k_):
             k_[f] = round(k_[f], 4)
@@ -337,15 +338,16 @@ def main():
         "dtype": "i8",
         "data": "synthetic",
         "config": {"workload": "LLaMA-2-7B layer, M=2048 tokens: R3+KV4 quant [1,2048,32,128]; "
-                               "act quant [2048,4096]; gate/up W4A4 [2048x4096]x[11008x4096]; "
+                               "act quant [2048,4096]; gate+up W4A4 [2048x4096]x[22016x4096] (stacked); "
                                "R4 H_172(x)S_64 + quant [2048,11008]; down W4A4 [2048x11008]x[4096x11008]",
                    "tokens": M, "hidden": HID, "intermediate": INTER, "heads": NH, "head_dim": HD,
                    "r4": f"H_{A} (x) S_{B}", "buffer_sets": args.sets},
+        # w4a4_gemm: the step's two launches (gate+up, down); achieved = their ops / their time
         "roofline": {"kernel": "w4a4_gemm", "bound": "mfma", "achieved": round(gemm_tops, 2),
                      "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
                      "traffic": measured_traffic(),
-                     "ops_per_launch": gemm_ops,
-                     "algorithmic_bytes_per_launch": round((2 * gemm_bytes(M, INTER, HID) + gemm_bytes(M, HID, INTER)) / 3)},
+                     "ops_per_launch": step_ops // 2,
+                     "algorithmic_bytes_per_launch": round((gemm_bytes(M, 2 * INTER, HID) + gemm_bytes(M, HID, INTER)) / 2)},
         "kernels": kernels,
         "wall_s": round(wall, 3),
     }
@@ -429,6 +431,7 @@ def kernel_report(torch, sq, workloads, dev):
         had = up(sq.hadamard_factor(sh.had_dense))
         xin, xdn = up(inp["x_in"]), up(inp["x_down"])
         wg = sq.pack_w4(up(inp["w_gate"]))
+        wgu = sq.pack_w4(up(np.concatenate([inp["w_gate"], inp["w_up"]])))
         wd = sq.pack_w4(up(inp["w_down"]), had, sh.had_pow2)
         qi = sq.had_quant_act(xin)[:3]
         qd = sq.had_quant_act(xdn, had, sh.had_pow2)[:3]
@@ -436,15 +439,18 @@ def kernel_report(torch, sq, workloads, dev):
         t_aq = timed(lambda: sq.had_quant_act(xin, out=qi))
         t_hq = timed(lambda: sq.had_quant_act(xdn, had, sh.had_pow2, out=qd))
         t_g = timed(lambda: sq.w4a4_linear(*qi, *wg))
+        t_gu = timed(lambda: sq.w4a4_linear(*qi, *wgu))
         t_d = timed(lambda: sq.w4a4_linear(*qd, *wd))
         rep.append(dict(config=sh.name,
                         act_quant=dict(ms=t_aq, GBps=had_bytes(M, sh.hidden) / t_aq / 1e6),
                         r4_had_quant=dict(ms=t_hq, GBps=had_bytes(M, sh.inter) / t_hq / 1e6),
                         gate_gemm=dict(ms=t_g, TOPS=2 * M * sh.inter * sh.hidden / t_g / 1e9,
                                        GBps=gemm_bytes(M, sh.inter, sh.hidden) / t_g / 1e6),
+                        gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * sh.inter * sh.hidden / t_gu / 1e9,
+                                          GBps=gemm_bytes(M, 2 * sh.inter, sh.hidden) / t_gu / 1e6),
                         down_gemm=dict(ms=t_d, TOPS=2 * M * sh.inter * sh.hidden / t_d / 1e9,
                                        GBps=gemm_bytes(M, sh.hidden, sh.inter) / t_d / 1e6)))
-        del inp, xin, xdn, wg, wd, qi, qd
+        del inp, xin, xdn, wg, wgu, wd, qi, qd
         torch.cuda.empty_cache()
     q, k, v = (up(t) for t in workloads.kv_inputs())
     o = sq.qk_had_kvquant(q, k, v)

@@ -30,6 +30,7 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ v4i expand_act(uint2 d) {
   v4i r;
@@ -153,6 +154,79 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const v16i (&ac
       }
     });
   });
+}
+
+// The same epilogue through LDS: the wave converts its TM x TN blocks to fp16 into its own
+// LDS region (row-major, padded pitch: the two lane halves hit different banks), then reads
+// 16 bytes (8 columns of one row) per lane and stores them, so each store instruction
+// writes whole 128-byte row segments instead of 4-byte pairs.  Needs 16-byte aligned
+// output rows (ldy % 8 == 0, y 16-byte aligned); columns past N are stored one by one.
+template <int TM, int TN>
+struct EpiStage {
+  static constexpr int PITCH = TN * 32 + 8;  // fp16 elements per staged row
+  static constexpr int BYTES = TM * 32 * PITCH * 2;
+};
+
+template <int TM, int TN>
+__device__ __forceinline__ void tile_epilogue_lds(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
+                                                  int lane, uint16_t* __restrict__ stage) {
+  constexpr int PITCH = EpiStage<TM, TN>::PITCH;
+  const int c = lane & 31;
+  const int gh = lane >> 5;
+  float csn[TN], cwr[TN], cbn[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int64_t n = nw + j * 32 + c;
+    const int64_t nc = n < g.N ? n : g.N - 1;
+    csn[j] = g.wa[nc];
+    cwr[j] = __fmul_rn(csn[j], static_cast<float>(g.rs[nc]));
+    cbn[j] = g.bias ? h2f(g.bias[nc]) : 0.0f;
+  }
+  static_for<TM>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    const int64_t mb = mw + i * 32 + 4 * gh;
+    float ra_[16], rb_[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t m = mb + 8 * (r >> 2) + (r & 3);
+      const int64_t mc = m < g.M ? m : g.M - 1;
+      ra_[r] = g.xa[mc];
+      rb_[r] = g.xb[mc];
+    }
+    static_for<TN>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int a = acc[i][j][r] >> 4;
+        float yv = __fmaf_rn(__fmul_rn(ra_[r], csn[j]), static_cast<float>(a), __fmul_rn(rb_[r], cwr[j]));
+        if (g.bias) yv = __fadd_rn(yv, cbn[j]);
+        const int row = i * 32 + 8 * (r >> 2) + 4 * gh + (r & 3);
+        stage[row * PITCH + j * 32 + c] = static_cast<uint16_t>(f2h(yv));
+      }
+    });
+  });
+  // each row of the wave's block is TN * 4 chunks of 8 columns
+  constexpr int CPR = TN * 4;
+  constexpr int ITER = TM * 32 * CPR / 64;
+#pragma unroll
+  for (int t = 0; t < ITER; ++t) {
+    const int idx = t * 64 + lane;
+    const int row = idx / CPR;
+    const int ch = idx % CPR;
+    const v4u v = *reinterpret_cast<const v4u*>(stage + row * PITCH + ch * 8);
+    const int64_t m = mw + row;
+    const int64_t n = nw + ch * 8;
+    if (m < g.M) {
+      uint16_t* dst = g.y + m * g.ldy + n;
+      if (n + 8 <= g.N) {
+        *reinterpret_cast<v4u*>(dst) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (n + e < g.N) dst[e] = static_cast<uint16_t>((v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ prefill tile kernel
@@ -317,8 +391,6 @@ w4a4_gemm_tile(GemmArgs g) {
 // which expand into the operands of two MFMA k-steps.  Both operands use the same k-slot
 // order, so the dot product is unchanged.  Rows past M or N and chunks past K are out of the
 // buffer range and land as zeros.
-typedef unsigned v4u __attribute__((ext_vector_type(4)));
-
 template <int WAVES_M, int WAVES_N, int TM, int TN, int NS>
 struct Ring {
   static constexpr int WAVES = WAVES_M * WAVES_N;
@@ -330,7 +402,8 @@ struct Ring {
   static constexpr int ADPW = ABLK / WAVES;  // block copies per wave per stage
   static constexpr int DPW = (ABLK + BBLK) / WAVES;
   static constexpr int STAGE = (ABLK + BBLK) * 1024;
-  static constexpr int LDS = NS * STAGE;
+  static constexpr int EPI = WAVES * EpiStage<TM, TN>::BYTES;  // epilogue staging reuses the ring
+  static constexpr int LDS = NS * STAGE > EPI ? NS * STAGE : EPI;
   static_assert(ADPW * WAVES == ABLK && DPW * WAVES == ABLK + BBLK, "blocks split evenly over waves");
   static_assert(NS >= 2 && (NS - 1) * DPW <= 63, "outstanding copies fit the vmcnt counter");
 };
@@ -497,7 +570,15 @@ w4a4_gemm_ring(GemmArgs g) {
   wait_vm_lgkm0<0>();
   asm volatile("" ::: "memory");
 
-  tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
+  const bool vec = ((g.ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && (g.dbg_acc == nullptr);
+  if (vec) {
+    __builtin_amdgcn_s_barrier();  // every wave is done with the ring; each now stages its own block
+    asm volatile("" ::: "memory");
+    uint16_t* stage = reinterpret_cast<uint16_t*>(lds + wave * EpiStage<TM, TN>::BYTES);
+    tile_epilogue_lds(g, acc, m0 + wm * 32, n0 + wn * 32, lane, stage);
+  } else {
+    tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
+  }
 }
 
 template <int WM, int WN, int TM, int TN, int NS>

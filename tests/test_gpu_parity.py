@@ -213,6 +213,17 @@ def test_pack_w4_tiny_and_kronecker():
     assert check_w(z, 1, 1) == 0
 
 
+def test_pack_w4_stacked_rows_equal_separate():
+    say("pack_w4 of stacked gate/up rows equals the two packs stacked")
+    rng = workloads.rng_for(12)
+    w1, w2 = workloads.weights(rng, 64, 512), workloads.weights(rng, 40, 512)
+    both = [host(t) for t in sq.pack_w4(dev(np.concatenate([w1, w2])))]
+    a = [host(t) for t in sq.pack_w4(dev(w1))]
+    b = [host(t) for t in sq.pack_w4(dev(w2))]
+    for u, x, y in zip(both, a, b):
+        np.testing.assert_array_equal(u, np.concatenate([x, y]))
+
+
 def test_pack_w4_llama2_7b_down_full():
     say("pack_w4 LLaMA-2-7B down [4096,11008] folded with H172xH64")
     w = workloads.mlp_inputs(workloads.LLAMA2_7B_MLP, rows=1)["w_down"]
@@ -375,3 +386,8 @@ def test_gemm_tile_variants(variant, monkeypatch):
         sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: unpaired stores
         np.testing.assert_array_equal(host(wide[:, :N]), host(y_dbg))
         assert not host(wide[:, N:]).any()
+        w8 = (N + 1 + 7) // 8 * 8                              # ldy % 8 == 0: 16-byte row stores,
+        wide8 = torch.zeros((M, w8), dtype=torch.float16, device=DEV)   # column tail one by one
+        sq.w4a4_linear(*args, out=wide8[:, :N])
+        np.testing.assert_array_equal(host(wide8[:, :N]), host(y_dbg))
+        assert not host(wide8[:, N:]).any()
