@@ -412,42 +412,47 @@ had_quant_kron(RotQuantArgs args) {
 }
 
 // ---------------------------------------------------------------- row-pair kernel
-// Rows whose dense factor needs several N tiles (a = 172: 6 tiles of 32 j_a).  Two waves
-// share a row, each taking NT/2 of the N tiles, so a wave holds only its share of the
-// rotated row; a workgroup of 8 waves (two per SIMD) works on 4 rows at a time, one LDS
-// slot per row, one workgroup per CU.
-//   * the B fragments of H_a (fp16 +-1) sit in LDS, built once per workgroup;
+// Two waves share a row; a workgroup of 8 waves (two per SIMD) works on 4 rows at a
+// time, one LDS slot per row, one workgroup per CU.
+//   * Fold F: the top log2(F) bits of i_b join the dense factor, D = H_a (x) S_F acting on
+//     (i_a, i_b_hi), so the Sylvester part left is S_{B/F} over i_b_lo and a wave's share
+//     of the row fits in its registers (F = 2 for H_28 (x) S_512).  The MFMA N tiles are
+//     the columns of D (NT of them, NT/F per value of j_b_hi); each wave of the pair takes
+//     NT/2 of them, so neither wave needs the other's values.
+//   * the B fragments of D (fp16 +-1) sit in LDS, built once per workgroup;
 //   * the next rows are loaded with 16-byte loads into registers while the current rows
 //     are transformed, and written to their slots once both waves of a row have read it;
-//   * A fragments are gathered from the slot one k-step ahead of their MFMAs;
-//   * Sylvester stages as in the kernel above; per-row min/max (the two waves of a row
-//     meet in LDS); codes use one fma per value and v_cvt_pk_u8_f32 (round half to even),
-//     which can move a code by one only on a rounding boundary.
-template <int A, int APAD, int NT, int B>
+//   * A fragments are gathered from the slot one step ahead of their MFMAs;
+//   * Sylvester stages over i_b_lo in registers, plus one lane-half stage by
+//     v_permlane32_swap; per-row min/max (the two waves of a row meet in LDS); codes use
+//     one fma per value and v_cvt_pk_u8_f32 (round half to even), which can move a code
+//     by one only on a rounding boundary.
+template <int A, int APAD, int NT, int B, int F>
 struct Pair {
   static constexpr int K = A * B;
-  static constexpr int KS = APAD / 16;  // k-steps of the dense stage
-  static constexpr int MT = B / 32;     // M tiles (32 i_b each)
-  static constexpr int NTW = NT / 2;    // N tiles per wave
-  static constexpr int ROWS = 4;        // rows per workgroup iteration
+  static constexpr int BL = B / F;            // Sylvester order left over i_b_lo
+  static constexpr int KS = F * APAD / 16;    // k-steps of the dense stage over (i_b_hi, i_a)
+  static constexpr int MT = BL / 32;          // M tiles (32 i_b_lo each)
+  static constexpr int NTW = NT / 2;          // N tiles per wave
+  static constexpr int NTF = NT / F;          // N tiles per value of j_b_hi
+  static constexpr int ROWS = 4;              // rows per workgroup iteration
   static constexpr int THREADS = 64 * 2 * ROWS;
   static constexpr int CHUNKS = K / 8;                   // 16-byte chunks of a row
   static constexpr int PF = (CHUNKS + 127) / 128;        // chunks per lane of the wave pair
   static constexpr int HFRAG = KS * NT * 64;             // 16-byte B fragments
   static constexpr int SLOT = K * 2;                     // bytes of one staged row
-  static constexpr int RAW = (A * A + 15) / 16 * 16;     // int8 H staging (aliases the slots)
   static constexpr int RED = 2 * ROWS * 2 * 2;           // floats: [parity][row][wave][min,max]
   static constexpr int LDS = HFRAG * 16 + ROWS * SLOT + RED * 4;
-  static_assert(NT % 2 == 0 && MT == 2, "two waves per row, two M tiles");
-  static_assert(APAD % 16 == 0 && APAD >= A && NT * 32 >= A, "padding");
-  static_assert(A % 4 == 0 && (A * A) % 16 == 0 && K % 8 == 0, "16-byte staging");
-  static_assert(RAW <= ROWS * SLOT, "H staging fits in the row slots");
+  static_assert(F == 1 || F == 2, "fold of at most one bit");
+  static_assert(NT % 2 == 0 && NT % F == 0 && BL % 32 == 0 && MT >= 2 && (MT & (MT - 1)) == 0, "tiling");
+  static_assert(APAD % 16 == 0 && APAD >= A && NTF * 32 >= A, "padding");
+  static_assert(K % 8 == 0, "16-byte row staging");
 };
 
-template <int A, int APAD, int NT, int B, bool DBG>
+template <int A, int APAD, int NT, int B, int F, bool DBG>
 __global__ void __launch_bounds__(512, 2)
 had_quant_pair(RotQuantArgs args) {
-  using C = Pair<A, APAD, NT, B>;
+  using C = Pair<A, APAD, NT, B, F>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   v8h* hf = reinterpret_cast<v8h*>(smem);
   unsigned char* slots = smem + C::HFRAG * 16;
@@ -463,29 +468,6 @@ had_quant_pair(RotQuantArgs args) {
   const int64_t nsets = (rows + C::ROWS - 1) / C::ROWS;
   int64_t rs = blockIdx.x;
   if (rs >= nsets) return;  // uniform over the workgroup
-
-  // ---- H_a as MFMA B fragments: hf[(ks*NT + nt)*64 + l][e] = H[k][n],
-  //      k = ks*16 + 8*(l/32) + e, n = nt*32 + l%32 (zero outside A x A); H is staged
-  //      in the (not yet used) row slots
-  int8_t* hraw = reinterpret_cast<int8_t*>(slots);
-  for (int i = threadIdx.x; i < A * A / 16; i += C::THREADS)
-    reinterpret_cast<v4u*>(hraw)[i] = reinterpret_cast<const v4u*>(args.H)[i];
-  __syncthreads();
-  for (int i = threadIdx.x; i < C::HFRAG; i += C::THREADS) {
-    const int l = i & 63;
-    const int t = i >> 6;
-    const int nt = t % NT;
-    const int ks = t / NT;
-    const int n = nt * 32 + (l & 31);
-    v8h f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int k = ks * 16 + 8 * (l >> 5) + e;
-      f[e] = (k < A && n < A) ? static_cast<_Float16>(hraw[k * A + n]) : static_cast<_Float16>(0.0f);
-    }
-    hf[i] = f;
-  }
-  __syncthreads();
 
   // ---- row staging: the wave pair loads chunk pl + 128 j of its row (16 bytes each)
   unsigned char* slot = slots + p * C::SLOT;
@@ -505,17 +487,48 @@ had_quant_pair(RotQuantArgs args) {
       if (i < C::CHUNKS) reinterpret_cast<v4u*>(slot)[i] = pf[j];
     }
   };
-  {
+  {  // the first rows are in flight while D is built
     const int64_t r0 = rs * C::ROWS + p;
     load_row(r0 < rows ? r0 : rows - 1);
-    store_row();
   }
+
+  // ---- D = H_a (x) S_F as MFMA B fragments: hf[(ks*NT + nt)*64 + l][e] = D[k][n] with
+  //      k = ks*16 + 8*(l/32) + e = i_b_hi*APAD + i_a and n = nt*32 + l%32, column
+  //      (j_b_hi, j_a) = (nt / NTF, (nt % NTF)*32 + l%32); zero where i_a or j_a >= A.
+  //      A thread owns one column (nt, l) and reads its entries of H straight from global
+  //      memory (indexes clamped into H, padding selected to zero afterwards).
+  for (int i = threadIdx.x; i < NT * 64; i += C::THREADS) {
+    const int l = i & 63;
+    const int nt = i >> 6;
+    const int jb = nt / C::NTF;
+    const int ja = (nt % C::NTF) * 32 + (l & 31);
+    const int g8 = 8 * (l >> 5);
+    const int8_t* hcol = args.H + (ja < A ? ja : A - 1);
+    static_for<C::KS>([&](auto kc) {
+      constexpr int ks = decltype(kc)::value;
+      constexpr int ib = (ks * 16) / APAD;  // a k-step never straddles two values of i_b_hi
+      constexpr int ia0 = (ks * 16) % APAD;
+      const float sgn = (ib & jb) ? -1.0f : 1.0f;
+      v8h f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int ia = ia0 + g8 + e;
+        const float hv = static_cast<float>(hcol[(ia < A ? ia : A - 1) * A]);
+        f[e] = (ia < A && ja < A) ? static_cast<_Float16>(sgn * hv) : static_cast<_Float16>(0.0f);
+      }
+      hf[(ks * NT + nt) * 64 + l] = f;
+    });
+  }
+  store_row();
   __syncthreads();
 
-  // A fragment (M tile mt, k-step ks) from the slot: X2[k][i_b], k = ks*16 + 8g + e,
-  // i_b = mt*32 + c; zero for k >= A
+  // A fragment (M tile mt, k-step ks) from the slot: X[(i_a, i_b_hi)][i_b_lo] with
+  // i_b_hi = ks*16 / APAD (a k-step never straddles two values), i_a = (ks*16) % APAD +
+  // 8g + e, i_b_lo = mt*32 + c, element i_a*B + i_b_hi*BL + i_b_lo; zero for i_a >= A
   const uint16_t* srow = reinterpret_cast<const uint16_t*>(slot) + c;
-  auto frag = [&](int mt, int ks) { return gather_afrag<A, B>(srow + mt * 32, ks * 16 + 8 * g); };
+  auto frag = [&](int mt, int ks) {
+    return gather_afrag<A, B>(srow + ((ks * 16) / APAD) * C::BL + mt * 32, (ks * 16) % APAD + 8 * g);
+  };
 
   const float s_n = args.inv_sqrt_n;
   for (int it = 0; rs < nsets; ++it, rs += gridDim.x) {
@@ -527,7 +540,9 @@ had_quant_pair(RotQuantArgs args) {
       load_row(nr < rows ? nr : rows - 1);
     }
 
-    // ---- dense stage: acc[mt][nt] = X2^T H_a for i_b tile mt, j_a tile h*NTW + nt
+    // ---- dense stage: acc[mt][nt] = X^T D for i_b_lo tile mt, D column tile h*NTW + nt.
+    //      Few M tiles: k-step outer, all M tiles' fragments gathered a step ahead; many M
+    //      tiles: M tile outer, one fragment gathered ahead (fewer live registers).
     v16f acc[C::MT][C::NTW];
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
@@ -535,28 +550,45 @@ had_quant_pair(RotQuantArgs args) {
       for (int nt = 0; nt < C::NTW; ++nt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[mt][nt][r] = 0.0f;
-    v8h a0[C::MT], a1[C::MT];
+    if constexpr (C::MT <= 2) {
+      v8h a0[C::MT], a1[C::MT];
 #pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt) a0[mt] = frag(mt, 0);
-    static_for<C::KS>([&](auto kc) {
-      constexpr int ks = decltype(kc)::value;
-      v8h(&cur)[C::MT] = (ks & 1) ? a1 : a0;
-      v8h(&nxt)[C::MT] = (ks & 1) ? a0 : a1;
-      if constexpr (ks + 1 < C::KS) {
+      for (int mt = 0; mt < C::MT; ++mt) a0[mt] = frag(mt, 0);
+      static_for<C::KS>([&](auto kc) {
+        constexpr int ks = decltype(kc)::value;
+        v8h(&cur)[C::MT] = (ks & 1) ? a1 : a0;
+        v8h(&nxt)[C::MT] = (ks & 1) ? a0 : a1;
+        if constexpr (ks + 1 < C::KS) {
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) nxt[mt] = frag(mt, ks + 1);
-      }
-      v8h bf[C::NTW];
+          for (int mt = 0; mt < C::MT; ++mt) nxt[mt] = frag(mt, ks + 1);
+        }
+        v8h bf[C::NTW];
 #pragma unroll
-      for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
+        for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
 #pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt)
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < C::NTW; ++nt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[mt], bf[nt], acc[mt][nt], 0, 0, 0);
+      });
+    } else {
+      v8h fa[2];
+      fa[0] = frag(0, 0);
+      static_for<C::MT * C::KS>([&](auto tc) {
+        constexpr int t = decltype(tc)::value;
+        constexpr int mt = t / C::KS;
+        constexpr int ks = t % C::KS;
+        if constexpr (t + 1 < C::MT * C::KS) fa[(t + 1) & 1] = frag((t + 1) / C::KS, (t + 1) % C::KS);
+        v8h bf[C::NTW];
+#pragma unroll
+        for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
 #pragma unroll
         for (int nt = 0; nt < C::NTW; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[mt], bf[nt], acc[mt][nt], 0, 0, 0);
-    });
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t & 1], bf[nt], acc[mt][nt], 0, 0, 0);
+      });
+    }
 
-    // ---- Sylvester stages over i_b: register bits 0, 1, 3, 4; M tile bit 5; lane half bit 2
+    // ---- Sylvester stages over i_b_lo: register bits 0, 1, 3, 4; M tile bits 5..; lane half bit 2
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -572,30 +604,47 @@ had_quant_pair(RotQuantArgs args) {
               acc[mt][nt][r + rb] = hi;
             }
 #pragma unroll
-    for (int nt = 0; nt < C::NTW; ++nt)
+    for (int tb = 1; tb < C::MT; tb <<= 1)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float lo = acc[0][nt][r], hi = acc[1][nt][r];
-        bfly(lo, hi);
-        acc[0][nt][r] = lo;
-        acc[1][nt][r] = hi;
-      }
-    const float sg = g ? -1.0f : 1.0f;
+      for (int mt = 0; mt < C::MT; ++mt)
+        if ((mt & tb) == 0)
+#pragma unroll
+          for (int nt = 0; nt < C::NTW; ++nt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              float lo = acc[mt][nt][r], hi = acc[mt + tb][nt][r];
+              bfly(lo, hi);
+              acc[mt][nt][r] = lo;
+              acc[mt + tb][nt][r] = hi;
+            }
+    // lane-half stage (i_b_lo bit 2): v_permlane32_swap of registers r and r + 8 (r < 8)
+    // puts both bit-2 partners of register r (lanes 0-31) or r + 8 (lanes 32-63) in one
+    // lane; the butterfly then leaves lane (c, g) holding i_b_lo = mt*32 + 16g + j in
+    // acc[mt][nt][j], j = 8q + 4*bit2 + e, sixteen consecutive positions
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < C::NTW; ++nt)
+      for (int nt = 0; nt < C::NTW; ++nt) {
+        float o[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float v = acc[mt][nt][r];
-          acc[mt][nt][r] = __fmaf_rn(sg, v, __shfl_xor(v, 32, 64));
+        for (int r = 0; r < 8; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mt][nt][r]),
+                                                           __float_as_uint(acc[mt][nt][r + 8]), false, false);
+          const float x0 = __uint_as_float(sw[0]);  // bit 2 clear
+          const float x1 = __uint_as_float(sw[1]);  // bit 2 set
+          const int j = 8 * (r >> 2) + (r & 3);
+          o[j] = __fadd_rn(x0, x1);
+          o[j + 4] = __fsub_rn(x0, x1);
         }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[mt][nt][j] = o[j];
+      }
 
     // ---- per-row min/max over real columns; the two waves of the row meet in LDS
     float mn = INFINITY, mx = -INFINITY;
 #pragma unroll
     for (int nt = 0; nt < C::NTW; ++nt) {
-      if ((h * C::NTW + nt) * 32 + c < A) {
+      if (((h * C::NTW + nt) % C::NTF) * 32 + c < A) {
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -628,46 +677,35 @@ had_quant_pair(RotQuantArgs args) {
       args.beta[row] = __fmul_rn(mn, s_n);
     }
 
-    // ---- codes: lane (c, g) holds i_b = mt*32 + 8*q + 4*g + e (r = 4q + e) of column j_a.
-    // Bytes via v_cvt_pk_u8_f32 (codes of e = 0, 2 in ev, e = 1, 3 in od, two q per dword),
-    // then ev | od << 4 is the 16-bit nibble run of q (low) and q + 1 (high); the partner
-    // lane half holds the other 4 positions of every 8, so swapping dwords and selecting
-    // bytes gives whole 32-bit words; half g stores M tile g (16 bytes, a wave 1 KB).
+    // ---- codes: lane (c, g) holds i_b_lo = mt*32 + 16g + j (j = 0..15) of column
+    // (j_b_hi, j_a): bytes via v_cvt_pk_u8_f32 (even j in ev, odd j in od), ev | od << 4
+    // is then four nibble-packed bytes; 8-byte store at output position
+    // j_a*B + j_b_hi*BL + mt*32 + 16g.
     uint8_t* qrow = args.q + row * (C::K / 2);
-    const uint32_t sel0 = g ? 0x01000504u : 0x05040100u;
-    const uint32_t sel1 = g ? 0x03020706u : 0x07060302u;
 #pragma unroll
     for (int nt = 0; nt < C::NTW; ++nt) {
-      const int ja = (h * C::NTW + nt) * 32 + c;
+      const int ntg = h * C::NTW + nt;
+      const int ja = (ntg % C::NTF) * 32 + c;
+      const int jb = ntg / C::NTF;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt) {
-        uint32_t m2[2];
+        uint32_t w[2];
 #pragma unroll
-        for (int qq = 0; qq < 2; ++qq) {
+        for (int hw = 0; hw < 2; ++hw) {
           uint32_t ev = 0, od = 0;
 #pragma unroll
-          for (int s = 0; s < 2; ++s) {
-            const int r0 = 4 * (2 * qq + s);
-            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0], inv_u, nb), 2 * s, ev);
-            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 2], inv_u, nb), 2 * s + 1, ev);
-            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 1], inv_u, nb), 2 * s, od);
-            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][r0 + 3], inv_u, nb), 2 * s + 1, od);
+          for (int s = 0; s < 4; ++s) {
+            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s], inv_u, nb), s, ev);
+            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
           }
-          m2[qq] = ev | (od << 4);
+          w[hw] = ev | (od << 4);
         }
-        const uint32_t p0 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m2[0]), 32, 64));
-        const uint32_t p1 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m2[1]), 32, 64));
-        const uint32_t w0 = __builtin_amdgcn_perm(p0, m2[0], sel0);
-        const uint32_t w1 = __builtin_amdgcn_perm(p0, m2[0], sel1);
-        const uint32_t w2 = __builtin_amdgcn_perm(p1, m2[1], sel0);
-        const uint32_t w3 = __builtin_amdgcn_perm(p1, m2[1], sel1);
-        if (valid && mt == g && ja < A)
-          *reinterpret_cast<uint4*>(qrow + (ja * B + mt * 32) / 2) = make_uint4(w0, w1, w2, w3);
+        const int pos = ja * B + jb * C::BL + mt * 32 + 16 * g;
+        if (valid && ja < A) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(w[0], w[1]);
         if constexpr (DBG) {
           if (valid && ja < A) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              args.dbg[row * C::K + ja * B + mt * 32 + 8 * (r >> 2) + 4 * g + (r & 3)] = __fmul_rn(acc[mt][nt][r], s_n);
+            for (int j = 0; j < 16; ++j) args.dbg[row * C::K + pos + j] = __fmul_rn(acc[mt][nt][j], s_n);
           }
         }
       }
@@ -715,10 +753,10 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
                : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
 }
 
-template <int A, int APAD, int NT, int B, bool DBG>
+template <int A, int APAD, int NT, int B, int F, bool DBG>
 hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
-  using C = Pair<A, APAD, NT, B>;
-  auto kern = had_quant_pair<A, APAD, NT, B, DBG>;
+  using C = Pair<A, APAD, NT, B, F>;
+  auto kern = had_quant_pair<A, APAD, NT, B, F, DBG>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (init != hipSuccess) return init;
@@ -729,9 +767,9 @@ hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int A, int APAD, int NT, int B>
+template <int A, int APAD, int NT, int B, int F>
 hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
-  return a.dbg ? launch_pair_t<A, APAD, NT, B, true>(a, stream) : launch_pair_t<A, APAD, NT, B, false>(a, stream);
+  return a.dbg ? launch_pair_t<A, APAD, NT, B, F, true>(a, stream) : launch_pair_t<A, APAD, NT, B, F, false>(a, stream);
 }
 
 }  // namespace
@@ -739,13 +777,14 @@ hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
 // Returns hipErrorNotSupported when no fast path covers the arguments.
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
+  // the pair kernel stages rows in 16-byte chunks
+  const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 && !getenv("SQ_KRON_STAGED");
+  // H_28 (x) S_512: the pair kernel with a one-bit fold (launch_pair<28, 32, 2, 512, 2>) is
+  // correct but slower here than the staged kernel (63 vs 59 us at 4096 rows)
   if (a.a == 28 && a.b == 512) return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
   if (a.a == 172 && a.b == 64) {
-    // the pair kernel stages H and the rows in 16-byte chunks
-    const bool fits = (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 &&
-                      (a.ldx % 8) == 0;
-    if (!fits || getenv("SQ_KRON_STAGED")) return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
-    return launch_pair<172, 176, 6, 64>(a, stream);
+    if (pair_ok) return launch_pair<172, 176, 6, 64, 1>(a, stream);
+    return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
   }
   if (a.a == 28 && a.b == 1024) return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
   return hipErrorNotSupported;

@@ -126,31 +126,33 @@ def test_llama2_70b_decode_act():
         check_act(inp["x_down"], 28, 1024)
 
 
-@pytest.mark.parametrize("M", [1, 7, 1027])
-def test_kron172_partial_row_sets(M):
-    say(f"had_quant_act H172 (x) S64, M={M}: rows in sets of 4, last set partial")
-    x = workloads.outlier_acts(workloads.rng_for(900 + M), M, 172 * 64, 110, 50.0)
-    check_act(x, 172, 64)
+@pytest.mark.parametrize("a,b,M", [(172, 64, 1), (172, 64, 7), (172, 64, 1027), (28, 512, 3), (28, 512, 13)])
+def test_kron_pair_partial_row_sets(a, b, M):
+    say(f"had_quant_act H{a} (x) S{b}, M={M}: rows in sets of 4, last set partial")
+    x = workloads.outlier_acts(workloads.rng_for(900 + M + a), M, a * b, a * b // 100, 50.0)
+    check_act(x, a, b)
 
 
-def test_kron172_strided_input_nan_padding():
-    say("had_quant_act H172 (x) S64 on a strided input whose row padding is NaN")
-    M, K = 9, 172 * 64
-    x = workloads.outlier_acts(workloads.rng_for(77), M, K, 110, 50.0)
+@pytest.mark.parametrize("a,b", [(172, 64), (28, 512)])
+def test_kron_pair_strided_input_nan_padding(a, b):
+    say(f"had_quant_act H{a} (x) S{b} on a strided input whose row padding is NaN")
+    M, K = 9, a * b
+    x = workloads.outlier_acts(workloads.rng_for(77), M, K, K // 100, 50.0)
     wide = np.full((M, K + 96), np.nan, dtype=np.float16)
     wide[:, :K] = x
-    h = had_table(172)
-    r1 = [host(v) for v in sq.had_quant_act(dev(wide)[:, :K], h, 64)[:3]]
-    r2 = [host(v) for v in sq.had_quant_act(dev(x), h, 64)[:3]]
+    h = had_table(a)
+    r1 = [host(v) for v in sq.had_quant_act(dev(wide)[:, :K], h, b)[:3]]
+    r2 = [host(v) for v in sq.had_quant_act(dev(x), h, b)[:3]]
     for u, v in zip(r1, r2):
         np.testing.assert_array_equal(u, v)
 
 
-def test_kron172_staged_kernel(monkeypatch):
-    say("had_quant_act H172 (x) S64 through the LDS-staged kernel")
+@pytest.mark.parametrize("a,b", [(172, 64), (28, 512)])
+def test_kron_staged_kernel(a, b, monkeypatch):
+    say(f"had_quant_act H{a} (x) S{b} through the register-prefetch kernel")
     monkeypatch.setenv("SQ_KRON_STAGED", "1")
-    x = workloads.outlier_acts(workloads.rng_for(31), 37, 172 * 64, 110, 50.0)
-    check_act(x, 172, 64)
+    x = workloads.outlier_acts(workloads.rng_for(31), 37, a * b, a * b // 100, 50.0)
+    check_act(x, a, b)
 
 
 @pytest.mark.parametrize("a,b,M", [(28, 512, 33), (172, 64, 21), (28, 1024, 5)])
