@@ -66,6 +66,20 @@ int32_t sq_abi_version(void);
 const char* sq_last_error(void);
 
 /*
+ * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
+ * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear or sq_qk_had_kvquant
+ * made by this host thread: start_event takes the start time of the first kernel that
+ * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
+ * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
+ * marker packets between kernels.
+ *   start_event, stop_event   hipEvent_t, created by the caller with timing enabled
+ * The events are consumed by that next call whatever its outcome; a call that returns
+ * an error, or enqueues nothing (M == 0), leaves them as they were.
+ * Errors: SQ_ERR_NULL for a NULL event.
+ */
+sq_status sq_time_next_call(void* start_event, void* stop_event);
+
+/*
  * sq_hadamard_factor -- host helper: writes the library's +-1 Hadamard matrix of order
  * n into out_host[n*n] (row-major int8, HOST memory), for use as `had_dense`.
  *   n = 1    : [1]

@@ -255,20 +255,16 @@ hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hip
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(a.rows)), dim3(kThreads), lds, stream, a);
-  return hipGetLastError();
+  return launch(kern, dim3(static_cast<unsigned>(a.rows)), dim3(kThreads), static_cast<uint32_t>(lds), stream, a);
 }
 
 }  // namespace
 
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream) {
   if (a.a == 1 && a.b == 1 && a.group == a.K) {
-    if (a.K <= 4 * 64 * 8 * 8) {
-      hipLaunchKernelGGL((quant_rows_identity<4, 8>), dim3(static_cast<unsigned>(a.rows)), dim3(256), 0, stream, a);
-    } else {
-      hipLaunchKernelGGL((quant_rows_identity<8, 8>), dim3(static_cast<unsigned>(a.rows)), dim3(512), 0, stream, a);
-    }
-    return hipGetLastError();
+    if (a.K <= 4 * 64 * 8 * 8)
+      return launch(quant_rows_identity<4, 8>, dim3(static_cast<unsigned>(a.rows)), dim3(256), 0, stream, a);
+    return launch(quant_rows_identity<8, 8>, dim3(static_cast<unsigned>(a.rows)), dim3(512), 0, stream, a);
   }
   const hipError_t e = launch_had_quant_kron(a, stream);
   if (e != hipErrorNotSupported) return e;

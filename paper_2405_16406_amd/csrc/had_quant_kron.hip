@@ -743,8 +743,7 @@ hipError_t launch_kron_t(const RotQuantArgs& a, hipStream_t stream) {
   if (init != hipSuccess) return init;
   const int64_t cap = static_cast<int64_t>(num_cus()) * blocks_per_cu;
   const unsigned grid = static_cast<unsigned>(a.rows < cap ? a.rows : cap);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
-  return hipGetLastError();
+  return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
 
 template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE>
@@ -763,8 +762,7 @@ hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   const int64_t sets = (a.rows + C::ROWS - 1) / C::ROWS;
   const int64_t cap = num_cus();
   const unsigned grid = static_cast<unsigned>(sets < cap ? sets : cap);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
-  return hipGetLastError();
+  return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
 
 template <int A, int APAD, int NT, int B, int F>

@@ -156,8 +156,7 @@ qk_had_kvquant_v2(KvArgs a) {
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream) {
   const int64_t threads = a.groups * 4;
   const unsigned blocks = static_cast<unsigned>((threads + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(qk_had_kvquant_v2, dim3(blocks), dim3(kThreads), 0, stream, a);
-  return hipGetLastError();
+  return launch(qk_had_kvquant_v2, dim3(blocks), dim3(kThreads), 0, stream, a);
 }
 
 }  // namespace sq

@@ -15,6 +15,12 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local sq::LaunchTiming g_timing;
+
+// Disarms sq_time_next_call's events when the entry point returns, on every path.
+struct TimingScope {
+  ~TimingScope() { g_timing = sq::LaunchTiming{}; }
+};
 
 sq_status fail(sq_status s, const char* fmt, ...) {
   char buf[512];
@@ -88,11 +94,20 @@ float inv_sqrt(int64_t n) { return static_cast<float>(1.0 / std::sqrt(static_cas
 
 }  // namespace
 
+sq::LaunchTiming& sq::launch_timing() { return g_timing; }
+
 extern "C" {
 
 int32_t sq_abi_version(void) { return SQ_ABI_VERSION; }
 
 const char* sq_last_error(void) { return g_last_error.c_str(); }
+
+sq_status sq_time_next_call(void* start_event, void* stop_event) {
+  if (!start_event || !stop_event) return fail(SQ_ERR_NULL, "start_event and stop_event are required");
+  g_timing.start = static_cast<hipEvent_t>(start_event);
+  g_timing.stop = static_cast<hipEvent_t>(stop_event);
+  return ok();
+}
 
 sq_status sq_hadamard_factor(int32_t n, int8_t* out_host) {
   if (!out_host) return fail(SQ_ERR_NULL, "out_host is NULL");
@@ -107,6 +122,7 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                            int32_t bits, int32_t group,
                            uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
                            void* stream) {
+  TimingScope timing_scope;
   if (!x || !q_out || !alpha || !beta) return fail(SQ_ERR_NULL, "x, q_out, alpha and beta are required");
   sq_status s = check_rows(M, K, ldx, "M");
   if (s != SQ_OK) return s;
@@ -145,6 +161,7 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
 sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
                      int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
                      uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream) {
+  TimingScope timing_scope;
   if (!w || !wq || !w_alpha || !w_rowsum) return fail(SQ_ERR_NULL, "w, wq, w_alpha and w_rowsum are required");
   sq_status s = check_rows(N, K, ldw, "N");
   if (s != SQ_OK) return s;
@@ -177,6 +194,7 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
                          const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
                          int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
                          int32_t* dbg_acc, void* stream) {
+  TimingScope timing_scope;
   if (!xq || !x_alpha || !x_beta || !wq || !w_alpha || !w_rowsum || !y)
     return fail(SQ_ERR_NULL, "xq, x_alpha, x_beta, wq, w_alpha, w_rowsum and y are required");
   if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
@@ -217,6 +235,7 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                             void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
                             uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
                             void* stream) {
+  TimingScope timing_scope;
   if (!q || !k || !v || !q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta)
     return fail(SQ_ERR_NULL, "q, k, v, q_rot, k_q, k_alpha, k_beta, v_q, v_alpha and v_beta are required");
   if (B < 0 || S < 0 || H < 0) return fail(SQ_ERR_SHAPE, "negative B, S or H");

@@ -1,6 +1,7 @@
 // Internal declarations shared by the host API and the kernel translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -72,5 +73,23 @@ struct KvArgs {
 };
 
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream);
+
+// Timing of one entry-point call (armed by sq_time_next_call, per host thread): the start
+// event is taken with the first kernel the call launches and the stop event with each
+// kernel, so the last one sets it.  Both are null when timing is not armed.
+struct LaunchTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+LaunchTiming& launch_timing();
+
+// Every kernel of the library is launched through here.
+template <typename... Params, typename... Args>
+hipError_t launch(void (*kern)(Params...), dim3 grid, dim3 block, uint32_t lds, hipStream_t stream, Args... args) {
+  LaunchTiming& t = launch_timing();
+  hipExtLaunchKernelGGL(kern, grid, block, lds, stream, t.start, t.stop, 0, args...);
+  t.start = nullptr;  // later kernels of the same call only move the stop event
+  return hipGetLastError();
+}
 
 }  // namespace sq

@@ -597,8 +597,7 @@ hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, R::LDS);
   if (init != hipSuccess) return init;
   const dim3 grid(static_cast<unsigned>((g.N + R::BN - 1) / R::BN), static_cast<unsigned>((g.M + R::BM - 1) / R::BM));
-  hipLaunchKernelGGL(kern, grid, dim3(R::THREADS), R::LDS, stream, g);
-  return hipGetLastError();
+  return launch(kern, grid, dim3(R::THREADS), R::LDS, stream, g);
 }
 
 // ------------------------------------------------------------------ small-M kernel
@@ -672,10 +671,10 @@ w4a4_gemm_v1(GemmArgs g) {
 }
 
 template <int WM, int WN, int TM, int TN>
-void launch_tile(const GemmArgs& g, hipStream_t stream) {
+hipError_t launch_tile(const GemmArgs& g, hipStream_t stream) {
   constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
   const dim3 grid(static_cast<unsigned>((g.N + BN - 1) / BN), static_cast<unsigned>((g.M + BM - 1) / BM));
-  hipLaunchKernelGGL((w4a4_gemm_tile<WM, WN, TM, TN>), grid, dim3(64 * WM * WN), 0, stream, g);
+  return launch(w4a4_gemm_tile<WM, WN, TM, TN>, grid, dim3(64 * WM * WN), 0, stream, g);
 }
 
 }  // namespace
@@ -685,12 +684,12 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
   const char* env = getenv("SQ_GEMM_VARIANT");
   const int v = env ? atoi(env) : -1;
   switch (v) {
-    case 0: launch_tile<2, 2, 4, 2>(g, stream); break;   // 256 x 128, 4 waves of 128 x 64
-    case 1: launch_tile<2, 2, 2, 2>(g, stream); break;   // 128 x 128, 4 waves of 64 x 64
-    case 2: launch_tile<2, 2, 4, 4>(g, stream); break;   // 256 x 256, 4 waves of 128 x 128
-    case 3: launch_tile<2, 1, 4, 4>(g, stream); break;   // 256 x 128, 2 waves of 128 x 128
-    case 4: launch_tile<1, 2, 4, 4>(g, stream); break;   // 128 x 256, 2 waves of 128 x 128
-    case 5: launch_tile<2, 4, 4, 2>(g, stream); break;   // 256 x 256, 8 waves of 128 x 64
+    case 0: return launch_tile<2, 2, 4, 2>(g, stream);   // 256 x 128, 4 waves of 128 x 64
+    case 1: return launch_tile<2, 2, 2, 2>(g, stream);   // 128 x 128, 4 waves of 64 x 64
+    case 2: return launch_tile<2, 2, 4, 4>(g, stream);   // 256 x 256, 4 waves of 128 x 128
+    case 3: return launch_tile<2, 1, 4, 4>(g, stream);   // 256 x 128, 2 waves of 128 x 128
+    case 4: return launch_tile<1, 2, 4, 4>(g, stream);   // 128 x 256, 2 waves of 128 x 128
+    case 5: return launch_tile<2, 4, 4, 2>(g, stream);   // 256 x 256, 8 waves of 128 x 64
     case 10: if (fits_ring<2, 2, 4, 2, 4>(g)) return launch_ring<2, 2, 4, 2, 4>(g, stream); break;  // 256 x 128
     case 11: if (fits_ring<2, 2, 4, 4, 4>(g)) return launch_ring<2, 2, 4, 4, 4>(g, stream); break;  // 256 x 256
     case 12: if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream); break;  // 256 x 256, 8 waves
@@ -698,8 +697,7 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
     case 9: {
       const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
-      hipLaunchKernelGGL(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
-      break;
+      return launch(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
     }
     default: {
       // Measured on MI355X (LLaMA MLP shapes): decode-sized M runs 128 x 128 ring tiles;
@@ -709,18 +707,18 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
       const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
       if (g.M <= 128) {
         if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream);
-        launch_tile<2, 2, 2, 2>(g, stream);
-      } else if (tiles256 >= 256 && (tiles256 % 256 == 0 || tiles256 % 256 >= 192)) {
-        if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
-        launch_tile<2, 4, 4, 2>(g, stream);
-      } else {
-        if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
-        launch_tile<2, 4, 4, 2>(g, stream);
+        return launch_tile<2, 2, 2, 2>(g, stream);
       }
-      break;
+      if (tiles256 >= 256 && (tiles256 % 256 == 0 || tiles256 % 256 >= 192)) {
+        if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
+        return launch_tile<2, 4, 4, 2>(g, stream);
+      }
+      if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
+      return launch_tile<2, 4, 4, 2>(g, stream);
     }
   }
-  return hipGetLastError();
+  // a tuning variant whose ring offsets do not fit: the default path
+  return launch_tile<2, 4, 4, 2>(g, stream);
 }
 
 }  // namespace sq

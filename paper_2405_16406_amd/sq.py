@@ -19,7 +19,7 @@ SQ_OK, SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS
 STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSUPPORTED",
                 4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
 
-EXPORTS = ("sq_abi_version", "sq_last_error", "sq_hadamard_factor", "sq_had_quant_act",
+EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
            "sq_pack_w4", "sq_w4a4_linear", "sq_qk_had_kvquant")
 
 
@@ -47,6 +47,8 @@ def lib() -> ctypes.CDLL:
     L.sq_abi_version.argtypes = []
     L.sq_last_error.restype = ctypes.c_char_p
     L.sq_last_error.argtypes = []
+    L.sq_time_next_call.restype = _I32
+    L.sq_time_next_call.argtypes = [_P, _P]
     L.sq_hadamard_factor.restype = _I32
     L.sq_hadamard_factor.argtypes = [_I32, _P]
     L.sq_had_quant_act.restype = _I32
@@ -82,6 +84,16 @@ def _need(t: torch.Tensor, dtype, name: str):
 
 def abi_version() -> int:
     return int(lib().sq_abi_version())
+
+
+def time_next_call(start: "torch.cuda.Event", stop: "torch.cuda.Event") -> None:
+    """Arm two timing events (torch.cuda.Event(enable_timing=True)) for this thread's next
+    library call: start.elapsed_time(stop) is then that call's kernel time on the device."""
+    for e in (start, stop):
+        if e.cuda_event == 0:  # torch creates the HIP event on its first record
+            e.record()
+    _check(lib().sq_time_next_call(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event)),
+           "sq_time_next_call")
 
 
 def hadamard_factor(n: int) -> np.ndarray:

@@ -132,3 +132,12 @@ def test_kv_validation(L):
     assert kvq(L, qr=fake(0)) == sq.SQ_ERR_ALIAS
     assert kvq(L, kq=ctypes.c_void_p(fake(4).value + 4)) == sq.SQ_ERR_ALIGN
     assert kvq(L, B=0) == sq.SQ_OK
+
+
+def test_time_next_call_host_checks(L):
+    assert L.sq_time_next_call(None, fake(1)) == sq.SQ_ERR_NULL
+    assert L.sq_time_next_call(fake(0), None) == sq.SQ_ERR_NULL
+    assert L.sq_time_next_call(fake(0), fake(1)) == sq.SQ_OK
+    # the next entry-point call consumes the armed events even when it fails its checks
+    assert hqa(L, K=250, ldx=256) == sq.SQ_ERR_SHAPE
+    assert hqa(L, x=None) == sq.SQ_ERR_NULL

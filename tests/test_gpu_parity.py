@@ -393,3 +393,30 @@ def test_gemm_tile_variants(variant, monkeypatch):
         sq.w4a4_linear(*args, out=wide8[:, :N])
         np.testing.assert_array_equal(host(wide8[:, :N]), host(y_dbg))
         assert not host(wide8[:, N:]).any()
+
+
+def test_time_next_call_events():
+    say("sq_time_next_call around w4a4_linear [512x1024]x[768x1024] and a rotated act quant")
+    rng = workloads.rng_for(77)
+    M, N, K = 512, 768, 1024
+    qa = rng.integers(0, 16, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    args = (dev(oq.pack_nibbles(qa)), dev(rng.uniform(0.1, 1, M).astype(np.float32)),
+            dev(rng.uniform(-5, 0, M).astype(np.float32)), dev(oq.pack_nibbles(qw)),
+            dev(rng.uniform(1e-3, 1e-2, N).astype(np.float32)), dev(qw.sum(1).astype(np.int32)))
+    ref, _ = sq.w4a4_linear(*args)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    sq.time_next_call(a, b)
+    y, _ = sq.w4a4_linear(*args)
+    y2, _ = sq.w4a4_linear(*args)  # not timed: the events were consumed
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b)
+    assert 0 < ms < 50
+    assert torch.equal(y, ref) and torch.equal(y2, ref)
+    x = dev(workloads.outlier_acts(rng, 64, 28 * 512, 8, 50.0))
+    q0 = sq.had_quant_act(x, had_table(28), 512)[0]
+    sq.time_next_call(a, b)
+    q1 = sq.had_quant_act(x, had_table(28), 512)[0]
+    torch.cuda.synchronize()
+    assert 0 < a.elapsed_time(b) < 50
+    assert torch.equal(q0, q1)
