@@ -443,19 +443,41 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));
 }
 
-template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE>
-__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N, WPE)
+// LDS of a ring kernel with KS groups of waves splitting K: one ring per group, reused at
+// the end for the groups' exchange of partial sums and for the epilogue staging.
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int KS>
+constexpr int ring_lds() {
+  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
+  constexpr int rings = KS * NS * R::STAGE;
+  constexpr int xch = KS == 1 ? 0 : KS * R::WAVES * (TM / 2) * TN * 16 * 64 * 4;
+  constexpr int epi = KS * R::WAVES * EpiStage<TM / KS, TN>::BYTES;
+  return rings > xch ? (rings > epi ? rings : epi) : (xch > epi ? xch : epi);
+}
+
+// KS = 2: two groups of WAVES_M x WAVES_N waves share the tile and split its k-stages in
+// two halves, each group with its own ring (twice the waves per SIMD when the tile count
+// leaves the CUs one workgroup each).  At the end each group hands the other the int32
+// partial sums of the half of its block that the other finishes (through LDS; integer
+// sums, so the result is bit-identical to KS = 1), and each finishes half of the rows.
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE, int KS>
+__global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS, WPE)
 w4a4_gemm_ring(GemmArgs g) {
   using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
+  static_assert(KS == 1 || (KS == 2 && TM % 2 == 0), "K split of two needs an even TM");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wid / R::WAVES;   // K slice of this wave's group
+  const int wave = wid % R::WAVES;  // wave within the group
+  uint8_t* const ring = lds + grp * NS * R::STAGE;
   int64_t m0, n0;
   tile_origin(R::BM, R::BN, m0, n0);
   const int wm = (wave / WAVES_N) * TM;  // first 32-row group of this wave in the tile
   const int wn = (wave % WAVES_N) * TN;
   const uint32_t KB = static_cast<uint32_t>(g.K / 2);
-  const int nstage = static_cast<int>((KB + 63) / 64);
+  // stages per group; the group's stage st is stage st0 + st of the whole K (past K: zeros)
+  const int nstage = static_cast<int>(((KB + 63) / 64 + KS - 1) / KS);
+  const uint32_t st0 = static_cast<uint32_t>(grp * nstage);
 
   // Buffer ranges: offsets are 32-bit and (M + BM) * K/2 < 2^31 is checked on the host.
   const __amdgpu_buffer_rsrc_t rsa =
@@ -473,13 +495,15 @@ w4a4_gemm_ring(GemmArgs g) {
     colofs[d] = (bl & 1) * 32 + (lane >> 5) * 16;
   });
   auto issue = [&](int st) {
-    uint8_t* sb = lds + (st % NS) * R::STAGE;
-    const uint32_t k0 = static_cast<uint32_t>(st) * 64;
+    uint8_t* sb = ring + (st % NS) * R::STAGE;
+    const uint32_t k0 = (st0 + static_cast<uint32_t>(st)) * 64;
+    const bool live = st < nstage;
     static_for<R::DPW>([&](auto dc) {
       constexpr int d = decltype(dc)::value;
       const uint32_t col = k0 + colofs[d];
-      // past K (or a stage past the end, issued only to keep the copy count uniform): out of range
-      const uint32_t off = (col < KB) ? rowoff[d] + col : 0x80000000u;
+      // past K, or a stage past the group's end (issued only to keep the copy count
+      // uniform; it may lie in the next group's slice): out of range, lands as zeros
+      const uint32_t off = (live && col < KB) ? rowoff[d] + col : 0x80000000u;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
           reinterpret_cast<uintptr_t>(sb + (wave + R::WAVES * d) * 1024));
       if constexpr (d < R::ADPW)
@@ -489,7 +513,7 @@ w4a4_gemm_ring(GemmArgs g) {
     });
   };
   auto read = [&](RingPacked<TM, TN>& P, int st, int p) {
-    const uint8_t* sb = lds + (st % NS) * R::STAGE + lane * 16 + p * 1024;
+    const uint8_t* sb = ring + (st % NS) * R::STAGE + lane * 16 + p * 1024;
 #pragma unroll
     for (int i = 0; i < TM; ++i) P.a[i] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 2048);
 #pragma unroll
@@ -571,13 +595,65 @@ w4a4_gemm_ring(GemmArgs g) {
   asm volatile("" ::: "memory");
 
   const bool vec = ((g.ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && (g.dbg_acc == nullptr);
-  if (vec) {
-    __builtin_amdgcn_s_barrier();  // every wave is done with the ring; each now stages its own block
-    asm volatile("" ::: "memory");
-    uint16_t* stage = reinterpret_cast<uint16_t*>(lds + wave * EpiStage<TM, TN>::BYTES);
-    tile_epilogue_lds(g, acc, m0 + wm * 32, n0 + wn * 32, lane, stage);
+  if constexpr (KS == 1) {
+    if (vec) {
+      __builtin_amdgcn_s_barrier();  // every wave is done with the ring; each now stages its own block
+      asm volatile("" ::: "memory");
+      uint16_t* stage = reinterpret_cast<uint16_t*>(lds + wave * EpiStage<TM, TN>::BYTES);
+      tile_epilogue_lds(g, acc, m0 + wm * 32, n0 + wn * 32, lane, stage);
+    } else {
+      tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
+    }
   } else {
-    tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
+    // group h finishes row blocks [h*HT, h*HT + HT) of the wave's block
+    constexpr int HT = TM / 2;
+    constexpr int XW = HT * TN * 16;  // ints per lane handed over
+    int* const xch = reinterpret_cast<int*>(lds);
+    __builtin_amdgcn_s_barrier();  // both rings are drained and read for the last time
+    asm volatile("" ::: "memory");
+    auto put = [&](auto hc) {  // hand over half hc to the other group
+      constexpr int h = decltype(hc)::value;
+      int* dst = xch + (grp * R::WAVES + wave) * XW * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < HT; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[((i * TN + j) * 16 + r) * 64] = acc[h * HT + i][j][r];
+    };
+    auto take = [&](auto hc) {  // add the other group's partial sums of half hc
+      constexpr int h = decltype(hc)::value;
+      const int* src = xch + ((1 - grp) * R::WAVES + wave) * XW * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < HT; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[h * HT + i][j][r] += src[((i * TN + j) * 16 + r) * 64];
+    };
+    auto finish = [&](auto hc) {
+      constexpr int h = decltype(hc)::value;
+      v16i part[HT][TN];
+#pragma unroll
+      for (int i = 0; i < HT; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) part[i][j] = acc[h * HT + i][j];
+      const int64_t mw = m0 + (wm + h * HT) * 32, nw = n0 + wn * 32;
+      if (vec)
+        tile_epilogue_lds(g, part, mw, nw, lane,
+                          reinterpret_cast<uint16_t*>(lds + wid * EpiStage<HT, TN>::BYTES));
+      else
+        tile_epilogue(g, part, mw, nw, lane);
+    };
+    constexpr std::integral_constant<int, 0> lo{};
+    constexpr std::integral_constant<int, 1> hi{};
+    if (grp == 0) put(hi); else put(lo);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (grp == 0) take(lo); else take(hi);
+    __builtin_amdgcn_s_barrier();  // the exchange area is read; the epilogue staging reuses it
+    asm volatile("" ::: "memory");
+    if (grp == 0) finish(lo); else finish(hi);
   }
 }
 
@@ -588,16 +664,19 @@ bool fits_ring(const GemmArgs& g) {
   return (g.M + R::BM) * kb + 64 < (int64_t{1} << 31) && (g.N + R::BN) * kb + 64 < (int64_t{1} << 31);
 }
 
-// WPE: waves per SIMD the registers must allow (2 for two 4-wave workgroups per CU)
-template <int WM, int WN, int TM, int TN, int NS, int WPE = 1>
+// WPE: waves per SIMD the registers must allow (2 for two 4-wave workgroups per CU, or one
+// workgroup of two K groups); KS: groups of waves splitting K.
+template <int WM, int WN, int TM, int TN, int NS, int WPE = 1, int KS = 1>
 hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
   using R = Ring<WM, WN, TM, TN, NS>;
-  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE>;
+  constexpr int LDS = ring_lds<WM, WN, TM, TN, NS, KS>();
+  static_assert(LDS <= 160 * 1024, "LDS of one CU");
+  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, R::LDS);
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
   if (init != hipSuccess) return init;
   const dim3 grid(static_cast<unsigned>((g.N + R::BN - 1) / R::BN), static_cast<unsigned>((g.M + R::BM - 1) / R::BM));
-  return launch(kern, grid, dim3(R::THREADS), R::LDS, stream, g);
+  return launch(kern, grid, dim3(R::THREADS * KS), LDS, stream, g);
 }
 
 // ------------------------------------------------------------------ small-M kernel
@@ -695,21 +774,26 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 12: if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream); break;  // 256 x 256, 8 waves
     case 13: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream); break;  // 128 x 128
     case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
+    case 15: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2, 2>(g, stream); break;  // 256 x 128, K split
+    case 16: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream); break;  // 128 x 128, K split
     case 9: {
       const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
       return launch(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
     }
     default: {
-      // Measured on MI355X (LLaMA MLP shapes): decode-sized M runs 128 x 128 ring tiles;
-      // otherwise 256 x 128 ring tiles two workgroups per CU, unless the 256 x 256 tiles
-      // fill whole rounds of the 256 CUs (then the 8-wave 256 x 256 ring tile wins).
-      // Problems whose byte offsets do not fit 31 bits use the register-staged kernel.
+      // Measured on MI355X (LLaMA-2-7B / LLaMA-3-8B MLP shapes, same data, interleaved runs):
+      // the 8-wave 256 x 256 ring tile is fastest once there are at least as many of its
+      // tiles as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs
+      // 212 us); with fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).
+      // Decode-sized M runs 128 x 128 tiles with two K groups per workgroup (M = 16:
+      // 86 vs 114 us at K = 28672).  Problems whose byte offsets do not fit 31 bits use the
+      // register-staged kernel.
       const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
       if (g.M <= 128) {
-        if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream);
+        if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);
         return launch_tile<2, 2, 2, 2>(g, stream);
       }
-      if (tiles256 >= 256 && (tiles256 % 256 == 0 || tiles256 % 256 >= 192)) {
+      if (tiles256 >= 256) {
         if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
         return launch_tile<2, 4, 4, 2>(g, stream);
       }

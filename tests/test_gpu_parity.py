@@ -364,7 +364,7 @@ def test_kv_full_sampled():
     check_kv(q, k, v, sample)
 
 
-@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "9", "10", "11", "12", "13", "14"])
+@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "9", "10", "11", "12", "13", "14", "15", "16"])
 def test_gemm_tile_variants(variant, monkeypatch):
     say(f"w4a4_linear tile variant {variant}: ragged shapes, paired and unpaired stores")
     monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
