@@ -262,9 +262,14 @@ hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hip
 
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream) {
   if (a.a == 1 && a.b == 1 && a.group == a.K) {
-    if (a.K <= 4 * 64 * 8 * 8)
-      return launch(quant_rows_identity<4, 8>, dim3(static_cast<unsigned>(a.rows)), dim3(256), 0, stream, a);
-    return launch(quant_rows_identity<8, 8>, dim3(static_cast<unsigned>(a.rows)), dim3(512), 0, stream, a);
+    // chunks of 8 per thread sized to K, so that the registers (and with them the
+    // resident workgroups per CU) follow the row length
+    const dim3 grid(static_cast<unsigned>(a.rows));
+    const int64_t nch = a.K / 8;
+    if (nch <= 256 * 2) return launch(quant_rows_identity<4, 2>, grid, dim3(256), 0, stream, a);
+    if (nch <= 256 * 4) return launch(quant_rows_identity<4, 4>, grid, dim3(256), 0, stream, a);
+    if (nch <= 512 * 4) return launch(quant_rows_identity<8, 4>, grid, dim3(512), 0, stream, a);
+    return launch(quant_rows_identity<8, 8>, grid, dim3(512), 0, stream, a);
   }
   const hipError_t e = launch_had_quant_kron(a, stream);
   if (e != hipErrorNotSupported) return e;

@@ -67,6 +67,15 @@ def test_tiny_identity_quant_bit_exact():
     assert check_act(x, 1, 1) == 0
 
 
+@pytest.mark.parametrize("K", [8, 4096, 4104, 8192, 8200, 16384, 16392, 32768])
+def test_identity_quant_row_lengths(K):
+    # each row-length range has its own chunks-per-thread instantiation
+    say(f"had_quant_act identity K={K}")
+    rng = workloads.rng_for(K)
+    x = workloads.outlier_acts(rng, 5, K, max(1, K // 100), 50.0)
+    assert check_act(x, 1, 1) == 0
+
+
 def test_tiny_sylvester256():
     say("had_quant_act tiny Sylvester 256")
     x, _ = workloads.tiny_inputs()
