@@ -31,6 +31,21 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+// The epilogue rounds twice, fp32 then fp16 (round to nearest even), in both of its paths.
+// fp32_result pins a value as a rounded fp32 register so that the compiler cannot fuse the
+// final fma with the fp16 conversion into one single-rounding v_fma_mix.
+__device__ __forceinline__ float fp32_result(float v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+// two fp32 -> two fp16 (round to nearest even), packed low | high << 16
+__device__ __forceinline__ uint32_t f2h2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{lo, hi}, v2h));
+}
 
 __device__ __forceinline__ v4i expand_act(uint2 d) {
   v4i r;
@@ -156,74 +171,130 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const v16i (&ac
   });
 }
 
-// The same epilogue through LDS: the wave converts its TM x TN blocks to fp16 into its own
-// LDS region (row-major, padded pitch: the two lane halves hit different banks), then reads
-// 16 bytes (8 columns of one row) per lane and stores them, so each store instruction
-// writes whole 128-byte row segments instead of 4-byte pairs.  Needs 16-byte aligned
-// output rows (ldy % 8 == 0, y 16-byte aligned); columns past N are stored one by one.
-template <int TM, int TN>
-struct EpiStage {
-  static constexpr int PITCH = TN * 32 + 8;  // fp16 elements per staged row
-  static constexpr int BYTES = TM * 32 * PITCH * 2;
+// Epilogue of the ring kernel.  Its MFMAs take the weights as the A operand, so each 32 x 32
+// block is D[n][m]: lane (c, h) = (lane % 32, lane / 32) holds row m = mb + c and columns
+// n = nb + 8q + 4h + e in registers r = 4q + e, i.e. four consecutive outputs of one row per
+// q, written with one 8-byte store.  The accumulators hold 16 * acc (weights expanded as
+// 16 * code), so alpha_m / 16 is applied:
+//   y = fma(alpha_m/16, s_n * acc16, fma(beta_m, s_n rs_n, bias_n))   (bias_n = 0 without a bias).
+// Per-tile row and column scales are staged in LDS during the prologue (RingScales).
+template <int BM, int BN>
+struct RingScales {
+  // floats: rowA[BM] (alpha_m / 16), rowB[BM] (beta_m), colS[BN] (s_n), colR[BN] (rs_n), colB[BN] (bias_n)
+  static constexpr int COUNT = 2 * BM + 3 * BN;
+  static constexpr int BYTES = COUNT * 4;
 };
 
-template <int TM, int TN>
-__device__ __forceinline__ void tile_epilogue_lds(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
-                                                  int lane, uint16_t* __restrict__ stage) {
-  constexpr int PITCH = EpiStage<TM, TN>::PITCH;
-  const int c = lane & 31;
-  const int gh = lane >> 5;
-  float csn[TN], cwr[TN], cbn[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t n = nw + j * 32 + c;
-    const int64_t nc = n < g.N ? n : g.N - 1;
-    csn[j] = g.wa[nc];
-    cwr[j] = __fmul_rn(csn[j], static_cast<float>(g.rs[nc]));
-    cbn[j] = g.bias ? h2f(g.bias[nc]) : 0.0f;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes), 0x00020000);
+}
+
+// Loads scale value `idx` of a tile (RingScales layout); out-of-range rows/columns read 0.
+template <int BM, int BN>
+__device__ __forceinline__ float load_scale(const GemmArgs& g, int idx, int64_t m0, int64_t n0) {
+  if (idx < 2 * BM) {
+    const int64_t m = m0 + (idx % BM);
+    if (m >= g.M) return 0.0f;
+    return idx < BM ? __fmul_rn(g.xa[m], 0.0625f) : g.xb[m];
   }
-  static_for<TM>([&](auto ic) {
-    constexpr int i = decltype(ic)::value;
-    const int64_t mb = mw + i * 32 + 4 * gh;
-    float ra_[16], rb_[16];
+  const int t = idx - 2 * BM;
+  const int64_t n = n0 + (t % BN);
+  if (n >= g.N) return 0.0f;
+  if (t < BN) return g.wa[n];
+  if (t < 2 * BN) return static_cast<float>(g.rs[n]);
+  return g.bias ? h2f(g.bias[n]) : 0.0f;
+}
+
+// Fast path: the wave's columns lie inside N, rows past M are dropped by the buffer range,
+// output rows are 8-byte aligned and the output fits a 31-bit byte range.
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue_fast(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
+                                                   int tm, int tn, int lane, const float* __restrict__ sc) {
+  const int c = lane & 31;
+  const int h = lane >> 5;
+  const float* rowA = sc;
+  const float* rowB = sc + BM;
+  const float* colS = sc + 2 * BM;
+  const float* colR = colS + BN;
+  const float* colB = colR + BN;
+  const __amdgpu_buffer_rsrc_t ry = buf_rsrc(g.y, g.M * g.ldy * 2);
+  float ra[TM], rb[TM];
+  uint32_t yo[TM];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t m = mb + 8 * (r >> 2) + (r & 3);
-      const int64_t mc = m < g.M ? m : g.M - 1;
-      ra_[r] = g.xa[mc];
-      rb_[r] = g.xb[mc];
+  for (int i = 0; i < TM; ++i) {
+    const int r = (tm + i) * 32 + c;
+    ra[i] = rowA[r];
+    rb[i] = rowB[r];
+    const int64_t m = mw + i * 32 + c;
+    yo[i] = m < g.M ? static_cast<uint32_t>((m * g.ldy + nw + 4 * h) * 2) : 0x80000000u;
+  }
+  static_for<TN>([&](auto jc) {
+    constexpr int j = decltype(jc)::value;
+    float s[16], w[16], bv[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cb = (tn + j) * 32 + 8 * q + 4 * h;
+      const float4 sv = *reinterpret_cast<const float4*>(colS + cb);
+      const float4 rv = *reinterpret_cast<const float4*>(colR + cb);
+      const float4 bb = *reinterpret_cast<const float4*>(colB + cb);
+      const float s4[4] = {sv.x, sv.y, sv.z, sv.w}, r4[4] = {rv.x, rv.y, rv.z, rv.w}, b4[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[4 * q + e] = s4[e];
+        w[4 * q + e] = __fmul_rn(s4[e], r4[e]);
+        bv[4 * q + e] = b4[e];
+      }
     }
-    static_for<TN>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t pk[2];
+#pragma unroll
+        for (int e2 = 0; e2 < 2; ++e2) {
+          float yv[2];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int r = 4 * q + 2 * e2 + u;
+            const float t = __fmul_rn(s[r], static_cast<float>(acc[i][j][r]));
+            yv[u] = fp32_result(__fmaf_rn(ra[i], t, __fmaf_rn(rb[i], w[r], bv[r])));  // bias 0 without one
+          }
+          pk[e2] = f2h2(yv[0], yv[1]);
+        }
+        __builtin_amdgcn_raw_buffer_store_b64(v2u{pk[0], pk[1]}, ry, static_cast<int>(yo[i] + (j * 32 + 8 * q) * 2), 0, 0);
+      }
+    }
+  });
+}
+
+// Checked path: edge tiles, unaligned or large outputs, and the raw accumulator output.
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue_checked(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw,
+                                                      int64_t nw, int tm, int tn, int lane, const float* __restrict__ sc) {
+  const int c = lane & 31;
+  const int h = lane >> 5;
+  const float* rowA = sc;
+  const float* rowB = sc + BM;
+  const float* colS = sc + 2 * BM;
+  const float* colR = colS + BN;
+  const float* colB = colR + BN;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t m = mw + i * 32 + c;
+    if (m >= g.M) continue;
+    const float ra = rowA[(tm + i) * 32 + c], rb = rowB[(tm + i) * 32 + c];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int a = acc[i][j][r] >> 4;
-        float yv = __fmaf_rn(__fmul_rn(ra_[r], csn[j]), static_cast<float>(a), __fmul_rn(rb_[r], cwr[j]));
-        if (g.bias) yv = __fadd_rn(yv, cbn[j]);
-        const int row = i * 32 + 8 * (r >> 2) + 4 * gh + (r & 3);
-        stage[row * PITCH + j * 32 + c] = static_cast<uint16_t>(f2h(yv));
-      }
-    });
-  });
-  // each row of the wave's block is TN * 4 chunks of 8 columns
-  constexpr int CPR = TN * 4;
-  constexpr int ITER = TM * 32 * CPR / 64;
-#pragma unroll
-  for (int t = 0; t < ITER; ++t) {
-    const int idx = t * 64 + lane;
-    const int row = idx / CPR;
-    const int ch = idx % CPR;
-    const v4u v = *reinterpret_cast<const v4u*>(stage + row * PITCH + ch * 8);
-    const int64_t m = mw + row;
-    const int64_t n = nw + ch * 8;
-    if (m < g.M) {
-      uint16_t* dst = g.y + m * g.ldy + n;
-      if (n + 8 <= g.N) {
-        *reinterpret_cast<v4u*>(dst) = v;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (n + e < g.N) dst[e] = static_cast<uint16_t>((v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+        const int cl = (tn + j) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const int64_t n = nw + j * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (n >= g.N) continue;
+        const float s = colS[cl];
+        const float t = __fmul_rn(s, static_cast<float>(acc[i][j][r]));
+        const float yv = fp32_result(__fmaf_rn(ra, t, __fmaf_rn(rb, __fmul_rn(s, colR[cl]), colB[cl])));
+        g.y[m * g.ldy + n] = f2h(yv);
+        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = acc[i][j][r] >> 4;
       }
     }
   }
@@ -402,8 +473,6 @@ struct Ring {
   static constexpr int ADPW = ABLK / WAVES;  // block copies per wave per stage
   static constexpr int DPW = (ABLK + BBLK) / WAVES;
   static constexpr int STAGE = (ABLK + BBLK) * 1024;
-  static constexpr int EPI = WAVES * EpiStage<TM, TN>::BYTES;  // epilogue staging reuses the ring
-  static constexpr int LDS = NS * STAGE > EPI ? NS * STAGE : EPI;
   static_assert(ADPW * WAVES == ABLK && DPW * WAVES == ABLK + BBLK, "blocks split evenly over waves");
   static_assert(NS >= 2 && (NS - 1) * DPW <= 63, "outstanding copies fit the vmcnt counter");
 };
@@ -443,16 +512,16 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));
 }
 
-// LDS of a ring kernel with KS groups of waves splitting K: one ring per group, reused at
-// the end for the groups' exchange of partial sums and for the epilogue staging.
+// LDS of a ring kernel with KS groups of waves splitting K: one ring per group (reused at
+// the end for the groups' exchange of partial sums), then the tile's epilogue scales.
 template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int KS>
-constexpr int ring_lds() {
+struct RingLds {
   using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
-  constexpr int rings = KS * NS * R::STAGE;
-  constexpr int xch = KS == 1 ? 0 : KS * R::WAVES * (TM / 2) * TN * 16 * 64 * 4;
-  constexpr int epi = KS * R::WAVES * EpiStage<TM / KS, TN>::BYTES;
-  return rings > xch ? (rings > epi ? rings : epi) : (xch > epi ? xch : epi);
-}
+  static constexpr int RINGS = KS * NS * R::STAGE;
+  static constexpr int XCH = KS == 1 ? 0 : KS * R::WAVES * (TM / 2) * TN * 16 * 64 * 4;
+  static constexpr int SCALES = RINGS > XCH ? RINGS : XCH;  // byte offset of the scales
+  static constexpr int BYTES = SCALES + RingScales<R::BM, R::BN>::BYTES;
+};
 
 // KS = 2: two groups of WAVES_M x WAVES_N waves share the tile and split its k-stages in
 // two halves, each group with its own ring (twice the waves per SIMD when the tile count
@@ -463,8 +532,11 @@ template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE, int KS>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS, WPE)
 w4a4_gemm_ring(GemmArgs g) {
   using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
+  using L = RingLds<WAVES_M, WAVES_N, TM, TN, NS, KS>;
+  using SC = RingScales<R::BM, R::BN>;
   static_assert(KS == 1 || (KS == 2 && TM % 2 == 0), "K split of two needs an even TM");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  float* const scales = reinterpret_cast<float*>(lds + L::SCALES);
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wid / R::WAVES;   // K slice of this wave's group
@@ -527,7 +599,7 @@ w4a4_gemm_ring(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(E.a[i], E.b[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(E.b[j], E.a[i], acc[i][j], 0, 0, 0);
   };
   // ds_reads (NR of them) first, then one MFMA per PER expansion ops
   auto interleave = [&](auto nr) {
@@ -559,8 +631,23 @@ w4a4_gemm_ring(GemmArgs g) {
   // k-steps before their first expansion, operands are expanded one k-step ahead of their
   // MFMAs, and the stage sync sits in the second k-step, after the last read of the
   // current stage's slot (which the copy issued right after it refills).
+  // epilogue scales of the tile: loaded now, written to LDS after the first copies have
+  // landed (the main loop's barriers publish them)
+  constexpr int TT = R::THREADS * KS;
+  constexpr int SPT = (SC::COUNT + TT - 1) / TT;
+  float sv[SPT];
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) {
+    const int idx = static_cast<int>(threadIdx.x) + u * TT;
+    sv[u] = idx < SC::COUNT ? load_scale<R::BM, R::BN>(g, idx, m0, n0) : 0.0f;
+  }
   for (int s = 0; s < NS - 1; ++s) issue(s);
   sync();
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) {
+    const int idx = static_cast<int>(threadIdx.x) + u * TT;
+    if (idx < SC::COUNT) scales[idx] = sv[u];
+  }
   issue(NS - 1);
   RingPacked<TM, TN> P0, P1;
   RingOps<TM, TN> E0, E1;
@@ -594,16 +681,14 @@ w4a4_gemm_ring(GemmArgs g) {
   wait_vm_lgkm0<0>();
   asm volatile("" ::: "memory");
 
-  const bool vec = ((g.ldy & 7) == 0) && ((reinterpret_cast<uintptr_t>(g.y) & 15) == 0) && (g.dbg_acc == nullptr);
+  // fast epilogue: the tile's columns inside N, 8-byte aligned output rows, 31-bit output range
+  const bool fast = g.dbg_acc == nullptr && (g.ldy & 3) == 0 && (reinterpret_cast<uintptr_t>(g.y) & 7) == 0 &&
+                    g.M * g.ldy * 2 < (int64_t{1} << 31) && n0 + R::BN <= g.N;
   if constexpr (KS == 1) {
-    if (vec) {
-      __builtin_amdgcn_s_barrier();  // every wave is done with the ring; each now stages its own block
-      asm volatile("" ::: "memory");
-      uint16_t* stage = reinterpret_cast<uint16_t*>(lds + wave * EpiStage<TM, TN>::BYTES);
-      tile_epilogue_lds(g, acc, m0 + wm * 32, n0 + wn * 32, lane, stage);
-    } else {
-      tile_epilogue(g, acc, m0 + wm * 32, n0 + wn * 32, lane);
-    }
+    if (fast)
+      ring_epilogue_fast<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales);
+    else
+      ring_epilogue_checked<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales);
   } else {
     // group h finishes row blocks [h*HT, h*HT + HT) of the wave's block
     constexpr int HT = TM / 2;
@@ -639,11 +724,10 @@ w4a4_gemm_ring(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) part[i][j] = acc[h * HT + i][j];
       const int64_t mw = m0 + (wm + h * HT) * 32, nw = n0 + wn * 32;
-      if (vec)
-        tile_epilogue_lds(g, part, mw, nw, lane,
-                          reinterpret_cast<uint16_t*>(lds + wid * EpiStage<HT, TN>::BYTES));
+      if (fast)
+        ring_epilogue_fast<HT, TN, R::BM, R::BN>(g, part, mw, nw, wm + h * HT, wn, lane, scales);
       else
-        tile_epilogue(g, part, mw, nw, lane);
+        ring_epilogue_checked<HT, TN, R::BM, R::BN>(g, part, mw, nw, wm + h * HT, wn, lane, scales);
     };
     constexpr std::integral_constant<int, 0> lo{};
     constexpr std::integral_constant<int, 1> hi{};
@@ -651,8 +735,6 @@ w4a4_gemm_ring(GemmArgs g) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     if (grp == 0) take(lo); else take(hi);
-    __builtin_amdgcn_s_barrier();  // the exchange area is read; the epilogue staging reuses it
-    asm volatile("" ::: "memory");
     if (grp == 0) finish(lo); else finish(hi);
   }
 }
@@ -669,7 +751,7 @@ bool fits_ring(const GemmArgs& g) {
 template <int WM, int WN, int TM, int TN, int NS, int WPE = 1, int KS = 1>
 hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
   using R = Ring<WM, WN, TM, TN, NS>;
-  constexpr int LDS = ring_lds<WM, WN, TM, TN, NS, KS>();
+  constexpr int LDS = RingLds<WM, WN, TM, TN, NS, KS>::BYTES;
   static_assert(LDS <= 160 * 1024, "LDS of one CU");
   auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),

@@ -252,13 +252,16 @@ def gemm_case(M, N, K, seed, bias=True, sample_rows=None):
     wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
     rs = qw.sum(1).astype(np.int32)
     bi = (rng.standard_normal(N) * 0.1).astype(np.float16) if bias else None
-    y, acc = sq.w4a4_linear(dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa),
-                            dev(rs), dev(bi) if bias else None, dbg=True)
+    args = (dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs),
+            dev(bi) if bias else None)
+    y, acc = sq.w4a4_linear(*args, dbg=True)      # element-wise epilogue with the raw accumulators
     gy, gacc = host(y), host(acc)
     rows = np.arange(M) if sample_rows is None else sample_rows
     oy, oacc = olin.w4a4_linear(qa[rows], xa[rows], xb[rows], qw, wa, rs, bi)
     np.testing.assert_array_equal(gacc[rows], oacc)
     parity.assert_out_close(gy[rows], oy)
+    y_fast, _ = sq.w4a4_linear(*args)             # vector-store epilogue: same arithmetic
+    np.testing.assert_array_equal(host(y_fast), gy)
 
 
 @pytest.mark.parametrize("M,N,K", [(16, 256, 256), (37, 200, 320), (1, 8, 64), (130, 129, 128),
@@ -375,7 +378,7 @@ def test_kv_full_sampled():
 
 @pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "9", "10", "11", "12", "13", "14", "15", "16"])
 def test_gemm_tile_variants(variant, monkeypatch):
-    say(f"w4a4_linear tile variant {variant}: ragged shapes, paired and unpaired stores")
+    say(f"w4a4_linear tile variant {variant}: ragged shapes, vector and element-wise stores")
     monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
     for (M, N, K) in [(300, 390, 448), (64, 130, 192), (257, 257, 128), (520, 600, 320), (384, 264, 2112)]:
         rng = workloads.rng_for(M + N + K)
@@ -391,14 +394,14 @@ def test_gemm_tile_variants(variant, monkeypatch):
         y_dbg, acc = sq.w4a4_linear(*args, dbg=True)
         np.testing.assert_array_equal(host(acc), oacc)
         parity.assert_out_close(host(y_dbg), oy)
-        y_fast, _ = sq.w4a4_linear(*args)                      # paired 32-bit stores
+        y_fast, _ = sq.w4a4_linear(*args)                      # vector stores inside N
         np.testing.assert_array_equal(host(y_fast), host(y_dbg))
         wide = torch.zeros((M, N + 3), dtype=torch.float16, device=DEV)
-        sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: unpaired stores
+        sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: element-wise stores
         np.testing.assert_array_equal(host(wide[:, :N]), host(y_dbg))
         assert not host(wide[:, N:]).any()
-        w8 = (N + 1 + 7) // 8 * 8                              # ldy % 8 == 0: 16-byte row stores,
-        wide8 = torch.zeros((M, w8), dtype=torch.float16, device=DEV)   # column tail one by one
+        w8 = (N + 1 + 7) // 8 * 8                              # ldy % 8 == 0: vector stores,
+        wide8 = torch.zeros((M, w8), dtype=torch.float16, device=DEV)   # edge tiles element-wise
         sq.w4a4_linear(*args, out=wide8[:, :N])
         np.testing.assert_array_equal(host(wide8[:, :N]), host(y_dbg))
         assert not host(wide8[:, N:]).any()
