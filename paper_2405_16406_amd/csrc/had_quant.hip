@@ -238,10 +238,16 @@ quant_rows_identity(RotQuantArgs args) {
   for (int j = 0; j < CHMAX; ++j) {
     const int ch = threadIdx.x + j * T;
     if (ch < nchunk) {
-      uint32_t word = 0;
+      // eq. 1's t = (v - mn) * inv, rounded after each step; v_cvt_pk_u8_f32 rounds half to
+      // even and saturates, and 0 <= t <= 15 (1 + 3 eps), so its byte is clamp(rint(t), 0, 15).
+      // Even positions go to ev, odd ones to od; ev | od << 4 is the nibble-packed word.
+      uint32_t ev = 0, od = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) word |= asym_code(v[j][i], p) << (4 * i);
-      qrow[ch] = word;
+      for (int i = 0; i < 4; ++i) {
+        ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i], p.mn), p.inv), i, ev);
+        od = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i + 1], p.mn), p.inv), i, od);
+      }
+      qrow[ch] = ev | (od << 4);
       if (args.dbg) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) args.dbg[row * args.K + ch * 8 + i] = v[j][i];

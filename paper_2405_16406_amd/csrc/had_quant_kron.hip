@@ -411,52 +411,71 @@ had_quant_kron(RotQuantArgs args) {
   }
 }
 
-// ---------------------------------------------------------------- row-pair kernel
-// Two waves share a row; a workgroup of 8 waves (two per SIMD) works on 4 rows at a
-// time, one LDS slot per row, one workgroup per CU.
-//   * Fold F: the top log2(F) bits of i_b join the dense factor, D = H_a (x) S_F acting on
-//     (i_a, i_b_hi), so the Sylvester part left is S_{B/F} over i_b_lo and a wave's share
-//     of the row fits in its registers (F = 2 for H_28 (x) S_512).  The MFMA N tiles are
-//     the columns of D (NT of them, NT/F per value of j_b_hi); each wave of the pair takes
-//     NT/2 of them, so neither wave needs the other's values.
-//   * the B fragments of D (fp16 +-1) sit in LDS, built once per workgroup;
+// ---------------------------------------------------------------- row-pair kernel (b = 64)
+// Rows of K = A * 64 (H_A (x) S_64).  Two waves share a row; a workgroup of 8 waves (two
+// per SIMD) works on 4 rows at a time, one LDS slot per row, one workgroup per CU.
+//   * slot: the row as APAD lines of 128 bytes (64 fp16, one i_a each), lines A..APAD-1
+//     zero; on odd lines the two 64-byte halves are swapped, so that the 8 lines one
+//     transposing read touches fall evenly on the two bank halves;
+//   * A fragments (8 consecutive i_a of one column i_b) come from two ds_read_b64_tr_b16:
+//     within each 16-lane group the instruction hands lane i element e = word i % 4 of the
+//     8-byte segment addressed by lane 4e + i / 4, so lane s addresses line
+//     kbase + 4t + s / 4, columns 4 (s % 4) .. +3 of its half (t = 0, 1: k 0-3 and 4-7);
+//   * the B fragments of H_A (fp16 +-1) sit in LDS, built once per workgroup; each wave of
+//     the pair takes NT/2 of the MFMA N tiles (the columns j_a), so neither wave needs the
+//     other's values;
 //   * the next rows are loaded with 16-byte loads into registers while the current rows
 //     are transformed, and written to their slots once both waves of a row have read it;
-//   * A fragments are gathered from the slot one step ahead of their MFMAs;
-//   * Sylvester stages over i_b_lo in registers, plus one lane-half stage by
+//   * Sylvester stages over i_b in registers, plus one lane-half stage by
 //     v_permlane32_swap; per-row min/max (the two waves of a row meet in LDS); codes use
 //     one fma per value and v_cvt_pk_u8_f32 (round half to even), which can move a code
-//     by one only on a rounding boundary.
-template <int A, int APAD, int NT, int B, int F>
+//     by one only on a rounding boundary;
+//   * the two waves of a row synchronise with each other only (progress counters in LDS),
+//     never with the other rows' waves, so each pair starts as soon as its own row is in.
+template <int A, int APAD, int NT>
 struct Pair {
+  static constexpr int B = 64;
   static constexpr int K = A * B;
-  static constexpr int BL = B / F;            // Sylvester order left over i_b_lo
-  static constexpr int KS = F * APAD / 16;    // k-steps of the dense stage over (i_b_hi, i_a)
-  static constexpr int MT = BL / 32;          // M tiles (32 i_b_lo each)
+  static constexpr int KS = APAD / 16;        // k-steps of the dense stage over i_a
+  static constexpr int MT = 2;                // M tiles (32 i_b each)
   static constexpr int NTW = NT / 2;          // N tiles per wave
-  static constexpr int NTF = NT / F;          // N tiles per value of j_b_hi
   static constexpr int ROWS = 4;              // rows per workgroup iteration
   static constexpr int THREADS = 64 * 2 * ROWS;
   static constexpr int CHUNKS = K / 8;                   // 16-byte chunks of a row
   static constexpr int PF = (CHUNKS + 127) / 128;        // chunks per lane of the wave pair
   static constexpr int HFRAG = KS * NT * 64;             // 16-byte B fragments
-  static constexpr int SLOT = K * 2;                     // bytes of one staged row
+  static constexpr int SLOT = APAD * 128;                // bytes of one staged row
+  static constexpr int ZERO_CHUNKS = (APAD - A) * 8;     // zero padding lines of a slot
   static constexpr int RED = 2 * ROWS * 2 * 2;           // floats: [parity][row][wave][min,max]
-  static constexpr int LDS = HFRAG * 16 + ROWS * SLOT + RED * 4;
-  static_assert(F == 1 || F == 2, "fold of at most one bit");
-  static_assert(NT % 2 == 0 && NT % F == 0 && BL % 32 == 0 && MT >= 2 && (MT & (MT - 1)) == 0, "tiling");
-  static_assert(APAD % 16 == 0 && APAD >= A && NTF * 32 >= A, "padding");
-  static_assert(K % 8 == 0, "16-byte row staging");
+  static constexpr int FLAGS = 2 * ROWS * 2;             // ints: [kind][row][wave] progress counters
+  static constexpr int LDS = HFRAG * 16 + ROWS * SLOT + RED * 4 + FLAGS * 4;
+  static_assert(NT % 2 == 0 && NT * 32 >= A, "N tiles");
+  static_assert(APAD % 16 == 0 && APAD >= A && A % 4 == 0, "padding");
+  static_assert(ZERO_CHUNKS <= 128, "one zero chunk per thread of a wave pair");
 };
 
-template <int A, int APAD, int NT, int B, int F, bool DBG>
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+// Progress counter of wave `me` of a row pair: published after the wave's LDS writes, and
+// awaited (counter of the partner wave >= target) before reading what the partner wrote.
+__device__ __forceinline__ void pair_publish(int* flag, int value) {
+  __hip_atomic_store(flag, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void pair_wait(const int* flag, int target) {
+  while (__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < target)
+    __builtin_amdgcn_s_sleep(1);
+}
+
+template <int A, int APAD, int NT, bool DBG>
 __global__ void __launch_bounds__(512, 2)
 had_quant_pair(RotQuantArgs args) {
-  using C = Pair<A, APAD, NT, B, F>;
+  using C = Pair<A, APAD, NT>;
+  constexpr int B = C::B;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   v8h* hf = reinterpret_cast<v8h*>(smem);
   unsigned char* slots = smem + C::HFRAG * 16;
   float* red = reinterpret_cast<float*>(smem + C::HFRAG * 16 + C::ROWS * C::SLOT);
+  int* flags = reinterpret_cast<int*>(smem + C::HFRAG * 16 + C::ROWS * C::SLOT + C::RED * 4);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int p = wave >> 1;  // row slot
@@ -483,51 +502,99 @@ had_quant_pair(RotQuantArgs args) {
   auto store_row = [&]() {
 #pragma unroll
     for (int j = 0; j < C::PF; ++j) {
-      const int i = pl + 128 * j;
-      if (i < C::CHUNKS) reinterpret_cast<v4u*>(slot)[i] = pf[j];
+      const int i = pl + 128 * j;  // line i / 8, chunk i % 8; odd lines swap their halves
+      if (i < C::CHUNKS) reinterpret_cast<v4u*>(slot)[i ^ ((i & 8) >> 1)] = pf[j];
     }
   };
+  // ---- H_A (int8 [A][A]) with coalesced 16-byte loads, issued before the first rows so
+  //      that waiting for it does not wait for them; staged as bytes in the (still empty)
+  //      slot area, from which the MFMA B fragments are built while the rows are in flight
+  constexpr int HCH = (A * A + 15) / 16;                  // 16-byte chunks of H
+  constexpr int HPT = (HCH + C::THREADS - 1) / C::THREADS;
+  static_assert(HCH * 16 <= C::ROWS * C::SLOT, "H staging fits the slots");
+  v4u hv[HPT];
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) {
+    const int i = threadIdx.x + j * C::THREADS;
+    if (i < HCH) {
+      if (i * 16 + 16 <= A * A) {
+        hv[j] = reinterpret_cast<const v4u*>(args.H)[i];
+      } else {  // the tail chunk, byte by byte
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        for (int b = 0; i * 16 + b < A * A; ++b)
+          w[b >> 2] |= static_cast<uint32_t>(static_cast<uint8_t>(args.H[i * 16 + b])) << (8 * (b & 3));
+        hv[j] = v4u{w[0], w[1], w[2], w[3]};
+      }
+    }
+  }
   {  // the first rows are in flight while D is built
     const int64_t r0 = rs * C::ROWS + p;
     load_row(r0 < rows ? r0 : rows - 1);
   }
-
-  // ---- D = H_a (x) S_F as MFMA B fragments: hf[(ks*NT + nt)*64 + l][e] = D[k][n] with
-  //      k = ks*16 + 8*(l/32) + e = i_b_hi*APAD + i_a and n = nt*32 + l%32, column
-  //      (j_b_hi, j_a) = (nt / NTF, (nt % NTF)*32 + l%32); zero where i_a or j_a >= A.
-  //      A thread owns one column (nt, l) and reads its entries of H straight from global
-  //      memory (indexes clamped into H, padding selected to zero afterwards).
-  for (int i = threadIdx.x; i < NT * 64; i += C::THREADS) {
-    const int l = i & 63;
-    const int nt = i >> 6;
-    const int jb = nt / C::NTF;
-    const int ja = (nt % C::NTF) * 32 + (l & 31);
-    const int g8 = 8 * (l >> 5);
-    const int8_t* hcol = args.H + (ja < A ? ja : A - 1);
-    static_for<C::KS>([&](auto kc) {
-      constexpr int ks = decltype(kc)::value;
-      constexpr int ib = (ks * 16) / APAD;  // a k-step never straddles two values of i_b_hi
-      constexpr int ia0 = (ks * 16) % APAD;
-      const float sgn = (ib & jb) ? -1.0f : 1.0f;
-      v8h f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int ia = ia0 + g8 + e;
-        const float hv = static_cast<float>(hcol[(ia < A ? ia : A - 1) * A]);
-        f[e] = (ia < A && ja < A) ? static_cast<_Float16>(sgn * hv) : static_cast<_Float16>(0.0f);
-      }
-      hf[(ks * NT + nt) * 64 + l] = f;
-    });
+  for (int j = 0; j < HPT; ++j) {
+    const int i = threadIdx.x + j * C::THREADS;
+    if (i < HCH) reinterpret_cast<v4u*>(slots)[i] = hv[j];
   }
-  store_row();
+  if (threadIdx.x < C::FLAGS) flags[threadIdx.x] = 0;
   __syncthreads();
 
-  // A fragment (M tile mt, k-step ks) from the slot: X[(i_a, i_b_hi)][i_b_lo] with
-  // i_b_hi = ks*16 / APAD (a k-step never straddles two values), i_a = (ks*16) % APAD +
-  // 8g + e, i_b_lo = mt*32 + c, element i_a*B + i_b_hi*BL + i_b_lo; zero for i_a >= A
-  const uint16_t* srow = reinterpret_cast<const uint16_t*>(slot) + c;
+  // ---- H_A as MFMA B fragments: hf[(ks*NT + nt)*64 + l][e] = H[k][n] with k = ks*16 +
+  //      8*(l/32) + e and n = nt*32 + l%32; zero where k or n >= A.  A thread owns one column
+  //      (nt, l) of the staged bytes.
+  {
+    const int8_t* hs = reinterpret_cast<const int8_t*>(slots);
+    for (int i = threadIdx.x; i < NT * 64; i += C::THREADS) {
+      const int l = i & 63;
+      const int nt = i >> 6;
+      const int ja = nt * 32 + (l & 31);
+      const int g8 = 8 * (l >> 5);
+      const int8_t* hcol = hs + (ja < A ? ja : A - 1);
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        v8h f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int ia = ks * 16 + g8 + e;
+          const float hv1 = static_cast<float>(hcol[(ia < A ? ia : A - 1) * A]);
+          f[e] = (ia < A && ja < A) ? static_cast<_Float16>(hv1) : static_cast<_Float16>(0.0f);
+        }
+        hf[(ks * NT + nt) * 64 + l] = f;
+      }
+    }
+  }
+  __syncthreads();  // the staged bytes are no longer read: the slots take the rows
+  if (pl < C::ZERO_CHUNKS)  // the pair's padding lines i_a >= A: zero, never rewritten
+    reinterpret_cast<v4u*>(slot)[A * 8 + pl] = v4u{0u, 0u, 0u, 0u};
+  // flags[k*2*ROWS + p*2 + h]: k = 0: min/max of iteration it published (it + 1);
+  //                            k = 1: rows of iteration it stored to the slot (it + 1)
+  int* const mine0 = flags + p * 2 + h;
+  int* const mine1 = flags + 2 * C::ROWS + p * 2 + h;
+  const int* const other0 = flags + p * 2 + (h ^ 1);
+  const int* const other1 = flags + 2 * C::ROWS + p * 2 + (h ^ 1);
+  // each pair starts as soon as its own first row is in its slot (counter value 1 before
+  // iteration 0; later iterations publish it + 1 for the rows of iteration it + 1)
+  store_row();
+  if (lane == 0) pair_publish(mine1, 1);
+  pair_wait(other1, 1);
+
+  // transposing reads of A fragments: lane (group G = lane/16, s = lane%16) addresses line
+  // 8*(G/2) + 4t + s/4 (+ 16 ks) and columns 32*mt + 16*(G%2) + 4*(s%4), whose half is
+  // swapped when the line is odd (s/4 odd)
+  const int tg = lane >> 4, ts = lane & 15;
+  const int tq = ts >> 2;
+  uint32_t tbase[C::MT];
+#pragma unroll
+  for (int mt = 0; mt < C::MT; ++mt)
+    tbase[mt] = static_cast<uint32_t>(p * C::SLOT + (8 * (tg >> 1) + tq) * 128 +
+                                      ((32 * (mt ^ (tq & 1))) + 16 * (tg & 1) + 4 * (ts & 3)) * 2);
   auto frag = [&](int mt, int ks) {
-    return gather_afrag<A, B>(srow + ((ks * 16) / APAD) * C::BL + mt * 32, (ks * 16) % APAD + 8 * g);
+    const unsigned char* a0 = slots + tbase[mt] + ks * 16 * 128;
+    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) v4s*>(reinterpret_cast<uintptr_t>(a0)));
+    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) v4s*>(reinterpret_cast<uintptr_t>(a0 + 4 * 128)));
+    return __builtin_bit_cast(v8h, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
   const float s_n = args.inv_sqrt_n;
@@ -540,9 +607,8 @@ had_quant_pair(RotQuantArgs args) {
       load_row(nr < rows ? nr : rows - 1);
     }
 
-    // ---- dense stage: acc[mt][nt] = X^T D for i_b_lo tile mt, D column tile h*NTW + nt.
-    //      Few M tiles: k-step outer, all M tiles' fragments gathered a step ahead; many M
-    //      tiles: M tile outer, one fragment gathered ahead (fewer live registers).
+    // ---- dense stage: acc[mt][nt] = X2^T H for i_b tile mt, H column tile h*NTW + nt;
+    //      both M tiles' fragments read a k-step ahead
     v16f acc[C::MT][C::NTW];
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
@@ -550,45 +616,35 @@ had_quant_pair(RotQuantArgs args) {
       for (int nt = 0; nt < C::NTW; ++nt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[mt][nt][r] = 0.0f;
-    if constexpr (C::MT <= 2) {
-      v8h a0[C::MT], a1[C::MT];
+    {
+      // A and B fragments of k-step ks + 1 are read while the MFMAs of k-step ks run
+      v8h a0[C::MT], a1[C::MT], b0[C::NTW], b1[C::NTW];
+      const v8h* hb = hf + h * C::NTW * 64 + lane;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt) a0[mt] = frag(mt, 0);
+#pragma unroll
+      for (int nt = 0; nt < C::NTW; ++nt) b0[nt] = hb[nt * 64];
       static_for<C::KS>([&](auto kc) {
         constexpr int ks = decltype(kc)::value;
         v8h(&cur)[C::MT] = (ks & 1) ? a1 : a0;
         v8h(&nxt)[C::MT] = (ks & 1) ? a0 : a1;
+        v8h(&bcur)[C::NTW] = (ks & 1) ? b1 : b0;
+        v8h(&bnxt)[C::NTW] = (ks & 1) ? b0 : b1;
         if constexpr (ks + 1 < C::KS) {
 #pragma unroll
           for (int mt = 0; mt < C::MT; ++mt) nxt[mt] = frag(mt, ks + 1);
-        }
-        v8h bf[C::NTW];
 #pragma unroll
-        for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
+          for (int nt = 0; nt < C::NTW; ++nt) bnxt[nt] = hb[((ks + 1) * NT + nt) * 64];
+        }
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
           for (int nt = 0; nt < C::NTW; ++nt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[mt], bf[nt], acc[mt][nt], 0, 0, 0);
-      });
-    } else {
-      v8h fa[2];
-      fa[0] = frag(0, 0);
-      static_for<C::MT * C::KS>([&](auto tc) {
-        constexpr int t = decltype(tc)::value;
-        constexpr int mt = t / C::KS;
-        constexpr int ks = t % C::KS;
-        if constexpr (t + 1 < C::MT * C::KS) fa[(t + 1) & 1] = frag((t + 1) / C::KS, (t + 1) % C::KS);
-        v8h bf[C::NTW];
-#pragma unroll
-        for (int nt = 0; nt < C::NTW; ++nt) bf[nt] = hf[(ks * NT + h * C::NTW + nt) * 64 + lane];
-#pragma unroll
-        for (int nt = 0; nt < C::NTW; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t & 1], bf[nt], acc[mt][nt], 0, 0, 0);
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[mt], bcur[nt], acc[mt][nt], 0, 0, 0);
       });
     }
 
-    // ---- Sylvester stages over i_b_lo: register bits 0, 1, 3, 4; M tile bits 5..; lane half bit 2
+    // ---- Sylvester stages over i_b: register bits 0, 1, 3, 4; M tile bit 5; lane half bit 2
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -604,23 +660,18 @@ had_quant_pair(RotQuantArgs args) {
               acc[mt][nt][r + rb] = hi;
             }
 #pragma unroll
-    for (int tb = 1; tb < C::MT; tb <<= 1)
+    for (int nt = 0; nt < C::NTW; ++nt)
 #pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt)
-        if ((mt & tb) == 0)
-#pragma unroll
-          for (int nt = 0; nt < C::NTW; ++nt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              float lo = acc[mt][nt][r], hi = acc[mt + tb][nt][r];
-              bfly(lo, hi);
-              acc[mt][nt][r] = lo;
-              acc[mt + tb][nt][r] = hi;
-            }
-    // lane-half stage (i_b_lo bit 2): v_permlane32_swap of registers r and r + 8 (r < 8)
-    // puts both bit-2 partners of register r (lanes 0-31) or r + 8 (lanes 32-63) in one
-    // lane; the butterfly then leaves lane (c, g) holding i_b_lo = mt*32 + 16g + j in
-    // acc[mt][nt][j], j = 8q + 4*bit2 + e, sixteen consecutive positions
+      for (int r = 0; r < 16; ++r) {
+        float lo = acc[0][nt][r], hi = acc[1][nt][r];
+        bfly(lo, hi);
+        acc[0][nt][r] = lo;
+        acc[1][nt][r] = hi;
+      }
+    // lane-half stage (i_b bit 2): v_permlane32_swap of registers r and r + 8 (r < 8) puts
+    // both bit-2 partners of register r (lanes 0-31) or r + 8 (lanes 32-63) in one lane;
+    // the butterfly then leaves lane (c, g) holding i_b = mt*32 + 16g + j in acc[mt][nt][j],
+    // j = 8q + 4*bit2 + e, sixteen consecutive positions
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
@@ -640,31 +691,40 @@ had_quant_pair(RotQuantArgs args) {
         for (int j = 0; j < 16; ++j) acc[mt][nt][j] = o[j];
       }
 
-    // ---- per-row min/max over real columns; the two waves of the row meet in LDS
+    // ---- per-row min/max over real columns (a lane's columns past A hold zeros: merged
+    //      per tile under one condition); the two waves of the row meet in LDS
     float mn = INFINITY, mx = -INFINITY;
 #pragma unroll
     for (int nt = 0; nt < C::NTW; ++nt) {
-      if (((h * C::NTW + nt) % C::NTF) * 32 + c < A) {
+      float tmn = acc[0][nt][0], tmx = acc[0][nt][0];
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
+      for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            mn = fminf(mn, acc[mt][nt][r]);
-            mx = fmaxf(mx, acc[mt][nt][r]);
-          }
+        for (int r = 0; r < 16; ++r) {
+          tmn = fminf(tmn, acc[mt][nt][r]);
+          tmx = fmaxf(tmx, acc[mt][nt][r]);
+        }
+      if ((h * C::NTW + nt) * 32 + 32 <= A || (h * C::NTW + nt) * 32 + c < A) {
+        mn = fminf(mn, tmn);
+        mx = fmaxf(mx, tmx);
       }
     }
     mn = wave_min(mn);
     mx = wave_max(mx);
-    float* rd = red + (it & 1) * (C::ROWS * 4);  // parity buffers
+    // the two waves of the row meet: parity buffers, so a wave can be one iteration ahead
+    float* rd = red + (it & 1) * (C::ROWS * 4);
     if (lane == 0) {
       rd[(p * 2 + h) * 2] = mn;
       rd[(p * 2 + h) * 2 + 1] = mx;
+      pair_publish(mine0, it + 1);
     }
-    __syncthreads();  // also: both waves of every row are done reading its slot
+    pair_wait(other0, it + 1);  // also: the partner is done reading the slot
     mn = fminf(rd[p * 4], rd[p * 4 + 2]);
     mx = fmaxf(rd[p * 4 + 1], rd[p * 4 + 3]);
-    if (more) store_row();
+    if (more) {
+      store_row();
+      if (lane == 0) pair_publish(mine1, it + 2);
+    }
 
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
     const float r_u = __fsub_rn(mx, mn);
@@ -677,16 +737,13 @@ had_quant_pair(RotQuantArgs args) {
       args.beta[row] = __fmul_rn(mn, s_n);
     }
 
-    // ---- codes: lane (c, g) holds i_b_lo = mt*32 + 16g + j (j = 0..15) of column
-    // (j_b_hi, j_a): bytes via v_cvt_pk_u8_f32 (even j in ev, odd j in od), ev | od << 4
-    // is then four nibble-packed bytes; 8-byte store at output position
-    // j_a*B + j_b_hi*BL + mt*32 + 16g.
+    // ---- codes: lane (c, g) holds i_b = mt*32 + 16g + j (j = 0..15) of column j_a: bytes
+    // via v_cvt_pk_u8_f32 (even j in ev, odd j in od), ev | od << 4 is then four
+    // nibble-packed bytes; 8-byte store at output position j_a*64 + mt*32 + 16g.
     uint8_t* qrow = args.q + row * (C::K / 2);
 #pragma unroll
     for (int nt = 0; nt < C::NTW; ++nt) {
-      const int ntg = h * C::NTW + nt;
-      const int ja = (ntg % C::NTF) * 32 + c;
-      const int jb = ntg / C::NTF;
+      const int ja = (h * C::NTW + nt) * 32 + c;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt) {
         uint32_t w[2];
@@ -700,7 +757,7 @@ had_quant_pair(RotQuantArgs args) {
           }
           w[hw] = ev | (od << 4);
         }
-        const int pos = ja * B + jb * C::BL + mt * 32 + 16 * g;
+        const int pos = ja * B + mt * 32 + 16 * g;
         if (valid && ja < A) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(w[0], w[1]);
         if constexpr (DBG) {
           if (valid && ja < A) {
@@ -710,7 +767,7 @@ had_quant_pair(RotQuantArgs args) {
         }
       }
     }
-    __syncthreads();  // the slots hold the next rows for every wave
+    if (more) pair_wait(other1, it + 2);  // the slot holds the next row, both halves
   }
 }
 
@@ -752,10 +809,10 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
                : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
 }
 
-template <int A, int APAD, int NT, int B, int F, bool DBG>
+template <int A, int APAD, int NT, bool DBG>
 hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
-  using C = Pair<A, APAD, NT, B, F>;
-  auto kern = had_quant_pair<A, APAD, NT, B, F, DBG>;
+  using C = Pair<A, APAD, NT>;
+  auto kern = had_quant_pair<A, APAD, NT, DBG>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (init != hipSuccess) return init;
@@ -765,9 +822,9 @@ hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
 
-template <int A, int APAD, int NT, int B, int F>
+template <int A, int APAD, int NT>
 hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
-  return a.dbg ? launch_pair_t<A, APAD, NT, B, F, true>(a, stream) : launch_pair_t<A, APAD, NT, B, F, false>(a, stream);
+  return a.dbg ? launch_pair_t<A, APAD, NT, true>(a, stream) : launch_pair_t<A, APAD, NT, false>(a, stream);
 }
 
 }  // namespace
@@ -776,12 +833,11 @@ hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
   // the pair kernel stages rows in 16-byte chunks
-  const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 && !getenv("SQ_KRON_STAGED");
-  // H_28 (x) S_512: the pair kernel with a one-bit fold (launch_pair<28, 32, 2, 512, 2>) is
-  // correct but slower here than the staged kernel (63 vs 59 us at 4096 rows)
+  const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && !getenv("SQ_KRON_STAGED");
   if (a.a == 28 && a.b == 512) return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
   if (a.a == 172 && a.b == 64) {
-    if (pair_ok) return launch_pair<172, 176, 6, 64, 1>(a, stream);
+    if (pair_ok) return launch_pair<172, 176, 6>(a, stream);
     return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
   }
   if (a.a == 28 && a.b == 1024) return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
