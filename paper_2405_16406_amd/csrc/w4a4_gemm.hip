@@ -831,11 +831,170 @@ w4a4_gemm_v1(GemmArgs g) {
     for (int i = 0; i < 2; ++i) store_block(g, acc[i][j], m0 + wm + i * 32, n0 + wn + j * 32 + (lane & 31), lane);
 }
 
+// ------------------------------------------------------------------ decode-sized kernel
+// M <= 16 (token-at-a-time decoding): the GEMM streams the packed weights once from HBM and
+// the activations (M x K/2 bytes) stay in L2.  A workgroup owns 16 * NB weight rows (NB
+// blocks of 16 output columns; NB is chosen so that there is about one workgroup per CU) and
+// its 8 waves split the K range; each wave streams its share of the rows straight into
+// registers, SD 64-byte steps ahead.  In a 64-byte step of a row (128 codes) lane
+// l = 16 s + r loads the 16 bytes at offset 16 s of activation row r and of weight rows
+// n0 + 16 j + r; both operands expand in the same nibble order into two
+// v_mfma_i32_16x16x64_i8 k-steps (lane l holds k-slots 16 s .. 16 s + 15 of row r), so the dot
+// product is unchanged.  Rows past M or N and bytes past K are out of their buffer ranges and
+// read as zeros.  The 8 partial sums are added in LDS; lane n + 16 (m / 4), register m % 4 of
+// a block holds D[m][n].
+template <int NB, int SD>
+struct Skinny {
+  static constexpr int WAVES = 8;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int BN = 16 * NB;
+  static constexpr int LDS = WAVES * NB * 4 * 64 * 4;  // partial sums: [wave][block][reg][lane] int32
+};
+
+template <int NB, int SD>
+__global__ void __launch_bounds__(512)
+w4a4_gemm_skinny(GemmArgs g) {
+  using S = Skinny<NB, SD>;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  int* const part = reinterpret_cast<int*>(lds);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15;
+  const int sg = lane >> 4;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * S::BN;
+  const uint32_t KB = static_cast<uint32_t>(g.K / 2);
+  // k range of this wave in bytes, whole 64-byte steps
+  const uint32_t kw = ((KB + S::WAVES * 64 - 1) / (S::WAVES * 64)) * 64;
+  const uint32_t k0 = wave * kw;
+  const int nsteps = static_cast<int>(kw / 64);
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
+  const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq, g.N * KB);
+  const uint32_t arow = static_cast<uint32_t>(r) * KB;
+  uint32_t brow[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) brow[j] = static_cast<uint32_t>(n0 + 16 * j + r) * KB;
+
+  v4u ra[SD], rb[SD][NB];
+  auto load = [&](int slot, int t) {
+    const uint32_t k = k0 + static_cast<uint32_t>(t) * 64 + 16 * sg;
+    const bool ok = k < KB && k < k0 + kw;
+    ra[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? arow + k : 0x80000000u, 0, 0));
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      rb[slot][j] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? brow[j] + k : 0x80000000u, 0, 0));
+  };
+  v4i acc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) acc[j] = v4i{0, 0, 0, 0};
+  auto step = [&](int slot) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const uint32_t a0 = ra[slot][2 * hh], a1 = ra[slot][2 * hh + 1];
+      const v4i ea = {static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
+                      static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const uint32_t b0 = rb[slot][j][2 * hh], b1 = rb[slot][j][2 * hh + 1];
+        const v4i eb = {static_cast<int>((b0 << 4) & 0xF0F0F0F0u), static_cast<int>(b0 & 0xF0F0F0F0u),
+                        static_cast<int>((b1 << 4) & 0xF0F0F0F0u), static_cast<int>(b1 & 0xF0F0F0F0u)};
+        acc[j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ea, eb, acc[j], 0, 0, 0);
+      }
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < SD; ++d) load(d, d);
+  for (int t0 = 0; t0 < nsteps; t0 += SD) {
+    static_for<SD>([&](auto dc) {
+      constexpr int d = decltype(dc)::value;
+      // branch-free: steps past the wave's range are loaded out of range (zeros) and add nothing
+      step(d);
+      load(d, t0 + d + SD);
+    });
+  }
+
+  // partial sums of the 8 waves meet in LDS; wave 0 adds them and runs the epilogue
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[((wave * NB + j) * 4 + i) * 64 + lane] = acc[j][i];
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 1; w < S::WAVES; ++w)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[j][i] += part[((w * NB + j) * 4 + i) * 64 + lane];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t n = n0 + 16 * j + r;
+    if (n >= g.N) continue;
+    const float sn = g.wa[n];
+    const float wn = __fmul_rn(sn, static_cast<float>(g.rs[n]));
+    const float bn = g.bias ? h2f(g.bias[n]) : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = 4 * sg + i;
+      if (m >= g.M) continue;
+      // same arithmetic as the ring kernel's epilogue (acc holds 16 * sum)
+      const float t = __fmul_rn(sn, static_cast<float>(acc[j][i]));
+      const float yv = fp32_result(__fmaf_rn(__fmul_rn(g.xa[m], 0.0625f), t, __fmaf_rn(g.xb[m], wn, bn)));
+      g.y[m * g.ldy + n] = f2h(yv);
+      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = acc[j][i] >> 4;
+    }
+  }
+}
+
+// Prefetch steps: (NB + 1) 16-byte loads per step.
+template <int NB>
+constexpr int skinny_depth() {
+  return NB <= 4 ? 32 / (NB + 1) : 24 / (NB + 1);
+}
+
+template <int NB, int SD>
+bool fits_skinny(const GemmArgs& g) {
+  const int64_t kb = g.K / 2;
+  return g.M <= 16 && g.M * kb + 64 < (int64_t{1} << 31) && (g.N + 16 * NB) * kb + 64 < (int64_t{1} << 31);
+}
+
+template <int NB, int SD>
+hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
+  using S = Skinny<NB, SD>;
+  auto kern = w4a4_gemm_skinny<NB, SD>;
+  const dim3 grid(static_cast<unsigned>((g.N + S::BN - 1) / S::BN));
+  return launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g);
+}
+
+// NB = ceil(N / 4096) blocks of 16 rows (at most 7): about one workgroup per CU of a 256-CU
+// part for N <= 28672.  Falls back to the register-staged tile kernel when the 31-bit buffer
+// offsets do not cover the operands.
+hipError_t launch_skinny_sized(const GemmArgs& g, hipStream_t stream);
+
 template <int WM, int WN, int TM, int TN>
 hipError_t launch_tile(const GemmArgs& g, hipStream_t stream) {
   constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
   const dim3 grid(static_cast<unsigned>((g.N + BN - 1) / BN), static_cast<unsigned>((g.M + BM - 1) / BM));
   return launch(w4a4_gemm_tile<WM, WN, TM, TN>, grid, dim3(64 * WM * WN), 0, stream, g);
+}
+
+template <int NB>
+hipError_t try_skinny(const GemmArgs& g, hipStream_t stream) {
+  constexpr int SD = skinny_depth<NB>();
+  if (fits_skinny<NB, SD>(g)) return launch_skinny<NB, SD>(g, stream);
+  return launch_tile<2, 2, 2, 2>(g, stream);
+}
+
+hipError_t launch_skinny_sized(const GemmArgs& g, hipStream_t stream) {
+  const int64_t nb = (g.N + 4095) / 4096;
+  switch (nb <= 1 ? 1 : (nb >= 7 ? 7 : nb)) {
+    case 1: return try_skinny<1>(g, stream);
+    case 2: return try_skinny<2>(g, stream);
+    case 3: return try_skinny<3>(g, stream);
+    case 4: return try_skinny<4>(g, stream);
+    case 5: return try_skinny<5>(g, stream);
+    case 6: return try_skinny<6>(g, stream);
+    default: return try_skinny<7>(g, stream);
+  }
 }
 
 }  // namespace
@@ -858,6 +1017,9 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
     case 15: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2, 2>(g, stream); break;  // 256 x 128, K split
     case 16: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream); break;  // 128 x 128, K split
+    case 20: if (fits_skinny<2, 8>(g)) return launch_skinny<2, 8>(g, stream); break;  // decode: 32 rows per workgroup
+    case 21: if (fits_skinny<4, 4>(g)) return launch_skinny<4, 4>(g, stream); break;  // decode: 64 rows per workgroup
+    case 22: return launch_skinny_sized(g, stream);                                     // decode: rows per workgroup from N
     case 9: {
       const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
       return launch(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
@@ -867,10 +1029,13 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
       // the 8-wave 256 x 256 ring tile is fastest once there are at least as many of its
       // tiles as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs
       // 212 us); with fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).
-      // Decode-sized M runs 128 x 128 tiles with two K groups per workgroup (M = 16:
-      // 86 vs 114 us at K = 28672).  Problems whose byte offsets do not fit 31 bits use the
-      // register-staged kernel.
+      // Decode-sized M (<= 16) streams the weights with the skinny kernel (LLaMA-2-70B,
+      // M = 16: down [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 34 vs
+      // 41 us against the tile kernels); M <= 128 runs 128 x 128 tiles with two K groups per
+      // workgroup.  Problems whose byte offsets do not fit 31 bits use the register-staged
+      // kernel.
       const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+      if (g.M <= 16) return launch_skinny_sized(g, stream);
       if (g.M <= 128) {
         if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);
         return launch_tile<2, 2, 2, 2>(g, stream);

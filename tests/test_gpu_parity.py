@@ -307,6 +307,18 @@ def test_gemm_llama2_70b_decode(M):
     gemm_case(M, 8192, 28672, seed=40 + M, bias=False)
 
 
+@pytest.mark.parametrize("variant", ["default", "20", "21"])
+def test_gemm_decode_kernel(variant, monkeypatch):
+    # M <= 16 runs the weight-streaming kernel: every M up to 16, ragged N (blocks of 16
+    # rows), K not a multiple of the 8 waves' 64-byte steps, and K shorter than one step
+    say(f"w4a4_linear decode kernel {variant}: M 1..16, ragged N and K")
+    if variant != "default":
+        monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
+    for (M, N, K) in [(1, 8, 64), (2, 40, 128), (7, 1000, 4160), (16, 130, 3136), (11, 4097, 640),
+                      (16, 28672 + 48, 192), (13, 96, 28672)]:
+        gemm_case(M, N, K, seed=M * 31 + N + K, bias=(M % 2 == 1))
+
+
 # ---------------------------------------------------------------- chain
 
 def test_tiny_rotated_linear_chain():
