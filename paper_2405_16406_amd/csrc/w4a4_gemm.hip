@@ -228,9 +228,12 @@ __device__ __forceinline__ void ring_epilogue_fast(const GemmArgs& g, const v16i
     const int64_t m = mw + i * 32 + c;
     yo[i] = m < g.M ? static_cast<uint32_t>((m * g.ldy + nw + 4 * h) * 2) : 0x80000000u;
   }
-  static_for<TN>([&](auto jc) {
-    constexpr int j = decltype(jc)::value;
-    float s[16], w[16], bv[16];
+  // column scales of all TN blocks first, then the stores row block by row block, so that
+  // the TN * 64 bytes a lane half writes per row go out in consecutive instructions (whole
+  // 128-byte lines reach L2 together instead of halves written back separately)
+  float s[TN][16], w[TN][16], bv[TN][16];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int cb = (tn + j) * 32 + 8 * q + 4 * h;
@@ -240,15 +243,17 @@ __device__ __forceinline__ void ring_epilogue_fast(const GemmArgs& g, const v16i
       const float s4[4] = {sv.x, sv.y, sv.z, sv.w}, r4[4] = {rv.x, rv.y, rv.z, rv.w}, b4[4] = {bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        s[4 * q + e] = s4[e];
-        w[4 * q + e] = __fmul_rn(s4[e], r4[e]);
-        bv[4 * q + e] = b4[e];
+        s[j][4 * q + e] = s4[e];
+        w[j][4 * q + e] = __fmul_rn(s4[e], r4[e]);
+        bv[j][4 * q + e] = b4[e];
       }
     }
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
         uint32_t pk[2];
 #pragma unroll
         for (int e2 = 0; e2 < 2; ++e2) {
@@ -256,15 +261,15 @@ __device__ __forceinline__ void ring_epilogue_fast(const GemmArgs& g, const v16i
 #pragma unroll
           for (int u = 0; u < 2; ++u) {
             const int r = 4 * q + 2 * e2 + u;
-            const float t = __fmul_rn(s[r], static_cast<float>(acc[i][j][r]));
-            yv[u] = fp32_result(__fmaf_rn(ra[i], t, __fmaf_rn(rb[i], w[r], bv[r])));  // bias 0 without one
+            const float t = __fmul_rn(s[j][r], static_cast<float>(acc[i][j][r]));
+            yv[u] = fp32_result(__fmaf_rn(ra[i], t, __fmaf_rn(rb[i], w[j][r], bv[j][r])));  // bias 0 without one
           }
           pk[e2] = f2h2(yv[0], yv[1]);
         }
         __builtin_amdgcn_raw_buffer_store_b64(v2u{pk[0], pk[1]}, ry, static_cast<int>(yo[i] + (j * 32 + 8 * q) * 2), 0, 0);
       }
     }
-  });
+  }
 }
 
 // Checked path: edge tiles, unaligned or large outputs, and the raw accumulator output.
