@@ -1022,6 +1022,8 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
     case 15: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2, 2>(g, stream); break;  // 256 x 128, K split
     case 16: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream); break;  // 128 x 128, K split
+    case 17: if (fits_ring<4, 2, 2, 2, 4>(g)) return launch_ring<4, 2, 2, 2, 4, 1>(g, stream); break;  // 256 x 128, 8 waves of 64 x 64
+    case 18: if (fits_ring<2, 4, 2, 2, 4>(g)) return launch_ring<2, 4, 2, 2, 4, 1>(g, stream); break;  // 128 x 256, 8 waves of 64 x 64
     case 20: if (fits_skinny<2, 8>(g)) return launch_skinny<2, 8>(g, stream); break;  // decode: 32 rows per workgroup
     case 21: if (fits_skinny<4, 4>(g)) return launch_skinny<4, 4>(g, stream); break;  // decode: 64 rows per workgroup
     case 22: return launch_skinny_sized(g, stream);                                     // decode: rows per workgroup from N
