@@ -13,12 +13,13 @@ Weights are packed once beforehand (sq_pack_w4, R4 folded into W_down), as in
 deployment; gate and up share the input, so their packed weights are stacked into one
 [22016, 4096] matrix (packing is per output row, so this changes no code) and run as one
 GEMM launch.  Inputs are synthetic (seeded, LLaMA-shaped, with outlier channels) and
-already resident in HBM; three input/weight sets are rotated so that consecutive steps
-do not hit the 256 MB Infinity Cache.
+already resident in HBM; eight input/weight sets (--sets) are rotated so that
+consecutive steps do not hit the 256 MB Infinity Cache.
 
 value = W4A4 linear ops of the step (3 x 2*M*N*K) / step time, in TOPS.  Per-kernel
-durations come from HIP events recorded around every launch on the stream the library
-runs on.  The CPU baseline times the oracle on a bounded slice of the same workload.
+durations come from a second pass over the same steps, in which the library attaches
+a pair of HIP events to each kernel launch (start/stop of the launch itself, on the
+stream the library runs on).  The CPU baseline times the oracle on a bounded slice of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--report PATH]
 """
@@ -94,6 +95,7 @@ PROFILE_COMMANDS = {
                    "python /root/repo/bench.py --calib-copy",
     "summary": "python bench.py --summarize DIR",
 }
+REPORT_SPAN_BYTES = 1 << 30  # bytes each --report kernel cycles through
 CALIB_BYTES = 512 << 20  # bytes read and written by each --calib-copy launch
 
 
@@ -436,22 +438,50 @@ def cpu_baseline(shape, target_s):
 
 
 def kernel_report(torch, sq, workloads, dev):
-    """Per-config kernel timings (HIP events, median of repeated launches) for the docs."""
+    """Per-config kernel timings (HIP events around back-to-back launches) for the docs.
+
+    Each kernel cycles through enough copies of its inputs and outputs that they add up to
+    more than the GPU's caches (256 MB of Infinity Cache, 4 MB of L2 per XCD), so repeated
+    launches read HBM as a single pass would, not the previous launch's cached bytes.
+    """
     up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
-    def timed(fn, reps=20):
-        """Median-free average over back-to-back launches (no host sync between them)."""
-        for _ in range(3):
-            fn()
+    def n_copies(nbytes):
+        return int(min(32, max(2, -(-REPORT_SPAN_BYTES // max(nbytes, 1)))))
+
+    def timed(fns, reps=None):
+        """Mean time per launch over back-to-back launches (no host sync between them)."""
+        reps = reps or max(20, 2 * len(fns))
+        for f in fns:
+            f()
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record()
-        for _ in range(reps):
-            fn()
+        for r in range(reps):
+            fns[r % len(fns)]()
         b.record()
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
+
+    def act_fns(x, had, pow2, nbytes):
+        """had_quant_act launches over distinct copies of x and of the outputs."""
+        fns = []
+        for _ in range(n_copies(nbytes)):
+            xc = x.clone()
+            o = sq.had_quant_act(xc, had, pow2)[:3]
+            fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, out=o))
+        return fns
+
+    def gemm_fns(qx, w, nbytes):
+        """w4a4_linear launches over distinct copies of the operands and of y."""
+        fns = []
+        for _ in range(n_copies(nbytes)):
+            qc = tuple(t.clone() for t in qx)
+            wc = tuple(t.clone() for t in w)
+            y = sq.w4a4_linear(*qc, *wc)[0]
+            fns.append(lambda qc=qc, wc=wc, y=y: sq.w4a4_linear(*qc, *wc, out=y))
+        return fns
 
     rep = []
     cfgs = [workloads.LLAMA2_7B_MLP, workloads.LLAMA3_8B_MLP] + workloads.LLAMA2_70B_DECODE
@@ -464,28 +494,31 @@ def kernel_report(torch, sq, workloads, dev):
         wd = sq.pack_w4(up(inp["w_down"]), had, sh.had_pow2)
         qi = sq.had_quant_act(xin)[:3]
         qd = sq.had_quant_act(xdn, had, sh.had_pow2)[:3]
-        M = sh.M
-        t_aq = timed(lambda: sq.had_quant_act(xin, out=qi))
-        t_hq = timed(lambda: sq.had_quant_act(xdn, had, sh.had_pow2, out=qd))
-        t_g = timed(lambda: sq.w4a4_linear(*qi, *wg))
-        t_gu = timed(lambda: sq.w4a4_linear(*qi, *wgu))
-        t_d = timed(lambda: sq.w4a4_linear(*qd, *wd))
+        M, H, I = sh.M, sh.hidden, sh.inter
+        b_aq, b_hq = had_bytes(M, H), had_bytes(M, I)
+        b_g, b_gu, b_d = gemm_bytes(M, I, H), gemm_bytes(M, 2 * I, H), gemm_bytes(M, H, I)
+        t_aq = timed(act_fns(xin, None, 1, b_aq))
+        t_hq = timed(act_fns(xdn, had, sh.had_pow2, b_hq))
+        t_g = timed(gemm_fns(qi, wg, b_g))
+        t_gu = timed(gemm_fns(qi, wgu, b_gu))
+        t_d = timed(gemm_fns(qd, wd, b_d))
         rep.append(dict(config=sh.name,
-                        act_quant=dict(ms=t_aq, GBps=had_bytes(M, sh.hidden) / t_aq / 1e6),
-                        r4_had_quant=dict(ms=t_hq, GBps=had_bytes(M, sh.inter) / t_hq / 1e6),
-                        gate_gemm=dict(ms=t_g, TOPS=2 * M * sh.inter * sh.hidden / t_g / 1e9,
-                                       GBps=gemm_bytes(M, sh.inter, sh.hidden) / t_g / 1e6),
-                        gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * sh.inter * sh.hidden / t_gu / 1e9,
-                                          GBps=gemm_bytes(M, 2 * sh.inter, sh.hidden) / t_gu / 1e6),
-                        down_gemm=dict(ms=t_d, TOPS=2 * M * sh.inter * sh.hidden / t_d / 1e9,
-                                       GBps=gemm_bytes(M, sh.hidden, sh.inter) / t_d / 1e6)))
+                        act_quant=dict(ms=t_aq, GBps=b_aq / t_aq / 1e6),
+                        r4_had_quant=dict(ms=t_hq, GBps=b_hq / t_hq / 1e6),
+                        gate_gemm=dict(ms=t_g, TOPS=2 * M * I * H / t_g / 1e9, GBps=b_g / t_g / 1e6),
+                        gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * I * H / t_gu / 1e9, GBps=b_gu / t_gu / 1e6),
+                        down_gemm=dict(ms=t_d, TOPS=2 * M * I * H / t_d / 1e9, GBps=b_d / t_d / 1e6)))
         del inp, xin, xdn, wg, wgu, wd, qi, qd
         torch.cuda.empty_cache()
     q, k, v = (up(t) for t in workloads.kv_inputs())
-    o = sq.qk_had_kvquant(q, k, v)
-    o.pop("k_rot")
-    t_kv = timed(lambda: sq.qk_had_kvquant(q, k, v, out=o))
     E = q.numel()
+    fns = []
+    for _ in range(n_copies(kv_bytes(E))):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc)
+        o.pop("k_rot")
+        fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o))
+    t_kv = timed(fns)
     rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6)))
     return rep
 
