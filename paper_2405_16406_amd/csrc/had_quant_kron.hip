@@ -771,6 +771,303 @@ had_quant_pair(RotQuantArgs args) {
   }
 }
 
+// ---------------------------------------------------------------- line kernel
+// Rows of K = A * F * 64 rotated by (H_A (x) S_{64F}) / sqrt(K).  The Sylvester factor
+// splits as S_{64F} = S_F (x) S_64 (the left factor on the high index bits), so with the
+// row viewed as AD = A*F lines of 64 fp16 (line L = i_a*F + i_b/64, column i_b % 64) the
+// rotation is D (x) S_64 with D = H_A (x) S_F of order AD acting on the line index.  F = 8
+// turns H_28 (x) S_512 into a 224-line dense stage with no padding (H_28 (x) S_1024: F = 16,
+// 448 lines), and the butterflies that remain (S_64) stay inside a line.
+//   * one workgroup of NT waves owns one row at a time; wave w computes the 32 output lines
+//     n = 32w .. 32w + 31 (one MFMA N tile) over all 64 columns (two M tiles), so every
+//     butterfly of the S_64 stage is inside the wave and the waves meet only for the row's
+//     min/max;
+//   * the B fragments (columns of D) stay in registers for the whole kernel: F being a
+//     multiple of 8, a fragment (8 consecutive k) lies in one entry of H_A, so a lane keeps
+//     one fp16 +-1 pattern of S_F and applies the H_A sign per k-step by flipping fp16 sign
+//     bits (the fragments themselves, 4 VGPRs per k-step, would not fit beside the row);
+//   * the row sits in LDS as APAD lines of 128 bytes (lines AD.. zero, odd lines with their
+//     64-byte halves swapped) and A fragments come from transposing reads, as in the
+//     row-pair kernel; the next row is loaded into registers while this one is transformed;
+//   * several workgroups share a CU, so one's loads, MFMAs and VALU work overlap another's.
+template <int A, int F, int NT>
+struct Lines {
+  static constexpr int AD = A * F;                    // lines of a row
+  static constexpr int KS = (AD + 15) / 16;           // k-steps of the dense stage
+  static constexpr int APAD = KS * 16;                // staged lines
+  static constexpr int K = AD * 64;
+  static constexpr int THREADS = 64 * NT;
+  static constexpr int CHUNKS = K / 8;                // 16-byte chunks of a row
+  static constexpr int PF = (CHUNKS + THREADS - 1) / THREADS;
+  static constexpr int SLOT = APAD * 128;
+  static constexpr int ZERO_CHUNKS = (APAD - AD) * 8;
+  static constexpr int HCH = (A * A + 15) / 16;       // 16-byte chunks of H_A
+  static constexpr int HPT = (HCH + THREADS - 1) / THREADS;
+  static constexpr int STAGE = SLOT > HCH * 16 ? SLOT : HCH * 16;  // row slot, or H at the start
+  static constexpr int LDS = STAGE + 2 * NT * 4;      // + per-wave min/max
+  static_assert(F == 8 || F == 16, "a fragment in one H_A entry, one S_F pattern for all k-steps");
+  static_assert(NT * 32 >= AD && (NT - 1) * 32 < AD, "one N tile per wave, none empty");
+  static_assert(ZERO_CHUNKS <= THREADS, "padding lines zeroed in one pass");
+  static_assert(KS <= 32, "k-step sign bits");
+};
+
+template <int A, int F, int NT, bool DBG>
+__global__ void __launch_bounds__(64 * NT, DBG ? 2 : 4)  // 4 waves per SIMD: 128 VGPRs
+had_quant_lines(RotQuantArgs args) {
+  using C = Lines<A, F, NT>;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  unsigned char* slot = smem;
+  float* red = reinterpret_cast<float*>(smem + C::STAGE);
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int g = lane >> 5;
+  const int c = lane & 31;
+  const int n = 32 * w + c;  // output line (column of D) of this lane
+  const int64_t rows = args.rows;
+  int64_t row = blockIdx.x;
+  if (row >= rows) return;  // uniform over the workgroup
+
+  // ---- row staging: thread t loads chunks t + THREADS * j (clamped in the row; the
+  //      duplicates are not stored)
+  v4u pf[C::PF];
+  auto load_row = [&](int64_t r) {
+    const v4u* xr = reinterpret_cast<const v4u*>(args.x + r * args.ldx);
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = threadIdx.x + C::THREADS * j;
+      pf[j] = xr[i < C::CHUNKS ? i : C::CHUNKS - 1];
+    }
+  };
+  auto store_row = [&]() {
+#pragma unroll
+    for (int j = 0; j < C::PF; ++j) {
+      const int i = threadIdx.x + C::THREADS * j;  // line i / 8, chunk i % 8
+      if (i < C::CHUNKS) reinterpret_cast<v4u*>(slot)[i ^ ((i & 8) >> 1)] = pf[j];
+    }
+  };
+  // H_A (int8 [A][A]) with coalesced 16-byte loads, staged as bytes in the slot (the rows
+  // go there once the fragments are built); the first row is requested first
+  load_row(row);
+  {
+    v4u hv[C::HPT];
+#pragma unroll
+    for (int j = 0; j < C::HPT; ++j) {
+      const int i = threadIdx.x + j * C::THREADS;
+      if (i < C::HCH) {
+        if (i * 16 + 16 <= A * A) {
+          hv[j] = reinterpret_cast<const v4u*>(args.H)[i];
+        } else {  // the tail chunk, byte by byte
+          uint32_t wd[4] = {0u, 0u, 0u, 0u};
+          for (int b = 0; i * 16 + b < A * A; ++b)
+            wd[b >> 2] |= static_cast<uint32_t>(static_cast<uint8_t>(args.H[i * 16 + b])) << (8 * (b & 3));
+          hv[j] = v4u{wd[0], wd[1], wd[2], wd[3]};
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < C::HPT; ++j) {
+      const int i = threadIdx.x + j * C::THREADS;
+      if (i < C::HCH) reinterpret_cast<v4u*>(slot)[i] = hv[j];
+    }
+  }
+  __syncthreads();
+  const int8_t* hs = reinterpret_cast<const int8_t*>(slot);
+
+  // ---- B fragments: B[k][n] = D[k][n] for k = 16 ks + 8 g + e; zero where k or n >= AD
+  // k = (16 ks + 8 g) + e: the fragment lies in H_A entry [(16 ks + 8 g) / F][n / F] and
+  // in S_F rows (8 g) % F + e, column n % F (the reads use clamped indices and are
+  // unconditional, so that they are all in flight at once)
+  v8h bf;
+  uint32_t sgn = 0;  // bit ks set when the k-step's H_A entry is -1
+  {
+    const int nt = n % F;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kt = (8 * g) % F + e;
+      bf[e] = (n < C::AD) ? static_cast<_Float16>((__popc(kt & nt) & 1) ? -1.0f : 1.0f)
+                          : static_cast<_Float16>(0.0f);
+    }
+    const int na = n < C::AD ? n / F : A - 1;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      const int ka = (16 * ks + 8 * g) / F;
+      const int8_t h = hs[(ka < A ? ka : A - 1) * A + na];
+      if (ka < A && n < C::AD && h < 0) sgn |= 1u << ks;
+    }
+  }
+  __syncthreads();  // the staged H is no longer read: the slot takes the rows
+  if (threadIdx.x < C::ZERO_CHUNKS)  // padding lines: zero, never rewritten
+    reinterpret_cast<v4u*>(slot)[C::AD * 8 + threadIdx.x] = v4u{0u, 0u, 0u, 0u};
+  store_row();
+  __syncthreads();
+
+  // transposing reads of A fragments (see the row-pair kernel): lane (G = lane/16,
+  // s = lane%16) addresses line 8*(G/2) + 4t + s/4 (+ 16 ks), columns 32*mt + 16*(G%2) +
+  // 4*(s%4), half-swapped on odd lines
+  const int tg = lane >> 4, ts = lane & 15;
+  const int tq = ts >> 2;
+  uint32_t tbase[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+    tbase[mt] = static_cast<uint32_t>((8 * (tg >> 1) + tq) * 128 +
+                                      ((32 * (mt ^ (tq & 1))) + 16 * (tg & 1) + 4 * (ts & 3)) * 2);
+  auto frag = [&](int mt, int ks) {
+    const unsigned char* a0 = slot + tbase[mt] + ks * 16 * 128;
+    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) v4s*>(reinterpret_cast<uintptr_t>(a0)));
+    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<__attribute__((address_space(3))) v4s*>(reinterpret_cast<uintptr_t>(a0 + 4 * 128)));
+    return __builtin_bit_cast(v8h, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  auto bfrag = [&](int ks) {
+    const uint32_t m = ((sgn >> ks) & 1u) ? 0x80008000u : 0u;
+    v4u b = __builtin_bit_cast(v4u, bf);
+    b ^= v4u{m, m, m, m};
+    return __builtin_bit_cast(v8h, b);
+  };
+
+  const float s_n = args.inv_sqrt_n;
+  const bool real = n < C::AD;
+  for (;;) {
+    const int64_t next = row + gridDim.x;
+    const bool more = next < rows;
+    if (more) load_row(next);  // in flight during this row
+    // keeps the sign flips inside the loop (hoisted out of it, the flipped fragments would
+    // take 4 VGPRs per k-step)
+    asm volatile("" : "+v"(sgn));
+
+    // ---- dense stage: acc[mt] = (X lines)^T D for columns 32 mt .. 32 mt + 31
+    v16f acc[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    {
+      v8h a0[2], a1[2];
+      a0[0] = frag(0, 0);
+      a0[1] = frag(1, 0);
+      static_for<C::KS>([&](auto kc) {
+        constexpr int ks = decltype(kc)::value;
+        v8h(&cur)[2] = (ks & 1) ? a1 : a0;
+        v8h(&nxt)[2] = (ks & 1) ? a0 : a1;
+        if constexpr (ks + 1 < C::KS) {
+          nxt[0] = frag(0, ks + 1);
+          nxt[1] = frag(1, ks + 1);
+        }
+        const v8h b = bfrag(ks);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[0], b, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur[1], b, acc[1], 0, 0, 0);
+      });
+    }
+
+    // ---- S_64 over the column: register bits 0, 1, 3, 4; M tile bit 5; lane half bit 2
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int rb = 1; rb < 16; rb <<= 1)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if ((r & rb) == 0) {
+            float lo = acc[mt][r], hi = acc[mt][r + rb];
+            bfly(lo, hi);
+            acc[mt][r] = lo;
+            acc[mt][r + rb] = hi;
+          }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float lo = acc[0][r], hi = acc[1][r];
+      bfly(lo, hi);
+      acc[0][r] = lo;
+      acc[1][r] = hi;
+    }
+    // after the swap and butterfly lane (c, g) holds column 32 mt + 16 g + j in acc[mt][j]
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      float o[16];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mt][r]),
+                                                         __float_as_uint(acc[mt][r + 8]), false, false);
+        const float x0 = __uint_as_float(sw[0]);
+        const float x1 = __uint_as_float(sw[1]);
+        const int j = 8 * (r >> 2) + (r & 3);
+        o[j] = __fadd_rn(x0, x1);
+        o[j + 4] = __fsub_rn(x0, x1);
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc[mt][j] = o[j];
+    }
+
+    // ---- row min/max over real lines (padding lines hold zeros)
+    float mn = acc[0][0], mx = acc[0][0];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        mn = fminf(mn, acc[mt][r]);
+        mx = fmaxf(mx, acc[mt][r]);
+      }
+    if (!real) {
+      mn = INFINITY;
+      mx = -INFINITY;
+    }
+    mn = wave_min(mn);
+    mx = wave_max(mx);
+    if (lane == 0) {
+      red[w] = mn;
+      red[NT + w] = mx;
+    }
+    __syncthreads();  // every wave is past its dense stage: the slot may take the next row
+    mn = red[0];
+    mx = red[NT];
+#pragma unroll
+    for (int v = 1; v < NT; ++v) {
+      mn = fminf(mn, red[v]);
+      mx = fmaxf(mx, red[NT + v]);
+    }
+    if (more) store_row();
+
+    // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
+    const float r_u = __fsub_rn(mx, mn);
+    const float a_u = __fdiv_rn(r_u, 15.0f);
+    const bool cst = __fmul_rn(a_u, s_n) < kMinNormal;
+    const float inv_u = cst ? 0.0f : __fdiv_rn(1.0f, a_u);
+    const float nb = -__fmul_rn(mn, inv_u);
+    if (threadIdx.x == 0) {
+      args.alpha[row] = cst ? 1.0f : __fmul_rn(a_u, s_n);
+      args.beta[row] = __fmul_rn(mn, s_n);
+    }
+
+    // ---- codes of line n, columns 32 mt + 16 g .. + 15: 8-byte stores
+    uint8_t* qrow = args.q + row * (C::K / 2);
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      uint32_t wd[2];
+#pragma unroll
+      for (int hw = 0; hw < 2; ++hw) {
+        uint32_t ev = 0, od = 0;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s], inv_u, nb), s, ev);
+          od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
+        }
+        wd[hw] = ev | (od << 4);
+      }
+      const int pos = n * 64 + mt * 32 + 16 * g;
+      if (real) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(wd[0], wd[1]);
+      if constexpr (DBG) {
+        if (real) {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) args.dbg[row * C::K + pos + j] = __fmul_rn(acc[mt][j], s_n);
+        }
+      }
+    }
+    __syncthreads();  // the slot holds the next row; the min/max slots are free again
+    if (!more) break;
+    row = next;
+  }
+}
+
 int g_num_cu = 0;
 std::once_flag g_cu_once;
 
@@ -827,20 +1124,50 @@ hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
   return a.dbg ? launch_pair_t<A, APAD, NT, true>(a, stream) : launch_pair_t<A, APAD, NT, false>(a, stream);
 }
 
+template <int A, int F, int NT, bool DBG>
+hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
+  using C = Lines<A, F, NT>;
+  auto kern = had_quant_lines<A, F, NT, DBG>;
+  static int blocks_per_cu = 0;
+  static const hipError_t init = [&] {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_per_cu, kern, C::THREADS, C::LDS);
+    if (blocks_per_cu < 1) blocks_per_cu = 1;
+    return e;
+  }();
+  if (init != hipSuccess) return init;
+  const int64_t cap = static_cast<int64_t>(num_cus()) * blocks_per_cu;
+  const unsigned grid = static_cast<unsigned>(a.rows < cap ? a.rows : cap);
+  return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
+}
+
+template <int A, int F, int NT>
+hipError_t launch_lines(const RotQuantArgs& a, hipStream_t stream) {
+  return a.dbg ? launch_lines_t<A, F, NT, true>(a, stream) : launch_lines_t<A, F, NT, false>(a, stream);
+}
+
 }  // namespace
 
 // Returns hipErrorNotSupported when no fast path covers the arguments.
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
-  // the pair kernel stages rows in 16-byte chunks
+  // the pair and line kernels stage rows in 16-byte chunks
   const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && !getenv("SQ_KRON_STAGED");
-  if (a.a == 28 && a.b == 512) return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
+  if (a.a == 28 && a.b == 512) {
+    if (pair_ok) return launch_lines<28, 8, 7>(a, stream);
+    return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);
+  }
   if (a.a == 172 && a.b == 64) {
     if (pair_ok) return launch_pair<172, 176, 6>(a, stream);
     return launch_kron<172, 176, 6, 64, 1, 6, true>(a, stream);
   }
-  if (a.a == 28 && a.b == 1024) return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
+  if (a.a == 28 && a.b == 1024) {
+    if (pair_ok) return launch_lines<28, 16, 14>(a, stream);
+    return launch_kron<28, 32, 1, 1024, 8, 1, false>(a, stream);
+  }
   return hipErrorNotSupported;
 }
 
