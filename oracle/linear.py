@@ -15,6 +15,8 @@ Forward of one quantized linear layer y = x W^T with an online rotation R in fro
          y[m, n] = sum_k (alpha_m qa[m,k] + beta_m) (s_n qw[n,k])
                  = s_n (alpha_m acc[m, n] + beta_m rowsum[n])
      computed in fp64 and rounded once to fp16.
+  5. swiglu_linear: the gate and up projections of the same input combined as
+     SiLU(gate) * up (the input of down_proj, which R4 rotates), rounded once to fp16.
 """
 
 import numpy as np
@@ -97,6 +99,26 @@ def w4a4_linear(qa, a_alpha, a_beta, qw, w_alpha, w_rowsum, bias=None):
     """GEMM + epilogue on unpacked codes.  Returns (y fp16 [M, N], acc int64 [M, N])."""
     acc = gemm_exact(qa, qw)
     return epilogue(acc, a_alpha, a_beta, w_alpha, w_rowsum, bias), acc
+
+
+def silu(v: np.ndarray) -> np.ndarray:
+    """SiLU(v) = v / (1 + e^-v) in fp64 (the gate activation of the LLaMA MLP)."""
+    v = np.asarray(v, dtype=np.float64)
+    with np.errstate(over="ignore"):
+        return v / (1.0 + np.exp(-v))
+
+
+def swiglu_linear(qa, a_alpha, a_beta, qw_gate, wa_gate, rs_gate, qw_up, wa_up, rs_up,
+                  bias_gate=None, bias_up=None):
+    """Gate and up projections of the MLP whose product feeds down_proj (Fig. 1(c): R4 sits
+    on that input), h = fp16( SiLU(g) * u ).
+
+    g and u are the dequantised products of the gate and up weights (epilogue_f64 of their
+    exact accumulators), combined in fp64 and rounded once.  Returns (h fp16 [M, I], g, u).
+    """
+    g = epilogue_f64(gemm_exact(qa, qw_gate), a_alpha, a_beta, wa_gate, rs_gate, bias_gate)
+    u = epilogue_f64(gemm_exact(qa, qw_up), a_alpha, a_beta, wa_up, rs_up, bias_up)
+    return (silu(g) * u).astype(np.float16), g, u
 
 
 def rotated_linear(x, w, had_dense=None, pow2_n: int = 1, bias=None):

@@ -110,3 +110,35 @@ def test_had_quant_act_code_range(bits):
     assert q.min() >= 0 and q.max() <= 2 ** bits - 1
     err = np.abs(quant.dequant(q, a, b) - y32.astype(np.float64))
     assert np.all(err <= a.astype(np.float64) * 0.5 * (1 + 1e-5))
+
+
+def test_silu_closed_forms():
+    # SiLU(v) = v sigma(v): sigma(0) = 1/2, sigma(ln 3) = 3/4, sigma(-ln 3) = 1/4, and
+    # SiLU(v) - SiLU(-v) = v (sigma(v) + sigma(-v) = 1); large v tends to v, large -v to 0
+    ln3 = np.log(3.0)
+    v = linear.silu(np.array([0.0, ln3, -ln3, 2.0, -2.0, 40.0, -40.0, -800.0]))
+    assert v[0] == 0.0
+    assert abs(v[1] - 0.75 * ln3) < 1e-15 and abs(v[2] + 0.25 * ln3) < 1e-15
+    assert abs((v[3] - v[4]) - 2.0) < 1e-15
+    assert abs(v[5] - 40.0) < 1e-15 and abs(v[6]) < 1e-15
+    assert v[7] == 0.0 and np.isfinite(v[7])
+
+
+def test_swiglu_linear_bruteforce():
+    # h[m, c] = fp16(SiLU(g) u) with g, u the dequantised gate/up products, element by element
+    import math
+    rng = np.random.default_rng(5)
+    M, I, K = 3, 5, 16
+    qa = rng.integers(0, 16, size=(M, K))
+    aa, ab = rng.uniform(0.01, 0.1, M), rng.uniform(-1, 0, M)
+    qg, qu = rng.integers(-7, 8, size=(I, K)), rng.integers(-7, 8, size=(I, K))
+    ga, ua = rng.uniform(0.001, 0.01, I), rng.uniform(0.001, 0.01, I)
+    bg, bu = rng.uniform(-0.1, 0.1, I), rng.uniform(-0.1, 0.1, I)
+    h, g, u = linear.swiglu_linear(qa, aa, ab, qg, ga, qg.sum(1), qu, ua, qu.sum(1), bg, bu)
+    for m in range(M):
+        for c in range(I):
+            gv = sum((aa[m] * qa[m, k] + ab[m]) * ga[c] * qg[c, k] for k in range(K)) + bg[c]
+            uv = sum((aa[m] * qa[m, k] + ab[m]) * ua[c] * qu[c, k] for k in range(K)) + bu[c]
+            assert abs(g[m, c] - gv) < 1e-12 and abs(u[m, c] - uv) < 1e-12
+            ref = gv / (1.0 + math.exp(-gv)) * uv
+            assert h[m, c] == np.float16(ref)
