@@ -473,14 +473,19 @@ def kernel_report(torch, sq, workloads, dev):
             fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, out=o))
         return fns
 
-    def gemm_fns(qx, w, nbytes):
-        """w4a4_linear launches over distinct copies of the operands and of y."""
+    def gemm_fns(qx, w, nbytes, swiglu=False):
+        """w4a4_linear (or w4a4_linear_swiglu) launches over distinct copies of the operands
+        and of the output."""
         fns = []
         for _ in range(n_copies(nbytes)):
             qc = tuple(t.clone() for t in qx)
             wc = tuple(t.clone() for t in w)
-            y = sq.w4a4_linear(*qc, *wc)[0]
-            fns.append(lambda qc=qc, wc=wc, y=y: sq.w4a4_linear(*qc, *wc, out=y))
+            if swiglu:
+                y = sq.w4a4_linear_swiglu(*qc, *wc)
+                fns.append(lambda qc=qc, wc=wc, y=y: sq.w4a4_linear_swiglu(*qc, *wc, out=y))
+            else:
+                y = sq.w4a4_linear(*qc, *wc)[0]
+                fns.append(lambda qc=qc, wc=wc, y=y: sq.w4a4_linear(*qc, *wc, out=y))
         return fns
 
     rep = []
@@ -491,24 +496,28 @@ def kernel_report(torch, sq, workloads, dev):
         xin, xdn = up(inp["x_in"]), up(inp["x_down"])
         wg = sq.pack_w4(up(inp["w_gate"]))
         wgu = sq.pack_w4(up(np.concatenate([inp["w_gate"], inp["w_up"]])))
+        wsw = sq.pack_w4(sq.interleave_gate_up(up(inp["w_gate"]), up(inp["w_up"])).contiguous())
         wd = sq.pack_w4(up(inp["w_down"]), had, sh.had_pow2)
         qi = sq.had_quant_act(xin)[:3]
         qd = sq.had_quant_act(xdn, had, sh.had_pow2)[:3]
         M, H, I = sh.M, sh.hidden, sh.inter
         b_aq, b_hq = had_bytes(M, H), had_bytes(M, I)
         b_g, b_gu, b_d = gemm_bytes(M, I, H), gemm_bytes(M, 2 * I, H), gemm_bytes(M, H, I)
+        b_sw = b_gu - 2 * M * I  # half the output: fp16 [M, I]
         t_aq = timed(act_fns(xin, None, 1, b_aq))
         t_hq = timed(act_fns(xdn, had, sh.had_pow2, b_hq))
         t_g = timed(gemm_fns(qi, wg, b_g))
         t_gu = timed(gemm_fns(qi, wgu, b_gu))
+        t_sw = timed(gemm_fns(qi, wsw, b_sw, swiglu=True))
         t_d = timed(gemm_fns(qd, wd, b_d))
         rep.append(dict(config=sh.name,
                         act_quant=dict(ms=t_aq, GBps=b_aq / t_aq / 1e6),
                         r4_had_quant=dict(ms=t_hq, GBps=b_hq / t_hq / 1e6),
                         gate_gemm=dict(ms=t_g, TOPS=2 * M * I * H / t_g / 1e9, GBps=b_g / t_g / 1e6),
                         gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * I * H / t_gu / 1e9, GBps=b_gu / t_gu / 1e6),
+                        gate_up_swiglu_gemm=dict(ms=t_sw, TOPS=4 * M * I * H / t_sw / 1e9, GBps=b_sw / t_sw / 1e6),
                         down_gemm=dict(ms=t_d, TOPS=2 * M * I * H / t_d / 1e9, GBps=b_d / t_d / 1e6)))
-        del inp, xin, xdn, wg, wgu, wd, qi, qd
+        del inp, xin, xdn, wg, wgu, wsw, wd, qi, qd
         torch.cuda.empty_cache()
     q, k, v = (up(t) for t in workloads.kv_inputs())
     E = q.numel()

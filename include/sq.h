@@ -67,7 +67,8 @@ const char* sq_last_error(void);
 
 /*
  * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
- * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear or sq_qk_had_kvquant
+ * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a4_linear_swiglu or
+ * sq_qk_had_kvquant
  * made by this host thread: start_event takes the start time of the first kernel that
  * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
  * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
@@ -158,6 +159,30 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
                          const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
                          int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
                          int32_t* dbg_acc, void* stream);
+
+/*
+ * sq_w4a4_linear_swiglu -- the gate and up projections of the MLP in one product, combined
+ * in the epilogue into the input of down_proj, the activation that R4 rotates (Sec. 3.1,
+ * Fig. 1(c)):
+ *     h[m,c] = fp16( SiLU(g[m,c]) * u[m,c] ),  SiLU(v) = v / (1 + e^-v),
+ * where g and u are the dequantised outputs of sq_w4a4_linear for the gate and up weights,
+ * kept in fp32 (not rounded to fp16) before they are combined.
+ *
+ *   xq, x_alpha, x_beta, M, K, stream   as for sq_w4a4_linear
+ *   wq, w_alpha, w_rowsum, bias   the gate and up weights packed by sq_pack_w4 as one
+ *              [N, K] matrix whose rows interleave them in blocks of 32: rows 64b .. 64b+31
+ *              are gate rows 32b .. 32b+31 and rows 64b+32 .. 64b+63 the up rows of the
+ *              same outputs (packing is per row, so this is the two matrices' packed rows
+ *              reordered); bias (optional) in the same order
+ *   N          2 * I (I outputs), N % 64 == 0
+ *   h          device fp16 [M, ldh], ldh >= N/2, 2-byte aligned
+ * No raw-accumulator output (sq_w4a4_linear gives the accumulators of the same product).
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_UNSUPPORTED (sizes
+ * whose byte offsets exceed 31 bits), SQ_ERR_HIP.
+ */
+sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                                const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                                int64_t N, int64_t K, const void* bias, void* h, int64_t ldh, void* stream);
 
 /*
  * sq_qk_had_kvquant -- R3 (Sec. 3.1) on post-RoPE queries and keys, per head,

@@ -230,6 +230,51 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
   return hip_status(sq::launch_w4a4_gemm(g, static_cast<hipStream_t>(stream)), "w4a4_linear launch");
 }
 
+sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                                const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                                int64_t N, int64_t K, const void* bias, void* h, int64_t ldh, void* stream) {
+  TimingScope timing_scope;
+  if (!xq || !x_alpha || !x_beta || !wq || !w_alpha || !w_rowsum || !h)
+    return fail(SQ_ERR_NULL, "xq, x_alpha, x_beta, wq, w_alpha, w_rowsum and h are required");
+  if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
+  if (N <= 0 || N % 64 != 0 || N > (int64_t{1} << 31) - 1)
+    return fail(SQ_ERR_SHAPE, "N=%lld must be a positive multiple of 64 (gate/up blocks of 32)", (long long)N);
+  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 24))
+    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^24)", (long long)K);
+  if (ldh < N / 2) return fail(SQ_ERR_SHAPE, "ldh=%lld < N/2=%lld", (long long)ldh, (long long)(N / 2));
+  if (!aligned(xq, 16) || !aligned(wq, 16) || !aligned(h, 2) || !aligned(x_alpha, 4) || !aligned(x_beta, 4) ||
+      !aligned(w_alpha, 4) || !aligned(w_rowsum, 4) || (bias && !aligned(bias, 2)))
+    return fail(SQ_ERR_ALIGN, "xq/wq need 16-byte, scales 4-byte and h 2-byte alignment");
+  const uint64_t um = static_cast<uint64_t>(M), un = static_cast<uint64_t>(N), uk = static_cast<uint64_t>(K);
+  const uint64_t hbytes = um ? ((um - 1) * ldh + un / 2) * 2 : 0;
+  sq_status s = check_alias({{xq, um * uk / 2, "xq"}, {x_alpha, um * 4, "x_alpha"}, {x_beta, um * 4, "x_beta"},
+                             {wq, un * uk / 2, "wq"}, {w_alpha, un * 4, "w_alpha"}, {w_rowsum, un * 4, "w_rowsum"},
+                             {bias, bias ? un * 2 : 0, "bias"}},
+                            {{h, hbytes, "h"}});
+  if (s != SQ_OK) return s;
+  if (M == 0) return ok();
+  sq::GemmArgs g{};
+  g.xq = xq;
+  g.xa = x_alpha;
+  g.xb = x_beta;
+  g.M = M;
+  g.wq = wq;
+  g.wa = w_alpha;
+  g.rs = w_rowsum;
+  g.N = N;
+  g.K = K;
+  g.bias = static_cast<const uint16_t*>(bias);
+  g.y = static_cast<uint16_t*>(h);
+  g.ldy = ldh;
+  g.dbg_acc = nullptr;
+  g.swiglu = 1;
+  const hipError_t e = sq::launch_w4a4_gemm(g, static_cast<hipStream_t>(stream));
+  if (e == hipErrorNotSupported)
+    return fail(SQ_ERR_UNSUPPORTED, "M=%lld N=%lld K=%lld: byte offsets beyond 31 bits", (long long)M,
+                (long long)N, (long long)K);
+  return hip_status(e, "w4a4_linear_swiglu launch");
+}
+
 sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                             int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
                             void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,

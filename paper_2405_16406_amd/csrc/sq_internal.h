@@ -52,8 +52,11 @@ struct GemmArgs {
   uint16_t* y;           // fp16 bits [M, ldy]
   int64_t ldy;
   int32_t* dbg_acc;      // optional [M, N]
+  int32_t swiglu;        // 1: rows of wq interleave gate and up in blocks of 32 (N % 64 == 0);
+                         //    y [M, ldy >= N/2] receives SiLU(gate) * up
 };
 
+// hipErrorNotSupported when no kernel covers the arguments (only with swiglu)
 hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
 
 struct KvArgs {

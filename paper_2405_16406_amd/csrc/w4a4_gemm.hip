@@ -305,6 +305,137 @@ __device__ __forceinline__ void ring_epilogue_checked(const GemmArgs& g, const v
   }
 }
 
+// SiLU(gate) * up of two dequantised fp32 outputs, as the fp16 input of down_proj:
+// g u / (1 + e^-g); for g -> -inf the denominator is +inf and the product 0.
+__device__ __forceinline__ float swiglu_value(float gv, float uv) {
+  return __fdividef(__fmul_rn(gv, uv), __fadd_rn(1.0f, __expf(-gv)));
+}
+
+// Gate/up epilogues: wq interleaves gate and up rows in blocks of 32, so the wave's block
+// pair (2p, 2p + 1) holds the gate and up outputs of the same 32 columns in the same lane
+// and registers; output column = (interleaved column of the gate block) / 2 + offset.
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue_swiglu_fast(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw,
+                                                          int64_t nw, int tm, int tn, int lane,
+                                                          const float* __restrict__ sc) {
+  static_assert(TN % 2 == 0, "gate/up block pairs");
+  const int c = lane & 31;
+  const int h = lane >> 5;
+  const float* rowA = sc;
+  const float* rowB = sc + BM;
+  const float* colS = sc + 2 * BM;
+  const float* colR = colS + BN;
+  const float* colB = colR + BN;
+  const __amdgpu_buffer_rsrc_t ry = buf_rsrc(g.y, g.M * g.ldy * 2);
+  float ra[TM], rb[TM];
+  uint32_t yo[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = (tm + i) * 32 + c;
+    ra[i] = rowA[r];
+    rb[i] = rowB[r];
+    const int64_t m = mw + i * 32 + c;
+    yo[i] = m < g.M ? static_cast<uint32_t>((m * g.ldy + nw / 2 + 4 * h) * 2) : 0x80000000u;
+  }
+  float s[TN][16], w[TN][16], bv[TN][16];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cb = (tn + j) * 32 + 8 * q + 4 * h;
+      const float4 sv = *reinterpret_cast<const float4*>(colS + cb);
+      const float4 rv = *reinterpret_cast<const float4*>(colR + cb);
+      const float4 bb = *reinterpret_cast<const float4*>(colB + cb);
+      const float s4[4] = {sv.x, sv.y, sv.z, sv.w}, r4[4] = {rv.x, rv.y, rv.z, rv.w}, b4[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[j][4 * q + e] = s4[e];
+        w[j][4 * q + e] = __fmul_rn(s4[e], r4[e]);
+        bv[j][4 * q + e] = b4[e];
+      }
+    }
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int p = 0; p < TN / 2; ++p) {
+        uint32_t pk[2];
+#pragma unroll
+        for (int e2 = 0; e2 < 2; ++e2) {
+          float hv[2];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int r = 4 * q + 2 * e2 + u;
+            const int jg = 2 * p, ju = 2 * p + 1;
+            const float tg = __fmul_rn(s[jg][r], static_cast<float>(acc[i][jg][r]));
+            const float tu = __fmul_rn(s[ju][r], static_cast<float>(acc[i][ju][r]));
+            const float gv = fp32_result(__fmaf_rn(ra[i], tg, __fmaf_rn(rb[i], w[jg][r], bv[jg][r])));
+            const float uv = fp32_result(__fmaf_rn(ra[i], tu, __fmaf_rn(rb[i], w[ju][r], bv[ju][r])));
+            hv[u] = fp32_result(swiglu_value(gv, uv));
+          }
+          pk[e2] = f2h2(hv[0], hv[1]);
+        }
+        __builtin_amdgcn_raw_buffer_store_b64(v2u{pk[0], pk[1]}, ry, static_cast<int>(yo[i] + (p * 32 + 8 * q) * 2), 0, 0);
+      }
+    }
+  }
+}
+
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue_swiglu_checked(const GemmArgs& g, const v16i (&acc)[TM][TN],
+                                                             int64_t mw, int64_t nw, int tm, int tn, int lane,
+                                                             const float* __restrict__ sc) {
+  static_assert(TN % 2 == 0, "gate/up block pairs");
+  const int c = lane & 31;
+  const int h = lane >> 5;
+  const float* rowA = sc;
+  const float* rowB = sc + BM;
+  const float* colS = sc + 2 * BM;
+  const float* colR = colS + BN;
+  const float* colB = colR + BN;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t m = mw + i * 32 + c;
+    if (m >= g.M) continue;
+    const float ra = rowA[(tm + i) * 32 + c], rb = rowB[(tm + i) * 32 + c];
+#pragma unroll
+    for (int p = 0; p < TN / 2; ++p) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int off = 8 * (r >> 2) + 4 * h + (r & 3);
+        const int cg = (tn + 2 * p) * 32 + off, cu = cg + 32;
+        const int64_t ng = nw + 64 * p + off;  // gate column; its up column ng + 32 < N (N % 64 == 0)
+        if (ng >= g.N) continue;
+        const float gv = fp32_result(__fmaf_rn(ra, __fmul_rn(colS[cg], static_cast<float>(acc[i][2 * p][r])),
+                                               __fmaf_rn(rb, __fmul_rn(colS[cg], colR[cg]), colB[cg])));
+        const float uv = fp32_result(__fmaf_rn(ra, __fmul_rn(colS[cu], static_cast<float>(acc[i][2 * p + 1][r])),
+                                               __fmaf_rn(rb, __fmul_rn(colS[cu], colR[cu]), colB[cu])));
+        g.y[m * g.ldy + (nw + 64 * p) / 2 + off] = f2h(fp32_result(swiglu_value(gv, uv)));
+      }
+    }
+  }
+}
+
+// Epilogue of a ring-kernel block: plain or gate/up, vector (fast) or element-wise stores.
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
+                                              int tm, int tn, int lane, const float* __restrict__ sc, bool fast) {
+  if (g.swiglu) {
+    if constexpr (TN % 2 == 0) {
+      if (fast)
+        ring_epilogue_swiglu_fast<TM, TN, BM, BN>(g, acc, mw, nw, tm, tn, lane, sc);
+      else
+        ring_epilogue_swiglu_checked<TM, TN, BM, BN>(g, acc, mw, nw, tm, tn, lane, sc);
+    }
+    return;
+  }
+  if (fast)
+    ring_epilogue_fast<TM, TN, BM, BN>(g, acc, mw, nw, tm, tn, lane, sc);
+  else
+    ring_epilogue_checked<TM, TN, BM, BN>(g, acc, mw, nw, tm, tn, lane, sc);
+}
+
 // ------------------------------------------------------------------ prefill tile kernel
 constexpr int kBKB = 64;               // packed bytes per row per stage (128 k)
 constexpr int kPitch = 72;             // LDS row pitch (bytes)
@@ -690,10 +821,7 @@ w4a4_gemm_ring(GemmArgs g) {
   const bool fast = g.dbg_acc == nullptr && (g.ldy & 3) == 0 && (reinterpret_cast<uintptr_t>(g.y) & 7) == 0 &&
                     g.M * g.ldy * 2 < (int64_t{1} << 31) && n0 + R::BN <= g.N;
   if constexpr (KS == 1) {
-    if (fast)
-      ring_epilogue_fast<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales);
-    else
-      ring_epilogue_checked<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales);
+    ring_epilogue<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales, fast);
   } else {
     // group h finishes row blocks [h*HT, h*HT + HT) of the wave's block
     constexpr int HT = TM / 2;
@@ -729,10 +857,7 @@ w4a4_gemm_ring(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) part[i][j] = acc[h * HT + i][j];
       const int64_t mw = m0 + (wm + h * HT) * 32, nw = n0 + wn * 32;
-      if (fast)
-        ring_epilogue_fast<HT, TN, R::BM, R::BN>(g, part, mw, nw, wm + h * HT, wn, lane, scales);
-      else
-        ring_epilogue_checked<HT, TN, R::BM, R::BN>(g, part, mw, nw, wm + h * HT, wn, lane, scales);
+      ring_epilogue<HT, TN, R::BM, R::BN>(g, part, mw, nw, wm + h * HT, wn, lane, scales, fast);
     };
     constexpr std::integral_constant<int, 0> lo{};
     constexpr std::integral_constant<int, 1> hi{};
@@ -930,6 +1055,32 @@ w4a4_gemm_skinny(GemmArgs g) {
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[j][i] += part[((w * NB + j) * 4 + i) * 64 + lane];
+  if (g.swiglu) {
+    // NB % 4 == 0 (n0 % 64 == 0): in each run of four blocks, blocks 0, 1 are gate rows and
+    // blocks 2, 3 the up rows of the same 32 output columns, in the same lanes and registers
+    if constexpr (NB % 4 == 0) {
+#pragma unroll
+      for (int jj = 0; jj < NB / 2; ++jj) {
+        const int j = 4 * (jj / 2) + (jj % 2);
+        const int64_t ng = n0 + 16 * j + r, nu = ng + 32;
+        if (ng >= g.N) continue;
+        const float scg = g.wa[ng], scu = g.wa[nu];
+        const float wg = __fmul_rn(scg, static_cast<float>(g.rs[ng])), wu = __fmul_rn(scu, static_cast<float>(g.rs[nu]));
+        const float bg = g.bias ? h2f(g.bias[ng]) : 0.0f, bu = g.bias ? h2f(g.bias[nu]) : 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t m = 4 * sg + i;
+          if (m >= g.M) continue;
+          const float ra = __fmul_rn(g.xa[m], 0.0625f);
+          const float gv = fp32_result(__fmaf_rn(ra, __fmul_rn(scg, static_cast<float>(acc[j][i])), __fmaf_rn(g.xb[m], wg, bg)));
+          const float uv = fp32_result(__fmaf_rn(ra, __fmul_rn(scu, static_cast<float>(acc[j + 2][i])), __fmaf_rn(g.xb[m], wu, bu)));
+          // gate block j = 4t + s (s = 0, 1) holds output columns n0/2 + 32t + 16s + r
+          g.y[m * g.ldy + n0 / 2 + 32 * (j / 4) + 16 * (j % 4) + r] = f2h(fp32_result(swiglu_value(gv, uv)));
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int64_t n = n0 + 16 * j + r;
@@ -970,9 +1121,11 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g);
 }
 
-// NB = ceil(N / 4096) blocks of 16 rows (at most 7): about one workgroup per CU of a 256-CU
-// part for N <= 28672.  Falls back to the register-staged tile kernel when the 31-bit buffer
-// offsets do not cover the operands.
+// NB = ceil(N / 4096) blocks of 16 rows, about one workgroup per CU of a 256-CU part; from
+// NB = 7 on, 8 blocks two steps ahead (measured on MI355X, LLaMA-2-70B: [M x 8192] x
+// [57344 x 8192] 58-64 vs 65-72 us, [M x 8192] x [28672 x 8192] 31-36 vs 33-37 us against
+// 7 blocks three steps ahead).  Falls back to the register-staged tile kernel when the
+// 31-bit buffer offsets do not cover the operands.
 hipError_t launch_skinny_sized(const GemmArgs& g, hipStream_t stream);
 
 template <int WM, int WN, int TM, int TN>
@@ -991,20 +1144,32 @@ hipError_t try_skinny(const GemmArgs& g, hipStream_t stream) {
 
 hipError_t launch_skinny_sized(const GemmArgs& g, hipStream_t stream) {
   const int64_t nb = (g.N + 4095) / 4096;
-  switch (nb <= 1 ? 1 : (nb >= 7 ? 7 : nb)) {
+  switch (nb <= 1 ? 1 : (nb >= 7 ? 8 : nb)) {
     case 1: return try_skinny<1>(g, stream);
     case 2: return try_skinny<2>(g, stream);
     case 3: return try_skinny<3>(g, stream);
     case 4: return try_skinny<4>(g, stream);
     case 5: return try_skinny<5>(g, stream);
     case 6: return try_skinny<6>(g, stream);
-    default: return try_skinny<7>(g, stream);
+    default: return try_skinny<8>(g, stream);
   }
 }
 
 }  // namespace
 
 hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
+  if (g.swiglu) {
+    // gate/up with SiLU: the ring kernels (block pairs per wave) and the decode kernel with
+    // four 16-row blocks (two gate, two up); the same size classes as below
+    constexpr int SD4 = skinny_depth<4>(), SD8 = skinny_depth<8>();
+    if (g.M <= 16 && g.N > 16384) return fits_skinny<8, SD8>(g) ? launch_skinny<8, SD8>(g, stream) : hipErrorNotSupported;
+    if (g.M <= 16) return fits_skinny<4, SD4>(g) ? launch_skinny<4, SD4>(g, stream) : hipErrorNotSupported;
+    if (g.M <= 128)
+      return fits_ring<2, 2, 2, 2, 4>(g) ? launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream) : hipErrorNotSupported;
+    const int64_t tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+    if (tiles >= 256) return fits_ring<2, 4, 4, 2, 4>(g) ? launch_ring<2, 4, 4, 2, 4>(g, stream) : hipErrorNotSupported;
+    return fits_ring<2, 2, 4, 2, 3>(g) ? launch_ring<2, 2, 4, 2, 3, 2>(g, stream) : hipErrorNotSupported;
+  }
   // SQ_GEMM_VARIANT selects a tile shape for tuning experiments (unset: the default).
   const char* env = getenv("SQ_GEMM_VARIANT");
   const int v = env ? atoi(env) : -1;
@@ -1027,6 +1192,9 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     case 20: if (fits_skinny<2, 8>(g)) return launch_skinny<2, 8>(g, stream); break;  // decode: 32 rows per workgroup
     case 21: if (fits_skinny<4, 4>(g)) return launch_skinny<4, 4>(g, stream); break;  // decode: 64 rows per workgroup
     case 22: return launch_skinny_sized(g, stream);                                     // decode: rows per workgroup from N
+    case 23: if (fits_skinny<8, 2>(g)) return launch_skinny<8, 2>(g, stream); break;  // decode: 128 rows, 2 steps ahead
+    case 24: if (fits_skinny<8, 3>(g)) return launch_skinny<8, 3>(g, stream); break;  // decode: 128 rows, 3 steps ahead
+    case 25: if (fits_skinny<7, 3>(g)) return launch_skinny<7, 3>(g, stream); break;  // decode: 112 rows, 3 steps ahead
     case 9: {
       const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
       return launch(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
@@ -1037,7 +1205,7 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
       // tiles as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs
       // 212 us); with fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).
       // Decode-sized M (<= 16) streams the weights with the skinny kernel (LLaMA-2-70B,
-      // M = 16: down [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 34 vs
+      // M = 16: down [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 36 vs
       // 41 us against the tile kernels); M <= 128 runs 128 x 128 tiles with two K groups per
       // workgroup.  Problems whose byte offsets do not fit 31 bits use the register-staged
       // kernel.

@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
                 4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
 
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
-           "sq_pack_w4", "sq_w4a4_linear", "sq_qk_had_kvquant")
+           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant")
 
 
 class SqError(RuntimeError):
@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
     L.sq_pack_w4.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _P, _P, _P]
     L.sq_w4a4_linear.restype = _I32
     L.sq_w4a4_linear.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P]
+    L.sq_w4a4_linear_swiglu.restype = _I32
+    L.sq_w4a4_linear_swiglu.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P]
     L.sq_qk_had_kvquant.restype = _I32
     L.sq_qk_had_kvquant.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32,
                                     _P, _P, _P, _P, _P, _P, _P, _P, _P]
@@ -170,6 +172,33 @@ def w4a4_linear(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None,
     _check(lib().sq_w4a4_linear(_ptr(xq), _ptr(x_alpha), _ptr(x_beta), M, _ptr(wq), _ptr(w_alpha), _ptr(w_rowsum),
                                 N, K, _ptr(bias), _ptr(y), y.stride(0), _ptr(acc), _stream(xq)), "sq_w4a4_linear")
     return y, acc
+
+
+def w4a4_linear_swiglu(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None):
+    """h = fp16(SiLU(gate) * up) from gate/up weights packed as one matrix whose rows
+    interleave them in blocks of 32 (see interleave_gate_up).  Returns h fp16 [M, N/2].
+    """
+    _need(xq, torch.uint8, "xq")
+    _need(wq, torch.uint8, "wq")
+    M, KB = xq.shape
+    N = wq.shape[0]
+    if wq.shape[1] != KB:
+        raise ValueError("xq and wq disagree on K")
+    h = torch.empty((M, N // 2), dtype=torch.float16, device=xq.device) if out is None else out
+    _check(lib().sq_w4a4_linear_swiglu(_ptr(xq), _ptr(x_alpha.reshape(-1)), _ptr(x_beta.reshape(-1)), M, _ptr(wq),
+                                       _ptr(w_alpha), _ptr(w_rowsum), N, 2 * KB, _ptr(bias), _ptr(h), h.stride(0),
+                                       _stream(xq)), "sq_w4a4_linear_swiglu")
+    return h
+
+
+def interleave_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
+    """Rows of gate [I, ...] and up [I, ...] interleaved in blocks of 32 (I % 32 == 0): the
+    row order sq_w4a4_linear_swiglu expects of its weights, scales, row sums and bias."""
+    I = gate.shape[0]
+    if up.shape != gate.shape or I % 32:
+        raise ValueError("gate and up need the same shape with a multiple of 32 rows")
+    return torch.stack([gate.reshape(I // 32, 32, *gate.shape[1:]), up.reshape(I // 32, 32, *up.shape[1:])],
+                       dim=1).reshape(2 * I, *gate.shape[1:])
 
 
 def qk_had_kvquant(q, k, v, dbg: bool = False, out=None):

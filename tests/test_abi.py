@@ -115,6 +115,38 @@ def test_w4a4_linear_validation(L):
     assert lin(L, M=0) == sq.SQ_OK
 
 
+def lin_sw(L, M=4, N=128, K=128, ldh=64, **kw):
+    ptrs = [fake(i) for i in range(7)]
+    for i, nm in enumerate(("xq", "xa", "xb", "wq", "wa", "rs", "h")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_w4a4_linear_swiglu(ptrs[0], ptrs[1], ptrs[2], M, ptrs[3], ptrs[4], ptrs[5], N, K, None,
+                                   ptrs[6], ldh, None)
+
+
+def test_w4a4_linear_swiglu_validation(L):
+    assert lin_sw(L, h=None) == sq.SQ_ERR_NULL
+    assert lin_sw(L, N=96, ldh=48) == sq.SQ_ERR_SHAPE      # gate/up blocks of 32 need N % 64 == 0
+    assert lin_sw(L, K=96) == sq.SQ_ERR_SHAPE
+    assert lin_sw(L, ldh=63) == sq.SQ_ERR_SHAPE            # output has N/2 columns
+    assert lin_sw(L, h=ctypes.c_void_p(P * 256 + 1)) == sq.SQ_ERR_ALIGN
+    assert lin_sw(L, h=ctypes.c_void_p(fake(3).value)) == sq.SQ_ERR_ALIAS
+    assert lin_sw(L, M=0) == sq.SQ_OK
+
+
+def test_interleave_gate_up_layout():
+    import torch
+    g = torch.arange(64 * 3).reshape(64, 3)
+    u = -g
+    w = sq.interleave_gate_up(g, u)
+    assert w.shape == (128, 3)
+    for b in range(2):
+        assert torch.equal(w[64 * b:64 * b + 32], g[32 * b:32 * b + 32])
+        assert torch.equal(w[64 * b + 32:64 * b + 64], u[32 * b:32 * b + 32])
+    with pytest.raises(ValueError):
+        sq.interleave_gate_up(g[:48], u[:48])
+
+
 def kvq(L, B=1, S=2, H=2, D=128, bits=4, group=128, **kw):
     ptrs = [fake(i) for i in range(10)]
     for i, nm in enumerate(("q", "k", "v", "qr", "kq", "ka", "kb", "vq", "va", "vb")):

@@ -322,6 +322,66 @@ def test_gemm_llama3_8b_down_sampled():
     gemm_case(4096, 4096, 14336, seed=22, bias=False, sample_rows=rows)
 
 
+def swiglu_case(M, I, K, seed, bias=True, ldh_pad=0, sample_rows=None):
+    """GPU sq_w4a4_linear_swiglu vs oracle.swiglu_linear; gate/up weights interleaved on the
+    device with interleave_gate_up (codes, scales, row sums and bias alike)."""
+    rng = workloads.rng_for(seed)
+    qa = rng.integers(0, 16, size=(M, K))
+    qg, qu = rng.integers(-7, 8, size=(I, K)), rng.integers(-7, 8, size=(I, K))
+    xa = rng.uniform(0.05, 3.0, M).astype(np.float32)
+    xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+    # weight scales shrink with sqrt(K) so that g and u stay O(10) and SiLU(g) u within fp16
+    ws = min(1.0, float(np.sqrt(256.0 / K)))
+    ga = (rng.uniform(1e-3, 2e-2, I) * ws).astype(np.float32)
+    ua = (rng.uniform(1e-3, 2e-2, I) * ws).astype(np.float32)
+    rsg, rsu = qg.sum(1).astype(np.int32), qu.sum(1).astype(np.int32)
+    bg = (rng.standard_normal(I) * 0.5).astype(np.float16) if bias else None
+    bu = (rng.standard_normal(I) * 0.5).astype(np.float16) if bias else None
+    il = sq.interleave_gate_up
+    wq = il(dev(oq.pack_nibbles(qg)), dev(oq.pack_nibbles(qu))).contiguous()
+    wa, rs = il(dev(ga), dev(ua)).contiguous(), il(dev(rsg), dev(rsu)).contiguous()
+    bi = il(dev(bg), dev(bu)).contiguous() if bias else None
+    full = torch.full((M, I + ldh_pad), float("nan"), dtype=torch.float16, device="cuda")
+    h = sq.w4a4_linear_swiglu(dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), wq, wa, rs, bias=bi, out=full[:, :I])
+    torch.cuda.synchronize()
+    rows = np.arange(M) if sample_rows is None else sample_rows
+    oh, og, ou = olin.swiglu_linear(qa[rows], xa[rows], xb[rows], qg, ga, rsg, qu, ua, rsu, bg, bu)
+    gh = host(h)[rows]
+    assert np.isfinite(gh).all()
+    parity.assert_out_close(gh, oh)
+    if ldh_pad:
+        assert torch.isnan(full[:, I:]).all(), "row padding of h was written"
+    return og
+
+
+@pytest.mark.parametrize("M,I,K,bias,pad", [(1, 32, 64, False, 0), (7, 96, 128, True, 0), (16, 224, 320, True, 3),
+                                            (17, 160, 256, True, 0), (33, 128, 128, False, 1),
+                                            (130, 352, 512, True, 8), (300, 96, 320, True, 0)])
+def test_swiglu_linear_shapes(M, I, K, bias, pad):
+    # decode kernel (M <= 16), 128 x 128 tiles (M <= 128), 256 x 128 tiles; ragged M and N,
+    # padded or odd output strides (element-wise stores)
+    say(f"w4a4_linear_swiglu M={M} I={I} K={K} bias={bias} ldh pad {pad}")
+    og = swiglu_case(M, I, K, seed=400 + M + I + K, bias=bias, ldh_pad=pad)
+    if M * I >= 2000:  # the gate values reach SiLU's flat, curved and linear parts
+        assert (og < -8).any() and (og > 8).any() and (np.abs(og) < 2).any()
+
+
+def test_swiglu_linear_llama2_7b_sampled():
+    say("w4a4_linear_swiglu LLaMA-2-7B gate+up [2048x4096]x[2x11008x4096], sampled rows")
+    swiglu_case(2048, 11008, 4096, seed=41, bias=False, sample_rows=np.array([0, 1, 255, 256, 1500, 2047]))
+
+
+def test_swiglu_linear_llama3_8b_sampled():
+    say("w4a4_linear_swiglu LLaMA-3-8B gate+up [4096x4096]x[2x14336x4096], sampled rows")
+    swiglu_case(4096, 14336, 4096, seed=42, bias=True, sample_rows=np.array([0, 4095]))
+
+
+@pytest.mark.parametrize("M", [1, 16])
+def test_swiglu_linear_llama2_70b_decode(M):
+    say(f"w4a4_linear_swiglu LLaMA-2-70B decode M={M}: [M,8192]x[2x28672,8192]")
+    swiglu_case(M, 28672, 8192, seed=43 + M, bias=False)
+
+
 @pytest.mark.parametrize("M", [1, 8, 16])
 def test_gemm_llama2_70b_decode(M):
     say(f"w4a4_linear LLaMA-2-70B decode M={M}: [M,8192]x[28672,8192] and [M,28672]x[8192,28672]")
@@ -329,7 +389,7 @@ def test_gemm_llama2_70b_decode(M):
     gemm_case(M, 8192, 28672, seed=40 + M, bias=False)
 
 
-@pytest.mark.parametrize("variant", ["default", "20", "21"])
+@pytest.mark.parametrize("variant", ["default", "20", "21", "24", "25"])
 def test_gemm_decode_kernel(variant, monkeypatch):
     # M <= 16 runs the weight-streaming kernel: every M up to 16, ragged N (blocks of 16
     # rows), K not a multiple of the 8 waves' 64-byte steps, and K shorter than one step
