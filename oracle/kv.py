@@ -14,7 +14,7 @@ paper does not state the KV group size).
 
 import numpy as np
 
-from .quant import pack_nibbles, quant_asym
+from .quant import dequant, pack_nibbles, quant_asym, unpack_nibbles
 from .rotate import rotate_rows
 
 
@@ -31,3 +31,29 @@ def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, g
     vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group)
     return dict(q_rot=q_rot, k_rot=k_rot, k_q=pack_nibbles(kc), k_alpha=ka, k_beta=kb,
                 v_q=pack_nibbles(vc), v_alpha=va, v_beta=vb, k_codes=kc, v_codes=vc)
+
+
+def attn_decode(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None):
+    """Attention of one new query per (batch, head) over the 4-bit cache written by
+    qk_had_kvquant, the step that consumes it.
+
+    Keys and values are dequantised by eq. 1, K_t = alpha_t c_t + beta_t (in the R3-rotated
+    basis for K); the query is rotated the same way, so q_rot . K_t is the score of the
+    unrotated pair up to the cache's quantization error (Sec. 3.1).
+      q_rot   fp16 [B, H, D]
+      k_q, v_q  uint8 [B, S, H, D/2]; alphas, betas fp32 [B, S, H] (or [B, S, H, 1])
+      scale   score scale, 1/sqrt(D) by default
+    Returns fp16 [B, H, D] = fp16( softmax_t(scale q_rot . K_t) V ), fp64 inside.
+    """
+    D = q_rot.shape[-1]
+    scale = 1.0 / np.sqrt(D) if scale is None else scale
+    B, S, H = k_q.shape[:3]
+    kc = unpack_nibbles(k_q, signed=False)
+    vc = unpack_nibbles(v_q, signed=False)
+    K = dequant(kc, np.reshape(k_alpha, (B, S, H, 1)), np.reshape(k_beta, (B, S, H, 1)), group=D)
+    V = dequant(vc, np.reshape(v_alpha, (B, S, H, 1)), np.reshape(v_beta, (B, S, H, 1)), group=D)
+    q = np.asarray(q_rot, dtype=np.float64)
+    s = np.einsum("bhd,bshd->bhs", q, K) * scale
+    p = np.exp(s - s.max(axis=-1, keepdims=True))
+    p /= p.sum(axis=-1, keepdims=True)
+    return np.einsum("bhs,bshd->bhd", p, V).astype(np.float16)

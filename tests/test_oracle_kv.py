@@ -62,3 +62,77 @@ def test_r3_lowers_k_quant_error_with_outlier_dims():
     c, a, b = quant.quant_asym(k.astype(np.float32), group=128)
     plain_err = np.mean((quant.dequant(c, a, b, 128) - k.astype(np.float64)) ** 2)
     assert rot_err < 0.5 * plain_err
+
+
+def _cache(rng, B, S, H, D=128):
+    """A random 4-bit cache: codes, alphas and betas as qk_had_kvquant would store them."""
+    kc = rng.integers(0, 16, size=(B, S, H, D))
+    vc = rng.integers(0, 16, size=(B, S, H, D))
+    ka, va = rng.uniform(0.01, 0.2, (B, S, H)), rng.uniform(0.01, 0.2, (B, S, H))
+    kb, vb = rng.uniform(-1.5, 0, (B, S, H)), rng.uniform(-1.5, 0, (B, S, H))
+    return quant.pack_nibbles(kc), ka, kb, quant.pack_nibbles(vc), va, vb, kc, vc
+
+
+def test_attn_decode_uniform_scores_give_mean_of_v():
+    # q = 0: every score is 0, softmax is uniform, the output is the mean of the values
+    rng = np.random.default_rng(0)
+    B, S, H = 2, 7, 3
+    kq, ka, kb, vq, va, vb, kc, vc = _cache(rng, B, S, H)
+    out = kv.attn_decode(np.zeros((B, H, 128), np.float16), kq, ka, kb, vq, va, vb)
+    V = va[..., None] * vc + vb[..., None]
+    np.testing.assert_array_equal(out, V.mean(axis=1).astype(np.float16))
+
+
+def test_attn_decode_single_token_and_dominant_key():
+    rng = np.random.default_rng(1)
+    kq, ka, kb, vq, va, vb, kc, vc = _cache(rng, 1, 9, 2)
+    V = va[..., None] * vc + vb[..., None]
+    q = rng.standard_normal((1, 2, 128)).astype(np.float16)
+    out1 = kv.attn_decode(q, kq[:, :1], ka[:, :1], kb[:, :1], vq[:, :1], va[:, :1], vb[:, :1])
+    np.testing.assert_array_equal(out1, V[:, 0].astype(np.float16))
+    # token 4's key made 40 x larger along q: its weight is 1 to fp16 precision
+    qs = np.sign(q.astype(np.float64))
+    kc2 = kc.copy()
+    kc2[:, 4] = np.where(qs > 0, 15, 0)
+    ka2 = ka.copy()
+    ka2[:, 4] = 40.0
+    kb2 = kb.copy()
+    kb2[:, 4] = -300.0
+    out2 = kv.attn_decode(q, quant.pack_nibbles(kc2), ka2, kb2, vq, va, vb)
+    np.testing.assert_array_equal(out2, V[:, 4].astype(np.float16))
+
+
+def test_attn_decode_is_convex_combination_and_r3_invariant():
+    # outputs lie between the values' extremes; and the scores of (q R, K R) equal those of
+    # (q, K): rotating the query and the dequantised keys back gives the same attention
+    rng = np.random.default_rng(2)
+    B, S, H = 2, 12, 2
+    kq, ka, kb, vq, va, vb, kc, vc = _cache(rng, B, S, H)
+    q = rng.standard_normal((B, H, 128)).astype(np.float16)
+    out = kv.attn_decode(q, kq, ka, kb, vq, va, vb).astype(np.float64)
+    V = va[..., None] * vc + vb[..., None]
+    assert np.all(out <= V.max(axis=1) + 1e-3) and np.all(out >= V.min(axis=1) - 1e-3)
+    K = ka[..., None] * kc + kb[..., None]
+    R = rotate.rotate_rows(np.eye(128), None, 128)          # rows of H/sqrt(128)
+    s_rot = np.einsum("bhd,bshd->bhs", q.astype(np.float64), K)
+    s_back = np.einsum("bhd,bshd->bhs", q.astype(np.float64) @ R.T, K @ R.T)
+    assert np.max(np.abs(s_rot - s_back)) <= 1e-10 * np.max(np.abs(s_rot))
+
+
+def test_attn_decode_bruteforce():
+    import math
+    rng = np.random.default_rng(3)
+    B, S, H = 1, 5, 2
+    kq, ka, kb, vq, va, vb, kc, vc = _cache(rng, B, S, H)
+    q = rng.standard_normal((B, H, 128)).astype(np.float16)
+    out = kv.attn_decode(q, kq, ka, kb, vq, va, vb, scale=0.1)
+    for h in range(H):
+        sc = []
+        for t in range(S):
+            sc.append(0.1 * sum(float(q[0, h, d]) * (ka[0, t, h] * kc[0, t, h, d] + kb[0, t, h]) for d in range(128)))
+        mx = max(sc)
+        w = [math.exp(x - mx) for x in sc]
+        z = sum(w)
+        for d in range(128):
+            ref = sum(w[t] / z * (va[0, t, h] * vc[0, t, h, d] + vb[0, t, h]) for t in range(S))
+            assert out[0, h, d] == np.float16(ref)
