@@ -206,6 +206,12 @@ def had_bytes(M, K, groups_per_row=1):
     return 2 * M * K + M * K // 2 + 8 * M * groups_per_row
 
 
+def attn_bytes(B, S, H, D=128):
+    """Decode attention over a 4-bit cache: K and V codes (D/2 bytes) and their fp32 alpha,
+    beta per cached (token, head), plus the fp16 query and output per head."""
+    return B * S * H * (2 * (D // 2) + 4 * 4) + 2 * B * H * D * 2
+
+
 def kv_bytes(E):
     return 3 * 2 * E + 2 * E + 2 * (E // 2) + 2 * 8 * (E // 128)
 
@@ -528,7 +534,21 @@ def kernel_report(torch, sq, workloads, dev):
         o.pop("k_rot")
         fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o))
     t_kv = timed(fns)
-    rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6)))
+    # decode attention of the last token's rotated query over that cache
+    B, S, H, D = q.shape
+    b_at = attn_bytes(B, S, H)
+    fns = []
+    for _ in range(n_copies(b_at)):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc)
+        qr = o["q_rot"][:, -1].contiguous()
+        oa = torch.empty_like(qr)
+        cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+        fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4(qr, *cache, out=oa))
+        del qc, kc, vc
+    t_at = timed(fns)
+    rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6),
+                    attn_decode=dict(ms=t_at, GBps=b_at / t_at / 1e6)))
     return rep
 
 

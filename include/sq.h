@@ -67,8 +67,8 @@ const char* sq_last_error(void);
 
 /*
  * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
- * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a4_linear_swiglu or
- * sq_qk_had_kvquant
+ * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a4_linear_swiglu,
+ * sq_qk_had_kvquant or sq_attn_decode_kv4
  * made by this host thread: start_event takes the start time of the first kernel that
  * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
  * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
@@ -204,6 +204,27 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                             void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
                             uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
                             void* stream);
+
+/*
+ * sq_attn_decode_kv4 -- attention of one new query per (batch, head) over the 4-bit KV
+ * cache written by sq_qk_had_kvquant, the step that consumes it.  Keys and values are
+ * dequantised group by group with eq. 1, K_t = k_alpha_t * c_t + k_beta_t (in the R3-rotated
+ * basis) and V_t likewise; the query is the R3-rotated one (q_rot of sq_qk_had_kvquant), so
+ * q_rot . K_t is the score of the unrotated query and key (Sec. 3.1):
+ *     out[b,h,:] = fp16( sum_t softmax_t(scale * q_rot[b,h,:] . K_t) V_t ),  t = 0 .. S-1.
+ *
+ *   q_rot      device fp16 [B, H, 128] (contiguous), 16-byte aligned
+ *   k_q, v_q   device uint8 [B, S, H, 64] (the sq_qk_had_kvquant layout), 16-byte aligned
+ *   k_alpha, k_beta, v_alpha, v_beta  device fp32 [B, S, H]
+ *   B, S, H    B >= 0 (0 is a no-op), S >= 1, H >= 1, B * H < 2^31, S * H * 64 < 2^31
+ *   D          128 (others: SQ_ERR_UNSUPPORTED)
+ *   scale      finite score scale, e.g. 1/sqrt(128)
+ *   out        device fp16 [B, H, 128] (contiguous), 16-byte aligned
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.
+ */
+sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
+                             const uint8_t* v_q, const float* v_alpha, const float* v_beta,
+                             int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -317,4 +317,42 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
   return hip_status(sq::launch_qk_had_kvquant(a, static_cast<hipStream_t>(stream)), "qk_had_kvquant launch");
 }
 
+sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
+                             const uint8_t* v_q, const float* v_alpha, const float* v_beta,
+                             int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream) {
+  TimingScope timing_scope;
+  if (!q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta || !out)
+    return fail(SQ_ERR_NULL, "q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta and out are required");
+  if (B < 0 || S < 1 || H < 1) return fail(SQ_ERR_SHAPE, "need B >= 0, S >= 1, H >= 1");
+  if (D != 128) return fail(SQ_ERR_UNSUPPORTED, "D=%lld: only head_dim 128 is implemented", (long long)D);
+  if (B * H >= (int64_t{1} << 31) || S >= (int64_t{1} << 31) / (H * 64))
+    return fail(SQ_ERR_SHAPE, "B*H=%lld or S*H*64 beyond 2^31", (long long)(B * H));
+  if (!(std::fabs(scale) < 3.0e38f)) return fail(SQ_ERR_SHAPE, "scale must be finite");
+  if (!aligned(q_rot, 16) || !aligned(k_q, 16) || !aligned(v_q, 16) || !aligned(out, 16) || !aligned(k_alpha, 4) ||
+      !aligned(k_beta, 4) || !aligned(v_alpha, 4) || !aligned(v_beta, 4))
+    return fail(SQ_ERR_ALIGN, "q_rot, k_q, v_q and out need 16-byte, scales 4-byte alignment");
+  const uint64_t heads = static_cast<uint64_t>(B) * static_cast<uint64_t>(H);
+  const uint64_t cache = heads * static_cast<uint64_t>(S);
+  sq_status s = check_alias({{q_rot, heads * 256, "q_rot"}, {k_q, cache * 64, "k_q"}, {v_q, cache * 64, "v_q"},
+                             {k_alpha, cache * 4, "k_alpha"}, {k_beta, cache * 4, "k_beta"},
+                             {v_alpha, cache * 4, "v_alpha"}, {v_beta, cache * 4, "v_beta"}},
+                            {{out, heads * 256, "out"}});
+  if (s != SQ_OK) return s;
+  if (B == 0) return ok();
+  sq::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q_rot);
+  a.kq = k_q;
+  a.ka = k_alpha;
+  a.kb = k_beta;
+  a.vq = v_q;
+  a.va = v_alpha;
+  a.vb = v_beta;
+  a.B = B;
+  a.S = S;
+  a.H = H;
+  a.scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  a.out = static_cast<uint16_t*>(out);
+  return hip_status(sq::launch_attn_decode_kv4(a, static_cast<hipStream_t>(stream)), "attn_decode_kv4 launch");
+}
+
 }  // extern "C"

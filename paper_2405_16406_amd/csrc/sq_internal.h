@@ -59,6 +59,21 @@ struct GemmArgs {
 // hipErrorNotSupported when no kernel covers the arguments (only with swiglu)
 hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
 
+struct AttnArgs {
+  const uint16_t* q;     // fp16 [B, H, 128], R3-rotated query of the new token
+  const uint8_t* kq;     // [B, S, H, 64] packed 4-bit codes
+  const float* ka;       // [B, S, H]
+  const float* kb;
+  const uint8_t* vq;
+  const float* va;
+  const float* vb;
+  int64_t B, S, H;       // S * H * 64 < 2^31 (32-bit buffer offsets per head)
+  float scale_log2e;     // score scale times log2(e)
+  uint16_t* out;         // fp16 [B, H, 128]
+};
+
+hipError_t launch_attn_decode_kv4(const AttnArgs& a, hipStream_t stream);
+
 struct KvArgs {
   const uint16_t* q;
   const uint16_t* k;

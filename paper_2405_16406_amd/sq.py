@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
                 4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
 
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
-           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant")
+           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_attn_decode_kv4")
 
 
 class SqError(RuntimeError):
@@ -62,6 +62,8 @@ def lib() -> ctypes.CDLL:
     L.sq_qk_had_kvquant.restype = _I32
     L.sq_qk_had_kvquant.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32,
                                     _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    L.sq_attn_decode_kv4.restype = _I32
+    L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, ctypes.c_float, _P, _P]
     _lib = L
     return L
 
@@ -227,4 +229,23 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None):
                                    _stream(q)), "sq_qk_had_kvquant")
     out = dict(out)
     out["k_rot"] = kr
+    return out
+
+
+def attn_decode_kv4(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None, out=None):
+    """Attention of one rotated query per (batch, head), q_rot fp16 [B, H, 128], over the
+    4-bit cache of qk_had_kvquant (k_q, v_q uint8 [B, S, H, 64], scales fp32 [B, S, H(, 1)]).
+    Returns out fp16 [B, H, 128]."""
+    _need(q_rot, torch.float16, "q_rot")
+    for t, nme in ((q_rot, "q_rot"), (k_q, "k_q"), (v_q, "v_q"), (k_alpha, "k_alpha"), (k_beta, "k_beta"),
+                   (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        if not t.is_contiguous():
+            raise ValueError(f"{nme} must be contiguous")
+    B, H, D = q_rot.shape
+    S = k_q.shape[1]
+    scale = 1.0 / D ** 0.5 if scale is None else scale
+    out = torch.empty_like(q_rot) if out is None else out
+    _check(lib().sq_attn_decode_kv4(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q), _ptr(v_alpha),
+                                    _ptr(v_beta), B, S, H, D, float(scale), _ptr(out), _stream(q_rot)),
+           "sq_attn_decode_kv4")
     return out

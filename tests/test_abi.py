@@ -147,6 +147,26 @@ def test_interleave_gate_up_layout():
         sq.interleave_gate_up(g[:48], u[:48])
 
 
+def attn(L, B=2, S=4, H=2, D=128, scale=0.1, **kw):
+    ptrs = [fake(i) for i in range(8)]
+    for i, nm in enumerate(("q", "kq", "ka", "kb", "vq", "va", "vb", "out")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_attn_decode_kv4(*ptrs[:7], B, S, H, D, ctypes.c_float(scale), ptrs[7], None)
+
+
+def test_attn_decode_validation(L):
+    assert attn(L, out=None) == sq.SQ_ERR_NULL
+    assert attn(L, S=0) == sq.SQ_ERR_SHAPE
+    assert attn(L, H=0) == sq.SQ_ERR_SHAPE
+    assert attn(L, D=64) == sq.SQ_ERR_UNSUPPORTED
+    assert attn(L, S=1 << 24, H=4) == sq.SQ_ERR_SHAPE           # S*H*64 beyond 31 bits
+    assert attn(L, scale=float("inf")) == sq.SQ_ERR_SHAPE
+    assert attn(L, out=ctypes.c_void_p(P * 256 + 8)) == sq.SQ_ERR_ALIGN
+    assert attn(L, out=ctypes.c_void_p(fake(4).value + 256)) == sq.SQ_ERR_ALIAS
+    assert attn(L, B=0) == sq.SQ_OK
+
+
 def kvq(L, B=1, S=2, H=2, D=128, bits=4, group=128, **kw):
     ptrs = [fake(i) for i in range(10)]
     for i, nm in enumerate(("q", "k", "v", "qr", "kq", "ka", "kb", "vq", "va", "vb")):

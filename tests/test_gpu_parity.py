@@ -401,6 +401,58 @@ def test_gemm_decode_kernel(variant, monkeypatch):
         gemm_case(M, N, K, seed=M * 31 + N + K, bias=(M % 2 == 1))
 
 
+# ---------------------------------------------------------------- decode attention
+
+def attn_case(B, S, H, seed, scale=None, qscale=2.0):
+    """GPU sq_attn_decode_kv4 vs oracle.attn_decode on a random 4-bit cache."""
+    rng = workloads.rng_for(seed)
+    kc, vc = rng.integers(0, 16, (B, S, H, 128)), rng.integers(0, 16, (B, S, H, 128))
+    ka, va = (rng.uniform(0.01, 0.2, (B, S, H)).astype(np.float32) for _ in range(2))
+    kb, vb = (rng.uniform(-1.5, 0.0, (B, S, H)).astype(np.float32) for _ in range(2))
+    q = (rng.standard_normal((B, H, 128)) * qscale).astype(np.float16)
+    kq, vq = oq.pack_nibbles(kc), oq.pack_nibbles(vc)
+    out = sq.attn_decode_kv4(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb), scale=scale)
+    ref = okv.attn_decode(q, kq, ka, kb, vq, va, vb, scale)
+    got = host(out)
+    assert np.isfinite(got).all()
+    parity.assert_out_close(got, ref)
+    return got, ref, (va[..., None] * vc + vb[..., None])
+
+
+@pytest.mark.parametrize("B,S,H", [(1, 1, 1), (1, 5, 3), (2, 17, 2), (3, 300, 5), (2, 1000, 8), (1, 129, 4),
+                                   (2, 4099, 4)])
+def test_attn_decode_shapes(B, S, H):
+    # one token up to several thousand; ragged batches of 16; head counts that are and are
+    # not a multiple of 8 (the XCD-aware head order applies to the former)
+    say(f"attn_decode_kv4 B={B} S={S} H={H}")
+    attn_case(B, S, H, seed=600 + B + S + H)
+
+
+def test_attn_decode_degenerate_scores():
+    say("attn_decode_kv4: scale 0 (mean of V), a sharp softmax, a single token")
+    got, ref, V = attn_case(2, 37, 3, seed=7, scale=0.0)
+    parity.assert_out_close(got, V.mean(axis=1).astype(np.float16))
+    attn_case(2, 200, 2, seed=8, scale=1.0, qscale=8.0)
+    got, ref, V = attn_case(1, 1, 4, seed=9)
+    parity.assert_out_close(got, V[:, 0].astype(np.float16))
+
+
+def test_attn_decode_after_kv_quant_full():
+    # the whole consumer chain at [8, 2048, 32, 128]: R3 + KV4 on the GPU, then the last
+    # token's rotated query attends over the cache the GPU wrote; oracle on two batches
+    say("qk_had_kvquant -> attn_decode_kv4 [8, 2048, 32, 128], last token's query")
+    q, k, v = workloads.kv_inputs()
+    o = sq.qk_had_kvquant(dev(q), dev(k), dev(v))
+    qr = o["q_rot"][:, -1].contiguous()
+    out = sq.attn_decode_kv4(qr, o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+    got = host(out)
+    for b in (0, 7):
+        sl = slice(b, b + 1)
+        ref = okv.attn_decode(host(qr)[sl], host(o["k_q"])[sl], host(o["k_alpha"])[sl], host(o["k_beta"])[sl],
+                              host(o["v_q"])[sl], host(o["v_alpha"])[sl], host(o["v_beta"])[sl])
+        parity.assert_out_close(got[sl], ref)
+
+
 # ---------------------------------------------------------------- chain
 
 def test_tiny_rotated_linear_chain():
