@@ -5,17 +5,20 @@
 //     out = softmax_t(scale * q . K_t) V,
 //     q . K_t = alpha_t (q . c_t) + beta_t sum(q).
 //
-// One workgroup of 8 waves per (batch, head).  Batch i of 16 cached tokens goes to wave
-// i % 8; lane l = 4 tok + qd holds token tok of the batch and head dims 32 qd .. 32 qd + 31,
-// i.e. one 16-byte load of K codes and one of V codes (a batch reads 16 x 64 contiguous
-// bytes of each), plus the token's four scales.
+// One workgroup of 16 waves (four per SIMD, to hide HBM latency) per (batch, head).
+// Batch i of 16 cached tokens goes to wave i % 16; lane l = 4 tok + qd holds token tok of
+// the batch and head dims 32 qd .. 32 qd + 31, i.e. one 16-byte load of K codes and one of
+// V codes (a batch reads 16 x 64 contiguous bytes of each); lane qd of the token loads its
+// scale number qd (k_alpha, k_beta, v_alpha, v_beta) and the quad shares them by DPP.
 //   * q . c_t: v_dot2_f32_f16 on code pairs made fp16 as 1024 + c (exact), minus 1024 times
 //     the lane's query sum; the four lanes of a token add their parts (DPP quad permutes).
-//   * Each lane keeps an online softmax over the tokens it sees, in base 2 (log2 e is folded
-//     into the scale): running maximum m, sum l, and acc_d = sum_t p_t alpha_t c_td,
-//     bsum = sum_t p_t beta_t for its 32 dims.
-//   * At the end the 16 token slots of a wave merge by butterflies over the lane index, and
-//     the 8 waves in LDS; out_d = (acc_d + bsum) / l.
+//   * Online softmax in base 2 (log2 e is folded into the scale) with one running maximum m
+//     per wave (the batch maximum by DPP row rotations and permlane swaps; a rescale only
+//     when it grows).  Each lane sums, over the tokens it sees, l = sum_t p_t,
+//     acc_d = sum_t p_t alpha_t (1024 + c_td) (v_fma_mix_f32 on the same fp16 code pairs),
+//     pa = sum_t p_t alpha_t and bsum = sum_t p_t beta_t; dim d is acc_d - 1024 pa + bsum.
+//   * At the end the 16 token slots of a wave add up in registers (same maximum), and the 16
+//     waves merge in LDS; out_d = (sum of the waves' rescaled dims) / (their rescaled l).
 // Workgroup i serves head index x(i) = (i % 8) * (G / 8) + i / 8 when the G = B * H heads
 // are a multiple of 8: workgroups go round-robin over the 8 XCDs, so heads h and h + 1 (the
 // two 64-byte halves of a 128-byte line of a token) are read through the same L2.
@@ -25,7 +28,7 @@
 namespace sq {
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 16;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kDepth = 4;  // batches in flight per wave
 
@@ -42,6 +45,25 @@ __device__ __forceinline__ float quad_xor(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, false));
 }
 
+// allreduce over the lanes with the same lane % 4 (the 16 token slots of a wave)
+template <typename Op>
+__device__ __forceinline__ float slots_reduce(float v, Op op) {
+  v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror:4
+  v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false)));  // row_ror:8
+  const bool odd_row = (threadIdx.x >> 4) & 1, upper = (threadIdx.x >> 5) & 1;
+  const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = op(v, __uint_as_float(odd_row ? s16[0] : s16[1]));  // the other row of the 32-lane half
+  const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = op(v, __uint_as_float(upper ? s32[0] : s32[1]));    // the other half
+  return v;
+}
+
+// value of lane L of this lane's quad
+template <int L>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), L * 0x55, 0xF, 0xF, false));
+}
+
 // 2^(a - b), 0 when a is -inf (an empty partial state)
 __device__ __forceinline__ float rescale(float a, float b) {
   return a == -INFINITY ? 0.0f : exp2f(__fsub_rn(a, b));
@@ -49,7 +71,7 @@ __device__ __forceinline__ float rescale(float a, float b) {
 
 __global__ void __launch_bounds__(kThreads)
 attn_decode_kv4(AttnArgs a) {
-  __shared__ float red_ml[kWaves][3];
+  __shared__ float red_ml[kWaves][2];
   __shared__ float red_acc[kWaves][128];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -87,37 +109,40 @@ attn_decode_kv4(AttnArgs a) {
 
   // ---- cache of this (batch, head): token t at byte t * H * 64 (codes) / t * H * 4 (scales)
   const int64_t row0 = b * S * a.H + h;
-  const int64_t cspan = ((S - 1) * a.H + 1) * 64, sspan = ((S - 1) * a.H + 1) * 4;
+  const int64_t cspan = ((S - 1) * a.H + 1) * 64;
   const __amdgpu_buffer_rsrc_t rk = rsrc(a.kq + row0 * 64, cspan);
   const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, cspan);
-  const __amdgpu_buffer_rsrc_t rka = rsrc(a.ka + row0, sspan);
-  const __amdgpu_buffer_rsrc_t rkb = rsrc(a.kb + row0, sspan);
-  const __amdgpu_buffer_rsrc_t rva = rsrc(a.va + row0, sspan);
-  const __amdgpu_buffer_rsrc_t rvb = rsrc(a.vb + row0, sspan);
-  const uint32_t cstride = static_cast<uint32_t>(a.H * 64), sstride = static_cast<uint32_t>(a.H * 4);
+  const float* pb = (qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb) + row0;  // this lane's scale
+  // token offsets fit 32 bits: S * H * 64 < 2^31 is checked on the host
+  const uint32_t H32 = static_cast<uint32_t>(a.H), S32 = static_cast<uint32_t>(S);
+  const uint32_t cstride = H32 * 64;
 
   const int nb = static_cast<int>((S + 15) / 16);  // batches of 16 tokens
   const int mine = nb > w ? (nb - w + kWaves - 1) / kWaves : 0;
   v4u kc[kDepth], vc[kDepth];
-  float ka[kDepth], kb[kDepth], va[kDepth], vb[kDepth];
+  float pv[kDepth];
   auto load = [&](int slot, int it) {
-    const int64_t t = static_cast<int64_t>(w + kWaves * it) * 16 + tok;
-    const bool ok = it < mine && t < S;  // past the end: out of range, reads zeros
-    const uint32_t co = ok ? static_cast<uint32_t>(t) * cstride + 16 * qd : 0x80000000u;
-    const uint32_t so = ok ? static_cast<uint32_t>(t) * sstride : 0x80000000u;
+    const uint32_t t = static_cast<uint32_t>(w + kWaves * it) * 16 + tok;
+    const bool ok = it < mine && t < S32;  // past the end: codes out of range (zeros), scale of token 0
+    const uint32_t co = ok ? t * cstride + 16 * qd : 0x80000000u;
     kc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rk, co, 0, 0));
     vc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rv, co, 0, 0));
-    ka[slot] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rka, so, 0, 0));
-    kb[slot] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rkb, so, 0, 0));
-    va[slot] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rva, so, 0, 0));
-    vb[slot] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rvb, so, 0, 0));
+    pv[slot] = pb[ok ? t * H32 : 0u];
   };
 
-  float m = -INFINITY, l = 0.0f, bsum = 0.0f;
+  float m = -INFINITY, l = 0.0f, bsum = 0.0f, pa_sum = 0.0f;
   float acc[32];
 #pragma unroll
   for (int d = 0; d < 32; ++d) acc[d] = 0.0f;
   const float cs = a.scale_log2e;
+  // code pair masks kept in registers (a VOP3 and-or takes no literal operands)
+  uint32_t kMask = 0x000F000Fu, kBase = 0x64006400u;
+  asm volatile("" : "+v"(kMask), "+v"(kBase));
+  // the four fp16 pairs (1024 + c) of a code word: (e0,e4) (e1,e5) (e2,e6) (e3,e7)
+  auto pairs = [&](uint32_t cw, v2h (&pr)[4]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pr[k] = __builtin_bit_cast(v2h, ((cw >> (4 * k)) & kMask) | kBase);
+  };
 
 #pragma unroll
   for (int d = 0; d < kDepth; ++d) load(d, d);
@@ -125,47 +150,49 @@ attn_decode_kv4(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
       const int it = it0 + d;
-      const int64_t t = static_cast<int64_t>(w + kWaves * it) * 16 + tok;
-      const bool ok = it < mine && t < S;  // uniform over the quad of a token
+      const uint32_t t = static_cast<uint32_t>(w + kWaves * it) * 16 + tok;
+      const bool ok = it < mine && t < S32;  // uniform over the quad of a token
       // q . c_t over the lane's 32 dims, then over the quad
       float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const uint32_t cw = kc[d][c];  // dims 8c .. 8c+7 of the lane: nibbles e = 0..7
-        const uint32_t pA = (cw & 0x000F000Fu) | 0x64006400u;          // (e0, e4)
-        const uint32_t pB = ((cw >> 4) & 0x000F000Fu) | 0x64006400u;   // (e1, e5)
-        const uint32_t pC = ((cw >> 8) & 0x000F000Fu) | 0x64006400u;   // (e2, e6)
-        const uint32_t pD = ((cw >> 12) & 0x000F000Fu) | 0x64006400u;  // (e3, e7)
-        s0 = __builtin_amdgcn_fdot2(qp[c][0], __builtin_bit_cast(v2h, pA), s0, false);
-        s1 = __builtin_amdgcn_fdot2(qp[c][1], __builtin_bit_cast(v2h, pB), s1, false);
-        s0 = __builtin_amdgcn_fdot2(qp[c][2], __builtin_bit_cast(v2h, pC), s0, false);
-        s1 = __builtin_amdgcn_fdot2(qp[c][3], __builtin_bit_cast(v2h, pD), s1, false);
+        v2h pr[4];
+        pairs(kc[d][c], pr);  // dims 8c .. 8c+7 of the lane
+        s0 = __builtin_amdgcn_fdot2(qp[c][0], pr[0], s0, false);
+        s1 = __builtin_amdgcn_fdot2(qp[c][1], pr[1], s1, false);
+        s0 = __builtin_amdgcn_fdot2(qp[c][2], pr[2], s0, false);
+        s1 = __builtin_amdgcn_fdot2(qp[c][3], pr[3], s1, false);
       }
       float dot = __fsub_rn(__fadd_rn(s0, s1), bias1024);
       dot = __fadd_rn(dot, quad_xor<1>(dot));
       dot = __fadd_rn(dot, quad_xor<2>(dot));
-      const float s = __fmul_rn(cs, __fmaf_rn(ka[d], dot, __fmul_rn(kb[d], qsum)));
-      if (ok) {
-        if (s > m) {  // new running maximum: rescale what has been summed
-          const float f = rescale(m, s);
-          l = __fmul_rn(l, f);
-          bsum = __fmul_rn(bsum, f);
+      const float ka = quad_bcast<0>(pv[d]), kb = quad_bcast<1>(pv[d]);
+      const float va = quad_bcast<2>(pv[d]), vb = quad_bcast<3>(pv[d]);
+      const float s = ok ? __fmul_rn(cs, __fmaf_rn(ka, dot, __fmul_rn(kb, qsum))) : -INFINITY;
+      const float mb = slots_reduce(s, [](float u, float v) { return fmaxf(u, v); });
+      if (mb > m) {  // (wave-uniform) new running maximum: rescale what has been summed
+        const float f = rescale(m, mb);
+        l = __fmul_rn(l, f);
+        bsum = __fmul_rn(bsum, f);
+        pa_sum = __fmul_rn(pa_sum, f);
 #pragma unroll
-          for (int e = 0; e < 32; ++e) acc[e] = __fmul_rn(acc[e], f);
-          m = s;
-        }
+        for (int e = 0; e < 32; ++e) acc[e] = __fmul_rn(acc[e], f);
+        m = mb;
+      }
+      if (ok) {
         const float p = exp2f(__fsub_rn(s, m));
         l = __fadd_rn(l, p);
-        bsum = __fmaf_rn(p, vb[d], bsum);
-        const float pa = __fmul_rn(p, va[d]);
+        bsum = __fmaf_rn(p, vb, bsum);
+        const float pa = __fmul_rn(p, va);
+        pa_sum = __fadd_rn(pa_sum, pa);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const uint32_t cw = vc[d][c];
-          const uint32_t lo = cw & 0x0F0F0F0Fu, hi = (cw >> 4) & 0x0F0F0F0Fu;  // even / odd dims
+          v2h pr[4];
+          pairs(vc[d][c], pr);
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            acc[8 * c + 2 * k] = __fmaf_rn(pa, static_cast<float>((lo >> (8 * k)) & 0xFFu), acc[8 * c + 2 * k]);
-            acc[8 * c + 2 * k + 1] = __fmaf_rn(pa, static_cast<float>((hi >> (8 * k)) & 0xFFu), acc[8 * c + 2 * k + 1]);
+          for (int k = 0; k < 4; ++k) {  // pair k holds dims 8c + k and 8c + k + 4
+            acc[8 * c + k] = __fmaf_rn(pa, static_cast<float>(pr[k][0]), acc[8 * c + k]);
+            acc[8 * c + k + 4] = __fmaf_rn(pa, static_cast<float>(pr[k][1]), acc[8 * c + k + 4]);
           }
         }
       }
@@ -173,48 +200,38 @@ attn_decode_kv4(AttnArgs a) {
     }
   }
 
-  // ---- the 16 token slots of the wave (lane bits 2..5) merge
+  // ---- the 16 token slots of the wave share m: their sums add up
+  auto add = [](float u, float v) { return __fadd_rn(u, v); };
+  l = slots_reduce(l, add);
+  bsum = slots_reduce(bsum, add);
+  pa_sum = slots_reduce(pa_sum, add);
 #pragma unroll
-  for (int off = 4; off < 64; off <<= 1) {
-    const float mo = __shfl_xor(m, off, 64);
-    const float lo_ = __shfl_xor(l, off, 64);
-    const float bo = __shfl_xor(bsum, off, 64);
-    const float mn = fmaxf(m, mo);
-    const float f = rescale(m, mn), fo = rescale(mo, mn);
-    l = __fmaf_rn(l, f, __fmul_rn(lo_, fo));
-    bsum = __fmaf_rn(bsum, f, __fmul_rn(bo, fo));
-#pragma unroll
-    for (int e = 0; e < 32; ++e) {
-      const float ao = __shfl_xor(acc[e], off, 64);
-      acc[e] = __fmaf_rn(acc[e], f, __fmul_rn(ao, fo));
-    }
-    m = mn;
-  }
+  for (int e = 0; e < 32; ++e) acc[e] = slots_reduce(acc[e], add);
+  // remove the 1024 offset of the code pairs and add the betas: the wave's dims
+  const float off = __fmul_rn(1024.0f, pa_sum);
   if (lane < 4) {
 #pragma unroll
-    for (int e = 0; e < 32; ++e) red_acc[w][32 * qd + e] = acc[e];
+    for (int e = 0; e < 32; ++e) red_acc[w][32 * qd + e] = __fadd_rn(__fsub_rn(acc[e], off), bsum);
     if (lane == 0) {
       red_ml[w][0] = m;
       red_ml[w][1] = l;
-      red_ml[w][2] = bsum;
     }
   }
   __syncthreads();
   if (w != 0) return;
-  // ---- the 8 waves merge; lane handles dims 2 lane, 2 lane + 1
+  // ---- the 16 waves merge; lane handles dims 2 lane, 2 lane + 1
   float M = -INFINITY;
 #pragma unroll
   for (int v = 0; v < kWaves; ++v) M = fmaxf(M, red_ml[v][0]);
-  float L = 0.0f, Bs = 0.0f, A0 = 0.0f, A1 = 0.0f;
+  float L = 0.0f, A0 = 0.0f, A1 = 0.0f;
 #pragma unroll
   for (int v = 0; v < kWaves; ++v) {
     const float f = rescale(red_ml[v][0], M);
     L = __fmaf_rn(red_ml[v][1], f, L);
-    Bs = __fmaf_rn(red_ml[v][2], f, Bs);
     A0 = __fmaf_rn(red_acc[v][2 * lane], f, A0);
     A1 = __fmaf_rn(red_acc[v][2 * lane + 1], f, A1);
   }
-  const float o0 = __fdiv_rn(__fadd_rn(A0, Bs), L), o1 = __fdiv_rn(__fadd_rn(A1, Bs), L);
+  const float o0 = __fdiv_rn(A0, L), o1 = __fdiv_rn(A1, L);
   reinterpret_cast<uint32_t*>(a.out + (b * a.H + h) * 128)[lane] =
       static_cast<uint32_t>(f2h(o0)) | (static_cast<uint32_t>(f2h(o1)) << 16);
 }
