@@ -444,7 +444,7 @@ def cpu_baseline(shape, target_s):
 
 
 def kernel_report(torch, sq, workloads, dev):
-    """Per-config kernel timings (HIP events around back-to-back launches) for the docs.
+    """Per-config kernel timings (each launch's own HIP events) for the docs.
 
     Each kernel cycles through enough copies of its inputs and outputs that they add up to
     more than the GPU's caches (256 MB of Infinity Cache, 4 MB of L2 per XCD), so repeated
@@ -456,19 +456,18 @@ def kernel_report(torch, sq, workloads, dev):
         return int(min(32, max(2, -(-REPORT_SPAN_BYTES // max(nbytes, 1)))))
 
     def timed(fns, reps=None):
-        """Mean time per launch over back-to-back launches (no host sync between them)."""
+        """Mean kernel time per launch over back-to-back launches: each call's own start/end
+        events (sq_time_next_call), so neither host gaps nor launch overhead count."""
         reps = reps or max(20, 2 * len(fns))
         for f in fns:
             f()
         torch.cuda.synchronize()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
         for r in range(reps):
+            sq.time_next_call(*evs[r])
             fns[r % len(fns)]()
-        b.record()
         torch.cuda.synchronize()
-        return a.elapsed_time(b) / reps
+        return sum(a.elapsed_time(b) for a, b in evs) / reps
 
     def act_fns(x, had, pow2, nbytes):
         """had_quant_act launches over distinct copies of x and of the outputs."""
