@@ -14,14 +14,15 @@ paper does not state the KV group size).
 
 import numpy as np
 
-from .quant import dequant, pack_nibbles, quant_asym, unpack_nibbles
+from .quant import dequant, pack_nibbles, quant_asym, store_codes, unpack_nibbles
 from .rotate import rotate_rows
 
 
 def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, group: int = 128):
     """q, k, v: fp16 [B, S, H, D].  Returns a dict with
     q_rot fp16 [B,S,H,D]; k_rot fp32 (quantizer input);
-    k_q, v_q uint8 [B,S,H,D/2]; k_alpha, k_beta, v_alpha, v_beta fp32 [B,S,H,D/group];
+    k_q, v_q uint8 [B,S,H,D/2] (bits 4) or [B,S,H,D] (bits 8);
+    k_alpha, k_beta, v_alpha, v_beta fp32 [B,S,H,D/group];
     k_codes, v_codes int64 [B,S,H,D].
     """
     D = q.shape[-1]
@@ -29,8 +30,8 @@ def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, g
     k_rot = rotate_rows(k, None, D).astype(np.float32)
     kc, ka, kb = quant_asym(k_rot, bits=bits, group=group)
     vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group)
-    return dict(q_rot=q_rot, k_rot=k_rot, k_q=pack_nibbles(kc), k_alpha=ka, k_beta=kb,
-                v_q=pack_nibbles(vc), v_alpha=va, v_beta=vb, k_codes=kc, v_codes=vc)
+    return dict(q_rot=q_rot, k_rot=k_rot, k_q=store_codes(kc, bits), k_alpha=ka, k_beta=kb,
+                v_q=store_codes(vc, bits), v_alpha=va, v_beta=vb, k_codes=kc, v_codes=vc)
 
 
 def attn_decode(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None):

@@ -21,7 +21,7 @@ Forward of one quantized linear layer y = x W^T with an online rotation R in fro
 
 import numpy as np
 
-from .quant import pack_nibbles, quant_asym, quant_sym
+from .quant import pack_nibbles, quant_asym, quant_sym, store_codes
 from .rotate import rotate_rows
 
 
@@ -30,8 +30,8 @@ def had_quant_act(x: np.ndarray, had_dense, pow2_n: int, bits: int = 4, group: i
 
     had_dense: int8 +-1 [a, a] or None (a = 1); pow2_n = b; rotation block n = a*b.
     (had_dense None, pow2_n 1) is the identity.  Returns
-    (packed uint8 [M, K/2], alpha fp32 [M, K/group], beta fp32 [M, K/group],
-     y_rot fp32 [M, K] = the quantizer input, codes int64 [M, K]).
+    (packed uint8 [M, K/2] (bits 4) or [M, K] (bits 8), alpha fp32 [M, K/group],
+     beta fp32 [M, K/group], y_rot fp32 [M, K] = the quantizer input, codes int64 [M, K]).
     """
     x = np.asarray(x)
     a = 1 if had_dense is None else had_dense.shape[0]
@@ -40,7 +40,7 @@ def had_quant_act(x: np.ndarray, had_dense, pow2_n: int, bits: int = 4, group: i
     else:
         y32 = rotate_rows(x, had_dense, pow2_n).astype(np.float32)
     q, alpha, beta = quant_asym(y32, bits=bits, group=group)
-    return pack_nibbles(q), alpha, beta, y32, q
+    return store_codes(q, bits), alpha, beta, y32, q
 
 
 def pack_w4(w: np.ndarray, had_dense=None, pow2_n: int = 1, bits: int = 4):

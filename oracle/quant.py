@@ -102,6 +102,17 @@ def pack_nibbles(q: np.ndarray) -> np.ndarray:
     return (lo | (hi << 4)).astype(np.uint8)
 
 
+def store_codes(q: np.ndarray, bits: int) -> np.ndarray:
+    """Storage of unsigned asymmetric codes: two per byte for 4 bits (pack_nibbles), one
+    per byte for 8 bits (the W4A8 and KV8 settings of Sec. 4.2 "Main results" and of the
+    speed measurement, Sec. 4.5)."""
+    if bits == 4:
+        return pack_nibbles(q)
+    if bits == 8:
+        return np.asarray(q, dtype=np.int64).astype(np.uint8)
+    raise ValueError(f"no storage for {bits}-bit codes")
+
+
 def unpack_nibbles(p: np.ndarray, signed: bool) -> np.ndarray:
     """Inverse of pack_nibbles: uint8 [..., K/2] -> int64 codes [..., K]."""
     b = np.asarray(p, dtype=np.int64)

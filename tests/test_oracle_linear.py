@@ -142,3 +142,26 @@ def test_swiglu_linear_bruteforce():
             assert abs(g[m, c] - gv) < 1e-12 and abs(u[m, c] - uv) < 1e-12
             ref = gv / (1.0 + math.exp(-gv)) * uv
             assert h[m, c] == np.float16(ref)
+
+
+def test_w4a8_gemm_and_epilogue_bruteforce():
+    # 8-bit activation codes against 4-bit weights: the same exact GEMM and epilogue
+    rng = np.random.default_rng(6)
+    qa = rng.integers(0, 256, size=(3, 40))
+    qw = rng.integers(-7, 8, size=(4, 40))
+    aa, ab = rng.uniform(0.01, 0.1, 3), rng.uniform(-3, 0, 3)
+    wa = rng.uniform(0.001, 0.01, 4)
+    y, acc = linear.w4a4_linear(qa, aa, ab, qw, wa, qw.sum(1))
+    for m in range(3):
+        for n in range(4):
+            s = sum(int(qa[m, k]) * int(qw[n, k]) for k in range(40))
+            assert acc[m, n] == s
+            ref = sum((aa[m] * qa[m, k] + ab[m]) * (wa[n] * qw[n, k]) for k in range(40))
+            assert y[m, n] == np.float16(ref)
+
+
+def test_had_quant_act_8bit_storage():
+    x = workloads.outlier_acts(workloads.rng_for(12), 4, 256, 4, 50.0)
+    p8, a8, b8, y8, q8 = linear.had_quant_act(x, None, 256, bits=8)
+    assert p8.shape == (4, 256) and p8.dtype == np.uint8 and np.array_equal(p8.astype(np.int64), q8)
+    assert q8.min() == 0 and q8.max() == 255

@@ -155,3 +155,22 @@ def test_sym_properties(v):
         err = np.abs(quant.dequant(q, a)[0] - v.astype(np.float64))
         assert np.all(err <= np.float64(a[0, 0]) * (0.5 + 4e-6))
     np.testing.assert_array_equal(quant.unpack_nibbles(quant.pack_nibbles(q), signed=True), q)
+
+
+def test_asym_8bit_closed_forms_and_storage():
+    # 8-bit asymmetric codes (the W4A8 / KV8 settings): min -> 0, max -> 255, every
+    # reconstruction within alpha/2, a linear ramp hits every level once, one code per byte
+    v = np.linspace(-3.0, 5.0, 256, dtype=np.float32)[None, :]
+    q, a, b = quant.quant_asym(v, bits=8)
+    np.testing.assert_array_equal(q[0], np.arange(256))
+    assert a[0] == np.float32(np.float32(8.0) / np.float32(255.0)) and b[0] == np.float32(-3.0)
+    rng = np.random.default_rng(8)
+    x = (rng.standard_normal((5, 96)) * 4).astype(np.float32)
+    q, a, b = quant.quant_asym(x, bits=8, group=32)
+    assert q.min() >= 0 and q.max() <= 255
+    err = np.abs(quant.dequant(q, a, b, group=32) - x.astype(np.float64))
+    assert np.all(err <= np.repeat(a, 32, axis=-1) * 0.5 * (1 + 1e-6))
+    s = quant.store_codes(q, 8)
+    assert s.dtype == np.uint8 and s.shape == q.shape and np.array_equal(s.astype(np.int64), q)
+    with pytest.raises(ValueError):
+        quant.store_codes(q, 6)
