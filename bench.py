@@ -469,13 +469,23 @@ def kernel_report(torch, sq, workloads, dev):
         torch.cuda.synchronize()
         return sum(a.elapsed_time(b) for a, b in evs) / reps
 
-    def act_fns(x, had, pow2, nbytes):
+    def act_fns(x, had, pow2, nbytes, bits=4):
         """had_quant_act launches over distinct copies of x and of the outputs."""
         fns = []
         for _ in range(n_copies(nbytes)):
             xc = x.clone()
-            o = sq.had_quant_act(xc, had, pow2)[:3]
-            fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, out=o))
+            o = sq.had_quant_act(xc, had, pow2, bits=bits)[:3]
+            fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, bits=bits, out=o))
+        return fns
+
+    def gemm8_fns(qx, w, nbytes):
+        """w4a8_linear launches over distinct copies of the operands and of y."""
+        fns = []
+        for _ in range(n_copies(nbytes)):
+            qc = tuple(t.clone() for t in qx)
+            wc = tuple(t.clone() for t in w)
+            y = sq.w4a8_linear(*qc, *wc)[0]
+            fns.append(lambda qc=qc, wc=wc, y=y: sq.w4a8_linear(*qc, *wc, out=y))
         return fns
 
     def gemm_fns(qx, w, nbytes, swiglu=False):
@@ -515,14 +525,27 @@ def kernel_report(torch, sq, workloads, dev):
         t_gu = timed(gemm_fns(qi, wgu, b_gu))
         t_sw = timed(gemm_fns(qi, wsw, b_sw, swiglu=True))
         t_d = timed(gemm_fns(qd, wd, b_d))
+        # W4A8: 8-bit activation codes (one byte each) into the same weights
+        qi8 = sq.had_quant_act(xin, bits=8)[:3]
+        qd8 = sq.had_quant_act(xdn, had, sh.had_pow2, bits=8)[:3]
+        b8_aq, b8_hq = had_bytes(M, H) + M * H // 2, had_bytes(M, I) + M * I // 2
+        b8_gu, b8_d = gemm_bytes(M, 2 * I, H) + M * H // 2, gemm_bytes(M, H, I) + M * I // 2
+        t8_aq = timed(act_fns(xin, None, 1, b8_aq, bits=8))
+        t8_hq = timed(act_fns(xdn, had, sh.had_pow2, b8_hq, bits=8))
+        t8_gu = timed(gemm8_fns(qi8, wgu, b8_gu))
+        t8_d = timed(gemm8_fns(qd8, wd, b8_d))
         rep.append(dict(config=sh.name,
                         act_quant=dict(ms=t_aq, GBps=b_aq / t_aq / 1e6),
                         r4_had_quant=dict(ms=t_hq, GBps=b_hq / t_hq / 1e6),
                         gate_gemm=dict(ms=t_g, TOPS=2 * M * I * H / t_g / 1e9, GBps=b_g / t_g / 1e6),
                         gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * I * H / t_gu / 1e9, GBps=b_gu / t_gu / 1e6),
                         gate_up_swiglu_gemm=dict(ms=t_sw, TOPS=4 * M * I * H / t_sw / 1e9, GBps=b_sw / t_sw / 1e6),
-                        down_gemm=dict(ms=t_d, TOPS=2 * M * I * H / t_d / 1e9, GBps=b_d / t_d / 1e6)))
-        del inp, xin, xdn, wg, wgu, wsw, wd, qi, qd
+                        down_gemm=dict(ms=t_d, TOPS=2 * M * I * H / t_d / 1e9, GBps=b_d / t_d / 1e6),
+                        act_quant_8bit=dict(ms=t8_aq, GBps=b8_aq / t8_aq / 1e6),
+                        r4_had_quant_8bit=dict(ms=t8_hq, GBps=b8_hq / t8_hq / 1e6),
+                        gate_up_w4a8=dict(ms=t8_gu, TOPS=4 * M * I * H / t8_gu / 1e9, GBps=b8_gu / t8_gu / 1e6),
+                        down_w4a8=dict(ms=t8_d, TOPS=2 * M * I * H / t8_d / 1e9, GBps=b8_d / t8_d / 1e6)))
+        del inp, xin, xdn, wg, wgu, wsw, wd, qi, qd, qi8, qd8
         torch.cuda.empty_cache()
     q, k, v = (up(t) for t in workloads.kv_inputs())
     E = q.numel()
@@ -533,6 +556,14 @@ def kernel_report(torch, sq, workloads, dev):
         o.pop("k_rot")
         fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o))
     t_kv = timed(fns)
+    fns = []
+    for _ in range(n_copies(kv_bytes(E) * 3 // 2)):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc, bits=8)
+        o.pop("k_rot")
+        fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, bits=8))
+    t_kv8 = timed(fns)
+    b_kv8 = kv_bytes(E) + E  # codes of K and V: one byte per element instead of half
     # decode attention of the last token's rotated query over that cache
     B, S, H, D = q.shape
     b_at = attn_bytes(B, S, H)
@@ -547,6 +578,7 @@ def kernel_report(torch, sq, workloads, dev):
         del qc, kc, vc
     t_at = timed(fns)
     rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6),
+                    kv_quant_8bit=dict(ms=t_kv8, GBps=b_kv8 / t_kv8 / 1e6),
                     attn_decode=dict(ms=t_at, GBps=b_at / t_at / 1e6)))
     return rep
 

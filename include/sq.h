@@ -53,7 +53,7 @@ typedef enum {
   SQ_OK = 0,
   SQ_ERR_NULL = 1,        /* a required pointer is NULL */
   SQ_ERR_SHAPE = 2,       /* sizes inconsistent or out of range */
-  SQ_ERR_UNSUPPORTED = 3, /* a valid request this build does not implement (e.g. bits != 4) */
+  SQ_ERR_UNSUPPORTED = 3, /* a valid request this build does not implement (e.g. bits = 6) */
   SQ_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
   SQ_ERR_ALIAS = 5,       /* an output overlaps an input or another output */
   SQ_ERR_HIP = 6          /* the HIP runtime reported an error (no device, launch failure) */
@@ -67,8 +67,8 @@ const char* sq_last_error(void);
 
 /*
  * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
- * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a4_linear_swiglu,
- * sq_qk_had_kvquant or sq_attn_decode_kv4
+ * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a8_linear,
+ * sq_w4a4_linear_swiglu, sq_qk_had_kvquant or sq_attn_decode_kv4
  * made by this host thread: start_event takes the start time of the first kernel that
  * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
  * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
@@ -94,7 +94,7 @@ sq_status sq_hadamard_factor(int32_t n, int8_t* out_host);
 
 /*
  * sq_had_quant_act -- online Hadamard rotation of every activation row (R4, Sec. 3.1) fused with asymmetric 4-bit quantization of
- * eq. 1 (Sec. 2) and nibble packing.
+ * eq. 1 (Sec. 2) and nibble packing, or 8-bit quantization (the W4A8 setting, Sec. 4.2).
  *
  *   x          device fp16 [M, ldx], row stride ldx elements; row m is x[m*ldx .. +K)
  *   M, K       rows (tokens) and row length; M >= 0 (M == 0 is a no-op), 0 < K <= SQ_MAX_ROW,
@@ -103,10 +103,12 @@ sq_status sq_hadamard_factor(int32_t n, int8_t* out_host);
  *   had_dense_n  a, order of the dense factor, 1 <= a <= SQ_MAX_DENSE
  *   had_dense  device int8 +-1 [a, a] row-major (must be a Hadamard matrix); NULL iff a == 1
  *   had_pow2_n b, power of two, 1 <= b <= 32768; n = a*b must divide K
- *   bits       4 (others: SQ_ERR_UNSUPPORTED)
+ *   bits       4 or 8 (others: SQ_ERR_UNSUPPORTED); 8-bit rows with a rotation take the
+ *              generic kernel, not the matrix-core ones
  *   group      quantization group length along the row: group | K, group % 2 == 0;
  *              group == K is per-token quantization (what sq_w4a4_linear consumes)
- *   q_out      device uint8 [M, K/2] (contiguous), 16-byte aligned: packed codes 0..15
+ *   q_out      device uint8, 16-byte aligned, contiguous: bits 4: [M, K/2] packed codes
+ *              0..15 (even k in the low nibble); bits 8: [M, K] codes 0..255
  *   alpha, beta device fp32 [M, K/group] (contiguous): scale and offset of each group
  *   dbg_rot    optional device fp32 [M, K]: the rotated rows (quantizer input); NULL to skip
  *   stream     hipStream_t
@@ -161,6 +163,22 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
                          int32_t* dbg_acc, void* stream);
 
 /*
+ * sq_w4a8_linear -- the quantized linear layer of the W4A8 setting (Sec. 4.2, 4.5): 8-bit
+ * per-token activation codes (sq_had_quant_act with bits = 8, group = K) against the 4-bit
+ * weights of sq_pack_w4.  acc[m,n] = sum_k qa[m,k] qw[n,k] exactly in int32 and
+ *     y[m,n] = fp16( w_alpha[n] * (x_alpha[m] * acc[m,n] + x_beta[m] * w_rowsum[n]) + bias[n] )
+ *
+ *   xq         device uint8 [M, K] (contiguous), 16-byte aligned: codes 0..255
+ *   x_alpha, x_beta, M, wq, w_alpha, w_rowsum, N, bias, y, ldy, dbg_acc   as for sq_w4a4_linear
+ *   K          > 0, K % 64 == 0, K <= 2^17 (the int32 sums of 16 x (qa - 128) x qw)
+ * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.
+ */
+sq_status sq_w4a8_linear(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                         const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                         int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
+                         int32_t* dbg_acc, void* stream);
+
+/*
  * sq_w4a4_linear_swiglu -- the gate and up projections of the MLP in one product, combined
  * in the epilogue into the input of down_proj, the activation that R4 rotates (Sec. 3.1,
  * Fig. 1(c)):
@@ -186,15 +204,16 @@ sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const f
 
 /*
  * sq_qk_had_kvquant -- R3 (Sec. 3.1) on post-RoPE queries and keys, per head,
- * R = S_D / sqrt(D); then asymmetric 4-bit quantization of eq. 1 of the rotated keys
+ * R = S_D / sqrt(D); then asymmetric 4-bit (or 8-bit: KV8) quantization of eq. 1 of the rotated keys
  * and of the (unrotated) values, one group per `group` contiguous elements of a head
  * vector (group == D: one (alpha, beta) per batch, token and head).
  *
  *   q, k, v    device fp16 [B, S, H, D] contiguous, 16-byte aligned
  *   B, S, H    >= 0 (any zero: no-op); D = 128
- *   bits       4; group = 128 (= D)
+ *   bits       4 or 8; group = 128 (= D)
  *   q_rot      device fp16 [B, S, H, D]: Q R, rounded to nearest fp16
- *   k_q, v_q   device uint8 [B, S, H, D/2], 16-byte aligned: packed codes 0..15
+ *   k_q, v_q   device uint8, 16-byte aligned: bits 4: [B, S, H, D/2] packed codes 0..15;
+ *              bits 8: [B, S, H, D] codes 0..255
  *   k_alpha, k_beta, v_alpha, v_beta   device fp32 [B, S, H, D/group]
  *   dbg_k_rot  optional device fp32 [B, S, H, D]: K R before quantization; NULL to skip
  * Errors: SQ_ERR_NULL, SQ_ERR_SHAPE, SQ_ERR_UNSUPPORTED, SQ_ERR_ALIGN, SQ_ERR_ALIAS, SQ_ERR_HIP.

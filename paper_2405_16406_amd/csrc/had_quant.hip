@@ -107,7 +107,9 @@ had_quant_act_generic(RotQuantArgs args) {
   if (args.dbg) {
     for (int i = threadIdx.x; i < K; i += kThreads) args.dbg[row * K + i] = buf[i];
   }
-  uint8_t* qrow = args.q + row * (K / 2);
+  const bool b8 = args.bits == 8;
+  const float levels = b8 ? 255.0f : 15.0f;
+  uint8_t* qrow = args.q + row * (b8 ? K : K / 2);
   const int G = K / args.group;
   if (G == 1) {
     float mn = INFINITY, mx = -INFINITY;
@@ -117,10 +119,14 @@ had_quant_act_generic(RotQuantArgs args) {
     }
     mn = block_min(mn, red_f);
     mx = block_max(mx, red_f);
-    const AsymParams p = asym_params(mn, mx);
+    const AsymParams p = asym_params(mn, mx, levels);
     if (threadIdx.x == 0) {
       args.alpha[row] = p.alpha;
       args.beta[row] = p.mn;
+    }
+    if (b8) {
+      for (int j = threadIdx.x; j < K; j += kThreads) qrow[j] = static_cast<uint8_t>(asym_code(buf[j], p));
+      return;
     }
     for (int j = threadIdx.x; j < K / 2; j += kThreads) {
       const uint32_t c0 = asym_code(buf[2 * j], p);
@@ -142,10 +148,14 @@ had_quant_act_generic(RotQuantArgs args) {
     }
     mn = wave_min(mn);
     mx = wave_max(mx);
-    const AsymParams p = asym_params(mn, mx);
+    const AsymParams p = asym_params(mn, mx, levels);
     if (lane == 0) {
       args.alpha[row * G + g] = p.alpha;
       args.beta[row * G + g] = p.mn;
+    }
+    if (b8) {
+      for (int i = lane; i < gs; i += kWave) qrow[g * gs + i] = static_cast<uint8_t>(asym_code(v[i], p));
+      continue;
     }
     for (int j = lane; j < gs / 2; j += kWave) {
       const uint32_t c0 = asym_code(v[2 * j], p);
@@ -184,7 +194,8 @@ pack_w4_generic(RotQuantArgs args) {
 }
 
 // Unrotated rows, per-token quantization: the row stays in registers.  Each thread owns
-// chunks of 8 consecutive elements (one 16-byte load, one 4-byte code store).
+// chunks of 8 consecutive elements (one 16-byte load, one 4-byte (4-bit) or 8-byte (8-bit)
+// code store).
 template <int W, int CHMAX>
 __global__ void __launch_bounds__(64 * W)
 quant_rows_identity(RotQuantArgs args) {
@@ -228,12 +239,13 @@ quant_rows_identity(RotQuantArgs args) {
     mn = fminf(mn, red[i]);
     mx = fmaxf(mx, red[W + i]);
   }
-  const AsymParams p = asym_params(mn, mx);
+  const bool b8 = args.bits == 8;
+  const AsymParams p = asym_params(mn, mx, b8 ? 255.0f : 15.0f);
   if (threadIdx.x == 0) {
     args.alpha[row] = p.alpha;
     args.beta[row] = p.mn;
   }
-  uint32_t* qrow = reinterpret_cast<uint32_t*>(args.q + row * (args.K / 2));
+  uint32_t* qrow = reinterpret_cast<uint32_t*>(args.q + row * (b8 ? args.K : args.K / 2));
 #pragma unroll
   for (int j = 0; j < CHMAX; ++j) {
     const int ch = threadIdx.x + j * T;
@@ -241,13 +253,23 @@ quant_rows_identity(RotQuantArgs args) {
       // eq. 1's t = (v - mn) * inv, rounded after each step; v_cvt_pk_u8_f32 rounds half to
       // even and saturates, and 0 <= t <= 15 (1 + 3 eps), so its byte is clamp(rint(t), 0, 15).
       // Even positions go to ev, odd ones to od; ev | od << 4 is the nibble-packed word.
-      uint32_t ev = 0, od = 0;
+      if (b8) {  // one code per byte (0 <= t <= 255 (1 + 3 eps)): positions 0-3, then 4-7
+        uint32_t w0 = 0, w1 = 0;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i], p.mn), p.inv), i, ev);
-        od = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i + 1], p.mn), p.inv), i, od);
+        for (int i = 0; i < 4; ++i) {
+          w0 = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][i], p.mn), p.inv), i, w0);
+          w1 = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][4 + i], p.mn), p.inv), i, w1);
+        }
+        reinterpret_cast<uint2*>(qrow)[ch] = make_uint2(w0, w1);
+      } else {
+        uint32_t ev = 0, od = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i], p.mn), p.inv), i, ev);
+          od = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i + 1], p.mn), p.inv), i, od);
+        }
+        qrow[ch] = ev | (od << 4);
       }
-      qrow[ch] = ev | (od << 4);
       if (args.dbg) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) args.dbg[row * args.K + ch * 8 + i] = v[j][i];

@@ -466,7 +466,7 @@ __device__ __forceinline__ void pair_wait(const int* flag, int target) {
     __builtin_amdgcn_s_sleep(1);
 }
 
-template <int A, int APAD, int NT, bool DBG>
+template <int A, int APAD, int NT, bool DBG, int BITS>
 __global__ void __launch_bounds__(512, 2)
 had_quant_pair(RotQuantArgs args) {
   using C = Pair<A, APAD, NT>;
@@ -728,7 +728,7 @@ had_quant_pair(RotQuantArgs args) {
 
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
     const float r_u = __fsub_rn(mx, mn);
-    const float a_u = __fdiv_rn(r_u, 15.0f);
+    const float a_u = __fdiv_rn(r_u, BITS == 8 ? 255.0f : 15.0f);
     const bool cst = __fmul_rn(a_u, s_n) < kMinNormal;
     const float inv_u = cst ? 0.0f : __fdiv_rn(1.0f, a_u);
     const float nb = -__fmul_rn(mn, inv_u);
@@ -740,25 +740,32 @@ had_quant_pair(RotQuantArgs args) {
     // ---- codes: lane (c, g) holds i_b = mt*32 + 16g + j (j = 0..15) of column j_a: bytes
     // via v_cvt_pk_u8_f32 (even j in ev, odd j in od), ev | od << 4 is then four
     // nibble-packed bytes; 8-byte store at output position j_a*64 + mt*32 + 16g.
-    uint8_t* qrow = args.q + row * (C::K / 2);
+    uint8_t* qrow = args.q + row * (C::K * BITS / 8);
 #pragma unroll
     for (int nt = 0; nt < C::NTW; ++nt) {
       const int ja = (h * C::NTW + nt) * 32 + c;
 #pragma unroll
       for (int mt = 0; mt < C::MT; ++mt) {
-        uint32_t w[2];
-#pragma unroll
-        for (int hw = 0; hw < 2; ++hw) {
-          uint32_t ev = 0, od = 0;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s], inv_u, nb), s, ev);
-            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
-          }
-          w[hw] = ev | (od << 4);
-        }
         const int pos = ja * B + mt * 32 + 16 * g;
-        if (valid && ja < A) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(w[0], w[1]);
+        if constexpr (BITS == 8) {  // one code per byte: 16-byte store
+          uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int j = 0; j < 16; ++j) w[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][j], inv_u, nb), j & 3, w[j >> 2]);
+          if (valid && ja < A) *reinterpret_cast<uint4*>(qrow + pos) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else {
+          uint32_t w[2];
+#pragma unroll
+          for (int hw = 0; hw < 2; ++hw) {
+            uint32_t ev = 0, od = 0;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+              ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s], inv_u, nb), s, ev);
+              od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
+            }
+            w[hw] = ev | (od << 4);
+          }
+          if (valid && ja < A) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(w[0], w[1]);
+        }
         if constexpr (DBG) {
           if (valid && ja < A) {
 #pragma unroll
@@ -811,7 +818,7 @@ struct Lines {
   static_assert(KS <= 32, "k-step sign bits");
 };
 
-template <int A, int F, int NT, bool DBG>
+template <int A, int F, int NT, bool DBG, int BITS>
 __global__ void __launch_bounds__(64 * NT, DBG ? 2 : 4)  // 4 waves per SIMD: 128 VGPRs
 had_quant_lines(RotQuantArgs args) {
   using C = Lines<A, F, NT>;
@@ -1029,7 +1036,7 @@ had_quant_lines(RotQuantArgs args) {
 
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
     const float r_u = __fsub_rn(mx, mn);
-    const float a_u = __fdiv_rn(r_u, 15.0f);
+    const float a_u = __fdiv_rn(r_u, BITS == 8 ? 255.0f : 15.0f);
     const bool cst = __fmul_rn(a_u, s_n) < kMinNormal;
     const float inv_u = cst ? 0.0f : __fdiv_rn(1.0f, a_u);
     const float nb = -__fmul_rn(mn, inv_u);
@@ -1039,22 +1046,29 @@ had_quant_lines(RotQuantArgs args) {
     }
 
     // ---- codes of line n, columns 32 mt + 16 g .. + 15: 8-byte stores
-    uint8_t* qrow = args.q + row * (C::K / 2);
+    uint8_t* qrow = args.q + row * (C::K * BITS / 8);
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      uint32_t wd[2];
-#pragma unroll
-      for (int hw = 0; hw < 2; ++hw) {
-        uint32_t ev = 0, od = 0;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s], inv_u, nb), s, ev);
-          od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
-        }
-        wd[hw] = ev | (od << 4);
-      }
       const int pos = n * 64 + mt * 32 + 16 * g;
-      if (real) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(wd[0], wd[1]);
+      if constexpr (BITS == 8) {  // one code per byte: 16-byte store
+        uint32_t wd[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) wd[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][j], inv_u, nb), j & 3, wd[j >> 2]);
+        if (real) *reinterpret_cast<uint4*>(qrow + pos) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+      } else {
+        uint32_t wd[2];
+#pragma unroll
+        for (int hw = 0; hw < 2; ++hw) {
+          uint32_t ev = 0, od = 0;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s], inv_u, nb), s, ev);
+            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
+          }
+          wd[hw] = ev | (od << 4);
+        }
+        if (real) *reinterpret_cast<uint2*>(qrow + pos / 2) = make_uint2(wd[0], wd[1]);
+      }
       if constexpr (DBG) {
         if (real) {
 #pragma unroll
@@ -1106,10 +1120,10 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
                : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
 }
 
-template <int A, int APAD, int NT, bool DBG>
+template <int A, int APAD, int NT, bool DBG, int BITS>
 hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Pair<A, APAD, NT>;
-  auto kern = had_quant_pair<A, APAD, NT, DBG>;
+  auto kern = had_quant_pair<A, APAD, NT, DBG, BITS>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (init != hipSuccess) return init;
@@ -1121,13 +1135,15 @@ hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
 
 template <int A, int APAD, int NT>
 hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
-  return a.dbg ? launch_pair_t<A, APAD, NT, true>(a, stream) : launch_pair_t<A, APAD, NT, false>(a, stream);
+  if (a.bits == 8)
+    return a.dbg ? launch_pair_t<A, APAD, NT, true, 8>(a, stream) : launch_pair_t<A, APAD, NT, false, 8>(a, stream);
+  return a.dbg ? launch_pair_t<A, APAD, NT, true, 4>(a, stream) : launch_pair_t<A, APAD, NT, false, 4>(a, stream);
 }
 
-template <int A, int F, int NT, bool DBG>
+template <int A, int F, int NT, bool DBG, int BITS>
 hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Lines<A, F, NT>;
-  auto kern = had_quant_lines<A, F, NT, DBG>;
+  auto kern = had_quant_lines<A, F, NT, DBG, BITS>;
   static int blocks_per_cu = 0;
   static const hipError_t init = [&] {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1145,17 +1161,22 @@ hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
 
 template <int A, int F, int NT>
 hipError_t launch_lines(const RotQuantArgs& a, hipStream_t stream) {
-  return a.dbg ? launch_lines_t<A, F, NT, true>(a, stream) : launch_lines_t<A, F, NT, false>(a, stream);
+  if (a.bits == 8)
+    return a.dbg ? launch_lines_t<A, F, NT, true, 8>(a, stream) : launch_lines_t<A, F, NT, false, 8>(a, stream);
+  return a.dbg ? launch_lines_t<A, F, NT, true, 4>(a, stream) : launch_lines_t<A, F, NT, false, 4>(a, stream);
 }
 
 }  // namespace
 
 // Returns hipErrorNotSupported when no fast path covers the arguments.
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
-  if (a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr) return hipErrorNotSupported;
-  // the pair and line kernels stage rows in 16-byte chunks
+  if ((a.bits != 4 && a.bits != 8) || a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr)
+    return hipErrorNotSupported;
+  // the pair and line kernels stage rows in 16-byte chunks (and write 4- or 8-bit codes);
+  // the register-prefetch kernels write 4-bit codes only
   const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && !getenv("SQ_KRON_STAGED");
+  if (!pair_ok && a.bits != 4) return hipErrorNotSupported;
   if (a.a == 28 && a.b == 512) {
     if (pair_ok) return launch_lines<28, 8, 7>(a, stream);
     return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);

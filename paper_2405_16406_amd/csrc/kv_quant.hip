@@ -1,4 +1,5 @@
-// R3 on post-RoPE Q and K (Sec. 3.1) fused with 4-bit asymmetric K/V cache quantization.
+// R3 on post-RoPE Q and K (Sec. 3.1) fused with 4-bit (or, for the KV8 setting, 8-bit)
+// asymmetric K/V cache quantization.
 //
 // One head vector (D = 128 fp16) is one quantization group.  Four lanes (a quad) own a
 // group; lane j of the quad holds the 32 elements i = 32*k + 8*j + e (k = 0..3, e = 0..7),
@@ -70,10 +71,11 @@ __device__ __forceinline__ void fwht128(float (&e)[32], int j) {
   for (int r = 0; r < 32; ++r) e[r] = __fmaf_rn(s2, e[r], quad_xor<2>(e[r]));
 }
 
-// eq. 1 asymmetric 4-bit codes of the quad's group; `scale` multiplies the reported alpha
-// and beta (1 when e holds the values themselves, and then the codes follow eq. 1 step
-// by step).  Element 32*k + 8*j + q -> byte 16*k + 4*j + q/2 of the group's 64 code bytes.
-template <bool EXACT>
+// eq. 1 asymmetric codes of the quad's group; `scale` multiplies the reported alpha and beta
+// (1 when e holds the values themselves, and then the codes follow eq. 1 step by step).
+// 4-bit: element 32*k + 8*j + q -> nibble of byte 16*k + 4*j + q/2 of the group's 64 bytes;
+// 8-bit: -> byte 32*k + 8*j + q of its 128 bytes.
+template <bool EXACT, int BITS>
 __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float scale, int64_t grp, uint8_t* q,
                                             float* alpha, float* beta) {
   float mn = e[0], mx = e[0];
@@ -88,13 +90,26 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
   mx = fmaxf(mx, quad_xor<2>(mx));
   // alpha of the reported (scaled) values decides the constant-group case
   const float r_u = __fsub_rn(mx, mn);
-  const float a_u = __fdiv_rn(r_u, 15.0f);
+  const float a_u = __fdiv_rn(r_u, BITS == 8 ? 255.0f : 15.0f);
   const bool cst = __fmul_rn(a_u, scale) < kMinNormal;
   const float inv = cst ? 1.0f : __fdiv_rn(1.0f, a_u);
   const float nb = -__fmul_rn(mn, inv);
-  uint8_t* qg = q + grp * (kD / 2);
+  uint8_t* qg = q + grp * (kD * BITS / 8);
+  if constexpr (BITS == 8) {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < 4; ++k) {
+      uint32_t w[2] = {0u, 0u};
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        const float v = e[8 * k + x];
+        const float t = EXACT ? __fmul_rn(__fsub_rn(v, mn), inv) : __fmaf_rn(v, inv, nb);
+        w[x >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(t, x & 3, w[x >> 2]);  // rounds half to even, clamps
+      }
+      *reinterpret_cast<uint2*>(qg + 32 * k + 8 * j) = make_uint2(w[0], w[1]);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < (BITS == 8 ? 0 : 4); ++k) {
     // bytes of the 8 codes q = 0..7, then even codes low nibble, odd codes high nibble
     uint32_t ev = 0, od = 0;
 #pragma unroll
@@ -123,7 +138,7 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
 // itself).  That takes 97 VGPRs (4 waves per SIMD); it pays when the grid has more
 // workgroups than that occupancy holds, and otherwise each vector is loaded just before its
 // transform.
-template <bool EARLY>
+template <bool EARLY, int BITS>
 __global__ void __launch_bounds__(kThreads)
 qk_had_kvquant_v2(KvArgs a) {
   const int64_t grp = (static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x) / 4;
@@ -161,12 +176,12 @@ qk_had_kvquant_v2(KvArgs a) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) a.dbg_k[base + 32 * k + 8 * j + q] = __fmul_rn(e[8 * k + q], a.inv_sqrt_d);
   }
-  quant_store<false>(e, j, a.inv_sqrt_d, grp, a.kq, a.ka, a.kb);
+  quant_store<false, BITS>(e, j, a.inv_sqrt_d, grp, a.kq, a.ka, a.kb);
 
   // V: quantize
   if constexpr (!EARLY) load_raw(a.v + base, j, rv);
   widen(rv, e);
-  quant_store<true>(e, j, 1.0f, grp, a.vq, a.va, a.vb);
+  quant_store<true, BITS>(e, j, 1.0f, grp, a.vq, a.va, a.vb);
 }
 
 }  // namespace
@@ -176,8 +191,12 @@ hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream) {
   const unsigned blocks = static_cast<unsigned>((threads + kThreads - 1) / kThreads);
   // Measured on MI355X: [8, 2048, 32, 128] (8192 workgroups) 112 vs 118 us with the early
   // loads; [1, 2048, 32, 128] (1024 workgroups, 4 per CU) 13.6 vs 15.1 us without them.
-  if (blocks >= 16 * 256) return launch(qk_had_kvquant_v2<true>, dim3(blocks), dim3(kThreads), 0, stream, a);
-  return launch(qk_had_kvquant_v2<false>, dim3(blocks), dim3(kThreads), 0, stream, a);
+  const bool early = blocks >= 16 * 256;
+  if (a.bits == 8)
+    return early ? launch(qk_had_kvquant_v2<true, 8>, dim3(blocks), dim3(kThreads), 0, stream, a)
+                 : launch(qk_had_kvquant_v2<false, 8>, dim3(blocks), dim3(kThreads), 0, stream, a);
+  return early ? launch(qk_had_kvquant_v2<true, 4>, dim3(blocks), dim3(kThreads), 0, stream, a)
+               : launch(qk_had_kvquant_v2<false, 4>, dim3(blocks), dim3(kThreads), 0, stream, a);
 }
 
 }  // namespace sq

@@ -127,7 +127,7 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   sq_status s = check_rows(M, K, ldx, "M");
   if (s != SQ_OK) return s;
   if ((s = check_rotation(K, had_dense_n, had_dense, had_pow2_n)) != SQ_OK) return s;
-  if (bits != 4) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: only 4-bit activations are implemented", bits);
+  if (bits != 4 && bits != 8) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: 4- and 8-bit activations are implemented", bits);
   if (group <= 0 || group % 2 != 0 || K % group != 0)
     return fail(SQ_ERR_SHAPE, "group=%d must be even and divide K=%lld", group, (long long)K);
   if (!aligned(x, 16) || !aligned(q_out, 16) || !aligned(alpha, 4) || !aligned(beta, 4) ||
@@ -137,7 +137,7 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   const uint64_t um = static_cast<uint64_t>(M);
   const uint64_t xbytes = um ? ((um - 1) * ldx + K) * 2 : 0;
   s = check_alias({{x, xbytes, "x"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"}},
-                  {{q_out, um * K / 2, "q_out"}, {alpha, um * G * 4, "alpha"}, {beta, um * G * 4, "beta"},
+                  {{q_out, um * K * bits / 8, "q_out"}, {alpha, um * G * 4, "alpha"}, {beta, um * G * 4, "beta"},
                    {dbg_rot, dbg_rot ? um * K * 4 : 0, "dbg_rot"}});
   if (s != SQ_OK) return s;
   if (M == 0) return ok();
@@ -150,6 +150,7 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   a.H = had_dense;
   a.b = had_pow2_n;
   a.group = group;
+  a.bits = bits;
   a.inv_sqrt_n = inv_sqrt(static_cast<int64_t>(had_dense_n) * had_pow2_n);
   a.q = q_out;
   a.alpha = alpha;
@@ -230,6 +231,46 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
   return hip_status(sq::launch_w4a4_gemm(g, static_cast<hipStream_t>(stream)), "w4a4_linear launch");
 }
 
+sq_status sq_w4a8_linear(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
+                         const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
+                         int64_t N, int64_t K, const void* bias, void* y, int64_t ldy,
+                         int32_t* dbg_acc, void* stream) {
+  TimingScope timing_scope;
+  if (!xq || !x_alpha || !x_beta || !wq || !w_alpha || !w_rowsum || !y)
+    return fail(SQ_ERR_NULL, "xq, x_alpha, x_beta, wq, w_alpha, w_rowsum and y are required");
+  if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
+  if (N <= 0 || N > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "N=%lld out of range", (long long)N);
+  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 17))
+    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^17)", (long long)K);
+  if (ldy < N) return fail(SQ_ERR_SHAPE, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+  if (!aligned(xq, 16) || !aligned(wq, 16) || !aligned(y, 2) || !aligned(x_alpha, 4) || !aligned(x_beta, 4) ||
+      !aligned(w_alpha, 4) || !aligned(w_rowsum, 4) || (bias && !aligned(bias, 2)) || (dbg_acc && !aligned(dbg_acc, 4)))
+    return fail(SQ_ERR_ALIGN, "xq/wq need 16-byte, scales 4-byte and y 2-byte alignment");
+  const uint64_t um = static_cast<uint64_t>(M), un = static_cast<uint64_t>(N), uk = static_cast<uint64_t>(K);
+  const uint64_t ybytes = um ? ((um - 1) * ldy + un) * 2 : 0;
+  sq_status s = check_alias({{xq, um * uk, "xq"}, {x_alpha, um * 4, "x_alpha"}, {x_beta, um * 4, "x_beta"},
+                             {wq, un * uk / 2, "wq"}, {w_alpha, un * 4, "w_alpha"}, {w_rowsum, un * 4, "w_rowsum"},
+                             {bias, bias ? un * 2 : 0, "bias"}},
+                            {{y, ybytes, "y"}, {dbg_acc, dbg_acc ? um * un * 4 : 0, "dbg_acc"}});
+  if (s != SQ_OK) return s;
+  if (M == 0) return ok();
+  sq::GemmArgs g{};
+  g.xq = xq;
+  g.xa = x_alpha;
+  g.xb = x_beta;
+  g.M = M;
+  g.wq = wq;
+  g.wa = w_alpha;
+  g.rs = w_rowsum;
+  g.N = N;
+  g.K = K;
+  g.bias = static_cast<const uint16_t*>(bias);
+  g.y = static_cast<uint16_t*>(y);
+  g.ldy = ldy;
+  g.dbg_acc = dbg_acc;
+  return hip_status(sq::launch_w4a8_gemm(g, static_cast<hipStream_t>(stream)), "w4a8_linear launch");
+}
+
 sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
                                 const uint8_t* wq, const float* w_alpha, const int32_t* w_rowsum,
                                 int64_t N, int64_t K, const void* bias, void* h, int64_t ldh, void* stream) {
@@ -285,7 +326,7 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
     return fail(SQ_ERR_NULL, "q, k, v, q_rot, k_q, k_alpha, k_beta, v_q, v_alpha and v_beta are required");
   if (B < 0 || S < 0 || H < 0) return fail(SQ_ERR_SHAPE, "negative B, S or H");
   if (D != 128) return fail(SQ_ERR_UNSUPPORTED, "D=%lld: only head_dim 128 is implemented", (long long)D);
-  if (bits != 4) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: only 4-bit KV is implemented", bits);
+  if (bits != 4 && bits != 8) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: 4- and 8-bit KV are implemented", bits);
   if (group != 128) return fail(SQ_ERR_UNSUPPORTED, "group=%d: only group 128 (= D) is implemented", group);
   const uint64_t groups = static_cast<uint64_t>(B) * static_cast<uint64_t>(S) * static_cast<uint64_t>(H);
   if (groups > (uint64_t{1} << 40)) return fail(SQ_ERR_SHAPE, "B*S*H too large");
@@ -295,8 +336,8 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
     return fail(SQ_ERR_ALIGN, "tensors need 16-byte, scales 4-byte alignment");
   const uint64_t E = groups * 128;
   sq_status s = check_alias({{q, E * 2, "q"}, {k, E * 2, "k"}, {v, E * 2, "v"}},
-                            {{q_rot, E * 2, "q_rot"}, {k_q, E / 2, "k_q"}, {k_alpha, groups * 4, "k_alpha"},
-                             {k_beta, groups * 4, "k_beta"}, {v_q, E / 2, "v_q"}, {v_alpha, groups * 4, "v_alpha"},
+                            {{q_rot, E * 2, "q_rot"}, {k_q, E * bits / 8, "k_q"}, {k_alpha, groups * 4, "k_alpha"},
+                             {k_beta, groups * 4, "k_beta"}, {v_q, E * bits / 8, "v_q"}, {v_alpha, groups * 4, "v_alpha"},
                              {v_beta, groups * 4, "v_beta"}, {dbg_k_rot, dbg_k_rot ? E * 4 : 0, "dbg_k_rot"}});
   if (s != SQ_OK) return s;
   if (groups == 0) return ok();
@@ -314,6 +355,7 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
   a.va = v_alpha;
   a.vb = v_beta;
   a.dbg_k = dbg_k_rot;
+  a.bits = bits;
   return hip_status(sq::launch_qk_had_kvquant(a, static_cast<hipStream_t>(stream)), "qk_had_kvquant launch");
 }
 

@@ -23,21 +23,21 @@ __device__ __forceinline__ uint16_t f2h(float v) {
 // alpha = 1, so 1 / alpha stays finite and every code is 0.
 constexpr float kMinNormal = 1.17549435e-38f;
 
-// Asymmetric eq. 1 parameters from a group's min and max (4-bit: L = 15).
+// Asymmetric eq. 1 parameters from a group's min and max, L = 2^bits - 1 levels (15 or 255).
 //   r = mx - mn;  alpha = r / L (1 if below kMinNormal);  inv = 1 / alpha  -- each one IEEE rounding.
 struct AsymParams {
-  float mn, alpha, inv;
+  float mn, alpha, inv, levels;
 };
-__device__ __forceinline__ AsymParams asym_params(float mn, float mx) {
+__device__ __forceinline__ AsymParams asym_params(float mn, float mx, float levels = 15.0f) {
   const float r = __fsub_rn(mx, mn);
-  const float a = __fdiv_rn(r, 15.0f);
+  const float a = __fdiv_rn(r, levels);
   const float alpha = (a < kMinNormal) ? 1.0f : a;  // zero or subnormal: constant group
-  return {mn, alpha, __fdiv_rn(1.0f, alpha)};
+  return {mn, alpha, __fdiv_rn(1.0f, alpha), levels};
 }
-// code = clamp(rint((v - mn) * inv), 0, 15)
+// code = clamp(rint((v - mn) * inv), 0, L)
 __device__ __forceinline__ uint32_t asym_code(float v, const AsymParams& p) {
   const float t = __fmul_rn(__fsub_rn(v, p.mn), p.inv);
-  return static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), 15.0f));
+  return static_cast<uint32_t>(fminf(fmaxf(rintf(t), 0.0f), p.levels));
 }
 
 // Symmetric eq. 1 (beta = 0, L = 7): alpha = amax / 7 (1 if below kMinNormal); code in [-7, 7].

@@ -22,17 +22,18 @@ struct RotQuantArgs {
   const int8_t* H;       // [a, a] +-1 (device), nullptr when a == 1
   int b;                 // Sylvester order
   int group;             // quantization group (asym mode)
+  int bits;              // activation codes: 4 (two per byte) or 8 (one per byte)
   float inv_sqrt_n;      // fl32(1 / sqrt(a * b))
-  uint8_t* q;            // packed codes [rows, K/2]
+  uint8_t* q;            // codes [rows, K/2] (4-bit, packed) or [rows, K] (8-bit)
   float* alpha;          // [rows, K/group] (asym) or [rows] (sym)
   float* beta;           // [rows, K/group] (asym only)
   int32_t* rowsum;       // [rows] (sym only)
   float* dbg;            // optional fp32 [rows, K]
 };
 
-// Rotation + asymmetric per-group 4-bit quantization of activation rows.
+// Rotation + asymmetric per-group 4- or 8-bit quantization of activation rows.
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream);
-// Fast path for K = a*b rows with a registered dense order, per-token groups;
+// Fast path for K = a*b rows with a registered dense order, per-token 4-bit groups;
 // hipErrorNotSupported when it does not apply.
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream);
 // Rotation + symmetric per-row 4-bit quantization of weight rows, with code row sums.
@@ -58,6 +59,10 @@ struct GemmArgs {
 
 // hipErrorNotSupported when no kernel covers the arguments (only with swiglu)
 hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
+// The same product with 8-bit activation codes (xq [M, K], one code per byte).
+hipError_t launch_w4a8_gemm(const GemmArgs& g, hipStream_t stream);
+// Its decode-sized (M <= 16) weight-streaming kernel; hipErrorNotSupported otherwise.
+hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream);
 
 struct AttnArgs {
   const uint16_t* q;     // fp16 [B, H, 128], R3-rotated query of the new token
@@ -88,6 +93,7 @@ struct KvArgs {
   float* va;
   float* vb;
   float* dbg_k;
+  int bits;              // cache codes: 4 (two per byte) or 8 (one per byte)
 };
 
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream);

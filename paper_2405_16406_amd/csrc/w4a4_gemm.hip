@@ -981,7 +981,18 @@ struct Skinny {
   static constexpr int LDS = WAVES * NB * 4 * 64 * 4;  // partial sums: [wave][block][reg][lane] int32
 };
 
-template <int NB, int SD>
+// A8: 8-bit activation codes (W4A8): a lane loads the 32 code bytes matching its 32 weight
+// codes, in the weights' k-slot order (v_perm_b32) and made signed (xor 0x80, codes - 128);
+// the epilogue adds the shift back through the zero-point term (beta + 128 alpha).
+__device__ __forceinline__ v4i act8_operand(const v4u d) {
+  const uint32_t f = 0x80808080u;
+  return v4i{static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x06040200u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x07050301u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x06040200u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x07050301u) ^ f)};
+}
+
+template <int NB, int SD, bool A8 = false>
 __global__ void __launch_bounds__(512)
 w4a4_gemm_skinny(GemmArgs g) {
   using S = Skinny<NB, SD>;
@@ -997,18 +1008,24 @@ w4a4_gemm_skinny(GemmArgs g) {
   const uint32_t kw = ((KB + S::WAVES * 64 - 1) / (S::WAVES * 64)) * 64;
   const uint32_t k0 = wave * kw;
   const int nsteps = static_cast<int>(kw / 64);
-  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
+  const uint32_t AB = A8 ? 2 * KB : KB;  // activation bytes per row
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * AB);
   const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq, g.N * KB);
-  const uint32_t arow = static_cast<uint32_t>(r) * KB;
+  const uint32_t arow = static_cast<uint32_t>(r) * AB;
   uint32_t brow[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) brow[j] = static_cast<uint32_t>(n0 + 16 * j + r) * KB;
 
-  v4u ra[SD], rb[SD][NB];
+  v4u ra[SD], ra2[A8 ? SD : 1], rb[SD][NB];
   auto load = [&](int slot, int t) {
     const uint32_t k = k0 + static_cast<uint32_t>(t) * 64 + 16 * sg;
     const bool ok = k < KB && k < k0 + kw;
-    ra[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? arow + k : 0x80000000u, 0, 0));
+    if constexpr (A8) {  // the 32 activation bytes of the lane's 32 weight codes
+      ra[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? arow + 2 * k : 0x80000000u, 0, 0));
+      ra2[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? arow + 2 * k + 16 : 0x80000000u, 0, 0));
+    } else {
+      ra[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? arow + k : 0x80000000u, 0, 0));
+    }
 #pragma unroll
     for (int j = 0; j < NB; ++j)
       rb[slot][j] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? brow[j] + k : 0x80000000u, 0, 0));
@@ -1019,9 +1036,14 @@ w4a4_gemm_skinny(GemmArgs g) {
   auto step = [&](int slot) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const uint32_t a0 = ra[slot][2 * hh], a1 = ra[slot][2 * hh + 1];
-      const v4i ea = {static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
-                      static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+      v4i ea;
+      if constexpr (A8) {
+        ea = act8_operand(hh == 0 ? ra[slot] : ra2[slot]);
+      } else {
+        const uint32_t a0 = ra[slot][2 * hh], a1 = ra[slot][2 * hh + 1];
+        ea = v4i{static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
+                 static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+      }
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const uint32_t b0 = rb[slot][j][2 * hh], b1 = rb[slot][j][2 * hh + 1];
@@ -1055,7 +1077,7 @@ w4a4_gemm_skinny(GemmArgs g) {
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[j][i] += part[((w * NB + j) * 4 + i) * 64 + lane];
-  if (g.swiglu) {
+  if (!A8 && g.swiglu) {
     // NB % 4 == 0 (n0 % 64 == 0): in each run of four blocks, blocks 0, 1 are gate rows and
     // blocks 2, 3 the up rows of the same 32 output columns, in the same lanes and registers
     if constexpr (NB % 4 == 0) {
@@ -1092,11 +1114,12 @@ w4a4_gemm_skinny(GemmArgs g) {
     for (int i = 0; i < 4; ++i) {
       const int64_t m = 4 * sg + i;
       if (m >= g.M) continue;
-      // same arithmetic as the ring kernel's epilogue (acc holds 16 * sum)
+      // same arithmetic as the ring kernel's epilogue (acc holds 16 * sum; A8: of qa - 128)
       const float t = __fmul_rn(sn, static_cast<float>(acc[j][i]));
-      const float yv = fp32_result(__fmaf_rn(__fmul_rn(g.xa[m], 0.0625f), t, __fmaf_rn(g.xb[m], wn, bn)));
+      const float xb = A8 ? __fmaf_rn(128.0f, g.xa[m], g.xb[m]) : g.xb[m];
+      const float yv = fp32_result(__fmaf_rn(__fmul_rn(g.xa[m], 0.0625f), t, __fmaf_rn(xb, wn, bn)));
       g.y[m * g.ldy + n] = f2h(yv);
-      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = acc[j][i] >> 4;
+      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = (acc[j][i] >> 4) + (A8 ? 128 * g.rs[n] : 0);
     }
   }
 }
@@ -1107,16 +1130,17 @@ constexpr int skinny_depth() {
   return NB <= 4 ? 32 / (NB + 1) : 24 / (NB + 1);
 }
 
-template <int NB, int SD>
+template <int NB, int SD, bool A8 = false>
 bool fits_skinny(const GemmArgs& g) {
   const int64_t kb = g.K / 2;
-  return g.M <= 16 && g.M * kb + 64 < (int64_t{1} << 31) && (g.N + 16 * NB) * kb + 64 < (int64_t{1} << 31);
+  return g.M <= 16 && g.M * kb * (A8 ? 2 : 1) + 64 < (int64_t{1} << 31) &&
+         (g.N + 16 * NB) * kb + 64 < (int64_t{1} << 31);
 }
 
-template <int NB, int SD>
+template <int NB, int SD, bool A8 = false>
 hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
   using S = Skinny<NB, SD>;
-  auto kern = w4a4_gemm_skinny<NB, SD>;
+  auto kern = w4a4_gemm_skinny<NB, SD, A8>;
   const dim3 grid(static_cast<unsigned>((g.N + S::BN - 1) / S::BN));
   return launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g);
 }
@@ -1155,7 +1179,24 @@ hipError_t launch_skinny_sized(const GemmArgs& g, hipStream_t stream) {
   }
 }
 
+// 8-bit activations take two loads per step: shallower prefetch, at most 4 blocks (8 blocks
+// spill at any depth); all three fit without spills.
+template <int NB>
+hipError_t try_skinny8(const GemmArgs& g, hipStream_t stream) {
+  static_assert(NB == 1 || NB == 2 || NB == 4, "A8 decode instantiations");
+  constexpr int SD = NB == 1 ? 8 : (NB == 2 ? 6 : 4);
+  return fits_skinny<NB, SD, true>(g) ? launch_skinny<NB, SD, true>(g, stream) : hipErrorNotSupported;
+}
+
 }  // namespace
+
+hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream) {
+  if (g.M > 16) return hipErrorNotSupported;
+  const int64_t nb = (g.N + 4095) / 4096;  // the rows-per-workgroup rule of the W4A4 decode kernel
+  if (nb <= 1) return try_skinny8<1>(g, stream);
+  if (nb <= 3) return try_skinny8<2>(g, stream);
+  return try_skinny8<4>(g, stream);
+}
 
 hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
   if (g.swiglu) {

@@ -20,7 +20,8 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
                 4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
 
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
-           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_attn_decode_kv4")
+           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a8_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant",
+           "sq_attn_decode_kv4")
 
 
 class SqError(RuntimeError):
@@ -57,6 +58,8 @@ def lib() -> ctypes.CDLL:
     L.sq_pack_w4.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _P, _P, _P]
     L.sq_w4a4_linear.restype = _I32
     L.sq_w4a4_linear.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P]
+    L.sq_w4a8_linear.restype = _I32
+    L.sq_w4a8_linear.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P]
     L.sq_w4a4_linear_swiglu.restype = _I32
     L.sq_w4a4_linear_swiglu.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P]
     L.sq_qk_had_kvquant.restype = _I32
@@ -109,9 +112,9 @@ def hadamard_factor(n: int) -> np.ndarray:
 
 def had_quant_act(x: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1,
                   group: int | None = None, bits: int = 4, dbg: bool = False, out=None):
-    """Rotate rows of x (fp16 [M, K], row stride x.stride(0)) and quantize (asym 4-bit).
+    """Rotate rows of x (fp16 [M, K], row stride x.stride(0)) and quantize (asym, 4 or 8 bits).
 
-    had: int8 +-1 [a, a] on the device or None.  Returns (q uint8 [M, K/2],
+    had: int8 +-1 [a, a] on the device or None.  Returns (q uint8 [M, K/2] (4-bit) or [M, K] (8-bit),
     alpha fp32 [M, K/group], beta fp32 [M, K/group], dbg_rot fp32 [M, K] or None).
     """
     _need(x, torch.float16, "x")
@@ -124,7 +127,7 @@ def had_quant_act(x: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 
         _need(had, torch.int8, "had")
     dev = x.device
     if out is None:
-        q = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        q = torch.empty((M, K * bits // 8), dtype=torch.uint8, device=dev)
         al = torch.empty((M, K // group), dtype=torch.float32, device=dev)
         be = torch.empty((M, K // group), dtype=torch.float32, device=dev)
     else:
@@ -176,6 +179,26 @@ def w4a4_linear(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None,
     return y, acc
 
 
+def w4a8_linear(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None, dbg=False):
+    """y = fp16(s_n (alpha_m acc + beta_m rowsum_n) + bias_n) with 8-bit activation codes
+    xq uint8 [M, K] (had_quant_act bits=8) and packed 4-bit weights wq uint8 [N, K/2].
+    Returns (y fp16 [M, N], acc int32 [M, N] or None).
+    """
+    _need(xq, torch.uint8, "xq")
+    _need(wq, torch.uint8, "wq")
+    M, K = xq.shape
+    N = wq.shape[0]
+    if 2 * wq.shape[1] != K:
+        raise ValueError("xq and wq disagree on K")
+    dev = xq.device
+    y = torch.empty((M, N), dtype=torch.float16, device=dev) if out is None else out
+    acc = torch.empty((M, N), dtype=torch.int32, device=dev) if dbg else None
+    _check(lib().sq_w4a8_linear(_ptr(xq), _ptr(x_alpha.reshape(-1)), _ptr(x_beta.reshape(-1)), M, _ptr(wq),
+                                _ptr(w_alpha), _ptr(w_rowsum), N, K, _ptr(bias), _ptr(y), y.stride(0), _ptr(acc),
+                                _stream(xq)), "sq_w4a8_linear")
+    return y, acc
+
+
 def w4a4_linear_swiglu(xq, x_alpha, x_beta, wq, w_alpha, w_rowsum, bias=None, out=None):
     """h = fp16(SiLU(gate) * up) from gate/up weights packed as one matrix whose rows
     interleave them in blocks of 32 (see interleave_gate_up).  Returns h fp16 [M, N/2].
@@ -203,8 +226,8 @@ def interleave_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
                        dim=1).reshape(2 * I, *gate.shape[1:])
 
 
-def qk_had_kvquant(q, k, v, dbg: bool = False, out=None):
-    """R3 on Q and K per head (D = 128) + 4-bit asymmetric K/V quantization, group 128.
+def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4):
+    """R3 on Q and K per head (D = 128) + 4-bit (or 8-bit) asymmetric K/V quantization, group 128.
 
     Returns dict(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, k_rot (or None)).
     """
@@ -216,14 +239,14 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None):
     dev = q.device
     if out is None:
         out = dict(q_rot=torch.empty_like(q),
-                   k_q=torch.empty((B, S, H, D // 2), dtype=torch.uint8, device=dev),
+                   k_q=torch.empty((B, S, H, D * bits // 8), dtype=torch.uint8, device=dev),
                    k_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
                    k_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
-                   v_q=torch.empty((B, S, H, D // 2), dtype=torch.uint8, device=dev),
+                   v_q=torch.empty((B, S, H, D * bits // 8), dtype=torch.uint8, device=dev),
                    v_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
                    v_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev))
     kr = torch.empty((B, S, H, D), dtype=torch.float32, device=dev) if dbg else None
-    _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, 4, 128,
+    _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128,
                                    _ptr(out["q_rot"]), _ptr(out["k_q"]), _ptr(out["k_alpha"]), _ptr(out["k_beta"]),
                                    _ptr(out["v_q"]), _ptr(out["v_alpha"]), _ptr(out["v_beta"]), _ptr(kr),
                                    _stream(q)), "sq_qk_had_kvquant")

@@ -73,7 +73,7 @@ def test_had_quant_act_validation(L):
     assert hqa(L, b=3) == sq.SQ_ERR_SHAPE
     assert hqa(L, a=28, H=fake(9), b=4, K=256) == sq.SQ_ERR_SHAPE  # 112 does not divide 256
     assert hqa(L, a=300, H=fake(9)) == sq.SQ_ERR_SHAPE
-    assert hqa(L, bits=8) == sq.SQ_ERR_UNSUPPORTED
+    assert hqa(L, bits=6) == sq.SQ_ERR_UNSUPPORTED          # 4 and 8 are implemented
     assert hqa(L, group=3) == sq.SQ_ERR_SHAPE
     assert hqa(L, group=96) == sq.SQ_ERR_SHAPE
     assert hqa(L, x=ctypes.c_void_p(P * 256 + 8)) == sq.SQ_ERR_ALIGN
@@ -113,6 +113,22 @@ def test_w4a4_linear_validation(L):
     assert lin(L, y=ctypes.c_void_p(fake(0).value)) == sq.SQ_ERR_ALIAS
     assert lin(L, acc=ctypes.c_void_p(fake(6).value + 64)) == sq.SQ_ERR_ALIAS
     assert lin(L, M=0) == sq.SQ_OK
+
+
+def lin8(L, xq=fake(0), xa=fake(1), xb=fake(2), M=4, wq=fake(3), wa=fake(4), rs=fake(5), N=64, K=256,
+         y=fake(6), ldy=64, acc=None):
+    return L.sq_w4a8_linear(xq, xa, xb, M, wq, wa, rs, N, K, None, y, ldy, acc, None)
+
+
+def test_w4a8_linear_validation(L):
+    assert lin8(L, y=None) == sq.SQ_ERR_NULL
+    assert lin8(L, K=96) == sq.SQ_ERR_SHAPE
+    assert lin8(L, K=1 << 18) == sq.SQ_ERR_SHAPE            # int32 sums of 16 (qa - 128) qw
+    assert lin8(L, ldy=32) == sq.SQ_ERR_SHAPE
+    assert lin8(L, xq=ctypes.c_void_p(P * 256 + 8)) == sq.SQ_ERR_ALIGN
+    # xq holds M x K bytes (one code each): an output inside that span overlaps it
+    assert lin8(L, y=ctypes.c_void_p(fake(0).value + 4 * 256 - 64)) == sq.SQ_ERR_ALIAS
+    assert lin8(L, M=0) == sq.SQ_OK
 
 
 def lin_sw(L, M=4, N=128, K=128, ldh=64, **kw):
@@ -178,7 +194,7 @@ def kvq(L, B=1, S=2, H=2, D=128, bits=4, group=128, **kw):
 def test_kv_validation(L):
     assert kvq(L, q=None) == sq.SQ_ERR_NULL
     assert kvq(L, D=64) == sq.SQ_ERR_UNSUPPORTED
-    assert kvq(L, bits=8) == sq.SQ_ERR_UNSUPPORTED
+    assert kvq(L, bits=6) == sq.SQ_ERR_UNSUPPORTED
     assert kvq(L, group=64) == sq.SQ_ERR_UNSUPPORTED
     assert kvq(L, B=-1) == sq.SQ_ERR_SHAPE
     assert kvq(L, qr=fake(0)) == sq.SQ_ERR_ALIAS

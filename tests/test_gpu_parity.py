@@ -61,6 +61,39 @@ def check_act(x, a, b, group=None, sample_rows=None, max_frac=1e-4):
 
 # ---------------------------------------------------------------- activations
 
+def check_act8(x, a, b, group=None):
+    """sq_had_quant_act with bits = 8 vs the oracle: one code per byte."""
+    K = x.shape[1]
+    group = K if group is None else group
+    ha = None if a == 1 else ohad.dense_factor(a)
+    q, al, be, rot = sq.had_quant_act(dev(x), had_table(a), b, group=group, bits=8, dbg=True)
+    gq, gal, gbe, grot = host(q), host(al), host(be), host(rot)
+    op, oal, obe, oy, oc = olin.had_quant_act(x, ha, b, bits=8, group=group)
+    assert gq.shape == (x.shape[0], K)
+    if a * b == 1:
+        np.testing.assert_array_equal(gq, op)
+        np.testing.assert_array_equal(gal, oal)
+        np.testing.assert_array_equal(gbe, obe)
+        return 0
+    parity.assert_rot_close(grot, oy)
+    parity.assert_params_close(gal, oal, gbe, obe)
+    return parity.code_flips(gq.astype(np.int64), oc, oy, oal, obe, group)
+
+
+@pytest.mark.parametrize("K", [8, 4096, 4104, 16392])
+def test_identity_quant_8bit_bit_exact(K):
+    say(f"had_quant_act 8-bit identity K={K}")
+    x = workloads.outlier_acts(workloads.rng_for(K + 8), 5, K, max(1, K // 100), 50.0)
+    assert check_act8(x, 1, 1) == 0
+
+
+@pytest.mark.parametrize("a,b,M,group", [(1, 256, 16, None), (28, 512, 6, None), (172, 64, 3, None), (28, 16, 9, 224)])
+def test_rotated_quant_8bit(a, b, M, group):
+    say(f"had_quant_act 8-bit a={a} b={b} M={M} group={group}")
+    x = workloads.outlier_acts(workloads.rng_for(a + b + M + 80), M, a * b, max(1, a * b // 100), 50.0)
+    check_act8(x, a, b, group)
+
+
 def test_tiny_identity_quant_bit_exact():
     say("had_quant_act tiny identity")
     x, _ = workloads.tiny_inputs()
@@ -401,6 +434,90 @@ def test_gemm_decode_kernel(variant, monkeypatch):
         gemm_case(M, N, K, seed=M * 31 + N + K, bias=(M % 2 == 1))
 
 
+# ---------------------------------------------------------------- W4A8
+
+def gemm8_case(M, N, K, seed, bias=True, sample_rows=None):
+    rng = workloads.rng_for(seed)
+    qa = rng.integers(0, 256, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    xa = rng.uniform(0.003, 0.2, M).astype(np.float32)
+    xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+    wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
+    rs = qw.sum(1).astype(np.int32)
+    bi = (rng.standard_normal(N) * 0.1).astype(np.float16) if bias else None
+    args = (dev(qa.astype(np.uint8)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs),
+            dev(bi) if bias else None)
+    y, acc = sq.w4a8_linear(*args, dbg=True)
+    rows = np.arange(M) if sample_rows is None else sample_rows
+    oy, oacc = olin.w4a4_linear(qa[rows], xa[rows], xb[rows], qw, wa, rs, bi)
+    np.testing.assert_array_equal(host(acc)[rows], oacc)
+    parity.assert_out_close(host(y)[rows], oy)
+    y2, _ = sq.w4a8_linear(*args)
+    np.testing.assert_array_equal(host(y2), host(y))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (37, 200, 320), (130, 129, 128), (256, 384, 1024), (8, 1000, 512),
+                                   (300, 390, 448)])
+def test_w4a8_gemm_small_shapes(M, N, K):
+    say(f"w4a8_linear M={M} N={N} K={K}")
+    gemm8_case(M, N, K, seed=M * 5 + N + K)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (2, 40, 128), (7, 1000, 4160), (16, 130, 3136), (11, 4097, 640),
+                                   (16, 28672, 8192), (1, 8192, 28672), (13, 96, 28672)])
+def test_w4a8_decode_shapes(M, N, K):
+    # M <= 16: the weight-streaming kernel with 8-bit activations (1, 2 or 4 blocks of 16 rows)
+    say(f"w4a8_linear decode M={M} N={N} K={K}")
+    gemm8_case(M, N, K, seed=M * 13 + N + K, bias=(M % 2 == 1))
+
+
+def test_w4a8_gemm_extreme_codes():
+    # the largest int32 sums the kernel forms: 16 x (255 - 128) x 7 and 16 x (0 - 128) x (-7)
+    # over K = 2^17
+    say("w4a8_linear extreme codes K=2^17")
+    M, N, K = 2, 64, 1 << 17
+    qa = np.full((M, K), 255)
+    qa[1] = 0
+    qw = np.full((N, K), 7)
+    qw[1::2] = -7
+    xa = np.full(M, 1e-6, np.float32)
+    xb = np.zeros(M, np.float32)
+    wa = np.full(N, 1e-2, np.float32)
+    rs = qw.sum(1).astype(np.int32)
+    y, acc = sq.w4a8_linear(dev(qa.astype(np.uint8)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs),
+                            None, dbg=True)
+    oy, oacc = olin.w4a4_linear(qa, xa, xb, qw, wa, rs)
+    np.testing.assert_array_equal(host(acc), oacc)
+    parity.assert_out_close(host(y), oy)
+
+
+def test_w4a8_gemm_llama_sampled():
+    say("w4a8_linear LLaMA-2-7B gate [2048x4096]x[11008x4096] and down [2048x11008]x[4096x11008], sampled rows")
+    rows = np.array([0, 127, 128, 2047])
+    gemm8_case(2048, 11008, 4096, seed=51, bias=False, sample_rows=rows)
+    gemm8_case(2048, 4096, 11008, seed=52, bias=False, sample_rows=rows)
+
+
+def test_w4a8_rotated_chain():
+    # fp16 rows -> rotated 8-bit codes -> W4A8 product, against the oracle's whole chain
+    say("W4A8 chain: had_quant_act(bits=8, Sylvester 256) -> pack_w4 -> w4a8_linear")
+    x, w = workloads.tiny_inputs()
+    q, al, be, _ = sq.had_quant_act(dev(x), None, 256, bits=8)
+    wq, wa, rs = sq.pack_w4(dev(w), None, 256)
+    y, acc = sq.w4a8_linear(q, al, be, wq, wa, rs, dbg=True)
+    op, oxa, oxb, oy_rot, oqa = olin.had_quant_act(x, None, 256, bits=8)
+    owp, owa, ors, oqw = olin.pack_w4(w, None, 256)
+    gqa = host(q).astype(np.int64)
+    if np.array_equal(gqa, oqa) and np.array_equal(parity.unpack(host(wq), signed=True), oqw):
+        oy, oacc = olin.w4a4_linear(oqa, oxa[:, 0], oxb[:, 0], oqw, owa, ors)
+        np.testing.assert_array_equal(host(acc), oacc)
+        parity.assert_out_close(host(y), oy)
+    else:  # a rounding-boundary flip upstream: the product of the GPU's own codes must still match
+        oy, oacc = olin.w4a4_linear(gqa, host(al)[:, 0], host(be)[:, 0], parity.unpack(host(wq), signed=True),
+                                    host(wa), host(rs))
+        np.testing.assert_array_equal(host(acc), oacc)
+
+
 # ---------------------------------------------------------------- decode attention
 
 def attn_case(B, S, H, seed, scale=None, qscale=2.0):
@@ -482,15 +599,16 @@ def test_tiny_rotated_linear_chain():
 
 # ---------------------------------------------------------------- KV
 
-def check_kv(q, k, v, sample=None):
-    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True)
+def check_kv(q, k, v, sample=None, bits=4):
+    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True, bits=bits)
     g = {n: host(t) for n, t in out.items() if t is not None}
     B, S, H, D = q.shape
     flat = lambda a: a.reshape(B * S * H, -1)
     idx = np.arange(B * S * H) if sample is None else sample
     qs, ks, vs = (flat(t)[idx][None, :, None, :] for t in (q, k, v))
-    o = okv.qk_had_kvquant(qs, ks, vs)
+    o = okv.qk_had_kvquant(qs, ks, vs, bits=bits)
     sel = lambda a: flat(a)[idx][None, :, None, :]
+    codes = (lambda a: parity.unpack(a, False)) if bits == 4 else (lambda a: a.astype(np.int64))
     # Q R: fp16 of an fp32 sum vs fp16 of the fp64 value: one fp16 ulp of rounding plus the
     # 1e-5 x row-max allowance of an fp32-accumulated rotation (matters for values near 0)
     gq = sel(g["q_rot"]).astype(np.float64)
@@ -500,7 +618,7 @@ def check_kv(q, k, v, sample=None):
     assert np.all(np.abs(gq - oq_) <= ulp + 1e-5 * rowmax)
     parity.assert_rot_close(sel(g["k_rot"]).reshape(-1, 128), o["k_rot"].reshape(-1, 128))
     parity.assert_params_close(sel(g["k_alpha"]), o["k_alpha"], sel(g["k_beta"]), o["k_beta"])
-    parity.code_flips(parity.unpack(sel(g["k_q"]), False).reshape(-1, 128), o["k_codes"].reshape(-1, 128),
+    parity.code_flips(codes(sel(g["k_q"])).reshape(-1, 128), o["k_codes"].reshape(-1, 128),
                       o["k_rot"].reshape(-1, 128), o["k_alpha"].reshape(-1, 1), o["k_beta"].reshape(-1, 1))
     np.testing.assert_array_equal(sel(g["v_q"]), o["v_q"])
     np.testing.assert_array_equal(sel(g["v_alpha"]), o["v_alpha"])
@@ -511,6 +629,17 @@ def test_kv_small():
     say("qk_had_kvquant small [2,16,4,128] and ragged [1,3,5,128]")
     check_kv(*workloads.kv_inputs(B=2, S=16, H=4, D=128))
     check_kv(*workloads.kv_inputs(B=1, S=3, H=5, D=128))
+
+
+def test_kv8_small_and_sampled():
+    # KV8: the same kernel storing one 8-bit code per byte
+    say("qk_had_kvquant 8-bit [2,16,4,128], [1,3,5,128] and [8,2048,32,128] sampled")
+    check_kv(*workloads.kv_inputs(B=2, S=16, H=4, D=128), bits=8)
+    check_kv(*workloads.kv_inputs(B=1, S=3, H=5, D=128), bits=8)
+    q, k, v = workloads.kv_inputs()
+    rng = np.random.default_rng(1)
+    sample = np.unique(np.concatenate([rng.choice(8 * 2048 * 32, 5000, replace=False), [0, 8 * 2048 * 32 - 1]]))
+    check_kv(q, k, v, sample, bits=8)
 
 
 def test_kv_full_sampled():
