@@ -18,18 +18,20 @@ from .quant import dequant, pack_nibbles, quant_asym, store_codes, unpack_nibble
 from .rotate import rotate_rows
 
 
-def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, group: int = 128):
+def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, group: int = 128,
+                   k_clip: float = 1.0, v_clip: float = 1.0):
     """q, k, v: fp16 [B, S, H, D].  Returns a dict with
     q_rot fp16 [B,S,H,D]; k_rot fp32 (quantizer input);
     k_q, v_q uint8 [B,S,H,D/2] (bits 4) or [B,S,H,D] (bits 8);
     k_alpha, k_beta, v_alpha, v_beta fp32 [B,S,H,D/group];
     k_codes, v_codes int64 [B,S,H,D].
+    k_clip, v_clip < 1 clip the groups' ranges (quant_asym; App. A uses 0.95 for the cache).
     """
     D = q.shape[-1]
     q_rot = rotate_rows(q, None, D).astype(np.float16)
     k_rot = rotate_rows(k, None, D).astype(np.float32)
-    kc, ka, kb = quant_asym(k_rot, bits=bits, group=group)
-    vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group)
+    kc, ka, kb = quant_asym(k_rot, bits=bits, group=group, clip=k_clip)
+    vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group, clip=v_clip)
     return dict(q_rot=q_rot, k_rot=k_rot, k_q=store_codes(kc, bits), k_alpha=ka, k_beta=kb,
                 v_q=store_codes(vc, bits), v_alpha=va, v_beta=vb, k_codes=kc, v_codes=vc)
 

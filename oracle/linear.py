@@ -25,36 +25,49 @@ from .quant import pack_nibbles, quant_asym, quant_sym, store_codes
 from .rotate import rotate_rows
 
 
-def had_quant_act(x: np.ndarray, had_dense, pow2_n: int, bits: int = 4, group: int | None = None):
+def _signed(x: np.ndarray, signs, n: int) -> np.ndarray:
+    """x with element i multiplied by signs[i % n]: the diagonal S of a random Hadamard
+    matrix S H (Sec. 2.2 footnote) applied to every rotation block; exact in fp64."""
+    x64 = np.asarray(x, dtype=np.float64)
+    if signs is None:
+        return x64
+    s = np.asarray(signs, dtype=np.float64)
+    return x64 * np.tile(s, x64.shape[-1] // n)
+
+
+def had_quant_act(x: np.ndarray, had_dense, pow2_n: int, bits: int = 4, group: int | None = None,
+                  clip: float = 1.0, signs=None):
     """Rotate each row of x (fp16 [M, K]) and quantize it asymmetrically per group.
 
     had_dense: int8 +-1 [a, a] or None (a = 1); pow2_n = b; rotation block n = a*b.
-    (had_dense None, pow2_n 1) is the identity.  Returns
+    (had_dense None, pow2_n 1) is the identity.  clip < 1 clips the range (quant_asym);
+    signs (+-1 [a * pow2_n] or None) make the rotation S (H_a (x) S_b) / sqrt(n), a random
+    Hadamard matrix.  Returns
     (packed uint8 [M, K/2] (bits 4) or [M, K] (bits 8), alpha fp32 [M, K/group],
      beta fp32 [M, K/group], y_rot fp32 [M, K] = the quantizer input, codes int64 [M, K]).
     """
     x = np.asarray(x)
     a = 1 if had_dense is None else had_dense.shape[0]
-    if a * pow2_n == 1:
+    if a * pow2_n == 1 and signs is None:
         y32 = x.astype(np.float32)
     else:
-        y32 = rotate_rows(x, had_dense, pow2_n).astype(np.float32)
-    q, alpha, beta = quant_asym(y32, bits=bits, group=group)
+        y32 = rotate_rows(_signed(x, signs, a * pow2_n), had_dense, pow2_n).astype(np.float32)
+    q, alpha, beta = quant_asym(y32, bits=bits, group=group, clip=clip)
     return store_codes(q, bits), alpha, beta, y32, q
 
 
-def pack_w4(w: np.ndarray, had_dense=None, pow2_n: int = 1, bits: int = 4):
+def pack_w4(w: np.ndarray, had_dense=None, pow2_n: int = 1, bits: int = 4, signs=None):
     """Offline weight preparation: W' = W R (optional), per-row symmetric quant, pack.
 
-    w: fp16 [N, K].  Returns (packed uint8 [N, K/2], alpha fp32 [N], rowsum int32 [N],
-    codes int64 [N, K]).
+    w: fp16 [N, K].  signs as in had_quant_act (the same R folded into the weights).
+    Returns (packed uint8 [N, K/2], alpha fp32 [N], rowsum int32 [N], codes int64 [N, K]).
     """
     w = np.asarray(w)
     a = 1 if had_dense is None else had_dense.shape[0]
-    if a * pow2_n == 1:
+    if a * pow2_n == 1 and signs is None:
         w32 = w.astype(np.float32)
     else:
-        w32 = rotate_rows(w, had_dense, pow2_n).astype(np.float32)
+        w32 = rotate_rows(_signed(w, signs, a * pow2_n), had_dense, pow2_n).astype(np.float32)
     q, alpha = quant_sym(w32, bits=bits)
     rowsum = q.sum(axis=-1).astype(np.int32)
     return pack_nibbles(q), alpha[..., 0], rowsum, q

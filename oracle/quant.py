@@ -38,11 +38,13 @@ def _groups(v: np.ndarray, group: int) -> np.ndarray:
     return v.reshape(*v.shape[:-1], K // group, group)
 
 
-def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None):
+def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: float = 1.0):
     """Asymmetric min-max quantization of eq. 1 over contiguous groups of the last axis.
 
     v: fp32-representable values [..., K].  Returns (codes int64 [..., K] in [0, 2^N-1],
     alpha fp32 [..., K/group], beta fp32 [..., K/group]).
+    clip < 1 quantizes the range [clip * min, clip * max] (each end rounded to fp32; the
+    range clipping ablated in App. A "Quantization choice"); codes outside it clamp.
     """
     v32 = np.asarray(v, dtype=F32)
     group = v32.shape[-1] if group is None else group
@@ -50,6 +52,9 @@ def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None):
     levels = F32(2 ** bits - 1)
     mn = g.min(axis=-1)
     mx = g.max(axis=-1)
+    if clip != 1.0:
+        mn = (mn * F32(clip)).astype(F32)
+        mx = (mx * F32(clip)).astype(F32)
     r = (mx - mn).astype(F32)
     alpha = (r / levels).astype(F32)
     alpha = np.where(alpha < TINY, F32(1), alpha).astype(F32)

@@ -136,3 +136,12 @@ def test_attn_decode_bruteforce():
         for d in range(128):
             ref = sum(w[t] / z * (va[0, t, h] * vc[0, t, h, d] + vb[0, t, h]) for t in range(S))
             assert out[0, h, d] == np.float16(ref)
+
+
+def test_kv_clip_matches_quantizer_clip():
+    q, k, v = _small()
+    out = kv.qk_had_kvquant(q, k, v, k_clip=0.95, v_clip=0.95)
+    c, a, b = quant.quant_asym(v.astype(np.float32), group=128, clip=0.95)
+    np.testing.assert_array_equal(out["v_codes"], c)
+    np.testing.assert_array_equal(out["v_alpha"], a)
+    assert out["k_codes"].min() == 0 and out["k_codes"].max() == 15

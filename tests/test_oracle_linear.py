@@ -165,3 +165,24 @@ def test_had_quant_act_8bit_storage():
     p8, a8, b8, y8, q8 = linear.had_quant_act(x, None, 256, bits=8)
     assert p8.shape == (4, 256) and p8.dtype == np.uint8 and np.array_equal(p8.astype(np.int64), q8)
     assert q8.min() == 0 and q8.max() == 255
+
+
+def test_random_sign_hadamard_rotation():
+    # R = S (H_28 (x) S_4) / sqrt(112) with a random +-1 diagonal S is orthonormal; all-plus
+    # signs give the plain rotation; folding the same R into the weights keeps x W^T
+    rng = np.random.default_rng(13)
+    had = hadamard.dense_factor(28)
+    s = rng.choice([-1, 1], 112).astype(np.int8)
+    R = rotate.rotate_rows(np.diag(s.astype(np.float64)), had, 4)      # rows of S H / sqrt(n)
+    np.testing.assert_allclose(R @ R.T, np.eye(112), atol=1e-12)
+    x = rng.standard_normal((3, 224)).astype(np.float16)
+    plus = np.ones(112, np.int8)
+    np.testing.assert_array_equal(linear.had_quant_act(x, had, 4, signs=plus)[3], linear.had_quant_act(x, had, 4)[3])
+    y = linear.had_quant_act(x, had, 4, signs=s)[3].astype(np.float64)
+    x64 = x.astype(np.float64)
+    np.testing.assert_allclose(y[:, :112], x64[:, :112] @ R, rtol=0, atol=1e-5 * np.abs(y).max())
+    w = rng.standard_normal((5, 224)).astype(np.float16)
+    wr = linear._signed(w, s, 112)
+    wr = rotate.rotate_rows(wr, had, 4)
+    yr = rotate.rotate_rows(linear._signed(x, s, 112), had, 4)
+    np.testing.assert_allclose(yr @ wr.T, x64 @ w.astype(np.float64).T, rtol=0, atol=1e-10 * 224)

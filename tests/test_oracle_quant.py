@@ -174,3 +174,18 @@ def test_asym_8bit_closed_forms_and_storage():
     assert s.dtype == np.uint8 and s.shape == q.shape and np.array_equal(s.astype(np.int64), q)
     with pytest.raises(ValueError):
         quant.store_codes(q, 6)
+
+
+def test_asym_clip_closed_form():
+    # clip r: the range [r min, r max]; a ramp on [-4, 4] with r = 0.5 quantizes [-2, 2]:
+    # alpha = 4/15, beta = -2, values beyond the clipped ends clamp to 0 and 15
+    v = np.linspace(-4.0, 4.0, 33, dtype=np.float32)[None, :]
+    q, a, b = quant.quant_asym(v, clip=0.5)
+    assert b[0] == np.float32(-2.0) and a[0] == np.float32(np.float32(4.0) / np.float32(15.0))
+    assert np.all(q[0, v[0] <= -2.0] == 0) and np.all(q[0, v[0] >= 2.0] == 15)
+    inside = (v[0] > -2.0) & (v[0] < 2.0)
+    err = np.abs(quant.dequant(q, a, b)[0, inside] - v[0, inside])
+    assert np.all(err <= a[0] * 0.5 * (1 + 1e-6))
+    q1, a1, b1 = quant.quant_asym(v, clip=1.0)
+    q0, a0, b0 = quant.quant_asym(v)
+    assert np.array_equal(q1, q0) and np.array_equal(a1, a0)
