@@ -469,13 +469,14 @@ def kernel_report(torch, sq, workloads, dev):
         torch.cuda.synchronize()
         return sum(a.elapsed_time(b) for a, b in evs) / reps
 
-    def act_fns(x, had, pow2, nbytes, bits=4):
-        """had_quant_act launches over distinct copies of x and of the outputs."""
+    def act_fns(x, had, pow2, nbytes, bits=4, **var):
+        """had_quant_act launches over distinct copies of x and of the outputs (var: clip,
+        signs of the _ex entry point)."""
         fns = []
         for _ in range(n_copies(nbytes)):
             xc = x.clone()
-            o = sq.had_quant_act(xc, had, pow2, bits=bits)[:3]
-            fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, bits=bits, out=o))
+            o = sq.had_quant_act(xc, had, pow2, bits=bits, **var)[:3]
+            fns.append(lambda xc=xc, o=o: sq.had_quant_act(xc, had, pow2, bits=bits, out=o, **var))
         return fns
 
     def gemm8_fns(qx, w, nbytes):
@@ -534,9 +535,14 @@ def kernel_report(torch, sq, workloads, dev):
         t8_hq = timed(act_fns(xdn, had, sh.had_pow2, b8_hq, bits=8))
         t8_gu = timed(gemm8_fns(qi8, wgu, b8_gu))
         t8_d = timed(gemm8_fns(qd8, wd, b8_d))
+        # the variants: random-sign Hadamard S H with a clipped range (S adds K bytes per row
+        # set, read from cache; not counted)
+        sgn = up(np.where(workloads.rng_for(7).random(I) < 0.5, -1, 1).astype(np.int8))
+        tv_hq = timed(act_fns(xdn, had, sh.had_pow2, b_hq, signs=sgn, clip=0.9))
         rep.append(dict(config=sh.name,
                         act_quant=dict(ms=t_aq, GBps=b_aq / t_aq / 1e6),
                         r4_had_quant=dict(ms=t_hq, GBps=b_hq / t_hq / 1e6),
+                        r4_had_quant_signs_clip=dict(ms=tv_hq, GBps=b_hq / tv_hq / 1e6),
                         gate_gemm=dict(ms=t_g, TOPS=2 * M * I * H / t_g / 1e9, GBps=b_g / t_g / 1e6),
                         gate_up_gemm=dict(ms=t_gu, TOPS=4 * M * I * H / t_gu / 1e9, GBps=b_gu / t_gu / 1e6),
                         gate_up_swiglu_gemm=dict(ms=t_sw, TOPS=4 * M * I * H / t_sw / 1e9, GBps=b_sw / t_sw / 1e6),
@@ -545,7 +551,7 @@ def kernel_report(torch, sq, workloads, dev):
                         r4_had_quant_8bit=dict(ms=t8_hq, GBps=b8_hq / t8_hq / 1e6),
                         gate_up_w4a8=dict(ms=t8_gu, TOPS=4 * M * I * H / t8_gu / 1e9, GBps=b8_gu / t8_gu / 1e6),
                         down_w4a8=dict(ms=t8_d, TOPS=2 * M * I * H / t8_d / 1e9, GBps=b8_d / t8_d / 1e6)))
-        del inp, xin, xdn, wg, wgu, wsw, wd, qi, qd, qi8, qd8
+        del inp, xin, xdn, wg, wgu, wsw, wd, qi, qd, qi8, qd8, sgn
         torch.cuda.empty_cache()
     q, k, v = (up(t) for t in workloads.kv_inputs())
     E = q.numel()
@@ -563,6 +569,13 @@ def kernel_report(torch, sq, workloads, dev):
         o.pop("k_rot")
         fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, bits=8))
     t_kv8 = timed(fns)
+    fns = []
+    for _ in range(n_copies(kv_bytes(E))):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc, k_clip=0.95, v_clip=0.95)
+        o.pop("k_rot")
+        fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, k_clip=0.95, v_clip=0.95))
+    t_kvc = timed(fns)
     b_kv8 = kv_bytes(E) + E  # codes of K and V: one byte per element instead of half
     # decode attention of the last token's rotated query over that cache
     B, S, H, D = q.shape
@@ -579,6 +592,7 @@ def kernel_report(torch, sq, workloads, dev):
     t_at = timed(fns)
     rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6),
                     kv_quant_8bit=dict(ms=t_kv8, GBps=b_kv8 / t_kv8 / 1e6),
+                    kv_quant_clip95=dict(ms=t_kvc, GBps=kv_bytes(E) / t_kvc / 1e6),
                     attn_decode=dict(ms=t_at, GBps=b_at / t_at / 1e6)))
     return rep
 

@@ -67,8 +67,8 @@ const char* sq_last_error(void);
 
 /*
  * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
- * the next call of sq_had_quant_act, sq_pack_w4, sq_w4a4_linear, sq_w4a8_linear,
- * sq_w4a4_linear_swiglu, sq_qk_had_kvquant or sq_attn_decode_kv4
+ * the next call of sq_had_quant_act(_ex), sq_pack_w4(_ex), sq_w4a4_linear, sq_w4a8_linear,
+ * sq_w4a4_linear_swiglu, sq_qk_had_kvquant(_ex) or sq_attn_decode_kv4
  * made by this host thread: start_event takes the start time of the first kernel that
  * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
  * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
@@ -103,8 +103,7 @@ sq_status sq_hadamard_factor(int32_t n, int8_t* out_host);
  *   had_dense_n  a, order of the dense factor, 1 <= a <= SQ_MAX_DENSE
  *   had_dense  device int8 +-1 [a, a] row-major (must be a Hadamard matrix); NULL iff a == 1
  *   had_pow2_n b, power of two, 1 <= b <= 32768; n = a*b must divide K
- *   bits       4 or 8 (others: SQ_ERR_UNSUPPORTED); 8-bit rows with a rotation take the
- *              generic kernel, not the matrix-core ones
+ *   bits       4 or 8 (others: SQ_ERR_UNSUPPORTED)
  *   group      quantization group length along the row: group | K, group % 2 == 0;
  *              group == K is per-token quantization (what sq_w4a4_linear consumes)
  *   q_out      device uint8, 16-byte aligned, contiguous: bits 4: [M, K/2] packed codes
@@ -119,6 +118,29 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
                            int32_t bits, int32_t group,
                            uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
                            void* stream);
+
+/*
+ * sq_had_quant_act_ex -- sq_had_quant_act with the two variants the paper compares its
+ * choices against (sq_had_quant_act is this call with signs = NULL and clip = 1):
+ *   signs      optional device int8 [a*b] (a = had_dense_n, b = had_pow2_n): the diagonal
+ *              S of a random Hadamard matrix S H (Sec. 2.2), so that each block of n = a*b
+ *              elements is multiplied by S (H_a (x) S_b) / sqrt(n); element i of a block is
+ *              multiplied by signs[i] first.  Entries are +1 or -1 (only their sign is read:
+ *              negative = -1).  NULL for none.  Any alignment; the matrix-core kernels take
+ *              8-byte aligned arrays, others go to the generic kernel.
+ *   clip       range clipping ratio r, 0 < r <= 1 (App. A "Quantization choice"): each group
+ *              is quantized over [r min, r max] (each end rounded to fp32), so
+ *              alpha = fl(fl(r max) - fl(r min)) / L, beta = fl(r min), and codes of values
+ *              outside the range clamp to 0 or L.  1 is plain min-max.
+ *              Outside (0, 1] (NaN included): SQ_ERR_SHAPE.
+ * Every other argument, layout and error as sq_had_quant_act; signs is an input for the
+ * overlap check.
+ */
+sq_status sq_had_quant_act_ex(const void* x, int64_t M, int64_t K, int64_t ldx,
+                              int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                              const int8_t* signs, int32_t bits, int32_t group, float clip,
+                              uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
+                              void* stream);
 
 /*
  * sq_pack_w4 -- offline weight preparation: optionally absorb the online
@@ -138,6 +160,19 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
 sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
                      int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
                      uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream);
+
+/*
+ * sq_pack_w4_ex -- sq_pack_w4 absorbing the random Hadamard rotation S H of Sec. 2.2:
+ * W' = W R with R = S (H_a (x) S_b) / sqrt(n) blockwise, the same R that
+ * sq_had_quant_act_ex applies to the activations with the same signs, so that
+ * (x R)(W R)^T = x W^T.
+ *   signs      optional device int8 [a*b], +1 or -1 (sign read), as in sq_had_quant_act_ex;
+ *              NULL makes this call sq_pack_w4
+ * Every other argument, layout and error as sq_pack_w4.
+ */
+sq_status sq_pack_w4_ex(const void* w, int64_t N, int64_t K, int64_t ldw,
+                        int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n, const int8_t* signs,
+                        uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream);
 
 /*
  * sq_w4a4_linear -- the quantized linear layer y = x W^T on 4-bit codes.  The int4 x int4 products
@@ -223,6 +258,23 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                             void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
                             uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
                             void* stream);
+
+/*
+ * sq_qk_had_kvquant_ex -- sq_qk_had_kvquant with range clipping of the cache groups
+ * (App. A "Quantization choice" compares clipped and unclipped KV quantizers);
+ * sq_qk_had_kvquant is this call with k_clip = v_clip = 1.
+ *   k_clip, v_clip  clipping ratios r, 0 < r <= 1, of the key and value groups: a group is
+ *              quantized over [r min, r max] (ends rounded to fp32; for keys the min and max
+ *              of the rotated values), codes outside clamp to 0 or L.
+ *              Outside (0, 1] (NaN included): SQ_ERR_SHAPE.
+ * Every other argument, layout and error as sq_qk_had_kvquant.
+ */
+sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
+                               int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
+                               float k_clip, float v_clip,
+                               void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
+                               uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                               void* stream);
 
 /*
  * sq_attn_decode_kv4 -- attention of one new query per (batch, head) over the 4-bit KV

@@ -7,7 +7,10 @@
 //   2. Walsh-Hadamard butterflies over i_b (contiguous), one LDS pass per stage
 //   3. scale by fl32(1/sqrt(n))
 // then the quantizer: asymmetric per group (activations) or symmetric per row with the
-// code row sum (weights).
+// code row sum (weights).  Variants: a +-1 diagonal S in front of the rotation (the random
+// Hadamard matrix S H of Sec. 2.2) flips the sign of input element i when S[i % n] < 0,
+// which is exact; a clipping ratio r < 1 quantizes the range [r min, r max] of each group
+// (App. A "Quantization choice") with the codes outside it clamped.
 #include "sq_device.h"
 #include "sq_internal.h"
 
@@ -51,13 +54,21 @@ __device__ int block_sum(int v, int* red) {
   return r;
 }
 
+// fp16 element i of a row, its sign flipped where S[i % n] < 0 (signs may be null)
+__device__ __forceinline__ float signed_elem(const uint16_t* __restrict__ xr, int i,
+                                            const int8_t* __restrict__ signs, int n) {
+  uint16_t v = xr[i];
+  if (signs && signs[i % n] < 0) v ^= 0x8000u;
+  return h2f(v);
+}
+
 // Fills buf[0..K) with the rotated row (fp32).  Ends with a barrier.
 __device__ void rotate_row_to_lds(const uint16_t* __restrict__ xr, int K, int a,
                                   const int8_t* __restrict__ H, int b, float inv_sqrt_n,
-                                  float* __restrict__ buf) {
+                                  const int8_t* __restrict__ signs, float* __restrict__ buf) {
   const int n = a * b;
   if (a == 1) {
-    for (int i = threadIdx.x; i < K; i += kThreads) buf[i] = h2f(xr[i]);
+    for (int i = threadIdx.x; i < K; i += kThreads) buf[i] = signed_elem(xr, i, signs, n);
   } else {
     // element i of block blk is (j_a, i_b) with i = blk*n + j_a*b + i_b
     for (int i = threadIdx.x; i < K; i += kThreads) {
@@ -65,11 +76,11 @@ __device__ void rotate_row_to_lds(const uint16_t* __restrict__ xr, int K, int a,
       const int r = i - blk * n;
       const int ja = r / b;
       const int ib = r - ja * b;
-      const uint16_t* col = xr + blk * n + ib;
+      const uint16_t* blkp = xr + blk * n;
       float acc = 0.0f;
       for (int ia = 0; ia < a; ++ia) {
         const float h = static_cast<float>(H[ia * a + ja]);
-        acc = __fadd_rn(acc, __fmul_rn(h2f(col[ia * b]), h));
+        acc = __fadd_rn(acc, __fmul_rn(signed_elem(blkp, ia * b + ib, signs, n), h));
       }
       buf[i] = acc;
     }
@@ -103,7 +114,7 @@ had_quant_act_generic(RotQuantArgs args) {
   __shared__ float red_f[kWaves];
   const int64_t row = blockIdx.x;
   const int K = static_cast<int>(args.K);
-  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, buf);
+  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, args.signs, buf);
   if (args.dbg) {
     for (int i = threadIdx.x; i < K; i += kThreads) args.dbg[row * K + i] = buf[i];
   }
@@ -117,8 +128,8 @@ had_quant_act_generic(RotQuantArgs args) {
       mn = fminf(mn, buf[i]);
       mx = fmaxf(mx, buf[i]);
     }
-    mn = block_min(mn, red_f);
-    mx = block_max(mx, red_f);
+    mn = __fmul_rn(block_min(mn, red_f), args.clip);
+    mx = __fmul_rn(block_max(mx, red_f), args.clip);
     const AsymParams p = asym_params(mn, mx, levels);
     if (threadIdx.x == 0) {
       args.alpha[row] = p.alpha;
@@ -146,8 +157,8 @@ had_quant_act_generic(RotQuantArgs args) {
       mn = fminf(mn, v[i]);
       mx = fmaxf(mx, v[i]);
     }
-    mn = wave_min(mn);
-    mx = wave_max(mx);
+    mn = __fmul_rn(wave_min(mn), args.clip);
+    mx = __fmul_rn(wave_max(mx), args.clip);
     const AsymParams p = asym_params(mn, mx, levels);
     if (lane == 0) {
       args.alpha[row * G + g] = p.alpha;
@@ -172,7 +183,7 @@ pack_w4_generic(RotQuantArgs args) {
   __shared__ int red_i[kWaves];
   const int64_t row = blockIdx.x;
   const int K = static_cast<int>(args.K);
-  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, buf);
+  rotate_row_to_lds(args.x + row * args.ldx, K, args.a, args.H, args.b, args.inv_sqrt_n, args.signs, buf);
   float amax = 0.0f;
   for (int i = threadIdx.x; i < K; i += kThreads) amax = fmaxf(amax, fabsf(buf[i]));
   amax = block_max(amax, red_f);
@@ -240,7 +251,7 @@ quant_rows_identity(RotQuantArgs args) {
     mx = fmaxf(mx, red[W + i]);
   }
   const bool b8 = args.bits == 8;
-  const AsymParams p = asym_params(mn, mx, b8 ? 255.0f : 15.0f);
+  const AsymParams p = asym_params(__fmul_rn(mn, args.clip), __fmul_rn(mx, args.clip), b8 ? 255.0f : 15.0f);
   if (threadIdx.x == 0) {
     args.alpha[row] = p.alpha;
     args.beta[row] = p.mn;
@@ -250,23 +261,24 @@ quant_rows_identity(RotQuantArgs args) {
   for (int j = 0; j < CHMAX; ++j) {
     const int ch = threadIdx.x + j * T;
     if (ch < nchunk) {
-      // eq. 1's t = (v - mn) * inv, rounded after each step; v_cvt_pk_u8_f32 rounds half to
-      // even and saturates, and 0 <= t <= 15 (1 + 3 eps), so its byte is clamp(rint(t), 0, 15).
-      // Even positions go to ev, odd ones to od; ev | od << 4 is the nibble-packed word.
-      if (b8) {  // one code per byte (0 <= t <= 255 (1 + 3 eps)): positions 0-3, then 4-7
+      // eq. 1's t = (v - mn) * inv, rounded after each step and clamped to [0, L] (t leaves
+      // that range only with a clipped range, or by 3 ulp at the top); v_cvt_pk_u8_f32 then
+      // rounds half to even, so its byte is clamp(rint(t), 0, L).  4-bit: even positions go
+      // to ev, odd ones to od, and ev | od << 4 is the nibble-packed word.
+      if (b8) {  // one code per byte: positions 0-3, then 4-7
         uint32_t w0 = 0, w1 = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          w0 = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][i], p.mn), p.inv), i, w0);
-          w1 = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][4 + i], p.mn), p.inv), i, w1);
+          w0 = __builtin_amdgcn_cvt_pk_u8_f32(asym_t(v[j][i], p), i, w0);
+          w1 = __builtin_amdgcn_cvt_pk_u8_f32(asym_t(v[j][4 + i], p), i, w1);
         }
         reinterpret_cast<uint2*>(qrow)[ch] = make_uint2(w0, w1);
       } else {
         uint32_t ev = 0, od = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i], p.mn), p.inv), i, ev);
-          od = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(__fsub_rn(v[j][2 * i + 1], p.mn), p.inv), i, od);
+          ev = __builtin_amdgcn_cvt_pk_u8_f32(asym_t(v[j][2 * i], p), i, ev);
+          od = __builtin_amdgcn_cvt_pk_u8_f32(asym_t(v[j][2 * i + 1], p), i, od);
         }
         qrow[ch] = ev | (od << 4);
       }
@@ -289,7 +301,7 @@ hipError_t launch_generic(void (*kern)(RotQuantArgs), const RotQuantArgs& a, hip
 }  // namespace
 
 hipError_t launch_had_quant_act(const RotQuantArgs& a, hipStream_t stream) {
-  if (a.a == 1 && a.b == 1 && a.group == a.K) {
+  if (a.a == 1 && a.b == 1 && a.group == a.K && a.signs == nullptr) {
     // chunks of 8 per thread sized to K, so that the registers (and with them the
     // resident workgroups per CU) follow the row length
     const dim3 grid(static_cast<unsigned>(a.rows));

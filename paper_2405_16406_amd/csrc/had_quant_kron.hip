@@ -100,6 +100,21 @@ __device__ __forceinline__ uint32_t rne_bits(float t) {
   return __float_as_uint(__fadd_rn(t, 8388608.0f));
 }
 
+// Variant kernels (VAR): the sign flips of S (random Hadamard S H, Sec. 2.2) as the fp16
+// sign-bit mask of one 16-byte chunk, from the chunk's 8 int8 entries of S (+-1: bit 7 of
+// byte e is the sign of element e)
+__device__ __forceinline__ v4u sign_mask(const uint2 s) {
+  return v4u{((s.x << 8) & 0x8000u) | ((s.x << 16) & 0x80000000u), ((s.x >> 8) & 0x8000u) | (s.x & 0x80000000u),
+             ((s.y << 8) & 0x8000u) | ((s.y << 16) & 0x80000000u), ((s.y >> 8) & 0x8000u) | (s.y & 0x80000000u)};
+}
+// and the code argument t clamped to [0, L], which a clipped range needs (v_cvt_pk_u8_f32
+// alone saturates at 255 only)
+template <bool VAR, int BITS>
+__device__ __forceinline__ float code_arg(float t) {
+  if constexpr (VAR) return __builtin_amdgcn_fmed3f(t, 0.0f, BITS == 8 ? 255.0f : 15.0f);
+  return t;
+}
+
 template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE, bool DBG>
 __global__ void __launch_bounds__(64 * MW * NW)
 had_quant_kron(RotQuantArgs args) {
@@ -466,7 +481,7 @@ __device__ __forceinline__ void pair_wait(const int* flag, int target) {
     __builtin_amdgcn_s_sleep(1);
 }
 
-template <int A, int APAD, int NT, bool DBG, int BITS>
+template <int A, int APAD, int NT, bool DBG, int BITS, bool VAR>
 __global__ void __launch_bounds__(512, 2)
 had_quant_pair(RotQuantArgs args) {
   using C = Pair<A, APAD, NT>;
@@ -500,6 +515,19 @@ had_quant_pair(RotQuantArgs args) {
     }
   };
   auto store_row = [&]() {
+    if constexpr (VAR) {
+      if (args.signs) {  // S flips element signs as the row goes to its slot
+        const uint2* sg = reinterpret_cast<const uint2*>(args.signs);
+        uint2 sv[C::PF];
+#pragma unroll
+        for (int j = 0; j < C::PF; ++j) {
+          const int i = pl + 128 * j;
+          sv[j] = sg[i < C::CHUNKS ? i : C::CHUNKS - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < C::PF; ++j) pf[j] ^= sign_mask(sv[j]);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < C::PF; ++j) {
       const int i = pl + 128 * j;  // line i / 8, chunk i % 8; odd lines swap their halves
@@ -725,6 +753,10 @@ had_quant_pair(RotQuantArgs args) {
       store_row();
       if (lane == 0) pair_publish(mine1, it + 2);
     }
+    if constexpr (VAR) {  // clipped range [r min, r max]
+      mn = __fmul_rn(mn, args.clip);
+      mx = __fmul_rn(mx, args.clip);
+    }
 
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
     const float r_u = __fsub_rn(mx, mn);
@@ -750,7 +782,7 @@ had_quant_pair(RotQuantArgs args) {
         if constexpr (BITS == 8) {  // one code per byte: 16-byte store
           uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-          for (int j = 0; j < 16; ++j) w[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][j], inv_u, nb), j & 3, w[j >> 2]);
+          for (int j = 0; j < 16; ++j) w[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][nt][j], inv_u, nb)), j & 3, w[j >> 2]);
           if (valid && ja < A) *reinterpret_cast<uint4*>(qrow + pos) = make_uint4(w[0], w[1], w[2], w[3]);
         } else {
           uint32_t w[2];
@@ -759,8 +791,8 @@ had_quant_pair(RotQuantArgs args) {
             uint32_t ev = 0, od = 0;
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-              ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s], inv_u, nb), s, ev);
-              od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
+              ev = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s], inv_u, nb)), s, ev);
+              od = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][nt][8 * hw + 2 * s + 1], inv_u, nb)), s, od);
             }
             w[hw] = ev | (od << 4);
           }
@@ -818,7 +850,7 @@ struct Lines {
   static_assert(KS <= 32, "k-step sign bits");
 };
 
-template <int A, int F, int NT, bool DBG, int BITS>
+template <int A, int F, int NT, bool DBG, int BITS, bool VAR>
 __global__ void __launch_bounds__(64 * NT, DBG ? 2 : 4)  // 4 waves per SIMD: 128 VGPRs
 had_quant_lines(RotQuantArgs args) {
   using C = Lines<A, F, NT>;
@@ -846,6 +878,19 @@ had_quant_lines(RotQuantArgs args) {
     }
   };
   auto store_row = [&]() {
+    if constexpr (VAR) {
+      if (args.signs) {  // S flips element signs as the row goes to the slot
+        const uint2* sg = reinterpret_cast<const uint2*>(args.signs);
+        uint2 sv[C::PF];
+#pragma unroll
+        for (int j = 0; j < C::PF; ++j) {
+          const int i = threadIdx.x + C::THREADS * j;
+          sv[j] = sg[i < C::CHUNKS ? i : C::CHUNKS - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < C::PF; ++j) pf[j] ^= sign_mask(sv[j]);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < C::PF; ++j) {
       const int i = threadIdx.x + C::THREADS * j;  // line i / 8, chunk i % 8
@@ -1033,6 +1078,10 @@ had_quant_lines(RotQuantArgs args) {
       mx = fmaxf(mx, red[NT + v]);
     }
     if (more) store_row();
+    if constexpr (VAR) {  // clipped range [r min, r max]
+      mn = __fmul_rn(mn, args.clip);
+      mx = __fmul_rn(mx, args.clip);
+    }
 
     // eq. 1 in the unscaled domain; reported alpha, beta carry the 1/sqrt(K) scale
     const float r_u = __fsub_rn(mx, mn);
@@ -1053,7 +1102,7 @@ had_quant_lines(RotQuantArgs args) {
       if constexpr (BITS == 8) {  // one code per byte: 16-byte store
         uint32_t wd[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int j = 0; j < 16; ++j) wd[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][j], inv_u, nb), j & 3, wd[j >> 2]);
+        for (int j = 0; j < 16; ++j) wd[j >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][j], inv_u, nb)), j & 3, wd[j >> 2]);
         if (real) *reinterpret_cast<uint4*>(qrow + pos) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
       } else {
         uint32_t wd[2];
@@ -1062,8 +1111,8 @@ had_quant_lines(RotQuantArgs args) {
           uint32_t ev = 0, od = 0;
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
-            ev = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s], inv_u, nb), s, ev);
-            od = __builtin_amdgcn_cvt_pk_u8_f32(__fmaf_rn(acc[mt][8 * hw + 2 * s + 1], inv_u, nb), s, od);
+            ev = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][8 * hw + 2 * s], inv_u, nb)), s, ev);
+            od = __builtin_amdgcn_cvt_pk_u8_f32(code_arg<VAR, BITS>(__fmaf_rn(acc[mt][8 * hw + 2 * s + 1], inv_u, nb)), s, od);
           }
           wd[hw] = ev | (od << 4);
         }
@@ -1120,10 +1169,10 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
                : launch_kron_t<A, APAD, NT, B, MW, NW, STAGE, false>(a, stream);
 }
 
-template <int A, int APAD, int NT, bool DBG, int BITS>
+template <int A, int APAD, int NT, bool DBG, int BITS, bool VAR>
 hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Pair<A, APAD, NT>;
-  auto kern = had_quant_pair<A, APAD, NT, DBG, BITS>;
+  auto kern = had_quant_pair<A, APAD, NT, DBG, BITS, VAR>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (init != hipSuccess) return init;
@@ -1133,17 +1182,33 @@ hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
 
-template <int A, int APAD, int NT>
-hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
-  if (a.bits == 8)
-    return a.dbg ? launch_pair_t<A, APAD, NT, true, 8>(a, stream) : launch_pair_t<A, APAD, NT, false, 8>(a, stream);
-  return a.dbg ? launch_pair_t<A, APAD, NT, true, 4>(a, stream) : launch_pair_t<A, APAD, NT, false, 4>(a, stream);
+// Calls f(dbg, b8, var) with each flag as a std::bool_constant, so that one call site
+// instantiates every combination of the kernels' compile-time switches.
+template <typename Fn>
+hipError_t with_flags(bool dbg, bool b8, bool var, Fn&& f) {
+  using T = std::true_type;
+  using N = std::false_type;
+  if (dbg) {
+    if (b8) return var ? f(T{}, T{}, T{}) : f(T{}, T{}, N{});
+    return var ? f(T{}, N{}, T{}) : f(T{}, N{}, N{});
+  }
+  if (b8) return var ? f(N{}, T{}, T{}) : f(N{}, T{}, N{});
+  return var ? f(N{}, N{}, T{}) : f(N{}, N{}, N{});
 }
 
-template <int A, int F, int NT, bool DBG, int BITS>
+bool is_variant(const RotQuantArgs& a) { return a.clip != 1.0f || a.signs != nullptr; }
+
+template <int A, int APAD, int NT>
+hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
+  return with_flags(a.dbg != nullptr, a.bits == 8, is_variant(a), [&](auto dbg, auto b8, auto var) {
+    return launch_pair_t<A, APAD, NT, decltype(dbg)::value, decltype(b8)::value ? 8 : 4, decltype(var)::value>(a, stream);
+  });
+}
+
+template <int A, int F, int NT, bool DBG, int BITS, bool VAR>
 hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Lines<A, F, NT>;
-  auto kern = had_quant_lines<A, F, NT, DBG, BITS>;
+  auto kern = had_quant_lines<A, F, NT, DBG, BITS, VAR>;
   static int blocks_per_cu = 0;
   static const hipError_t init = [&] {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1161,9 +1226,9 @@ hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
 
 template <int A, int F, int NT>
 hipError_t launch_lines(const RotQuantArgs& a, hipStream_t stream) {
-  if (a.bits == 8)
-    return a.dbg ? launch_lines_t<A, F, NT, true, 8>(a, stream) : launch_lines_t<A, F, NT, false, 8>(a, stream);
-  return a.dbg ? launch_lines_t<A, F, NT, true, 4>(a, stream) : launch_lines_t<A, F, NT, false, 4>(a, stream);
+  return with_flags(a.dbg != nullptr, a.bits == 8, is_variant(a), [&](auto dbg, auto b8, auto var) {
+    return launch_lines_t<A, F, NT, decltype(dbg)::value, decltype(b8)::value ? 8 : 4, decltype(var)::value>(a, stream);
+  });
 }
 
 }  // namespace
@@ -1172,11 +1237,13 @@ hipError_t launch_lines(const RotQuantArgs& a, hipStream_t stream) {
 hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   if ((a.bits != 4 && a.bits != 8) || a.group != a.K || a.K != static_cast<int64_t>(a.a) * a.b || a.H == nullptr)
     return hipErrorNotSupported;
-  // the pair and line kernels stage rows in 16-byte chunks (and write 4- or 8-bit codes);
-  // the register-prefetch kernels write 4-bit codes only
+  // the pair and line kernels stage rows in 16-byte chunks (and write 4- or 8-bit codes,
+  // with or without the clipping and sign variants; S is read 8 entries at a time); the
+  // register-prefetch kernels write plain 4-bit codes only
   const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 &&
-                       (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 && !getenv("SQ_KRON_STAGED");
-  if (!pair_ok && a.bits != 4) return hipErrorNotSupported;
+                       (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.signs) & 7) == 0 && !getenv("SQ_KRON_STAGED");
+  if (!pair_ok && (a.bits != 4 || is_variant(a))) return hipErrorNotSupported;
   if (a.a == 28 && a.b == 512) {
     if (pair_ok) return launch_lines<28, 8, 7>(a, stream);
     return launch_kron<28, 32, 1, 512, 4, 1, false>(a, stream);

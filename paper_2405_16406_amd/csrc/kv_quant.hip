@@ -13,6 +13,9 @@
 //   K (rotated, 1/sqrt(128) folded into alpha and beta): rint(fma(v, 1/alpha, -mn/alpha));
 //     this can move a code by one only where the value sits on a rounding boundary, which
 //     the rotated path allows anyway.
+// A clipping ratio r in (0, 1] per cache (App. A "Quantization choice") quantizes each
+// group's range [r min, r max]; the code argument is clamped to [0, L] before the
+// conversion (which by itself saturates at 255 only), so values outside take the end codes.
 #include "sq_device.h"
 #include "sq_internal.h"
 
@@ -76,8 +79,8 @@ __device__ __forceinline__ void fwht128(float (&e)[32], int j) {
 // 4-bit: element 32*k + 8*j + q -> nibble of byte 16*k + 4*j + q/2 of the group's 64 bytes;
 // 8-bit: -> byte 32*k + 8*j + q of its 128 bytes.
 template <bool EXACT, int BITS>
-__device__ __forceinline__ void quant_store(const float (&e)[32], int j, float scale, int64_t grp, uint8_t* q,
-                                            float* alpha, float* beta) {
+__device__ __forceinline__ void quant_store(const float (&e)[32], int j, float scale, float clip, int64_t grp,
+                                            uint8_t* q, float* alpha, float* beta) {
   float mn = e[0], mx = e[0];
 #pragma unroll
   for (int r = 1; r < 32; ++r) {
@@ -86,11 +89,12 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
   }
   mn = fminf(mn, quad_xor<1>(mn));
   mx = fmaxf(mx, quad_xor<1>(mx));
-  mn = fminf(mn, quad_xor<2>(mn));
-  mx = fmaxf(mx, quad_xor<2>(mx));
+  mn = __fmul_rn(fminf(mn, quad_xor<2>(mn)), clip);
+  mx = __fmul_rn(fmaxf(mx, quad_xor<2>(mx)), clip);
+  constexpr float kL = BITS == 8 ? 255.0f : 15.0f;
   // alpha of the reported (scaled) values decides the constant-group case
   const float r_u = __fsub_rn(mx, mn);
-  const float a_u = __fdiv_rn(r_u, BITS == 8 ? 255.0f : 15.0f);
+  const float a_u = __fdiv_rn(r_u, kL);
   const bool cst = __fmul_rn(a_u, scale) < kMinNormal;
   const float inv = cst ? 1.0f : __fdiv_rn(1.0f, a_u);
   const float nb = -__fmul_rn(mn, inv);
@@ -103,7 +107,7 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
       for (int x = 0; x < 8; ++x) {
         const float v = e[8 * k + x];
         const float t = EXACT ? __fmul_rn(__fsub_rn(v, mn), inv) : __fmaf_rn(v, inv, nb);
-        w[x >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(t, x & 3, w[x >> 2]);  // rounds half to even, clamps
+        w[x >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(t, 0.0f, kL), x & 3, w[x >> 2]);
       }
       *reinterpret_cast<uint2*>(qg + 32 * k + 8 * j) = make_uint2(w[0], w[1]);
     }
@@ -122,8 +126,9 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
         t0 = __fmaf_rn(e[8 * k + 2 * i], inv, nb);
         t1 = __fmaf_rn(e[8 * k + 2 * i + 1], inv, nb);
       }
-      ev = __builtin_amdgcn_cvt_pk_u8_f32(t0, i, ev);  // rounds half to even, clamps to [0, 255]
-      od = __builtin_amdgcn_cvt_pk_u8_f32(t1, i, od);
+      // rounds half to even
+      ev = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(t0, 0.0f, kL), i, ev);
+      od = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(t1, 0.0f, kL), i, od);
     }
     *reinterpret_cast<uint32_t*>(qg + 16 * k + 4 * j) = ev | (od << 4);
   }
@@ -176,12 +181,12 @@ qk_had_kvquant_v2(KvArgs a) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) a.dbg_k[base + 32 * k + 8 * j + q] = __fmul_rn(e[8 * k + q], a.inv_sqrt_d);
   }
-  quant_store<false, BITS>(e, j, a.inv_sqrt_d, grp, a.kq, a.ka, a.kb);
+  quant_store<false, BITS>(e, j, a.inv_sqrt_d, a.k_clip, grp, a.kq, a.ka, a.kb);
 
   // V: quantize
   if constexpr (!EARLY) load_raw(a.v + base, j, rv);
   widen(rv, e);
-  quant_store<true, BITS>(e, j, 1.0f, grp, a.vq, a.va, a.vb);
+  quant_store<true, BITS>(e, j, 1.0f, a.v_clip, grp, a.vq, a.va, a.vb);
 }
 
 }  // namespace

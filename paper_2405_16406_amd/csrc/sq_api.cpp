@@ -90,6 +90,12 @@ sq_status check_rows(int64_t M, int64_t K, int64_t ld, const char* mname) {
   return SQ_OK;
 }
 
+// A range clipping ratio: finite, 0 < r <= 1.
+sq_status check_clip(float r, const char* name) {
+  if (!(r > 0.0f && r <= 1.0f)) return fail(SQ_ERR_SHAPE, "%s=%g outside (0, 1]", name, static_cast<double>(r));
+  return SQ_OK;
+}
+
 float inv_sqrt(int64_t n) { return static_cast<float>(1.0 / std::sqrt(static_cast<double>(n))); }
 
 }  // namespace
@@ -117,11 +123,11 @@ sq_status sq_hadamard_factor(int32_t n, int8_t* out_host) {
   return ok();
 }
 
-sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
-                           int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
-                           int32_t bits, int32_t group,
-                           uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
-                           void* stream) {
+sq_status sq_had_quant_act_ex(const void* x, int64_t M, int64_t K, int64_t ldx,
+                              int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                              const int8_t* signs, int32_t bits, int32_t group, float clip,
+                              uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
+                              void* stream) {
   TimingScope timing_scope;
   if (!x || !q_out || !alpha || !beta) return fail(SQ_ERR_NULL, "x, q_out, alpha and beta are required");
   sq_status s = check_rows(M, K, ldx, "M");
@@ -130,13 +136,16 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   if (bits != 4 && bits != 8) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: 4- and 8-bit activations are implemented", bits);
   if (group <= 0 || group % 2 != 0 || K % group != 0)
     return fail(SQ_ERR_SHAPE, "group=%d must be even and divide K=%lld", group, (long long)K);
+  if ((s = check_clip(clip, "clip")) != SQ_OK) return s;
   if (!aligned(x, 16) || !aligned(q_out, 16) || !aligned(alpha, 4) || !aligned(beta, 4) ||
       (dbg_rot && !aligned(dbg_rot, 4)))
     return fail(SQ_ERR_ALIGN, "x and q_out must be 16-byte aligned, scales 4-byte aligned");
   const uint64_t G = static_cast<uint64_t>(K / group);
   const uint64_t um = static_cast<uint64_t>(M);
   const uint64_t xbytes = um ? ((um - 1) * ldx + K) * 2 : 0;
-  s = check_alias({{x, xbytes, "x"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"}},
+  const uint64_t n = static_cast<uint64_t>(had_dense_n) * had_pow2_n;
+  s = check_alias({{x, xbytes, "x"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"},
+                   {signs, signs ? n : 0, "signs"}},
                   {{q_out, um * K * bits / 8, "q_out"}, {alpha, um * G * 4, "alpha"}, {beta, um * G * 4, "beta"},
                    {dbg_rot, dbg_rot ? um * K * 4 : 0, "dbg_rot"}});
   if (s != SQ_OK) return s;
@@ -151,6 +160,8 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   a.b = had_pow2_n;
   a.group = group;
   a.bits = bits;
+  a.clip = clip;
+  a.signs = signs;
   a.inv_sqrt_n = inv_sqrt(static_cast<int64_t>(had_dense_n) * had_pow2_n);
   a.q = q_out;
   a.alpha = alpha;
@@ -159,9 +170,18 @@ sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
   return hip_status(sq::launch_had_quant_act(a, static_cast<hipStream_t>(stream)), "had_quant_act launch");
 }
 
-sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
-                     int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
-                     uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream) {
+sq_status sq_had_quant_act(const void* x, int64_t M, int64_t K, int64_t ldx,
+                           int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                           int32_t bits, int32_t group,
+                           uint8_t* q_out, float* alpha, float* beta, float* dbg_rot,
+                           void* stream) {
+  return sq_had_quant_act_ex(x, M, K, ldx, had_dense_n, had_dense, had_pow2_n, nullptr, bits, group, 1.0f, q_out,
+                             alpha, beta, dbg_rot, stream);
+}
+
+sq_status sq_pack_w4_ex(const void* w, int64_t N, int64_t K, int64_t ldw,
+                        int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n, const int8_t* signs,
+                        uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream) {
   TimingScope timing_scope;
   if (!w || !wq || !w_alpha || !w_rowsum) return fail(SQ_ERR_NULL, "w, wq, w_alpha and w_rowsum are required");
   sq_status s = check_rows(N, K, ldw, "N");
@@ -171,7 +191,9 @@ sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
     return fail(SQ_ERR_ALIGN, "w and wq must be 16-byte aligned, w_alpha and w_rowsum 4-byte aligned");
   const uint64_t un = static_cast<uint64_t>(N);
   const uint64_t wbytes = un ? ((un - 1) * ldw + K) * 2 : 0;
-  s = check_alias({{w, wbytes, "w"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"}},
+  const uint64_t n = static_cast<uint64_t>(had_dense_n) * had_pow2_n;
+  s = check_alias({{w, wbytes, "w"}, {had_dense, static_cast<uint64_t>(had_dense_n) * had_dense_n, "had_dense"},
+                   {signs, signs ? n : 0, "signs"}},
                   {{wq, un * K / 2, "wq"}, {w_alpha, un * 4, "w_alpha"}, {w_rowsum, un * 4, "w_rowsum"}});
   if (s != SQ_OK) return s;
   if (N == 0) return ok();
@@ -184,11 +206,19 @@ sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
   a.H = had_dense;
   a.b = had_pow2_n;
   a.group = static_cast<int>(K);
+  a.clip = 1.0f;
+  a.signs = signs;
   a.inv_sqrt_n = inv_sqrt(static_cast<int64_t>(had_dense_n) * had_pow2_n);
   a.q = wq;
   a.alpha = w_alpha;
   a.rowsum = w_rowsum;
   return hip_status(sq::launch_pack_w4(a, static_cast<hipStream_t>(stream)), "pack_w4 launch");
+}
+
+sq_status sq_pack_w4(const void* w, int64_t N, int64_t K, int64_t ldw,
+                     int32_t had_dense_n, const int8_t* had_dense, int32_t had_pow2_n,
+                     uint8_t* wq, float* w_alpha, int32_t* w_rowsum, void* stream) {
+  return sq_pack_w4_ex(w, N, K, ldw, had_dense_n, had_dense, had_pow2_n, nullptr, wq, w_alpha, w_rowsum, stream);
 }
 
 sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x_beta, int64_t M,
@@ -316,11 +346,12 @@ sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const f
   return hip_status(e, "w4a4_linear_swiglu launch");
 }
 
-sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
-                            int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
-                            void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
-                            uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
-                            void* stream) {
+sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
+                               int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
+                               float k_clip, float v_clip,
+                               void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
+                               uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                               void* stream) {
   TimingScope timing_scope;
   if (!q || !k || !v || !q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta)
     return fail(SQ_ERR_NULL, "q, k, v, q_rot, k_q, k_alpha, k_beta, v_q, v_alpha and v_beta are required");
@@ -328,6 +359,8 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
   if (D != 128) return fail(SQ_ERR_UNSUPPORTED, "D=%lld: only head_dim 128 is implemented", (long long)D);
   if (bits != 4 && bits != 8) return fail(SQ_ERR_UNSUPPORTED, "bits=%d: 4- and 8-bit KV are implemented", bits);
   if (group != 128) return fail(SQ_ERR_UNSUPPORTED, "group=%d: only group 128 (= D) is implemented", group);
+  sq_status s = check_clip(k_clip, "k_clip");
+  if (s != SQ_OK || (s = check_clip(v_clip, "v_clip")) != SQ_OK) return s;
   const uint64_t groups = static_cast<uint64_t>(B) * static_cast<uint64_t>(S) * static_cast<uint64_t>(H);
   if (groups > (uint64_t{1} << 40)) return fail(SQ_ERR_SHAPE, "B*S*H too large");
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(q_rot, 16) || !aligned(k_q, 16) ||
@@ -335,7 +368,7 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
       !aligned(v_beta, 4) || (dbg_k_rot && !aligned(dbg_k_rot, 4)))
     return fail(SQ_ERR_ALIGN, "tensors need 16-byte, scales 4-byte alignment");
   const uint64_t E = groups * 128;
-  sq_status s = check_alias({{q, E * 2, "q"}, {k, E * 2, "k"}, {v, E * 2, "v"}},
+  s = check_alias({{q, E * 2, "q"}, {k, E * 2, "k"}, {v, E * 2, "v"}},
                             {{q_rot, E * 2, "q_rot"}, {k_q, E * bits / 8, "k_q"}, {k_alpha, groups * 4, "k_alpha"},
                              {k_beta, groups * 4, "k_beta"}, {v_q, E * bits / 8, "v_q"}, {v_alpha, groups * 4, "v_alpha"},
                              {v_beta, groups * 4, "v_beta"}, {dbg_k_rot, dbg_k_rot ? E * 4 : 0, "dbg_k_rot"}});
@@ -356,7 +389,18 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
   a.vb = v_beta;
   a.dbg_k = dbg_k_rot;
   a.bits = bits;
+  a.k_clip = k_clip;
+  a.v_clip = v_clip;
   return hip_status(sq::launch_qk_had_kvquant(a, static_cast<hipStream_t>(stream)), "qk_had_kvquant launch");
+}
+
+sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
+                            int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
+                            void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
+                            uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                            void* stream) {
+  return sq_qk_had_kvquant_ex(q, k, v, B, S, H, D, bits, group, 1.0f, 1.0f, q_rot, k_q, k_alpha, k_beta, v_q,
+                              v_alpha, v_beta, dbg_k_rot, stream);
 }
 
 sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,

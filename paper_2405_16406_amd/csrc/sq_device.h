@@ -34,6 +34,10 @@ __device__ __forceinline__ AsymParams asym_params(float mn, float mx, float leve
   const float alpha = (a < kMinNormal) ? 1.0f : a;  // zero or subnormal: constant group
   return {mn, alpha, __fdiv_rn(1.0f, alpha), levels};
 }
+// t = (v - mn) * inv clamped to [0, L]: rint(t) is then the code
+__device__ __forceinline__ float asym_t(float v, const AsymParams& p) {
+  return __builtin_amdgcn_fmed3f(__fmul_rn(__fsub_rn(v, p.mn), p.inv), 0.0f, p.levels);
+}
 // code = clamp(rint((v - mn) * inv), 0, L)
 __device__ __forceinline__ uint32_t asym_code(float v, const AsymParams& p) {
   const float t = __fmul_rn(__fsub_rn(v, p.mn), p.inv);

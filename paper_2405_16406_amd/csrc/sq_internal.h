@@ -23,6 +23,8 @@ struct RotQuantArgs {
   int b;                 // Sylvester order
   int group;             // quantization group (asym mode)
   int bits;              // activation codes: 4 (two per byte) or 8 (one per byte)
+  float clip = 1.0f;     // range clipping ratio in (0, 1] (asym mode; 1 = plain min-max)
+  const int8_t* signs = nullptr;  // +-1 [a * b] (device): diagonal S of a random Hadamard S H
   float inv_sqrt_n;      // fl32(1 / sqrt(a * b))
   uint8_t* q;            // codes [rows, K/2] (4-bit, packed) or [rows, K] (8-bit)
   float* alpha;          // [rows, K/group] (asym) or [rows] (sym)
@@ -94,6 +96,8 @@ struct KvArgs {
   float* vb;
   float* dbg_k;
   int bits;              // cache codes: 4 (two per byte) or 8 (one per byte)
+  float k_clip = 1.0f;   // range clipping ratios of the K and V groups, in (0, 1]
+  float v_clip = 1.0f;
 };
 
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream);

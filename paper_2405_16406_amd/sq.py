@@ -20,8 +20,8 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
                 4: "SQ_ERR_ALIGN", 5: "SQ_ERR_ALIAS", 6: "SQ_ERR_HIP"}
 
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
-           "sq_pack_w4", "sq_w4a4_linear", "sq_w4a8_linear", "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant",
-           "sq_attn_decode_kv4")
+           "sq_had_quant_act_ex", "sq_pack_w4", "sq_pack_w4_ex", "sq_w4a4_linear", "sq_w4a8_linear",
+           "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_qk_had_kvquant_ex", "sq_attn_decode_kv4")
 
 
 class SqError(RuntimeError):
@@ -34,6 +34,7 @@ _lib = None
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
 _I32 = ctypes.c_int32
+_F32 = ctypes.c_float
 
 
 def lib() -> ctypes.CDLL:
@@ -54,8 +55,13 @@ def lib() -> ctypes.CDLL:
     L.sq_hadamard_factor.argtypes = [_I32, _P]
     L.sq_had_quant_act.restype = _I32
     L.sq_had_quant_act.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]
+    L.sq_had_quant_act_ex.restype = _I32
+    L.sq_had_quant_act_ex.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _I32, _I32, _F32,
+                                      _P, _P, _P, _P, _P]
     L.sq_pack_w4.restype = _I32
     L.sq_pack_w4.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _P, _P, _P]
+    L.sq_pack_w4_ex.restype = _I32
+    L.sq_pack_w4_ex.argtypes = [_P, _I64, _I64, _I64, _I32, _P, _I32, _P, _P, _P, _P, _P]
     L.sq_w4a4_linear.restype = _I32
     L.sq_w4a4_linear.argtypes = [_P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P]
     L.sq_w4a8_linear.restype = _I32
@@ -65,8 +71,11 @@ def lib() -> ctypes.CDLL:
     L.sq_qk_had_kvquant.restype = _I32
     L.sq_qk_had_kvquant.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32,
                                     _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    L.sq_qk_had_kvquant_ex.restype = _I32
+    L.sq_qk_had_kvquant_ex.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _F32, _F32,
+                                       _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.sq_attn_decode_kv4.restype = _I32
-    L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, ctypes.c_float, _P, _P]
+    L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _P, _P]
     _lib = L
     return L
 
@@ -111,11 +120,14 @@ def hadamard_factor(n: int) -> np.ndarray:
 
 
 def had_quant_act(x: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1,
-                  group: int | None = None, bits: int = 4, dbg: bool = False, out=None):
+                  group: int | None = None, bits: int = 4, dbg: bool = False, out=None,
+                  clip: float = 1.0, signs: torch.Tensor | None = None):
     """Rotate rows of x (fp16 [M, K], row stride x.stride(0)) and quantize (asym, 4 or 8 bits).
 
-    had: int8 +-1 [a, a] on the device or None.  Returns (q uint8 [M, K/2] (4-bit) or [M, K] (8-bit),
-    alpha fp32 [M, K/group], beta fp32 [M, K/group], dbg_rot fp32 [M, K] or None).
+    had: int8 +-1 [a, a] on the device or None.  clip (range clipping ratio in (0, 1]) and
+    signs (int8 +-1 [a * pow2] on the device: the random Hadamard S H) select sq_had_quant_act_ex.
+    Returns (q uint8 [M, K/2] (4-bit) or [M, K] (8-bit), alpha fp32 [M, K/group],
+    beta fp32 [M, K/group], dbg_rot fp32 [M, K] or None).
     """
     _need(x, torch.float16, "x")
     if x.dim() != 2 or x.stride(1) != 1:
@@ -133,15 +145,23 @@ def had_quant_act(x: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 
     else:
         q, al, be = out
     rot = torch.empty((M, K), dtype=torch.float32, device=dev) if dbg else None
-    _check(lib().sq_had_quant_act(_ptr(x), M, K, x.stride(0), a, _ptr(had), pow2, bits, group,
-                                  _ptr(q), _ptr(al), _ptr(be), _ptr(rot), _stream(x)), "sq_had_quant_act")
+    if clip == 1.0 and signs is None:
+        _check(lib().sq_had_quant_act(_ptr(x), M, K, x.stride(0), a, _ptr(had), pow2, bits, group,
+                                      _ptr(q), _ptr(al), _ptr(be), _ptr(rot), _stream(x)), "sq_had_quant_act")
+    else:
+        if signs is not None:
+            _need(signs, torch.int8, "signs")
+        _check(lib().sq_had_quant_act_ex(_ptr(x), M, K, x.stride(0), a, _ptr(had), pow2, _ptr(signs), bits, group,
+                                         float(clip), _ptr(q), _ptr(al), _ptr(be), _ptr(rot), _stream(x)),
+               "sq_had_quant_act_ex")
     return q, al, be, rot
 
 
-def pack_w4(w: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1):
+def pack_w4(w: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1, signs: torch.Tensor | None = None):
     """Offline: W' = W R (optional), symmetric per-row 4-bit quant, pack.
 
-    Returns (wq uint8 [N, K/2], w_alpha fp32 [N], w_rowsum int32 [N]).
+    signs (int8 +-1 [a * pow2] on the device) fold the random Hadamard S H instead
+    (sq_pack_w4_ex).  Returns (wq uint8 [N, K/2], w_alpha fp32 [N], w_rowsum int32 [N]).
     """
     _need(w, torch.float16, "w")
     if w.dim() != 2 or w.stride(1) != 1:
@@ -152,8 +172,13 @@ def pack_w4(w: torch.Tensor, had: torch.Tensor | None = None, pow2: int = 1):
     wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
     wa = torch.empty((N,), dtype=torch.float32, device=dev)
     rs = torch.empty((N,), dtype=torch.int32, device=dev)
-    _check(lib().sq_pack_w4(_ptr(w), N, K, w.stride(0), a, _ptr(had), pow2, _ptr(wq), _ptr(wa), _ptr(rs),
-                            _stream(w)), "sq_pack_w4")
+    if signs is None:
+        _check(lib().sq_pack_w4(_ptr(w), N, K, w.stride(0), a, _ptr(had), pow2, _ptr(wq), _ptr(wa), _ptr(rs),
+                                _stream(w)), "sq_pack_w4")
+    else:
+        _need(signs, torch.int8, "signs")
+        _check(lib().sq_pack_w4_ex(_ptr(w), N, K, w.stride(0), a, _ptr(had), pow2, _ptr(signs), _ptr(wq), _ptr(wa),
+                                   _ptr(rs), _stream(w)), "sq_pack_w4_ex")
     return wq, wa, rs
 
 
@@ -226,9 +251,11 @@ def interleave_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
                        dim=1).reshape(2 * I, *gate.shape[1:])
 
 
-def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4):
+def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4, k_clip: float = 1.0,
+                   v_clip: float = 1.0):
     """R3 on Q and K per head (D = 128) + 4-bit (or 8-bit) asymmetric K/V quantization, group 128.
 
+    k_clip, v_clip: range clipping ratios in (0, 1] (other than 1: sq_qk_had_kvquant_ex).
     Returns dict(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, k_rot (or None)).
     """
     for t, nme in ((q, "q"), (k, "k"), (v, "v")):
@@ -246,10 +273,13 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4):
                    v_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
                    v_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev))
     kr = torch.empty((B, S, H, D), dtype=torch.float32, device=dev) if dbg else None
-    _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128,
-                                   _ptr(out["q_rot"]), _ptr(out["k_q"]), _ptr(out["k_alpha"]), _ptr(out["k_beta"]),
-                                   _ptr(out["v_q"]), _ptr(out["v_alpha"]), _ptr(out["v_beta"]), _ptr(kr),
-                                   _stream(q)), "sq_qk_had_kvquant")
+    outs = (_ptr(out["q_rot"]), _ptr(out["k_q"]), _ptr(out["k_alpha"]), _ptr(out["k_beta"]), _ptr(out["v_q"]),
+            _ptr(out["v_alpha"]), _ptr(out["v_beta"]), _ptr(kr), _stream(q))
+    if k_clip == 1.0 and v_clip == 1.0:
+        _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128, *outs), "sq_qk_had_kvquant")
+    else:
+        _check(lib().sq_qk_had_kvquant_ex(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128, float(k_clip),
+                                          float(v_clip), *outs), "sq_qk_had_kvquant_ex")
     out = dict(out)
     out["k_rot"] = kr
     return out

@@ -209,3 +209,57 @@ def test_time_next_call_host_checks(L):
     # the next entry-point call consumes the armed events even when it fails its checks
     assert hqa(L, K=250, ldx=256) == sq.SQ_ERR_SHAPE
     assert hqa(L, x=None) == sq.SQ_ERR_NULL
+
+
+def hqa_ex(L, x=fake(0), M=4, K=256, ldx=256, a=1, H=None, b=1, signs=None, bits=4, group=None, clip=1.0,
+           q=fake(1), al=fake(2), be=fake(3), dbg=None):
+    group = K if group is None else group
+    return L.sq_had_quant_act_ex(x, M, K, ldx, a, H, b, signs, bits, group, ctypes.c_float(clip), q, al, be, dbg,
+                                 None)
+
+
+def test_had_quant_act_ex_validation(L):
+    # the plain entry point's checks hold unchanged
+    assert hqa_ex(L, x=None) == sq.SQ_ERR_NULL
+    assert hqa_ex(L, ldx=260) == sq.SQ_ERR_ALIGN
+    assert hqa_ex(L, bits=6) == sq.SQ_ERR_UNSUPPORTED
+    # clipping ratio: 0 < r <= 1
+    for r in (0.0, -0.5, 1.0001, float("nan"), float("inf")):
+        assert hqa_ex(L, clip=r) == sq.SQ_ERR_SHAPE, r
+    assert b"clip" in L.sq_last_error()
+    # signs are an input: an output inside the a*b bytes overlaps them
+    assert hqa_ex(L, b=256, signs=fake(5), q=ctypes.c_void_p(fake(5).value + 128)) == sq.SQ_ERR_ALIAS
+    assert b"signs" in L.sq_last_error()
+    # ...and one past them does not (M == 0: no-op after the checks)
+    assert hqa_ex(L, M=0, b=256, signs=fake(5), q=ctypes.c_void_p(fake(5).value + 256)) == sq.SQ_OK
+    # any alignment of signs is accepted (the matrix-core kernels need 8 bytes; others take any)
+    assert hqa_ex(L, M=0, b=256, signs=ctypes.c_void_p(P * 256 + 3), clip=0.9) == sq.SQ_OK
+
+
+def test_pack_w4_ex_validation(L):
+    def call(w=fake(0), N=8, K=256, ldw=256, a=1, H=None, b=256, signs=fake(7), wq=fake(1), wa=fake(2), rs=fake(3)):
+        return L.sq_pack_w4_ex(w, N, K, ldw, a, H, b, signs, wq, wa, rs, None)
+    assert call(rs=None) == sq.SQ_ERR_NULL
+    assert call(K=100, ldw=100) == sq.SQ_ERR_SHAPE
+    assert call(wa=ctypes.c_void_p(fake(7).value + 200)) == sq.SQ_ERR_ALIAS
+    assert call(N=0) == sq.SQ_OK
+    assert call(N=0, signs=None) == sq.SQ_OK
+
+
+def kvq_ex(L, B=1, S=2, H=2, D=128, bits=4, group=128, k_clip=1.0, v_clip=1.0, **kw):
+    ptrs = [fake(i) for i in range(10)]
+    for i, nm in enumerate(("q", "k", "v", "qr", "kq", "ka", "kb", "vq", "va", "vb")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_qk_had_kvquant_ex(ptrs[0], ptrs[1], ptrs[2], B, S, H, D, bits, group, ctypes.c_float(k_clip),
+                                  ctypes.c_float(v_clip), *ptrs[3:], None, None)
+
+
+def test_kv_ex_validation(L):
+    assert kvq_ex(L, q=None) == sq.SQ_ERR_NULL
+    assert kvq_ex(L, D=64) == sq.SQ_ERR_UNSUPPORTED
+    for r in (0.0, 1.5, float("nan")):
+        assert kvq_ex(L, k_clip=r) == sq.SQ_ERR_SHAPE
+        assert kvq_ex(L, v_clip=r) == sq.SQ_ERR_SHAPE
+    assert kvq_ex(L, qr=fake(0)) == sq.SQ_ERR_ALIAS
+    assert kvq_ex(L, B=0, k_clip=0.95, v_clip=0.95) == sq.SQ_OK

@@ -94,6 +94,115 @@ def test_rotated_quant_8bit(a, b, M, group):
     check_act8(x, a, b, group)
 
 
+def check_act_var(x, a, b, bits=4, group=None, clip=1.0, signs=None, h_gpu=None, s_gpu=None):
+    """sq_had_quant_act_ex (clip ratio, random-sign Hadamard S H) vs the oracle.  h_gpu and
+    s_gpu replace the uploads of H_a and signs (views at other alignments)."""
+    K = x.shape[1]
+    group = K if group is None else group
+    ha = None if a == 1 else ohad.dense_factor(a)
+    if s_gpu is None and signs is not None:
+        s_gpu = dev(signs.astype(np.int8))
+    q, al, be, rot = sq.had_quant_act(dev(x), had_table(a) if h_gpu is None else h_gpu, b, group=group, bits=bits,
+                                      dbg=True, clip=clip, signs=s_gpu)
+    gq, gal, gbe, grot = host(q), host(al), host(be), host(rot)
+    op, oal, obe, oy, oc = olin.had_quant_act(x, ha, b, bits=bits, group=group, clip=clip, signs=signs)
+    gc = parity.unpack(gq, signed=False) if bits == 4 else gq.astype(np.int64)
+    if a * b == 1:
+        np.testing.assert_array_equal(grot, oy)
+        np.testing.assert_array_equal(gq, op)
+        np.testing.assert_array_equal(gal, oal)
+        np.testing.assert_array_equal(gbe, obe)
+        return 0
+    parity.assert_rot_close(grot, oy)
+    parity.assert_params_close(gal, oal, gbe, obe)
+    return parity.code_flips(gc, oc, oy, oal, obe, group)
+
+
+def rand_signs(n, seed):
+    return np.where(workloads.rng_for(seed).random(n) < 0.5, -1, 1).astype(np.int8)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("K", [8, 4096, 16392])
+def test_identity_quant_clipped_bit_exact(bits, K):
+    # the unrotated per-token kernel with a clipped range; and S alone (n = 1) on the generic one
+    say(f"had_quant_act_ex identity {bits}-bit K={K} clip 0.9 / 0.95, signs [-1]")
+    x = workloads.outlier_acts(workloads.rng_for(K + 90), 5, K, max(1, K // 100), 50.0)
+    assert check_act_var(x, 1, 1, bits, clip=0.9) == 0
+    assert check_act_var(x, 1, 1, bits, clip=0.95) == 0
+    assert check_act_var(x, 1, 1, bits, signs=np.array([-1], np.int8), clip=0.95) == 0
+
+
+# R4 shapes on the matrix-core kernels (pair: 172 x 64; lines: 28 x 512, 28 x 1024), a
+# Sylvester-only and a per-group case on the generic kernel; signs, clip, or both
+VAR_SHAPES = [(172, 64, 5, None), (28, 512, 4, None), (28, 1024, 3, None), (1, 256, 6, None), (28, 16, 5, 224)]
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("a,b,M,group", VAR_SHAPES)
+def test_rotated_quant_variants(a, b, M, group, bits):
+    say(f"had_quant_act_ex {bits}-bit a={a} b={b} M={M} group={group}: signs, clip 0.9, both")
+    n = a * b
+    x = workloads.outlier_acts(workloads.rng_for(a + b + M + 91), M, 2 * n if n < 1024 else n,
+                               max(1, n // 100), 50.0)
+    s = rand_signs(n, a + b)
+    check_act_var(x, a, b, bits, group, signs=s)
+    check_act_var(x, a, b, bits, group, clip=0.9)
+    check_act_var(x, a, b, bits, group, clip=0.95, signs=s)
+    # all-plus signs are the plain rotation: the same codes as sq_had_quant_act
+    plain = [host(t) for t in sq.had_quant_act(dev(x), had_table(a), b, group=group, bits=bits)[:3]]
+    ones = [host(t) for t in sq.had_quant_act(dev(x), had_table(a), b, group=group, bits=bits,
+                                              signs=dev(np.ones(n, np.int8)))[:3]]
+    for u, v in zip(plain, ones):
+        np.testing.assert_array_equal(u, v)
+
+
+def test_rotated_quant_variants_other_layouts():
+    # an H_a or an S that is not 16- resp. 8-byte aligned leaves the matrix-core kernels for
+    # the generic one; the results still follow the oracle
+    say("had_quant_act_ex 172x64: H at +1 byte, signs at +1 byte")
+    a, b, M = 172, 64, 4
+    n = a * b
+    x = workloads.outlier_acts(workloads.rng_for(92), M, n, n // 100, 50.0)
+    hbuf = dev(np.concatenate([[0], ohad.dense_factor(a).reshape(-1)]).astype(np.int8))
+    hg = hbuf[1:].view(a, a)
+    s = rand_signs(n, 93)
+    sbuf = dev(np.concatenate([[1], s]).astype(np.int8))
+    check_act_var(x, a, b, 4, h_gpu=hg, signs=s, clip=0.9)
+    check_act_var(x, a, b, 4, signs=s, s_gpu=sbuf[1:], clip=0.95)
+    check_act_var(x, a, b, 8, signs=s, s_gpu=sbuf[1:])
+
+
+def test_pack_w4_random_sign_chain():
+    # the random Hadamard R = S H folded into the weights and applied to the activations
+    # with the same S: the product keeps x W^T (Sec. 2.2; rotation invariance of Sec. 3.1)
+    say("pack_w4_ex + had_quant_act_ex (signs) -> w4a4_linear, 28 x 32")
+    a, b = 28, 32
+    n = a * b
+    rng = workloads.rng_for(94)
+    w = workloads.weights(rng, 64, n)
+    x = workloads.outlier_acts(rng, 16, n, 8, 20.0)
+    s = rand_signs(n, 95)
+    sg = dev(s)
+    wq, wa, rs = sq.pack_w4(dev(w), had_table(a), b, signs=sg)
+    owp, owa, ors, oqw = olin.pack_w4(w, ohad.dense_factor(a), b, signs=s)
+    gqw = parity.unpack(host(wq), signed=True)
+    np.testing.assert_array_equal(host(rs), gqw.sum(1))
+    parity.assert_params_close(host(wa), owa)
+    parity.code_flips(gqw, oqw)
+    q, al, be, _ = sq.had_quant_act(dev(x), had_table(a), b, signs=sg)
+    y, acc = sq.w4a4_linear(q, al, be, wq, wa, rs, dbg=True)
+    # the GPU's own codes through the exact product
+    oy, oacc = olin.w4a4_linear(parity.unpack(host(q), signed=False), host(al)[:, 0], host(be)[:, 0], gqw,
+                                host(wa), host(rs))
+    np.testing.assert_array_equal(host(acc), oacc)
+    parity.assert_out_close(host(y), oy)
+    # and the result approximates x W^T as the plain rotation does (4-bit error bound)
+    ref = x.astype(np.float64) @ w.astype(np.float64).T
+    err = np.abs(host(y).astype(np.float64) - ref).max() / np.abs(ref).max()
+    assert err < 0.25, err
+
+
 def test_tiny_identity_quant_bit_exact():
     say("had_quant_act tiny identity")
     x, _ = workloads.tiny_inputs()
@@ -599,14 +708,14 @@ def test_tiny_rotated_linear_chain():
 
 # ---------------------------------------------------------------- KV
 
-def check_kv(q, k, v, sample=None, bits=4):
-    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True, bits=bits)
+def check_kv(q, k, v, sample=None, bits=4, k_clip=1.0, v_clip=1.0):
+    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True, bits=bits, k_clip=k_clip, v_clip=v_clip)
     g = {n: host(t) for n, t in out.items() if t is not None}
     B, S, H, D = q.shape
     flat = lambda a: a.reshape(B * S * H, -1)
     idx = np.arange(B * S * H) if sample is None else sample
     qs, ks, vs = (flat(t)[idx][None, :, None, :] for t in (q, k, v))
-    o = okv.qk_had_kvquant(qs, ks, vs, bits=bits)
+    o = okv.qk_had_kvquant(qs, ks, vs, bits=bits, k_clip=k_clip, v_clip=v_clip)
     sel = lambda a: flat(a)[idx][None, :, None, :]
     codes = (lambda a: parity.unpack(a, False)) if bits == 4 else (lambda a: a.astype(np.int64))
     # Q R: fp16 of an fp32 sum vs fp16 of the fp64 value: one fp16 ulp of rounding plus the
@@ -629,6 +738,22 @@ def test_kv_small():
     say("qk_had_kvquant small [2,16,4,128] and ragged [1,3,5,128]")
     check_kv(*workloads.kv_inputs(B=2, S=16, H=4, D=128))
     check_kv(*workloads.kv_inputs(B=1, S=3, H=5, D=128))
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_kv_clipped(bits):
+    # range clipping of the cache groups (0.95 is the cache ratio App. A compares against
+    # unclipped min-max; 0.9 clips more); V codes stay bit-exact, K codes boundary-exact
+    say(f"qk_had_kvquant_ex {bits}-bit, k_clip 0.9 / v_clip 0.95 and k_clip 0.95 / v_clip 1")
+    q, k, v = workloads.kv_inputs(B=2, S=16, H=4, D=128)
+    check_kv(q, k, v, bits=bits, k_clip=0.9, v_clip=0.95)
+    check_kv(q, k, v, bits=bits, k_clip=0.95, v_clip=1.0)
+    # clipping moves codes: the outermost values of a group take the end codes 0 and L
+    out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), bits=bits, k_clip=1.0, v_clip=0.5)
+    vc = host(out["v_q"])
+    vc = parity.unpack(vc, False) if bits == 4 else vc.astype(np.int64)
+    L = 2 ** bits - 1
+    assert np.all(vc.max(-1) == L) and np.all(vc.min(-1) == 0)
 
 
 def test_kv8_small_and_sampled():
