@@ -19,19 +19,22 @@ from .rotate import rotate_rows
 
 
 def qk_had_kvquant(q: np.ndarray, k: np.ndarray, v: np.ndarray, bits: int = 4, group: int = 128,
-                   k_clip: float = 1.0, v_clip: float = 1.0):
+                   k_clip: float = 1.0, v_clip: float = 1.0, param_fp16: bool = False):
     """q, k, v: fp16 [B, S, H, D].  Returns a dict with
     q_rot fp16 [B,S,H,D]; k_rot fp32 (quantizer input);
     k_q, v_q uint8 [B,S,H,D/2] (bits 4) or [B,S,H,D] (bits 8);
-    k_alpha, k_beta, v_alpha, v_beta fp32 [B,S,H,D/group];
+    k_alpha, k_beta, v_alpha, v_beta fp32 (fp16 with param_fp16) [B,S,H,D/group];
     k_codes, v_codes int64 [B,S,H,D].
     k_clip, v_clip < 1 clip the groups' ranges (quant_asym; App. A uses 0.95 for the cache).
+    param_fp16: the group parameters stored in fp16 (quant_asym), halving their share of
+    the cache.
     """
     D = q.shape[-1]
     q_rot = rotate_rows(q, None, D).astype(np.float16)
     k_rot = rotate_rows(k, None, D).astype(np.float32)
-    kc, ka, kb = quant_asym(k_rot, bits=bits, group=group, clip=k_clip)
-    vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group, clip=v_clip)
+    kc, ka, kb = quant_asym(k_rot, bits=bits, group=group, clip=k_clip, param_fp16=param_fp16)
+    vc, va, vb = quant_asym(np.asarray(v, dtype=np.float32), bits=bits, group=group, clip=v_clip,
+                            param_fp16=param_fp16)
     return dict(q_rot=q_rot, k_rot=k_rot, k_q=store_codes(kc, bits), k_alpha=ka, k_beta=kb,
                 v_q=store_codes(vc, bits), v_alpha=va, v_beta=vb, k_codes=kc, v_codes=vc)
 
@@ -44,7 +47,7 @@ def attn_decode(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None):
     basis for K); the query is rotated the same way, so q_rot . K_t is the score of the
     unrotated pair up to the cache's quantization error (Sec. 3.1).
       q_rot   fp16 [B, H, D]
-      k_q, v_q  uint8 [B, S, H, D/2]; alphas, betas fp32 [B, S, H] (or [B, S, H, 1])
+      k_q, v_q  uint8 [B, S, H, D/2]; alphas, betas fp32 or fp16 [B, S, H] (or [B, S, H, 1])
       scale   score scale, 1/sqrt(D) by default
     Returns fp16 [B, H, D] = fp16( softmax_t(scale q_rot . K_t) V ), fp64 inside.
     """

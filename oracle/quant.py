@@ -38,13 +38,28 @@ def _groups(v: np.ndarray, group: int) -> np.ndarray:
     return v.reshape(*v.shape[:-1], K // group, group)
 
 
-def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: float = 1.0):
+F16_MAX = F32(65504.0)  # largest finite fp16
+
+
+def to_fp16_sat(x: np.ndarray) -> np.ndarray:
+    """fp32 -> fp16, round to nearest even, saturating at +-65504 instead of overflowing."""
+    return np.clip(np.asarray(x, dtype=F32), -F16_MAX, F16_MAX).astype(np.float16)
+
+
+def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: float = 1.0,
+               param_fp16: bool = False):
     """Asymmetric min-max quantization of eq. 1 over contiguous groups of the last axis.
 
     v: fp32-representable values [..., K].  Returns (codes int64 [..., K] in [0, 2^N-1],
     alpha fp32 [..., K/group], beta fp32 [..., K/group]).
     clip < 1 quantizes the range [clip * min, clip * max] (each end rounded to fp32; the
     range clipping ablated in App. A "Quantization choice"); codes outside it clamp.
+    param_fp16 stores alpha and beta as fp16 (returned as float16 arrays).  Reading: they
+    are computed in fp32 as above, then rounded to fp16 (to_fp16_sat); a group whose fp32
+    alpha is below 2^-126 or whose fp16 alpha is 0 is constant (alpha 1, codes 0); and the
+    codes are taken from the stored pair, inv = fl32(1 / alpha16),
+    q = clamp(rint(fl32(fl32(v - beta16) * inv)), 0, L), so that they dequantize to the
+    nearest level of what is stored.
     """
     v32 = np.asarray(v, dtype=F32)
     group = v32.shape[-1] if group is None else group
@@ -57,6 +72,14 @@ def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: flo
         mx = (mx * F32(clip)).astype(F32)
     r = (mx - mn).astype(F32)
     alpha = (r / levels).astype(F32)
+    if param_fp16:
+        a16 = to_fp16_sat(alpha)
+        a16 = np.where((alpha < TINY) | (a16 == 0), np.float16(1), a16).astype(np.float16)
+        b16 = to_fp16_sat(mn)
+        inv = (F32(1) / a16.astype(F32)).astype(F32)
+        t = ((g - b16.astype(F32)[..., None]).astype(F32) * inv[..., None]).astype(F32)
+        q = np.clip(np.rint(t), 0, levels).astype(np.int64)
+        return q.reshape(v32.shape), a16, b16
     alpha = np.where(alpha < TINY, F32(1), alpha).astype(F32)
     inv = (F32(1) / alpha).astype(F32)
     t = ((g - mn[..., None]).astype(F32) * inv[..., None]).astype(F32)

@@ -145,3 +145,22 @@ def test_kv_clip_matches_quantizer_clip():
     np.testing.assert_array_equal(out["v_codes"], c)
     np.testing.assert_array_equal(out["v_alpha"], a)
     assert out["k_codes"].min() == 0 and out["k_codes"].max() == 15
+
+
+def test_kv_fp16_params_follow_quantizer_and_attention():
+    # fp16 cache parameters: the same quantizer with param_fp16 on the same inputs, and the
+    # attention step consumes them as their values
+    q, k, v = workloads.kv_inputs(B=1, S=6, H=2, D=128)
+    o = kv.qk_had_kvquant(q, k, v, param_fp16=True, v_clip=0.95)
+    for nm in ("k_alpha", "k_beta", "v_alpha", "v_beta"):
+        assert o[nm].dtype == np.float16
+    vc, va, vb = quant.quant_asym(v.astype(np.float32), group=128, clip=0.95, param_fp16=True)
+    np.testing.assert_array_equal(o["v_codes"], vc)
+    np.testing.assert_array_equal(o["v_alpha"], va)
+    kc, ka, kb = quant.quant_asym(o["k_rot"], group=128, param_fp16=True)
+    np.testing.assert_array_equal(o["k_codes"], kc)
+    qr = o["q_rot"][:, -1]
+    args = [o[n] for n in ("k_q", "k_alpha", "k_beta", "v_q", "v_alpha", "v_beta")]
+    a16 = kv.attn_decode(qr, *args)
+    a32 = kv.attn_decode(qr, *[x.astype(np.float32) if x.dtype == np.float16 else x for x in args])
+    np.testing.assert_array_equal(a16, a32)

@@ -189,3 +189,51 @@ def test_asym_clip_closed_form():
     q1, a1, b1 = quant.quant_asym(v, clip=1.0)
     q0, a0, b0 = quant.quant_asym(v)
     assert np.array_equal(q1, q0) and np.array_equal(a1, a0)
+
+
+def test_asym_fp16_params_exact_case_equals_fp32():
+    # range 7.5 over 15 levels: alpha = 0.5 and beta = -3.5 are fp16 numbers, so storing the
+    # parameters in fp16 changes nothing: same codes, same values
+    rng = np.random.default_rng(5)
+    v = np.concatenate([[-3.5, 4.0], rng.uniform(-3.5, 4.0, 62)]).astype(np.float32)[None]
+    q32, a32, b32 = quant.quant_asym(v)
+    q16, a16, b16 = quant.quant_asym(v, param_fp16=True)
+    assert a16.dtype == np.float16 and b16.dtype == np.float16
+    assert a16[0] == np.float16(0.5) and b16[0] == np.float16(-3.5)
+    np.testing.assert_array_equal(q16, q32)
+    np.testing.assert_array_equal(a16.astype(np.float32), a32)
+    np.testing.assert_array_equal(b16.astype(np.float32), b32)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_asym_fp16_params_nearest_stored_level(bits):
+    # with fp16 parameters every code is the nearest level a16 c + b16 of what is stored
+    # (brute force over all 2^N levels; exact ties within 1e-3 of a step may go either way)
+    rng = np.random.default_rng(6 + bits)
+    v = (rng.standard_normal((50, 128)) * rng.uniform(0.01, 300, (50, 1))).astype(np.float32)
+    q, a16, b16 = quant.quant_asym(v, bits=bits, param_fp16=True)
+    a16, b16 = a16.reshape(-1), b16.reshape(-1)
+    levels = np.arange(2 ** bits, dtype=np.float64)
+    deq_all = a16.astype(np.float64)[:, None, None] * levels[None, None, :] + b16.astype(np.float64)[:, None, None]
+    err_all = np.abs(deq_all - v.astype(np.float64)[:, :, None])
+    best = err_all.min(axis=-1)
+    mine = np.take_along_axis(err_all, q[:, :, None], axis=-1)[..., 0]
+    assert np.all(mine <= best + 1e-3 * a16.astype(np.float64)[:, None])
+    # and the stored pair is the fp32 pair rounded to nearest fp16
+    _, a32, b32 = quant.quant_asym(v, bits=bits)
+    np.testing.assert_array_equal(a16, a32.reshape(-1).astype(np.float16))
+    np.testing.assert_array_equal(b16, b32.reshape(-1).astype(np.float16))
+
+
+def test_asym_fp16_params_saturate_and_degenerate():
+    # a range beyond fp16: alpha and beta saturate at 65504 instead of becoming inf
+    v = np.array([[-1.0e6, 1.0e6, 0.0, 5.0e5]], np.float32)
+    q, a16, b16 = quant.quant_asym(v, param_fp16=True)
+    assert a16[0] == np.float16(65504) and b16[0] == np.float16(-65504)
+    t = np.rint((v.astype(np.float64) + 65504.0) / 65504.0)
+    np.testing.assert_array_equal(q, np.clip(t, 0, 15).astype(np.int64))
+    # a constant group, and a range whose alpha underflows fp16 to 0: both constant
+    for row in (np.full(16, 2.5, np.float32), np.linspace(1.0, 1.0 + 15 * 2e-8, 16).astype(np.float32)):
+        q, a16, b16 = quant.quant_asym(row[None], param_fp16=True)
+        assert a16[0] == np.float16(1.0) and np.all(q == 0)
+        assert b16[0] == np.float16(row.min())
