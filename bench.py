@@ -576,6 +576,14 @@ def kernel_report(torch, sq, workloads, dev):
         o.pop("k_rot")
         fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, k_clip=0.95, v_clip=0.95))
     t_kvc = timed(fns)
+    fns = []
+    for _ in range(n_copies(kv_bytes(E))):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc, param_dtype=torch.float16)
+        o.pop("k_rot")
+        fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, param_dtype=torch.float16))
+    t_kvh = timed(fns)
+    b_kvh = kv_bytes(E) - 8 * (E // 128)  # 2 x 4 bytes fewer per group
     b_kv8 = kv_bytes(E) + E  # codes of K and V: one byte per element instead of half
     # decode attention of the last token's rotated query over that cache
     B, S, H, D = q.shape
@@ -590,10 +598,23 @@ def kernel_report(torch, sq, workloads, dev):
         fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4(qr, *cache, out=oa))
         del qc, kc, vc
     t_at = timed(fns)
+    b_ath = b_at - B * S * H * 8  # fp16 group parameters
+    fns = []
+    for _ in range(n_copies(b_ath)):
+        qc, kc, vc = q.clone(), k.clone(), v.clone()
+        o = sq.qk_had_kvquant(qc, kc, vc, param_dtype=torch.float16)
+        qr = o["q_rot"][:, -1].contiguous()
+        oa = torch.empty_like(qr)
+        cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+        fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4(qr, *cache, out=oa))
+        del qc, kc, vc
+    t_ath = timed(fns)
     rep.append(dict(config=workloads.R3_KV["name"], kv_quant=dict(ms=t_kv, GBps=kv_bytes(E) / t_kv / 1e6),
                     kv_quant_8bit=dict(ms=t_kv8, GBps=b_kv8 / t_kv8 / 1e6),
                     kv_quant_clip95=dict(ms=t_kvc, GBps=kv_bytes(E) / t_kvc / 1e6),
-                    attn_decode=dict(ms=t_at, GBps=b_at / t_at / 1e6)))
+                    kv_quant_fp16_params=dict(ms=t_kvh, GBps=b_kvh / t_kvh / 1e6),
+                    attn_decode=dict(ms=t_at, GBps=b_at / t_at / 1e6),
+                    attn_decode_fp16_params=dict(ms=t_ath, GBps=b_ath / t_ath / 1e6)))
     return rep
 
 

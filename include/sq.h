@@ -68,7 +68,7 @@ const char* sq_last_error(void);
 /*
  * sq_time_next_call -- measurement hook, not part of the method.  Arms two events for
  * the next call of sq_had_quant_act(_ex), sq_pack_w4(_ex), sq_w4a4_linear, sq_w4a8_linear,
- * sq_w4a4_linear_swiglu, sq_qk_had_kvquant(_ex) or sq_attn_decode_kv4
+ * sq_w4a4_linear_swiglu, sq_qk_had_kvquant(_ex) or sq_attn_decode_kv4(_ex)
  * made by this host thread: start_event takes the start time of the first kernel that
  * call launches and stop_event the end time of its last kernel (hipExtLaunchKernel
  * events), so hipEventElapsedTime(start, stop) is the call's time on the device without
@@ -261,19 +261,27 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
 
 /*
  * sq_qk_had_kvquant_ex -- sq_qk_had_kvquant with range clipping of the cache groups
- * (App. A "Quantization choice" compares clipped and unclipped KV quantizers);
- * sq_qk_had_kvquant is this call with k_clip = v_clip = 1.
+ * (App. A "Quantization choice" compares clipped and unclipped KV quantizers) and an fp16
+ * storage of the group parameters; sq_qk_had_kvquant is this call with k_clip = v_clip = 1
+ * and param_bits = 32.
  *   k_clip, v_clip  clipping ratios r, 0 < r <= 1, of the key and value groups: a group is
  *              quantized over [r min, r max] (ends rounded to fp32; for keys the min and max
  *              of the rotated values), codes outside clamp to 0 or L.
  *              Outside (0, 1] (NaN included): SQ_ERR_SHAPE.
+ *   param_bits 32: k_alpha, k_beta, v_alpha, v_beta are fp32 [B, S, H, D/group] (4-byte
+ *              aligned); 16: fp16 of the same shape (2-byte aligned), half the parameter
+ *              bytes of the cache.  fp16 parameters are the fp32 ones rounded to nearest even,
+ *              saturated at +-65504; a group whose fp16 alpha is 0 is constant (alpha 1,
+ *              codes 0); codes are then taken from the stored pair,
+ *              c = clamp(rint((x - beta16) / alpha16), 0, L), each step rounded in fp32.
+ *              Other values: SQ_ERR_UNSUPPORTED.
  * Every other argument, layout and error as sq_qk_had_kvquant.
  */
 sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
                                int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
-                               float k_clip, float v_clip,
-                               void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
-                               uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                               float k_clip, float v_clip, int32_t param_bits,
+                               void* q_rot, uint8_t* k_q, void* k_alpha, void* k_beta,
+                               uint8_t* v_q, void* v_alpha, void* v_beta, float* dbg_k_rot,
                                void* stream);
 
 /*
@@ -296,6 +304,18 @@ sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
 sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
                              const uint8_t* v_q, const float* v_alpha, const float* v_beta,
                              int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream);
+
+/*
+ * sq_attn_decode_kv4_ex -- sq_attn_decode_kv4 over a cache whose group parameters are stored
+ * as written by sq_qk_had_kvquant_ex with the same param_bits (32: fp32, 16: fp16 [B, S, H],
+ * aligned to their size); sq_attn_decode_kv4 is this call with param_bits = 32.
+ * Other param_bits: SQ_ERR_UNSUPPORTED.  Every other argument, layout and error as
+ * sq_attn_decode_kv4.
+ */
+sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                                const uint8_t* v_q, const void* v_alpha, const void* v_beta,
+                                int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
+                                void* out, void* stream);
 
 #ifdef __cplusplus
 }

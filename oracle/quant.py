@@ -46,6 +46,20 @@ def to_fp16_sat(x: np.ndarray) -> np.ndarray:
     return np.clip(np.asarray(x, dtype=F32), -F16_MAX, F16_MAX).astype(np.float16)
 
 
+def asym_codes(v: np.ndarray, alpha: np.ndarray, beta: np.ndarray, bits: int = 4,
+               group: int | None = None) -> np.ndarray:
+    """Codes of eq. 1 for given per-group parameters (fp32 or fp16 arrays [..., K/group]):
+    inv = fl32(1 / alpha), q = clamp(rint(fl32(fl32(v - beta) * inv)), 0, 2^N - 1)."""
+    v32 = np.asarray(v, dtype=F32)
+    group = v32.shape[-1] if group is None else group
+    g = _groups(v32, group)
+    a32 = np.asarray(alpha).astype(F32).reshape(g.shape[:-1])
+    b32 = np.asarray(beta).astype(F32).reshape(g.shape[:-1])
+    inv = (F32(1) / a32).astype(F32)
+    t = ((g - b32[..., None]).astype(F32) * inv[..., None]).astype(F32)
+    return np.clip(np.rint(t), 0, 2 ** bits - 1).astype(np.int64).reshape(v32.shape)
+
+
 def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: float = 1.0,
                param_fp16: bool = False):
     """Asymmetric min-max quantization of eq. 1 over contiguous groups of the last axis.
@@ -76,15 +90,9 @@ def quant_asym(v: np.ndarray, bits: int = 4, group: int | None = None, clip: flo
         a16 = to_fp16_sat(alpha)
         a16 = np.where((alpha < TINY) | (a16 == 0), np.float16(1), a16).astype(np.float16)
         b16 = to_fp16_sat(mn)
-        inv = (F32(1) / a16.astype(F32)).astype(F32)
-        t = ((g - b16.astype(F32)[..., None]).astype(F32) * inv[..., None]).astype(F32)
-        q = np.clip(np.rint(t), 0, levels).astype(np.int64)
-        return q.reshape(v32.shape), a16, b16
+        return asym_codes(v32, a16, b16, bits, group), a16, b16
     alpha = np.where(alpha < TINY, F32(1), alpha).astype(F32)
-    inv = (F32(1) / alpha).astype(F32)
-    t = ((g - mn[..., None]).astype(F32) * inv[..., None]).astype(F32)
-    q = np.clip(np.rint(t), 0, levels).astype(np.int64)
-    return q.reshape(v32.shape), alpha, mn.astype(F32)
+    return asym_codes(v32, alpha, mn, bits, group), alpha, mn.astype(F32)
 
 
 def quant_sym(v: np.ndarray, bits: int = 4, group: int | None = None):

@@ -19,6 +19,7 @@
 //     pa = sum_t p_t alpha_t and bsum = sum_t p_t beta_t; dim d is acc_d - 1024 pa + bsum.
 //   * At the end the 16 token slots of a wave add up in registers (same maximum), and the 16
 //     waves merge in LDS; out_d = (sum of the waves' rescaled dims) / (their rescaled l).
+// The group parameters are fp32, or fp16 (P16: half the parameter bytes of the cache).
 // Workgroup i serves head index x(i) = (i % 8) * (G / 8) + i / 8 when the G = B * H heads
 // are a multiple of 8: workgroups go round-robin over the 8 XCDs, so heads h and h + 1 (the
 // two 64-byte halves of a 128-byte line of a token) are read through the same L2.
@@ -69,6 +70,7 @@ __device__ __forceinline__ float rescale(float a, float b) {
   return a == -INFINITY ? 0.0f : exp2f(__fsub_rn(a, b));
 }
 
+template <bool P16>
 __global__ void __launch_bounds__(kThreads)
 attn_decode_kv4(AttnArgs a) {
   __shared__ float red_ml[kWaves][2];
@@ -112,7 +114,7 @@ attn_decode_kv4(AttnArgs a) {
   const int64_t cspan = ((S - 1) * a.H + 1) * 64;
   const __amdgpu_buffer_rsrc_t rk = rsrc(a.kq + row0 * 64, cspan);
   const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, cspan);
-  const float* pb = (qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb) + row0;  // this lane's scale
+  const void* pb = qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb;  // this lane's scale array
   // token offsets fit 32 bits: S * H * 64 < 2^31 is checked on the host
   const uint32_t H32 = static_cast<uint32_t>(a.H), S32 = static_cast<uint32_t>(S);
   const uint32_t cstride = H32 * 64;
@@ -127,7 +129,11 @@ attn_decode_kv4(AttnArgs a) {
     const uint32_t co = ok ? t * cstride + 16 * qd : 0x80000000u;
     kc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rk, co, 0, 0));
     vc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rv, co, 0, 0));
-    pv[slot] = pb[ok ? t * H32 : 0u];
+    const int64_t pi = row0 + (ok ? t * H32 : 0u);
+    if constexpr (P16)
+      pv[slot] = h2f(static_cast<const uint16_t*>(pb)[pi]);
+    else
+      pv[slot] = static_cast<const float*>(pb)[pi];
   };
 
   float m = -INFINITY, l = 0.0f, bsum = 0.0f, pa_sum = 0.0f;
@@ -240,7 +246,8 @@ attn_decode_kv4(AttnArgs a) {
 
 hipError_t launch_attn_decode_kv4(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = static_cast<unsigned>(a.B * a.H);
-  return launch(attn_decode_kv4, dim3(blocks), dim3(kThreads), 0, stream, a);
+  return a.param16 ? launch(attn_decode_kv4<true>, dim3(blocks), dim3(kThreads), 0, stream, a)
+                   : launch(attn_decode_kv4<false>, dim3(blocks), dim3(kThreads), 0, stream, a);
 }
 
 }  // namespace sq

@@ -16,8 +16,14 @@
 // A clipping ratio r in (0, 1] per cache (App. A "Quantization choice") quantizes each
 // group's range [r min, r max]; the code argument is clamped to [0, L] before the
 // conversion (which by itself saturates at 255 only), so values outside take the end codes.
+// P16 stores alpha and beta as fp16: the fp32 pair (of the reported values) rounded to
+// nearest with saturation, a zero fp16 alpha making the group constant, and the codes taken
+// from the stored pair (V: fl(fl(v - beta16) * fl(1/alpha16)) as eq. 1's steps; K: one fma
+// in the unscaled domain).
 #include "sq_device.h"
 #include "sq_internal.h"
+
+#include <type_traits>
 
 namespace sq {
 namespace {
@@ -78,9 +84,9 @@ __device__ __forceinline__ void fwht128(float (&e)[32], int j) {
 // (1 when e holds the values themselves, and then the codes follow eq. 1 step by step).
 // 4-bit: element 32*k + 8*j + q -> nibble of byte 16*k + 4*j + q/2 of the group's 64 bytes;
 // 8-bit: -> byte 32*k + 8*j + q of its 128 bytes.
-template <bool EXACT, int BITS>
+template <bool EXACT, int BITS, bool P16>
 __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float scale, float clip, int64_t grp,
-                                            uint8_t* q, float* alpha, float* beta) {
+                                            uint8_t* q, void* alpha, void* beta) {
   float mn = e[0], mx = e[0];
 #pragma unroll
   for (int r = 1; r < 32; ++r) {
@@ -95,9 +101,24 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
   // alpha of the reported (scaled) values decides the constant-group case
   const float r_u = __fsub_rn(mx, mn);
   const float a_u = __fdiv_rn(r_u, kL);
-  const bool cst = __fmul_rn(a_u, scale) < kMinNormal;
-  const float inv = cst ? 1.0f : __fdiv_rn(1.0f, a_u);
-  const float nb = -__fmul_rn(mn, inv);
+  const float a_s = __fmul_rn(a_u, scale);
+  float inv, nb, mn_t = mn;  // code argument: fma(v, inv, nb), or (v - mn_t) * inv (EXACT)
+  uint16_t a16 = 0, b16 = 0;
+  bool cst;
+  if constexpr (P16) {
+    a16 = f2h_sat(a_s);
+    cst = a_s < kMinNormal || (a16 & 0x7FFFu) == 0;
+    if (cst) a16 = 0x3C00u;  // 1.0
+    b16 = f2h_sat(__fmul_rn(mn, scale));
+    const float inv16 = __fdiv_rn(1.0f, h2f(a16));
+    mn_t = h2f(b16);  // EXACT: scale is 1
+    inv = EXACT ? inv16 : __fmul_rn(scale, inv16);
+    nb = -__fmul_rn(mn_t, inv16);
+  } else {
+    cst = a_s < kMinNormal;
+    inv = cst ? 1.0f : __fdiv_rn(1.0f, a_u);
+    nb = -__fmul_rn(mn, inv);
+  }
   uint8_t* qg = q + grp * (kD * BITS / 8);
   if constexpr (BITS == 8) {
 #pragma unroll
@@ -106,7 +127,7 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
 #pragma unroll
       for (int x = 0; x < 8; ++x) {
         const float v = e[8 * k + x];
-        const float t = EXACT ? __fmul_rn(__fsub_rn(v, mn), inv) : __fmaf_rn(v, inv, nb);
+        const float t = EXACT ? __fmul_rn(__fsub_rn(v, mn_t), inv) : __fmaf_rn(v, inv, nb);
         w[x >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(t, 0.0f, kL), x & 3, w[x >> 2]);
       }
       *reinterpret_cast<uint2*>(qg + 32 * k + 8 * j) = make_uint2(w[0], w[1]);
@@ -120,8 +141,8 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
     for (int i = 0; i < 4; ++i) {
       float t0, t1;
       if constexpr (EXACT) {
-        t0 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i], mn), inv);
-        t1 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i + 1], mn), inv);
+        t0 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i], mn_t), inv);
+        t1 = __fmul_rn(__fsub_rn(e[8 * k + 2 * i + 1], mn_t), inv);
       } else {
         t0 = __fmaf_rn(e[8 * k + 2 * i], inv, nb);
         t1 = __fmaf_rn(e[8 * k + 2 * i + 1], inv, nb);
@@ -133,8 +154,13 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
     *reinterpret_cast<uint32_t*>(qg + 16 * k + 4 * j) = ev | (od << 4);
   }
   if (j == 0) {
-    alpha[grp] = cst ? 1.0f : __fmul_rn(a_u, scale);
-    beta[grp] = __fmul_rn(mn, scale);
+    if constexpr (P16) {
+      static_cast<uint16_t*>(alpha)[grp] = a16;
+      static_cast<uint16_t*>(beta)[grp] = b16;
+    } else {
+      static_cast<float*>(alpha)[grp] = cst ? 1.0f : a_s;
+      static_cast<float*>(beta)[grp] = __fmul_rn(mn, scale);
+    }
   }
 }
 
@@ -143,7 +169,7 @@ __device__ __forceinline__ void quant_store(const float (&e)[32], int j, float s
 // itself).  That takes 97 VGPRs (4 waves per SIMD); it pays when the grid has more
 // workgroups than that occupancy holds, and otherwise each vector is loaded just before its
 // transform.
-template <bool EARLY, int BITS>
+template <bool EARLY, int BITS, bool P16>
 __global__ void __launch_bounds__(kThreads)
 qk_had_kvquant_v2(KvArgs a) {
   const int64_t grp = (static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x) / 4;
@@ -181,12 +207,12 @@ qk_had_kvquant_v2(KvArgs a) {
 #pragma unroll
       for (int q = 0; q < 8; ++q) a.dbg_k[base + 32 * k + 8 * j + q] = __fmul_rn(e[8 * k + q], a.inv_sqrt_d);
   }
-  quant_store<false, BITS>(e, j, a.inv_sqrt_d, a.k_clip, grp, a.kq, a.ka, a.kb);
+  quant_store<false, BITS, P16>(e, j, a.inv_sqrt_d, a.k_clip, grp, a.kq, a.ka, a.kb);
 
   // V: quantize
   if constexpr (!EARLY) load_raw(a.v + base, j, rv);
   widen(rv, e);
-  quant_store<true, BITS>(e, j, 1.0f, a.v_clip, grp, a.vq, a.va, a.vb);
+  quant_store<true, BITS, P16>(e, j, 1.0f, a.v_clip, grp, a.vq, a.va, a.vb);
 }
 
 }  // namespace
@@ -197,11 +223,16 @@ hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream) {
   // Measured on MI355X: [8, 2048, 32, 128] (8192 workgroups) 112 vs 118 us with the early
   // loads; [1, 2048, 32, 128] (1024 workgroups, 4 per CU) 13.6 vs 15.1 us without them.
   const bool early = blocks >= 16 * 256;
-  if (a.bits == 8)
-    return early ? launch(qk_had_kvquant_v2<true, 8>, dim3(blocks), dim3(kThreads), 0, stream, a)
-                 : launch(qk_had_kvquant_v2<false, 8>, dim3(blocks), dim3(kThreads), 0, stream, a);
-  return early ? launch(qk_had_kvquant_v2<true, 4>, dim3(blocks), dim3(kThreads), 0, stream, a)
-               : launch(qk_had_kvquant_v2<false, 4>, dim3(blocks), dim3(kThreads), 0, stream, a);
+  const dim3 grid(blocks), block(kThreads);
+  auto go = [&](auto early_c, auto p16_c) -> hipError_t {
+    constexpr bool E = decltype(early_c)::value, P = decltype(p16_c)::value;
+    return a.bits == 8 ? launch(qk_had_kvquant_v2<E, 8, P>, grid, block, 0, stream, a)
+                       : launch(qk_had_kvquant_v2<E, 4, P>, grid, block, 0, stream, a);
+  };
+  using T = std::true_type;
+  using N = std::false_type;
+  if (a.param16) return early ? go(T{}, T{}) : go(N{}, T{});
+  return early ? go(T{}, N{}) : go(N{}, N{});
 }
 
 }  // namespace sq

@@ -348,9 +348,9 @@ sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const f
 
 sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
                                int64_t B, int64_t S, int64_t H, int64_t D, int32_t bits, int32_t group,
-                               float k_clip, float v_clip,
-                               void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
-                               uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
+                               float k_clip, float v_clip, int32_t param_bits,
+                               void* q_rot, uint8_t* k_q, void* k_alpha, void* k_beta,
+                               uint8_t* v_q, void* v_alpha, void* v_beta, float* dbg_k_rot,
                                void* stream) {
   TimingScope timing_scope;
   if (!q || !k || !v || !q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta)
@@ -361,17 +361,21 @@ sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
   if (group != 128) return fail(SQ_ERR_UNSUPPORTED, "group=%d: only group 128 (= D) is implemented", group);
   sq_status s = check_clip(k_clip, "k_clip");
   if (s != SQ_OK || (s = check_clip(v_clip, "v_clip")) != SQ_OK) return s;
+  if (param_bits != 32 && param_bits != 16)
+    return fail(SQ_ERR_UNSUPPORTED, "param_bits=%d: fp32 (32) and fp16 (16) group parameters are implemented",
+                param_bits);
   const uint64_t groups = static_cast<uint64_t>(B) * static_cast<uint64_t>(S) * static_cast<uint64_t>(H);
   if (groups > (uint64_t{1} << 40)) return fail(SQ_ERR_SHAPE, "B*S*H too large");
+  const uint64_t pb = static_cast<uint64_t>(param_bits / 8);  // bytes per group parameter
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(q_rot, 16) || !aligned(k_q, 16) ||
-      !aligned(v_q, 16) || !aligned(k_alpha, 4) || !aligned(k_beta, 4) || !aligned(v_alpha, 4) ||
-      !aligned(v_beta, 4) || (dbg_k_rot && !aligned(dbg_k_rot, 4)))
-    return fail(SQ_ERR_ALIGN, "tensors need 16-byte, scales 4-byte alignment");
+      !aligned(v_q, 16) || !aligned(k_alpha, pb) || !aligned(k_beta, pb) || !aligned(v_alpha, pb) ||
+      !aligned(v_beta, pb) || (dbg_k_rot && !aligned(dbg_k_rot, 4)))
+    return fail(SQ_ERR_ALIGN, "tensors need 16-byte alignment, group parameters their own size");
   const uint64_t E = groups * 128;
   s = check_alias({{q, E * 2, "q"}, {k, E * 2, "k"}, {v, E * 2, "v"}},
-                            {{q_rot, E * 2, "q_rot"}, {k_q, E * bits / 8, "k_q"}, {k_alpha, groups * 4, "k_alpha"},
-                             {k_beta, groups * 4, "k_beta"}, {v_q, E * bits / 8, "v_q"}, {v_alpha, groups * 4, "v_alpha"},
-                             {v_beta, groups * 4, "v_beta"}, {dbg_k_rot, dbg_k_rot ? E * 4 : 0, "dbg_k_rot"}});
+                  {{q_rot, E * 2, "q_rot"}, {k_q, E * bits / 8, "k_q"}, {k_alpha, groups * pb, "k_alpha"},
+                   {k_beta, groups * pb, "k_beta"}, {v_q, E * bits / 8, "v_q"}, {v_alpha, groups * pb, "v_alpha"},
+                   {v_beta, groups * pb, "v_beta"}, {dbg_k_rot, dbg_k_rot ? E * 4 : 0, "dbg_k_rot"}});
   if (s != SQ_OK) return s;
   if (groups == 0) return ok();
   sq::KvArgs a{};
@@ -391,6 +395,7 @@ sq_status sq_qk_had_kvquant_ex(const void* q, const void* k, const void* v,
   a.bits = bits;
   a.k_clip = k_clip;
   a.v_clip = v_clip;
+  a.param16 = param_bits == 16;
   return hip_status(sq::launch_qk_had_kvquant(a, static_cast<hipStream_t>(stream)), "qk_had_kvquant launch");
 }
 
@@ -399,13 +404,14 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                             void* q_rot, uint8_t* k_q, float* k_alpha, float* k_beta,
                             uint8_t* v_q, float* v_alpha, float* v_beta, float* dbg_k_rot,
                             void* stream) {
-  return sq_qk_had_kvquant_ex(q, k, v, B, S, H, D, bits, group, 1.0f, 1.0f, q_rot, k_q, k_alpha, k_beta, v_q,
+  return sq_qk_had_kvquant_ex(q, k, v, B, S, H, D, bits, group, 1.0f, 1.0f, 32, q_rot, k_q, k_alpha, k_beta, v_q,
                               v_alpha, v_beta, dbg_k_rot, stream);
 }
 
-sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
-                             const uint8_t* v_q, const float* v_alpha, const float* v_beta,
-                             int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream) {
+sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                                const uint8_t* v_q, const void* v_alpha, const void* v_beta,
+                                int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
+                                void* out, void* stream) {
   TimingScope timing_scope;
   if (!q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta || !out)
     return fail(SQ_ERR_NULL, "q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta and out are required");
@@ -414,14 +420,18 @@ sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float*
   if (B * H >= (int64_t{1} << 31) || S >= (int64_t{1} << 31) / (H * 64))
     return fail(SQ_ERR_SHAPE, "B*H=%lld or S*H*64 beyond 2^31", (long long)(B * H));
   if (!(std::fabs(scale) < 3.0e38f)) return fail(SQ_ERR_SHAPE, "scale must be finite");
-  if (!aligned(q_rot, 16) || !aligned(k_q, 16) || !aligned(v_q, 16) || !aligned(out, 16) || !aligned(k_alpha, 4) ||
-      !aligned(k_beta, 4) || !aligned(v_alpha, 4) || !aligned(v_beta, 4))
-    return fail(SQ_ERR_ALIGN, "q_rot, k_q, v_q and out need 16-byte, scales 4-byte alignment");
+  if (param_bits != 32 && param_bits != 16)
+    return fail(SQ_ERR_UNSUPPORTED, "param_bits=%d: fp32 (32) and fp16 (16) group parameters are implemented",
+                param_bits);
+  const uint64_t pb = static_cast<uint64_t>(param_bits / 8);
+  if (!aligned(q_rot, 16) || !aligned(k_q, 16) || !aligned(v_q, 16) || !aligned(out, 16) || !aligned(k_alpha, pb) ||
+      !aligned(k_beta, pb) || !aligned(v_alpha, pb) || !aligned(v_beta, pb))
+    return fail(SQ_ERR_ALIGN, "q_rot, k_q, v_q and out need 16-byte alignment, group parameters their own size");
   const uint64_t heads = static_cast<uint64_t>(B) * static_cast<uint64_t>(H);
   const uint64_t cache = heads * static_cast<uint64_t>(S);
   sq_status s = check_alias({{q_rot, heads * 256, "q_rot"}, {k_q, cache * 64, "k_q"}, {v_q, cache * 64, "v_q"},
-                             {k_alpha, cache * 4, "k_alpha"}, {k_beta, cache * 4, "k_beta"},
-                             {v_alpha, cache * 4, "v_alpha"}, {v_beta, cache * 4, "v_beta"}},
+                             {k_alpha, cache * pb, "k_alpha"}, {k_beta, cache * pb, "k_beta"},
+                             {v_alpha, cache * pb, "v_alpha"}, {v_beta, cache * pb, "v_beta"}},
                             {{out, heads * 256, "out"}});
   if (s != SQ_OK) return s;
   if (B == 0) return ok();
@@ -437,8 +447,15 @@ sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float*
   a.S = S;
   a.H = H;
   a.scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
+  a.param16 = param_bits == 16;
   a.out = static_cast<uint16_t*>(out);
   return hip_status(sq::launch_attn_decode_kv4(a, static_cast<hipStream_t>(stream)), "attn_decode_kv4 launch");
+}
+
+sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
+                             const uint8_t* v_q, const float* v_alpha, const float* v_beta,
+                             int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream) {
+  return sq_attn_decode_kv4_ex(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, B, S, H, D, scale, 32, out, stream);
 }
 
 }  // extern "C"

@@ -17,6 +17,10 @@ __device__ __forceinline__ float h2f(uint16_t bits) {
 __device__ __forceinline__ uint16_t f2h(float v) {
   return __half_as_ushort(__float2half_rn(v));
 }
+// fp16 bits of v rounded to nearest even, saturating at +-65504 (the largest finite fp16)
+__device__ __forceinline__ uint16_t f2h_sat(float v) {
+  return f2h(fminf(fmaxf(v, -65504.0f), 65504.0f));
+}
 
 // Smallest normal fp32 (2^-126).  A group whose alpha would fall below it (zero or
 // subnormal: a constant group, or a range under L * 2^-126) is quantized as constant with

@@ -69,11 +69,12 @@ hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream);
 struct AttnArgs {
   const uint16_t* q;     // fp16 [B, H, 128], R3-rotated query of the new token
   const uint8_t* kq;     // [B, S, H, 64] packed 4-bit codes
-  const float* ka;       // [B, S, H]
-  const float* kb;
+  const void* ka;        // [B, S, H] group parameters: fp32, or fp16 bits when param16
+  const void* kb;
   const uint8_t* vq;
-  const float* va;
-  const float* vb;
+  const void* va;
+  const void* vb;
+  int param16;
   int64_t B, S, H;       // S * H * 64 < 2^31 (32-bit buffer offsets per head)
   float scale_log2e;     // score scale times log2(e)
   uint16_t* out;         // fp16 [B, H, 128]
@@ -89,15 +90,16 @@ struct KvArgs {
   float inv_sqrt_d;
   uint16_t* q_rot;
   uint8_t* kq;
-  float* ka;
-  float* kb;
+  void* ka;              // group parameters: fp32, or fp16 bits when param16
+  void* kb;
   uint8_t* vq;
-  float* va;
-  float* vb;
+  void* va;
+  void* vb;
   float* dbg_k;
   int bits;              // cache codes: 4 (two per byte) or 8 (one per byte)
   float k_clip = 1.0f;   // range clipping ratios of the K and V groups, in (0, 1]
   float v_clip = 1.0f;
+  int param16 = 0;       // 1: alpha and beta stored as fp16
 };
 
 hipError_t launch_qk_had_kvquant(const KvArgs& a, hipStream_t stream);

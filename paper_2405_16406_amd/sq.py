@@ -21,7 +21,8 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
 
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
            "sq_had_quant_act_ex", "sq_pack_w4", "sq_pack_w4_ex", "sq_w4a4_linear", "sq_w4a8_linear",
-           "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_qk_had_kvquant_ex", "sq_attn_decode_kv4")
+           "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_qk_had_kvquant_ex", "sq_attn_decode_kv4",
+           "sq_attn_decode_kv4_ex")
 
 
 class SqError(RuntimeError):
@@ -72,10 +73,12 @@ def lib() -> ctypes.CDLL:
     L.sq_qk_had_kvquant.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32,
                                     _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.sq_qk_had_kvquant_ex.restype = _I32
-    L.sq_qk_had_kvquant_ex.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _F32, _F32,
+    L.sq_qk_had_kvquant_ex.argtypes = [_P, _P, _P, _I64, _I64, _I64, _I64, _I32, _I32, _F32, _F32, _I32,
                                        _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.sq_attn_decode_kv4.restype = _I32
     L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _P, _P]
+    L.sq_attn_decode_kv4_ex.restype = _I32
+    L.sq_attn_decode_kv4_ex.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32, _P, _P]
     _lib = L
     return L
 
@@ -252,11 +255,13 @@ def interleave_gate_up(gate: torch.Tensor, up: torch.Tensor) -> torch.Tensor:
 
 
 def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4, k_clip: float = 1.0,
-                   v_clip: float = 1.0):
+                   v_clip: float = 1.0, param_dtype=torch.float32):
     """R3 on Q and K per head (D = 128) + 4-bit (or 8-bit) asymmetric K/V quantization, group 128.
 
-    k_clip, v_clip: range clipping ratios in (0, 1] (other than 1: sq_qk_had_kvquant_ex).
-    Returns dict(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, k_rot (or None)).
+    k_clip, v_clip: range clipping ratios in (0, 1]; param_dtype torch.float32 or
+    torch.float16 for the group parameters (either away from the default:
+    sq_qk_had_kvquant_ex).  Returns dict(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta,
+    k_rot (or None)).
     """
     for t, nme in ((q, "q"), (k, "k"), (v, "v")):
         _need(t, torch.float16, nme)
@@ -267,19 +272,22 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4, k_clip: 
     if out is None:
         out = dict(q_rot=torch.empty_like(q),
                    k_q=torch.empty((B, S, H, D * bits // 8), dtype=torch.uint8, device=dev),
-                   k_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
-                   k_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
+                   k_alpha=torch.empty((B, S, H, 1), dtype=param_dtype, device=dev),
+                   k_beta=torch.empty((B, S, H, 1), dtype=param_dtype, device=dev),
                    v_q=torch.empty((B, S, H, D * bits // 8), dtype=torch.uint8, device=dev),
-                   v_alpha=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev),
-                   v_beta=torch.empty((B, S, H, 1), dtype=torch.float32, device=dev))
+                   v_alpha=torch.empty((B, S, H, 1), dtype=param_dtype, device=dev),
+                   v_beta=torch.empty((B, S, H, 1), dtype=param_dtype, device=dev))
+    pbits = {torch.float32: 32, torch.float16: 16}[param_dtype]
+    for nme in ("k_alpha", "k_beta", "v_alpha", "v_beta"):
+        _need(out[nme], param_dtype, nme)
     kr = torch.empty((B, S, H, D), dtype=torch.float32, device=dev) if dbg else None
     outs = (_ptr(out["q_rot"]), _ptr(out["k_q"]), _ptr(out["k_alpha"]), _ptr(out["k_beta"]), _ptr(out["v_q"]),
             _ptr(out["v_alpha"]), _ptr(out["v_beta"]), _ptr(kr), _stream(q))
-    if k_clip == 1.0 and v_clip == 1.0:
+    if k_clip == 1.0 and v_clip == 1.0 and pbits == 32:
         _check(lib().sq_qk_had_kvquant(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128, *outs), "sq_qk_had_kvquant")
     else:
         _check(lib().sq_qk_had_kvquant_ex(_ptr(q), _ptr(k), _ptr(v), B, S, H, D, bits, 128, float(k_clip),
-                                          float(v_clip), *outs), "sq_qk_had_kvquant_ex")
+                                          float(v_clip), pbits, *outs), "sq_qk_had_kvquant_ex")
     out = dict(out)
     out["k_rot"] = kr
     return out
@@ -287,8 +295,8 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4, k_clip: 
 
 def attn_decode_kv4(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None, out=None):
     """Attention of one rotated query per (batch, head), q_rot fp16 [B, H, 128], over the
-    4-bit cache of qk_had_kvquant (k_q, v_q uint8 [B, S, H, 64], scales fp32 [B, S, H(, 1)]).
-    Returns out fp16 [B, H, 128]."""
+    4-bit cache of qk_had_kvquant (k_q, v_q uint8 [B, S, H, 64], group parameters fp32, or
+    fp16 through sq_attn_decode_kv4_ex, [B, S, H(, 1)]).  Returns out fp16 [B, H, 128]."""
     _need(q_rot, torch.float16, "q_rot")
     for t, nme in ((q_rot, "q_rot"), (k_q, "k_q"), (v_q, "v_q"), (k_alpha, "k_alpha"), (k_beta, "k_beta"),
                    (v_alpha, "v_alpha"), (v_beta, "v_beta")):
@@ -298,7 +306,16 @@ def attn_decode_kv4(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=Non
     S = k_q.shape[1]
     scale = 1.0 / D ** 0.5 if scale is None else scale
     out = torch.empty_like(q_rot) if out is None else out
-    _check(lib().sq_attn_decode_kv4(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q), _ptr(v_alpha),
-                                    _ptr(v_beta), B, S, H, D, float(scale), _ptr(out), _stream(q_rot)),
-           "sq_attn_decode_kv4")
+    pdt = k_alpha.dtype
+    for t, nme in ((k_alpha, "k_alpha"), (k_beta, "k_beta"), (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        _need(t, pdt, nme)
+    if pdt == torch.float32:
+        _check(lib().sq_attn_decode_kv4(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q),
+                                        _ptr(v_alpha), _ptr(v_beta), B, S, H, D, float(scale), _ptr(out),
+                                        _stream(q_rot)), "sq_attn_decode_kv4")
+    else:
+        _check(lib().sq_attn_decode_kv4_ex(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q),
+                                           _ptr(v_alpha), _ptr(v_beta), B, S, H, D, float(scale),
+                                           {torch.float16: 16}[pdt], _ptr(out), _stream(q_rot)),
+               "sq_attn_decode_kv4_ex")
     return out

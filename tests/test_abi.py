@@ -246,13 +246,13 @@ def test_pack_w4_ex_validation(L):
     assert call(N=0, signs=None) == sq.SQ_OK
 
 
-def kvq_ex(L, B=1, S=2, H=2, D=128, bits=4, group=128, k_clip=1.0, v_clip=1.0, **kw):
+def kvq_ex(L, B=1, S=2, H=2, D=128, bits=4, group=128, k_clip=1.0, v_clip=1.0, pbits=32, **kw):
     ptrs = [fake(i) for i in range(10)]
     for i, nm in enumerate(("q", "k", "v", "qr", "kq", "ka", "kb", "vq", "va", "vb")):
         if nm in kw:
             ptrs[i] = kw[nm]
     return L.sq_qk_had_kvquant_ex(ptrs[0], ptrs[1], ptrs[2], B, S, H, D, bits, group, ctypes.c_float(k_clip),
-                                  ctypes.c_float(v_clip), *ptrs[3:], None, None)
+                                  ctypes.c_float(v_clip), pbits, *ptrs[3:], None, None)
 
 
 def test_kv_ex_validation(L):
@@ -263,3 +263,26 @@ def test_kv_ex_validation(L):
         assert kvq_ex(L, v_clip=r) == sq.SQ_ERR_SHAPE
     assert kvq_ex(L, qr=fake(0)) == sq.SQ_ERR_ALIAS
     assert kvq_ex(L, B=0, k_clip=0.95, v_clip=0.95) == sq.SQ_OK
+    # group parameters: fp32 or fp16, aligned to their own size
+    assert kvq_ex(L, pbits=8) == sq.SQ_ERR_UNSUPPORTED
+    odd2 = ctypes.c_void_p(fake(5).value + 2)
+    assert kvq_ex(L, ka=odd2) == sq.SQ_ERR_ALIGN
+    assert kvq_ex(L, B=0, pbits=16, ka=odd2) == sq.SQ_OK
+    assert kvq_ex(L, pbits=16, ka=ctypes.c_void_p(fake(5).value + 1)) == sq.SQ_ERR_ALIGN
+    # fp16 parameters take half the bytes: 4 groups x 2 bytes end where fp32 ones would not
+    assert kvq_ex(L, kb=ctypes.c_void_p(fake(5).value + 8)) == sq.SQ_ERR_ALIAS
+    assert kvq_ex(L, B=0, pbits=16, kb=ctypes.c_void_p(fake(5).value + 8)) == sq.SQ_OK
+
+
+def test_attn_decode_ex_validation(L):
+    def call(pbits=32, B=2, **kw):
+        ptrs = [fake(i) for i in range(8)]
+        for i, nm in enumerate(("q", "kq", "ka", "kb", "vq", "va", "vb", "out")):
+            if nm in kw:
+                ptrs[i] = kw[nm]
+        return L.sq_attn_decode_kv4_ex(*ptrs[:7], B, 4, 2, 128, ctypes.c_float(0.1), pbits, ptrs[7], None)
+    assert call(out=None) == sq.SQ_ERR_NULL
+    assert call(pbits=0) == sq.SQ_ERR_UNSUPPORTED
+    assert call(va=ctypes.c_void_p(fake(5).value + 2)) == sq.SQ_ERR_ALIGN
+    assert call(B=0, pbits=16, va=ctypes.c_void_p(fake(5).value + 2)) == sq.SQ_OK
+    assert call(out=ctypes.c_void_p(fake(2).value)) == sq.SQ_ERR_ALIAS

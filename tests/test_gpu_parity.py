@@ -756,6 +756,54 @@ def test_kv_clipped(bits):
     assert np.all(vc.max(-1) == L) and np.all(vc.min(-1) == 0)
 
 
+@pytest.mark.parametrize("bits", [4, 8])
+def test_kv_fp16_params(bits):
+    # fp16 group parameters: V bit-exact (parameters and codes); K parameters within one fp16
+    # step of the oracle's (the rotation's fp32 rounding can tip the fp16 rounding), and K
+    # codes those of the oracle's quantizer applied with the GPU's own stored pair
+    say(f"qk_had_kvquant_ex {bits}-bit fp16 parameters [2,16,4,128] and [1,3,5,128], v_clip 0.95")
+    for shape in ((2, 16, 4, 128), (1, 3, 5, 128)):
+        q, k, v = workloads.kv_inputs(*shape)
+        out = sq.qk_had_kvquant(dev(q), dev(k), dev(v), dbg=True, bits=bits, v_clip=0.95,
+                                param_dtype=torch.float16)
+        g = {n: host(t) for n, t in out.items() if t is not None}
+        o = okv.qk_had_kvquant(q, k, v, bits=bits, v_clip=0.95, param_fp16=True)
+        for nm in ("k_alpha", "k_beta", "v_alpha", "v_beta"):
+            assert g[nm].dtype == np.float16
+        np.testing.assert_array_equal(g["v_q"], o["v_q"])
+        np.testing.assert_array_equal(g["v_alpha"], o["v_alpha"])
+        np.testing.assert_array_equal(g["v_beta"], o["v_beta"])
+        for nm in ("k_alpha", "k_beta"):
+            gg, oo = g[nm].astype(np.float64), o[nm].astype(np.float64)
+            assert np.all(np.abs(gg - oo) <= np.spacing(np.abs(o[nm])).astype(np.float64)), nm
+        codes = (lambda a: parity.unpack(a, False)) if bits == 4 else (lambda a: a.astype(np.int64))
+        kr = o["k_rot"].reshape(-1, 128)
+        ka, kb = g["k_alpha"].reshape(-1, 1), g["k_beta"].reshape(-1, 1)
+        parity.code_flips(codes(g["k_q"]).reshape(-1, 128), oq.asym_codes(kr, ka, kb, bits), kr,
+                          ka.astype(np.float32), kb.astype(np.float32))
+
+
+def test_attn_decode_fp16_params():
+    # the consumer reads fp16 parameters: a random cache with fp16 parameters against the
+    # oracle, and the whole chain from fp16-parameter KV quantization
+    say("attn_decode_kv4_ex fp16 parameters: random cache [2,300,5], chain [1,257,4]")
+    rng = workloads.rng_for(700)
+    B, S, H = 2, 300, 5
+    kc, vc = rng.integers(0, 16, (B, S, H, 128)), rng.integers(0, 16, (B, S, H, 128))
+    ka, va = (rng.uniform(0.01, 0.2, (B, S, H)).astype(np.float16) for _ in range(2))
+    kb, vb = (rng.uniform(-1.5, 0.0, (B, S, H)).astype(np.float16) for _ in range(2))
+    q = (rng.standard_normal((B, H, 128)) * 2).astype(np.float16)
+    kq, vq = oq.pack_nibbles(kc), oq.pack_nibbles(vc)
+    out = sq.attn_decode_kv4(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb))
+    parity.assert_out_close(host(out), okv.attn_decode(q, kq, ka, kb, vq, va, vb))
+    qh, kh, vh = workloads.kv_inputs(1, 257, 4, 128)
+    o = sq.qk_had_kvquant(dev(qh), dev(kh), dev(vh), param_dtype=torch.float16)
+    qr = o["q_rot"][:, -1].contiguous()
+    cache = [o[n] for n in ("k_q", "k_alpha", "k_beta", "v_q", "v_alpha", "v_beta")]
+    got = host(sq.attn_decode_kv4(qr, *cache))
+    parity.assert_out_close(got, okv.attn_decode(host(qr), *[host(t) for t in cache]))
+
+
 def test_kv8_small_and_sampled():
     # KV8: the same kernel storing one 8-bit code per byte
     say("qk_had_kvquant 8-bit [2,16,4,128], [1,3,5,128] and [8,2048,32,128] sampled")
