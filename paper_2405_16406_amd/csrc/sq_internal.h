@@ -57,6 +57,7 @@ struct GemmArgs {
   int32_t* dbg_acc;      // optional [M, N]
   int32_t swiglu;        // 1: rows of wq interleave gate and up in blocks of 32 (N % 64 == 0);
                          //    y [M, ldy >= N/2] receives SiLU(gate) * up
+  int32_t a8;            // 1: xq holds 8-bit codes [M, K] (set by the W4A8 launchers)
 };
 
 // hipErrorNotSupported when no kernel covers the arguments (only with swiglu)
@@ -65,6 +66,9 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
 hipError_t launch_w4a8_gemm(const GemmArgs& g, hipStream_t stream);
 // Its decode-sized (M <= 16) weight-streaming kernel; hipErrorNotSupported otherwise.
 hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream);
+// Its prefill kernel on the LDS ring of the W4A4 GEMM; hipErrorNotSupported where the 32-bit
+// buffer offsets do not cover the operands.
+hipError_t launch_w4a8_ring(const GemmArgs& g, hipStream_t stream);
 
 struct AttnArgs {
   const uint16_t* q;     // fp16 [B, H, 128], R3-rotated query of the new token

@@ -180,7 +180,8 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const v16i (&ac
 // Per-tile row and column scales are staged in LDS during the prologue (RingScales).
 template <int BM, int BN>
 struct RingScales {
-  // floats: rowA[BM] (alpha_m / 16), rowB[BM] (beta_m), colS[BN] (s_n), colR[BN] (rs_n), colB[BN] (bias_n)
+  // floats: rowA[BM] (alpha_m / 16), rowB[BM] (beta_m; 8-bit codes: beta_m + 128 alpha_m),
+  // colS[BN] (s_n), colR[BN] (rs_n), colB[BN] (bias_n)
   static constexpr int COUNT = 2 * BM + 3 * BN;
   static constexpr int BYTES = COUNT * 4;
 };
@@ -195,7 +196,8 @@ __device__ __forceinline__ float load_scale(const GemmArgs& g, int idx, int64_t 
   if (idx < 2 * BM) {
     const int64_t m = m0 + (idx % BM);
     if (m >= g.M) return 0.0f;
-    return idx < BM ? __fmul_rn(g.xa[m], 0.0625f) : g.xb[m];
+    if (idx < BM) return __fmul_rn(g.xa[m], 0.0625f);
+    return g.a8 ? __fmaf_rn(128.0f, g.xa[m], g.xb[m]) : g.xb[m];  // 8-bit codes enter as qa - 128
   }
   const int t = idx - 2 * BM;
   const int64_t n = n0 + (t % BN);
@@ -299,7 +301,7 @@ __device__ __forceinline__ void ring_epilogue_checked(const GemmArgs& g, const v
         const float t = __fmul_rn(s, static_cast<float>(acc[i][j][r]));
         const float yv = fp32_result(__fmaf_rn(ra, t, __fmaf_rn(rb, __fmul_rn(s, colR[cl]), colB[cl])));
         g.y[m * g.ldy + n] = f2h(yv);
-        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = acc[i][j][r] >> 4;
+        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = (acc[i][j][r] >> 4) + (g.a8 ? 128 * g.rs[n] : 0);
       }
     }
   }
@@ -598,13 +600,18 @@ w4a4_gemm_tile(GemmArgs g) {
 // which expand into the operands of two MFMA k-steps.  Both operands use the same k-slot
 // order, so the dot product is unchanged.  Rows past M or N and chunks past K are out of the
 // buffer range and land as zeros.
-template <int WAVES_M, int WAVES_N, int TM, int TN, int NS>
+// 8-bit activations (A8, the W4A8 setting): a stage row is 128 code bytes, 8 chunks, and the
+// A blocks are one per 32 rows and (chunk pair p, half H): lane l of the copying wave brings
+// row l % 32, chunk 4p + 2(l / 32) + H, so the lane (c, h) that reads it back holds exactly
+// the 16 codes of k-step (p, H) that the 4-bit expansion gives it (k = 64p + 32h + 16H + e);
+// v_perm_b32 puts them in the same slot order and an xor with 0x80 makes them signed.
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, bool A8 = false>
 struct Ring {
   static constexpr int WAVES = WAVES_M * WAVES_N;
   static constexpr int THREADS = 64 * WAVES;
   static constexpr int BM = WAVES_M * TM * 32;
   static constexpr int BN = WAVES_N * TN * 32;
-  static constexpr int ABLK = BM / 16;  // 1 KB blocks per stage: 32 rows x 2 chunk pairs
+  static constexpr int ABLK = BM / (A8 ? 8 : 16);  // 1 KB blocks per stage: 32 rows x 2 (A8: 4) chunk pairs
   static constexpr int BBLK = BN / 16;
   static constexpr int ADPW = ABLK / WAVES;  // block copies per wave per stage
   static constexpr int DPW = (ABLK + BBLK) / WAVES;
@@ -613,11 +620,21 @@ struct Ring {
   static_assert(NS >= 2 && (NS - 1) * DPW <= 63, "outstanding copies fit the vmcnt counter");
 };
 
-template <int TM, int TN>
+template <int TM, int TN, bool A8 = false>
 struct RingPacked {  // one chunk pair (two k-steps) of the wave's A and B blocks
-  v4u a[TM];
+  v4u a[TM][A8 ? 2 : 1];
   v4u b[TN];
 };
+
+// 16 8-bit activation codes k0..k15 (natural order) -> signed operand in the slot order of
+// the nibble expansion (k0 k2 k4 k6 | k1 k3 k5 k7 | k8 ...)
+__device__ __forceinline__ v4i act8_operand(const v4u d) {
+  const uint32_t f = 0x80808080u;
+  return v4i{static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x06040200u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x07050301u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x06040200u) ^ f),
+             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x07050301u) ^ f)};
+}
 template <int TM, int TN>
 struct RingOps {  // MFMA operands of one k-step
   v4i a[TM];
@@ -625,13 +642,17 @@ struct RingOps {  // MFMA operands of one k-step
 };
 
 // Operands of k-step H (0: dwords 0-1, 1: dwords 2-3) of a packed chunk pair.
-template <int H, int TM, int TN>
-__device__ __forceinline__ void expand_half(const RingPacked<TM, TN>& P, RingOps<TM, TN>& E) {
+template <int H, int TM, int TN, bool A8>
+__device__ __forceinline__ void expand_half(const RingPacked<TM, TN, A8>& P, RingOps<TM, TN>& E) {
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const uint32_t d0 = P.a[i][2 * H], d1 = P.a[i][2 * H + 1];
-    E.a[i] = v4i{static_cast<int>(d0 & 0x0F0F0F0Fu), static_cast<int>((d0 >> 4) & 0x0F0F0F0Fu),
-                 static_cast<int>(d1 & 0x0F0F0F0Fu), static_cast<int>((d1 >> 4) & 0x0F0F0F0Fu)};
+    if constexpr (A8) {
+      E.a[i] = act8_operand(P.a[i][H]);
+    } else {
+      const uint32_t d0 = P.a[i][0][2 * H], d1 = P.a[i][0][2 * H + 1];
+      E.a[i] = v4i{static_cast<int>(d0 & 0x0F0F0F0Fu), static_cast<int>((d0 >> 4) & 0x0F0F0F0Fu),
+                   static_cast<int>(d1 & 0x0F0F0F0Fu), static_cast<int>((d1 >> 4) & 0x0F0F0F0Fu)};
+    }
   }
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
@@ -650,9 +671,9 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
 
 // LDS of a ring kernel with KS groups of waves splitting K: one ring per group (reused at
 // the end for the groups' exchange of partial sums), then the tile's epilogue scales.
-template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int KS>
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int KS, bool A8 = false>
 struct RingLds {
-  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
+  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS, A8>;
   static constexpr int RINGS = KS * NS * R::STAGE;
   static constexpr int XCH = KS == 1 ? 0 : KS * R::WAVES * (TM / 2) * TN * 16 * 64 * 4;
   static constexpr int SCALES = RINGS > XCH ? RINGS : XCH;  // byte offset of the scales
@@ -664,11 +685,11 @@ struct RingLds {
 // leaves the CUs one workgroup each).  At the end each group hands the other the int32
 // partial sums of the half of its block that the other finishes (through LDS; integer
 // sums, so the result is bit-identical to KS = 1), and each finishes half of the rows.
-template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE, int KS>
+template <int WAVES_M, int WAVES_N, int TM, int TN, int NS, int WPE, int KS, bool A8 = false>
 __global__ void __launch_bounds__(64 * WAVES_M * WAVES_N * KS, WPE)
 w4a4_gemm_ring(GemmArgs g) {
-  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS>;
-  using L = RingLds<WAVES_M, WAVES_N, TM, TN, NS, KS>;
+  using R = Ring<WAVES_M, WAVES_N, TM, TN, NS, A8>;
+  using L = RingLds<WAVES_M, WAVES_N, TM, TN, NS, KS, A8>;
   using SC = RingScales<R::BM, R::BN>;
   static_assert(KS == 1 || (KS == 2 && TM % 2 == 0), "K split of two needs an even TM");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -683,13 +704,14 @@ w4a4_gemm_ring(GemmArgs g) {
   const int wm = (wave / WAVES_N) * TM;  // first 32-row group of this wave in the tile
   const int wn = (wave % WAVES_N) * TN;
   const uint32_t KB = static_cast<uint32_t>(g.K / 2);
+  const uint32_t KA = A8 ? 2 * KB : KB;  // activation bytes per row
   // stages per group; the group's stage st is stage st0 + st of the whole K (past K: zeros)
   const int nstage = static_cast<int>(((KB + 63) / 64 + KS - 1) / KS);
   const uint32_t st0 = static_cast<uint32_t>(grp * nstage);
 
-  // Buffer ranges: offsets are 32-bit and (M + BM) * K/2 < 2^31 is checked on the host.
+  // Buffer ranges: offsets are 32-bit and (M + BM) * KA < 2^31 is checked on the host.
   const __amdgpu_buffer_rsrc_t rsa =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.xq), 0, static_cast<int>(g.M * KB), 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.xq), 0, static_cast<int>(g.M * KA), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsb =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(g.wq), 0, static_cast<int>(g.N * KB), 0x00020000);
   // Copy d of this wave is block b = wave + WAVES d of a stage: A blocks first, then B.
@@ -698,9 +720,15 @@ w4a4_gemm_ring(GemmArgs g) {
     constexpr int d = decltype(dc)::value;
     const int b = wave + R::WAVES * d;
     const int bl = d < R::ADPW ? b : b - R::ABLK;
-    const int64_t row = (d < R::ADPW ? m0 : n0) + (bl >> 1) * 32 + (lane & 31);
-    rowoff[d] = static_cast<uint32_t>(row) * KB;
-    colofs[d] = (bl & 1) * 32 + (lane >> 5) * 16;
+    if (A8 && d < R::ADPW) {  // block (row group, p, H): chunk 4p + 2h + H of the 128-byte row
+      const int64_t row = m0 + (bl >> 2) * 32 + (lane & 31);
+      rowoff[d] = static_cast<uint32_t>(row) * KA;
+      colofs[d] = ((bl >> 1) & 1) * 64 + (lane >> 5) * 32 + (bl & 1) * 16;
+    } else {
+      const int64_t row = (d < R::ADPW ? m0 : n0) + (bl >> 1) * 32 + (lane & 31);
+      rowoff[d] = static_cast<uint32_t>(row) * KB;
+      colofs[d] = (bl & 1) * 32 + (lane >> 5) * 16;
+    }
   });
   auto issue = [&](int st) {
     uint8_t* sb = ring + (st % NS) * R::STAGE;
@@ -708,10 +736,11 @@ w4a4_gemm_ring(GemmArgs g) {
     const bool live = st < nstage;
     static_for<R::DPW>([&](auto dc) {
       constexpr int d = decltype(dc)::value;
-      const uint32_t col = k0 + colofs[d];
+      constexpr bool a8blk = A8 && d < R::ADPW;
+      const uint32_t col = (a8blk ? 2 * k0 : k0) + colofs[d];
       // past K, or a stage past the group's end (issued only to keep the copy count
       // uniform; it may lie in the next group's slice): out of range, lands as zeros
-      const uint32_t off = (live && col < KB) ? rowoff[d] + col : 0x80000000u;
+      const uint32_t off = (live && col < (a8blk ? KA : KB)) ? rowoff[d] + col : 0x80000000u;
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
           reinterpret_cast<uintptr_t>(sb + (wave + R::WAVES * d) * 1024));
       if constexpr (d < R::ADPW)
@@ -720,16 +749,23 @@ w4a4_gemm_ring(GemmArgs g) {
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, dst, 16, static_cast<int>(off), 0, 0, 0);
     });
   };
-  auto read = [&](RingPacked<TM, TN>& P, int st, int p) {
-    const uint8_t* sb = ring + (st % NS) * R::STAGE + lane * 16 + p * 1024;
+  auto read = [&](RingPacked<TM, TN, A8>& P, int st, int p) {
+    const uint8_t* sb = ring + (st % NS) * R::STAGE + lane * 16;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) P.a[i] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 2048);
+    for (int i = 0; i < TM; ++i) {
+      if constexpr (A8) {
+        P.a[i][0] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 4096 + (2 * p) * 1024);
+        P.a[i][1] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 4096 + (2 * p + 1) * 1024);
+      } else {
+        P.a[i][0] = *reinterpret_cast<const v4u*>(sb + (wm + i) * 2048 + p * 1024);
+      }
+    }
 #pragma unroll
-    for (int j = 0; j < TN; ++j) P.b[j] = *reinterpret_cast<const v4u*>(sb + (R::ABLK + 2 * (wn + j)) * 1024);
+    for (int j = 0; j < TN; ++j) P.b[j] = *reinterpret_cast<const v4u*>(sb + (R::ABLK + 2 * (wn + j) + p) * 1024);
   };
   // MFMAs of one k-step from E, with the next k-step's operands expanded into F in between
   constexpr int NM = TM * TN;
-  constexpr int NV = 6 * (TM + TN);
+  constexpr int NV = (A8 ? 8 : 6) * TM + 6 * TN;
   constexpr int PER = (NV + NM - 2) / (NM - 1);
   auto mma = [&](v16i (&acc)[TM][TN], const RingOps<TM, TN>& E) {
 #pragma unroll
@@ -785,7 +821,7 @@ w4a4_gemm_ring(GemmArgs g) {
     if (idx < SC::COUNT) scales[idx] = sv[u];
   }
   issue(NS - 1);
-  RingPacked<TM, TN> P0, P1;
+  RingPacked<TM, TN, A8> P0, P1;
   RingOps<TM, TN> E0, E1;
   read(P0, 0, 0);
   read(P1, 0, 1);
@@ -795,7 +831,7 @@ w4a4_gemm_ring(GemmArgs g) {
   // expands the stage after the end; those operands are never used.
   for (int st = 0; st < nstage; ++st) {
     constexpr std::integral_constant<int, 0> none{};
-    constexpr std::integral_constant<int, TM + TN> all{};
+    constexpr std::integral_constant<int, (A8 ? 2 : 1) * TM + TN> all{};  // ds_reads of one read()
     mma(acc, E0);                 // k-step 4 st
     expand_half<1>(P0, E1);
     interleave(none);
@@ -869,21 +905,21 @@ w4a4_gemm_ring(GemmArgs g) {
   }
 }
 
-template <int WM, int WN, int TM, int TN, int NS>
+template <int WM, int WN, int TM, int TN, int NS, bool A8 = false>
 bool fits_ring(const GemmArgs& g) {
-  using R = Ring<WM, WN, TM, TN, NS>;
-  const int64_t kb = g.K / 2;
-  return (g.M + R::BM) * kb + 64 < (int64_t{1} << 31) && (g.N + R::BN) * kb + 64 < (int64_t{1} << 31);
+  using R = Ring<WM, WN, TM, TN, NS, A8>;
+  const int64_t kb = g.K / 2, ka = A8 ? g.K : kb;
+  return (g.M + R::BM) * ka + 128 < (int64_t{1} << 31) && (g.N + R::BN) * kb + 64 < (int64_t{1} << 31);
 }
 
 // WPE: waves per SIMD the registers must allow (2 for two 4-wave workgroups per CU, or one
 // workgroup of two K groups); KS: groups of waves splitting K.
-template <int WM, int WN, int TM, int TN, int NS, int WPE = 1, int KS = 1>
+template <int WM, int WN, int TM, int TN, int NS, int WPE = 1, int KS = 1, bool A8 = false>
 hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
-  using R = Ring<WM, WN, TM, TN, NS>;
-  constexpr int LDS = RingLds<WM, WN, TM, TN, NS, KS>::BYTES;
+  using R = Ring<WM, WN, TM, TN, NS, A8>;
+  constexpr int LDS = RingLds<WM, WN, TM, TN, NS, KS, A8>::BYTES;
   static_assert(LDS <= 160 * 1024, "LDS of one CU");
-  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS>;
+  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS, A8>;
   static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
   if (init != hipSuccess) return init;
@@ -984,14 +1020,6 @@ struct Skinny {
 // A8: 8-bit activation codes (W4A8): a lane loads the 32 code bytes matching its 32 weight
 // codes, in the weights' k-slot order (v_perm_b32) and made signed (xor 0x80, codes - 128);
 // the epilogue adds the shift back through the zero-point term (beta + 128 alpha).
-__device__ __forceinline__ v4i act8_operand(const v4u d) {
-  const uint32_t f = 0x80808080u;
-  return v4i{static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x06040200u) ^ f),
-             static_cast<int>(__builtin_amdgcn_perm(d[1], d[0], 0x07050301u) ^ f),
-             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x06040200u) ^ f),
-             static_cast<int>(__builtin_amdgcn_perm(d[3], d[2], 0x07050301u) ^ f)};
-}
-
 template <int NB, int SD, bool A8 = false>
 __global__ void __launch_bounds__(512)
 w4a4_gemm_skinny(GemmArgs g) {
@@ -1189,6 +1217,20 @@ hipError_t try_skinny8(const GemmArgs& g, hipStream_t stream) {
 }
 
 }  // namespace
+
+// 8-bit activations on the ring: 128 x 256 tiles of 8 waves of 64 x 64, four stages.
+// Measured on MI355X (us) against 128 x 128 (2 per CU, 3 stages) / 256 x 128 (8 waves,
+// 3 stages) / 128 x 128 (4 stages) rings and the register-staged tile kernel:
+//   [2048 x 22016 x 4096]   290 vs 329 / 315 / 360 / 389
+//   [2048 x 4096 x 11008]   118 vs 150 / 131 / 155 / 165
+//   [4096 x 28672 x 4096]   688 vs 815 / 742 / 892 / 847
+//   [4096 x 4096 x 14336]   326 vs 402 / 356 / 410 / 362
+hipError_t launch_w4a8_ring(const GemmArgs& g0, hipStream_t stream) {
+  GemmArgs g = g0;
+  g.a8 = 1;
+  if (!fits_ring<2, 4, 2, 2, 4, true>(g)) return hipErrorNotSupported;
+  return launch_ring<2, 4, 2, 2, 4, 1, 1, true>(g, stream);
+}
 
 hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream) {
   if (g.M > 16) return hipErrorNotSupported;

@@ -580,6 +580,19 @@ def test_w4a8_decode_shapes(M, N, K):
     gemm8_case(M, N, K, seed=M * 13 + N + K, bias=(M % 2 == 1))
 
 
+@pytest.mark.parametrize("variant", ["default", "tile"])
+def test_w4a8_prefill_kernels(variant, monkeypatch):
+    # the ring kernel with 8-bit A blocks (default) and the register-staged tile kernel it
+    # falls back to for operands beyond 31-bit offsets: ragged M and N, K not a multiple of
+    # a 128-k stage, both tile widths of the fallback
+    say(f"w4a8_linear prefill kernel {variant}")
+    if variant != "default":
+        monkeypatch.setenv("SQ_W4A8_VARIANT", variant)
+    for (M, N, K) in [(300, 390, 448), (257, 600, 320), (129, 1000, 2112), (640, 520, 1024), (2048, 300, 256),
+                      (4096, 4096, 128)]:
+        gemm8_case(M, N, K, seed=M + N + K + 7)
+
+
 def test_w4a8_gemm_extreme_codes():
     # the largest int32 sums the kernel forms: 16 x (255 - 128) x 7 and 16 x (0 - 128) x (-7)
     # over K = 2^17
