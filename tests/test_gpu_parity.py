@@ -94,9 +94,10 @@ def test_rotated_quant_8bit(a, b, M, group):
     check_act8(x, a, b, group)
 
 
-def check_act_var(x, a, b, bits=4, group=None, clip=1.0, signs=None, h_gpu=None, s_gpu=None):
+def check_act_var(x, a, b, bits=4, group=None, clip=1.0, signs=None, h_gpu=None, s_gpu=None, sample_rows=None):
     """sq_had_quant_act_ex (clip ratio, random-sign Hadamard S H) vs the oracle.  h_gpu and
-    s_gpu replace the uploads of H_a and signs (views at other alignments)."""
+    s_gpu replace the uploads of H_a and signs (views at other alignments); sample_rows: the
+    GPU quantizes every row, the oracle those rows."""
     K = x.shape[1]
     group = K if group is None else group
     ha = None if a == 1 else ohad.dense_factor(a)
@@ -105,6 +106,8 @@ def check_act_var(x, a, b, bits=4, group=None, clip=1.0, signs=None, h_gpu=None,
     q, al, be, rot = sq.had_quant_act(dev(x), had_table(a) if h_gpu is None else h_gpu, b, group=group, bits=bits,
                                       dbg=True, clip=clip, signs=s_gpu)
     gq, gal, gbe, grot = host(q), host(al), host(be), host(rot)
+    if sample_rows is not None:
+        x, gq, gal, gbe, grot = x[sample_rows], gq[sample_rows], gal[sample_rows], gbe[sample_rows], grot[sample_rows]
     op, oal, obe, oy, oc = olin.had_quant_act(x, ha, b, bits=bits, group=group, clip=clip, signs=signs)
     gc = parity.unpack(gq, signed=False) if bits == 4 else gq.astype(np.int64)
     if a * b == 1:
@@ -155,6 +158,19 @@ def test_rotated_quant_variants(a, b, M, group, bits):
                                               signs=dev(np.ones(n, np.int8)))[:3]]
     for u, v in zip(plain, ones):
         np.testing.assert_array_equal(u, v)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_rotated_quant_variants_full(bits):
+    # the matrix-core kernels' variant instantiations at the full R4 sizes (every row on the
+    # GPU, sampled rows against the oracle): LLaMA-2-7B [2048, 11008] (pair kernel) and
+    # LLaMA-3-8B [4096, 14336] (line kernel), random signs with clip 0.9
+    for shape, a, rows in ((workloads.LLAMA2_7B_MLP, 172, [0, 1, 2, 3, 1023, 2044, 2047]),
+                           (workloads.LLAMA3_8B_MLP, 28, [0, 5, 2048, 4095])):
+        say(f"had_quant_act_ex {bits}-bit {shape.name}: signs + clip 0.9, sampled rows")
+        x = workloads.mlp_inputs(shape)["x_down"]
+        s = rand_signs(shape.inter, 96 + a)
+        check_act_var(x, a, shape.had_pow2, bits, signs=s, clip=0.9, sample_rows=np.array(rows))
 
 
 def test_rotated_quant_variants_other_layouts():
