@@ -186,7 +186,8 @@ sq_status sq_pack_w4_ex(const void* w, int64_t N, int64_t K, int64_t ldw,
  *   M          >= 0 (0 is a no-op)
  *   wq, w_alpha, w_rowsum   device, from sq_pack_w4: uint8 [N, K/2] (16-byte aligned), fp32 [N], int32 [N]
  *   N          >= 1
- *   K          > 0, K % 64 == 0
+ *   K          > 0, K % 64 == 0, K <= 2^20 (the int32 accumulator holds 16 x acc, and
+ *              16 x 15 x 7 x 2^20 < 2^31)
  *   bias       optional device fp16 [N]; NULL for none
  *   y          device fp16 [M, ldy], ldy >= N, 2-byte aligned
  *   dbg_acc    optional device int32 [M, N] (contiguous): the raw accumulators; NULL to skip
@@ -221,7 +222,7 @@ sq_status sq_w4a8_linear(const uint8_t* xq, const float* x_alpha, const float* x
  * where g and u are the dequantised outputs of sq_w4a4_linear for the gate and up weights,
  * kept in fp32 (not rounded to fp16) before they are combined.
  *
- *   xq, x_alpha, x_beta, M, K, stream   as for sq_w4a4_linear
+ *   xq, x_alpha, x_beta, M, K, stream   as for sq_w4a4_linear (K <= 2^20)
  *   wq, w_alpha, w_rowsum, bias   the gate and up weights packed by sq_pack_w4 as one
  *              [N, K] matrix whose rows interleave them in blocks of 32: rows 64b .. 64b+31
  *              are gate rows 32b .. 32b+31 and rows 64b+32 .. 64b+63 the up rows of the

@@ -29,7 +29,6 @@
 #include "sq_device.h"
 #include "sq_internal.h"
 
-#include <cstdlib>
 #include <mutex>
 #include <utility>
 
@@ -1147,18 +1146,12 @@ int num_cus() {
 template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE, bool DBG>
 hipError_t launch_kron_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Kron<A, APAD, NT, B, MW, NW, STAGE>;
-  auto kern = had_quant_kron<A, APAD, NT, B, MW, NW, STAGE, DBG>;
-  static int blocks_per_cu = 0;
-  static hipError_t init = [&] {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_per_cu, kern, C::THREADS, C::LDS);
-    if (blocks_per_cu < 1) blocks_per_cu = 1;
-    return e;
-  }();
-  if (init != hipSuccess) return init;
-  const int64_t cap = static_cast<int64_t>(num_cus()) * blocks_per_cu;
+  constexpr auto kern = had_quant_kron<A, APAD, NT, B, MW, NW, STAGE, DBG>;
+  hipError_t e = set_max_lds<kern>(C::LDS);
+  int per_cu = 1;
+  if (e == hipSuccess) e = blocks_per_cu<kern>(C::THREADS, C::LDS, &per_cu);
+  if (e != hipSuccess) return e;
+  const int64_t cap = static_cast<int64_t>(num_cus()) * per_cu;
   const unsigned grid = static_cast<unsigned>(a.rows < cap ? a.rows : cap);
   return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
@@ -1172,9 +1165,8 @@ hipError_t launch_kron(const RotQuantArgs& a, hipStream_t stream) {
 template <int A, int APAD, int NT, bool DBG, int BITS, bool VAR>
 hipError_t launch_pair_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Pair<A, APAD, NT>;
-  auto kern = had_quant_pair<A, APAD, NT, DBG, BITS, VAR>;
-  static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  constexpr auto kern = had_quant_pair<A, APAD, NT, DBG, BITS, VAR>;
+  const hipError_t init = set_max_lds<kern>(C::LDS);
   if (init != hipSuccess) return init;
   const int64_t sets = (a.rows + C::ROWS - 1) / C::ROWS;
   const int64_t cap = num_cus();
@@ -1208,18 +1200,12 @@ hipError_t launch_pair(const RotQuantArgs& a, hipStream_t stream) {
 template <int A, int F, int NT, bool DBG, int BITS, bool VAR>
 hipError_t launch_lines_t(const RotQuantArgs& a, hipStream_t stream) {
   using C = Lines<A, F, NT>;
-  auto kern = had_quant_lines<A, F, NT, DBG, BITS, VAR>;
-  static int blocks_per_cu = 0;
-  static const hipError_t init = [&] {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks_per_cu, kern, C::THREADS, C::LDS);
-    if (blocks_per_cu < 1) blocks_per_cu = 1;
-    return e;
-  }();
-  if (init != hipSuccess) return init;
-  const int64_t cap = static_cast<int64_t>(num_cus()) * blocks_per_cu;
+  constexpr auto kern = had_quant_lines<A, F, NT, DBG, BITS, VAR>;
+  hipError_t e = set_max_lds<kern>(C::LDS);
+  int per_cu = 1;
+  if (e == hipSuccess) e = blocks_per_cu<kern>(C::THREADS, C::LDS, &per_cu);
+  if (e != hipSuccess) return e;
+  const int64_t cap = static_cast<int64_t>(num_cus()) * per_cu;
   const unsigned grid = static_cast<unsigned>(a.rows < cap ? a.rows : cap);
   return launch(kern, dim3(grid), dim3(C::THREADS), C::LDS, stream, a);
 }
@@ -1242,7 +1228,7 @@ hipError_t launch_had_quant_kron(const RotQuantArgs& a, hipStream_t stream) {
   // register-prefetch kernels write plain 4-bit codes only
   const bool pair_ok = (reinterpret_cast<uintptr_t>(a.x) & 15) == 0 && (a.ldx % 8) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.H) & 15) == 0 &&
-                       (reinterpret_cast<uintptr_t>(a.signs) & 7) == 0 && !getenv("SQ_KRON_STAGED");
+                       (reinterpret_cast<uintptr_t>(a.signs) & 7) == 0;
   if (!pair_ok && (a.bits != 4 || is_variant(a))) return hipErrorNotSupported;
   if (a.a == 28 && a.b == 512) {
     if (pair_ok) return launch_lines<28, 8, 7>(a, stream);

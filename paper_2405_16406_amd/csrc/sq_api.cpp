@@ -230,8 +230,8 @@ sq_status sq_w4a4_linear(const uint8_t* xq, const float* x_alpha, const float* x
     return fail(SQ_ERR_NULL, "xq, x_alpha, x_beta, wq, w_alpha, w_rowsum and y are required");
   if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
   if (N <= 0 || N > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "N=%lld out of range", (long long)N);
-  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 24))
-    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^24)", (long long)K);
+  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 20))
+    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^20)", (long long)K);
   if (ldy < N) return fail(SQ_ERR_SHAPE, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
   if (!aligned(xq, 16) || !aligned(wq, 16) || !aligned(y, 2) || !aligned(x_alpha, 4) || !aligned(x_beta, 4) ||
       !aligned(w_alpha, 4) || !aligned(w_rowsum, 4) || (bias && !aligned(bias, 2)) || (dbg_acc && !aligned(dbg_acc, 4)))
@@ -310,8 +310,8 @@ sq_status sq_w4a4_linear_swiglu(const uint8_t* xq, const float* x_alpha, const f
   if (M < 0 || M > (int64_t{1} << 31) - 1) return fail(SQ_ERR_SHAPE, "M=%lld out of range", (long long)M);
   if (N <= 0 || N % 64 != 0 || N > (int64_t{1} << 31) - 1)
     return fail(SQ_ERR_SHAPE, "N=%lld must be a positive multiple of 64 (gate/up blocks of 32)", (long long)N);
-  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 24))
-    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^24)", (long long)K);
+  if (K <= 0 || K % 64 != 0 || K > (int64_t{1} << 20))
+    return fail(SQ_ERR_SHAPE, "K=%lld must be a positive multiple of 64 (and <= 2^20)", (long long)K);
   if (ldh < N / 2) return fail(SQ_ERR_SHAPE, "ldh=%lld < N/2=%lld", (long long)ldh, (long long)(N / 2));
   if (!aligned(xq, 16) || !aligned(wq, 16) || !aligned(h, 2) || !aligned(x_alpha, 4) || !aligned(x_beta, 4) ||
       !aligned(w_alpha, 4) || !aligned(w_rowsum, 4) || (bias && !aligned(bias, 2)))

@@ -4,6 +4,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <vector>
 
@@ -116,6 +117,34 @@ struct LaunchTiming {
   hipEvent_t stop = nullptr;
 };
 LaunchTiming& launch_timing();
+
+// Raises the dynamic LDS limit of kernel Kern to `bytes`, once per process.  A failed
+// attempt is not remembered: the next launch tries again and reports its own status.
+template <auto Kern>
+hipError_t set_max_lds(int bytes) {
+  static std::atomic<bool> done{false};
+  if (done.load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(Kern), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess) done.store(true, std::memory_order_release);
+  return e;
+}
+
+// Workgroups of kernel Kern (threads, dynamic LDS bytes) that fit one CU, queried once per
+// process (after set_max_lds); a failed query is not remembered.
+template <auto Kern>
+hipError_t blocks_per_cu(int threads, int lds, int* out) {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_acquire);
+  if (v == 0) {
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, Kern, threads, lds);
+    if (e != hipSuccess) return e;
+    if (v < 1) v = 1;
+    cached.store(v, std::memory_order_release);
+  }
+  *out = v;
+  return hipSuccess;
+}
 
 // Every kernel of the library is launched through here.
 template <typename... Params, typename... Args>

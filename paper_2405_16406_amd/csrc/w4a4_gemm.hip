@@ -18,8 +18,6 @@
 // two workgroups per CU) and 256 x 256 (8 waves of 128 x 64).
 // Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
 // used where 32-bit buffer offsets do not cover the operands.
-// Small kernel (w4a4_gemm_v1): 128 x 128 tiles, single-buffered; kept as a baseline.
-#include <cstdlib>
 #include <utility>
 
 #include "sq_device.h"
@@ -517,8 +515,10 @@ w4a4_gemm_tile(GemmArgs g) {
   auto gload = [&](int st) {
     const int64_t kb = static_cast<int64_t>(st) * kBKB;
     const bool kok = kb + scol < KB;
+    // a chunk past K (the second half of the last stage when K % 128 == 64) reads column
+    // scol of stage 0 instead, for both operands, so every load stays inside its row; the
+    // A chunk is then zeroed and the product adds nothing
     const int64_t ka = (kok ? kb : 0) + scol;
-    const int64_t kbb = (kb < KB ? kb : 0) + scol;  // B beyond K only meets zeroed A
 #pragma unroll
     for (int q = 0; q < kAChunks; ++q) {
       const int64_t r = m0 + srow + q * (THREADS / 4);
@@ -528,7 +528,7 @@ w4a4_gemm_tile(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < kBChunks; ++q) {
       const int64_t r = n0 + srow + q * (THREADS / 4);
-      rb[q] = *reinterpret_cast<const uint4*>(g.wq + (r < nb ? r : nb) * KB + kbb);
+      rb[q] = *reinterpret_cast<const uint4*>(g.wq + (r < nb ? r : nb) * KB + ka);
     }
   };
   auto lstore = [&](int buf) {
@@ -919,82 +919,11 @@ hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
   using R = Ring<WM, WN, TM, TN, NS, A8>;
   constexpr int LDS = RingLds<WM, WN, TM, TN, NS, KS, A8>::BYTES;
   static_assert(LDS <= 160 * 1024, "LDS of one CU");
-  auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS, A8>;
-  static const hipError_t init = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+  constexpr auto kern = w4a4_gemm_ring<WM, WN, TM, TN, NS, WPE, KS, A8>;
+  const hipError_t init = set_max_lds<kern>(LDS);
   if (init != hipSuccess) return init;
   const dim3 grid(static_cast<unsigned>((g.N + R::BN - 1) / R::BN), static_cast<unsigned>((g.M + R::BM - 1) / R::BM));
   return launch(kern, grid, dim3(R::THREADS * KS), LDS, stream, g);
-}
-
-// ------------------------------------------------------------------ small-M kernel
-constexpr int kSBM = 128;
-constexpr int kSBN = 128;
-constexpr int kSBKB = 32;
-constexpr int kSPitch = 40;
-
-__global__ void __launch_bounds__(256)
-w4a4_gemm_v1(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) uint8_t As[kSBM * kSPitch];
-  __shared__ __attribute__((aligned(16))) uint8_t Bs[kSBN * kSPitch];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * kSBM;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * kSBN;
-  const int wm = (wave >> 1) * 64;
-  const int wn = (wave & 1) * 64;
-  const int64_t KB = g.K / 2;
-
-  v16i acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
-
-  const int lr = tid >> 1;
-  const int lc = (tid & 1) * 16;
-  const int64_t am = m0 + lr;
-  const int64_t bn = n0 + lr;
-  const uint8_t* arow = g.xq + am * KB + lc;
-  const uint8_t* brow = g.wq + bn * KB + lc;
-  const bool aok = am < g.M;
-  const bool bok = bn < g.N;
-
-  for (int64_t kb = 0; kb < KB; kb += kSBKB) {
-    uint4 va = make_uint4(0, 0, 0, 0);
-    uint4 vb = make_uint4(0, 0, 0, 0);
-    if (aok) va = *reinterpret_cast<const uint4*>(arow + kb);
-    if (bok) vb = *reinterpret_cast<const uint4*>(brow + kb);
-    __syncthreads();
-    *reinterpret_cast<uint2*>(As + lr * kSPitch + lc) = make_uint2(va.x, va.y);
-    *reinterpret_cast<uint2*>(As + lr * kSPitch + lc + 8) = make_uint2(va.z, va.w);
-    *reinterpret_cast<uint2*>(Bs + lr * kSPitch + lc) = make_uint2(vb.x, vb.y);
-    *reinterpret_cast<uint2*>(Bs + lr * kSPitch + lc + 8) = make_uint2(vb.z, vb.w);
-    __syncthreads();
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int off = ks * 16 + (lane >> 5) * 8;
-      v4i af[2], bf[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = expand_act(*reinterpret_cast<const uint2*>(As + (wm + i * 32 + (lane & 31)) * kSPitch + off));
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bf[j] = expand_wgt(*reinterpret_cast<const uint2*>(Bs + (wn + j * 32 + (lane & 31)) * kSPitch + off));
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int i = 0; i < 2; ++i) store_block(g, acc[i][j], m0 + wm + i * 32, n0 + wn + j * 32 + (lane & 31), lane);
 }
 
 // ------------------------------------------------------------------ decode-sized kernel
@@ -1253,60 +1182,26 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     if (tiles >= 256) return fits_ring<2, 4, 4, 2, 4>(g) ? launch_ring<2, 4, 4, 2, 4>(g, stream) : hipErrorNotSupported;
     return fits_ring<2, 2, 4, 2, 3>(g) ? launch_ring<2, 2, 4, 2, 3, 2>(g, stream) : hipErrorNotSupported;
   }
-  // SQ_GEMM_VARIANT selects a tile shape for tuning experiments (unset: the default).
-  const char* env = getenv("SQ_GEMM_VARIANT");
-  const int v = env ? atoi(env) : -1;
-  switch (v) {
-    case 0: return launch_tile<2, 2, 4, 2>(g, stream);   // 256 x 128, 4 waves of 128 x 64
-    case 1: return launch_tile<2, 2, 2, 2>(g, stream);   // 128 x 128, 4 waves of 64 x 64
-    case 2: return launch_tile<2, 2, 4, 4>(g, stream);   // 256 x 256, 4 waves of 128 x 128
-    case 3: return launch_tile<2, 1, 4, 4>(g, stream);   // 256 x 128, 2 waves of 128 x 128
-    case 4: return launch_tile<1, 2, 4, 4>(g, stream);   // 128 x 256, 2 waves of 128 x 128
-    case 5: return launch_tile<2, 4, 4, 2>(g, stream);   // 256 x 256, 8 waves of 128 x 64
-    case 10: if (fits_ring<2, 2, 4, 2, 4>(g)) return launch_ring<2, 2, 4, 2, 4>(g, stream); break;  // 256 x 128
-    case 11: if (fits_ring<2, 2, 4, 4, 4>(g)) return launch_ring<2, 2, 4, 4, 4>(g, stream); break;  // 256 x 256
-    case 12: if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream); break;  // 256 x 256, 8 waves
-    case 13: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4>(g, stream); break;  // 128 x 128
-    case 14: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream); break;  // 256 x 128, 2/CU
-    case 15: if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2, 2>(g, stream); break;  // 256 x 128, K split
-    case 16: if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream); break;  // 128 x 128, K split
-    case 17: if (fits_ring<4, 2, 2, 2, 4>(g)) return launch_ring<4, 2, 2, 2, 4, 1>(g, stream); break;  // 256 x 128, 8 waves of 64 x 64
-    case 18: if (fits_ring<2, 4, 2, 2, 4>(g)) return launch_ring<2, 4, 2, 2, 4, 1>(g, stream); break;  // 128 x 256, 8 waves of 64 x 64
-    case 20: if (fits_skinny<2, 8>(g)) return launch_skinny<2, 8>(g, stream); break;  // decode: 32 rows per workgroup
-    case 21: if (fits_skinny<4, 4>(g)) return launch_skinny<4, 4>(g, stream); break;  // decode: 64 rows per workgroup
-    case 22: return launch_skinny_sized(g, stream);                                     // decode: rows per workgroup from N
-    case 23: if (fits_skinny<8, 2>(g)) return launch_skinny<8, 2>(g, stream); break;  // decode: 128 rows, 2 steps ahead
-    case 24: if (fits_skinny<8, 3>(g)) return launch_skinny<8, 3>(g, stream); break;  // decode: 128 rows, 3 steps ahead
-    case 25: if (fits_skinny<7, 3>(g)) return launch_skinny<7, 3>(g, stream); break;  // decode: 112 rows, 3 steps ahead
-    case 9: {
-      const dim3 grid(static_cast<unsigned>((g.N + kSBN - 1) / kSBN), static_cast<unsigned>((g.M + kSBM - 1) / kSBM));
-      return launch(w4a4_gemm_v1, grid, dim3(256), 0, stream, g);
-    }
-    default: {
-      // Measured on MI355X (LLaMA-2-7B / LLaMA-3-8B MLP shapes, same data, interleaved runs):
-      // the 8-wave 256 x 256 ring tile is fastest once there are at least as many of its
-      // tiles as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs
-      // 212 us); with fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).
-      // Decode-sized M (<= 16) streams the weights with the skinny kernel (LLaMA-2-70B,
-      // M = 16: down [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 36 vs
-      // 41 us against the tile kernels); M <= 128 runs 128 x 128 tiles with two K groups per
-      // workgroup.  Problems whose byte offsets do not fit 31 bits use the register-staged
-      // kernel.
-      const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-      if (g.M <= 16) return launch_skinny_sized(g, stream);
-      if (g.M <= 128) {
-        if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);
-        return launch_tile<2, 2, 2, 2>(g, stream);
-      }
-      if (tiles256 >= 256) {
-        if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
-        return launch_tile<2, 4, 4, 2>(g, stream);
-      }
-      if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
-      return launch_tile<2, 4, 4, 2>(g, stream);
-    }
+  // Measured on MI355X (LLaMA-2-7B / LLaMA-3-8B MLP shapes, same data, interleaved runs):
+  // the 8-wave 256 x 256 ring tile is fastest once there are at least as many of its tiles
+  // as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs 212 us); with
+  // fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).  Decode-sized M
+  // (<= 16) streams the weights with the skinny kernel (LLaMA-2-70B, M = 16: down
+  // [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 36 vs 41 us against
+  // the tile kernels); 16 < M <= 128 runs 128 x 128 tiles with two K groups per workgroup.
+  // Problems whose byte offsets do not fit 31 bits (operands of 2 GB and more) use the
+  // register-staged kernel.
+  if (g.M <= 16) return launch_skinny_sized(g, stream);
+  if (g.M <= 128) {
+    if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);
+    return launch_tile<2, 2, 2, 2>(g, stream);
   }
-  // a tuning variant whose ring offsets do not fit: the default path
+  const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  if (tiles256 >= 256) {
+    if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
+    return launch_tile<2, 4, 4, 2>(g, stream);
+  }
+  if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
   return launch_tile<2, 4, 4, 2>(g, stream);
 }
 

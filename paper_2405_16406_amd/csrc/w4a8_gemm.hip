@@ -17,8 +17,6 @@
 #include "sq_device.h"
 #include "sq_internal.h"
 
-#include <cstdlib>
-#include <cstring>
 
 namespace sq {
 namespace {
@@ -171,9 +169,8 @@ w4a8_gemm_tile(GemmArgs g) {
 template <int BN, int BK>
 hipError_t launch_tile(const GemmArgs& g, hipStream_t stream) {
   using T = Tile<BN, BK>;
-  auto kern = w4a8_gemm_tile<BN, BK>;
-  static const hipError_t init =
-      hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS);
+  constexpr auto kern = w4a8_gemm_tile<BN, BK>;
+  const hipError_t init = set_max_lds<kern>(T::LDS);
   if (init != hipSuccess) return init;
   const dim3 grid(static_cast<unsigned>((g.N + BN - 1) / BN), static_cast<unsigned>((g.M + kBM - 1) / kBM));
   return launch(kern, grid, dim3(256), T::LDS, stream, g);
@@ -186,13 +183,10 @@ hipError_t launch_w4a8_gemm(const GemmArgs& g, hipStream_t stream) {
   const hipError_t e = launch_w4a8_skinny(g, stream);
   if (e != hipErrorNotSupported) return e;
   // prefill: the LDS-ring kernel of the W4A4 GEMM with 8-bit A blocks; this file's
-  // register-staged tiles where its 32-bit buffer offsets do not cover the operands (and
-  // when SQ_W4A8_VARIANT=tile asks for them, so that tests reach that path)
-  const char* v = getenv("SQ_W4A8_VARIANT");
-  if (!(v && strcmp(v, "tile") == 0)) {
-    const hipError_t r = launch_w4a8_ring(g, stream);
-    if (r != hipErrorNotSupported) return r;
-  }
+  // register-staged tiles where its 32-bit buffer offsets do not cover the operands
+  // (operands of 2 GB and more)
+  const hipError_t r = launch_w4a8_ring(g, stream);
+  if (r != hipErrorNotSupported) return r;
   // Measured on MI355X (us, tiles 128x64 / 128x128 / 256x64 / 256x128 in N x k-stage):
   //   [2048 x 22016 x 4096]  404 / 401 / 417 / 387      [2048 x 4096 x 11008]  181 / 165 / 221 / 186
   //   [4096 x 28672 x 4096]  944 / 916 / 920 / 846      [4096 x 4096 x 14336]  446 / 397 / 390 / 362

@@ -45,7 +45,13 @@ def lib() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2405_16406_amd.build`")
-    L = ctypes.CDLL(LIB_PATH)
+    _lib = load(LIB_PATH)
+    return _lib
+
+
+def load(path: str) -> ctypes.CDLL:
+    """Open a build of the library at `path` and declare the signatures of include/sq.h."""
+    L = ctypes.CDLL(path)
     L.sq_abi_version.restype = _I32
     L.sq_abi_version.argtypes = []
     L.sq_last_error.restype = ctypes.c_char_p
@@ -79,7 +85,6 @@ def lib() -> ctypes.CDLL:
     L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _P, _P]
     L.sq_attn_decode_kv4_ex.restype = _I32
     L.sq_attn_decode_kv4_ex.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32, _P, _P]
-    _lib = L
     return L
 
 

@@ -22,8 +22,15 @@ def fake(i):
     return ctypes.c_void_p(P * (i + 1) << 8)
 
 
+# SQ_TEST_LIBRARY names another build of the library to check (the sanitizer build of
+# tests/test_sanitize.py); the binding's helpers then use it too
+TEST_LIBRARY = os.environ.get("SQ_TEST_LIBRARY")
+
+
 @pytest.fixture(scope="module")
 def L():
+    if TEST_LIBRARY:
+        sq._lib = sq.load(TEST_LIBRARY)
     return sq.lib()
 
 
@@ -106,6 +113,12 @@ def lin(L, xq=fake(0), xa=fake(1), xb=fake(2), M=4, wq=fake(3), wa=fake(4), rs=f
 def test_w4a4_linear_validation(L):
     assert lin(L, y=None) == sq.SQ_ERR_NULL
     assert lin(L, K=96) == sq.SQ_ERR_SHAPE
+    # the int32 accumulator holds 16 x acc: |16 x 15 x 7 x K| < 2^31 needs K <= 2^20
+    assert lin(L, K=(1 << 20) + 64) == sq.SQ_ERR_SHAPE
+    assert b"2^20" in L.sq_last_error()
+    assert lin(L, M=0, K=1 << 20) == sq.SQ_OK
+    assert lin_sw(L, K=(1 << 20) + 64) == sq.SQ_ERR_SHAPE
+    assert lin_sw(L, M=0, K=1 << 20) == sq.SQ_OK
     assert lin(L, N=0) == sq.SQ_ERR_SHAPE
     assert lin(L, ldy=32) == sq.SQ_ERR_SHAPE
     assert lin(L, y=ctypes.c_void_p(P * 256 + 1)) == sq.SQ_ERR_ALIGN
@@ -286,3 +299,22 @@ def test_attn_decode_ex_validation(L):
     assert call(va=ctypes.c_void_p(fake(5).value + 2)) == sq.SQ_ERR_ALIGN
     assert call(B=0, pbits=16, va=ctypes.c_void_p(fake(5).value + 2)) == sq.SQ_OK
     assert call(out=ctypes.c_void_p(fake(2).value)) == sq.SQ_ERR_ALIAS
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU driver is present: the calls below would "
+                    "launch kernels on fake pointers")
+def test_no_device_is_a_hip_error(L):
+    # valid arguments on a host without a GPU: the launch fails and the call reports
+    # SQ_ERR_HIP with the runtime's message, it does not abort
+    assert hqa(L) == sq.SQ_ERR_HIP
+    msg = L.sq_last_error()
+    assert msg.startswith(b"had_quant_act launch: ") and len(msg) > len(b"had_quant_act launch: ")
+    assert lin(L) == sq.SQ_ERR_HIP
+    assert lin8(L) == sq.SQ_ERR_HIP
+    assert lin_sw(L) == sq.SQ_ERR_HIP
+    assert kvq(L) == sq.SQ_ERR_HIP
+    assert attn(L) == sq.SQ_ERR_HIP
+    assert L.sq_pack_w4(fake(0), 8, 256, 256, 1, None, 1, fake(1), fake(2), fake(3), None) == sq.SQ_ERR_HIP
+    # a later failing check still reports its own status and message
+    assert hqa(L, x=None) == sq.SQ_ERR_NULL
+    assert b"required" in L.sq_last_error()

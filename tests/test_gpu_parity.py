@@ -336,12 +336,22 @@ def test_kron_pair_strided_input_nan_padding(a, b):
         np.testing.assert_array_equal(u, v)
 
 
-@pytest.mark.parametrize("a,b", [(172, 64), (28, 512)])
-def test_kron_staged_kernel(a, b, monkeypatch):
-    say(f"had_quant_act H{a} (x) S{b} through the register-prefetch kernel")
-    monkeypatch.setenv("SQ_KRON_STAGED", "1")
+@pytest.mark.parametrize("a,b", [(172, 64), (28, 512), (28, 1024)])
+def test_kron_unaligned_factor_kernel(a, b):
+    # an H_a that is not 16-byte aligned (plain 4-bit rotation, no variant) takes the
+    # register-prefetch kernel instead of the LDS-staged matrix-core kernels
+    say(f"had_quant_act H{a} (x) S{b} with H_a at +1 byte: register-prefetch kernel")
     x = workloads.outlier_acts(workloads.rng_for(31), 37, a * b, a * b // 100, 50.0)
-    check_act(x, a, b)
+    hbuf = dev(np.concatenate([[0], ohad.dense_factor(a).reshape(-1)]).astype(np.int8))
+    hg = hbuf[1:].view(a, a)
+    assert hg.data_ptr() % 16 != 0
+    ha = ohad.dense_factor(a)
+    q, al, be, rot = sq.had_quant_act(dev(x), hg, b, dbg=True)
+    gq, gal, gbe, grot = host(q), host(al), host(be), host(rot)
+    op, oal, obe, oy, oc = olin.had_quant_act(x, ha, b)
+    parity.assert_rot_close(grot, oy)
+    parity.assert_params_close(gal, oal, gbe, obe)
+    parity.code_flips(parity.unpack(gq, signed=False), oc, oy, oal, obe, a * b)
 
 
 @pytest.mark.parametrize("a,b,M", [(28, 512, 33), (172, 64, 21), (28, 1024, 5)])
@@ -547,14 +557,13 @@ def test_gemm_llama2_70b_decode(M):
     gemm_case(M, 8192, 28672, seed=40 + M, bias=False)
 
 
-@pytest.mark.parametrize("variant", ["default", "20", "21", "24", "25"])
-def test_gemm_decode_kernel(variant, monkeypatch):
+def test_gemm_decode_kernel():
     # M <= 16 runs the weight-streaming kernel: every M up to 16, ragged N (blocks of 16
-    # rows), K not a multiple of the 8 waves' 64-byte steps, and K shorter than one step
-    say(f"w4a4_linear decode kernel {variant}: M 1..16, ragged N and K")
-    if variant != "default":
-        monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
+    # rows; N picks 1 to 8 blocks per workgroup), K not a multiple of the 8 waves' 64-byte
+    # steps, and K shorter than one step
+    say("w4a4_linear decode kernel: M 1..16, ragged N and K, 1-8 row blocks per workgroup")
     for (M, N, K) in [(1, 8, 64), (2, 40, 128), (7, 1000, 4160), (16, 130, 3136), (11, 4097, 640),
+                      (3, 8200, 256), (5, 12300, 192), (9, 16390, 128), (4, 20500, 64), (6, 24600, 128),
                       (16, 28672 + 48, 192), (13, 96, 28672)]:
         gemm_case(M, N, K, seed=M * 31 + N + K, bias=(M % 2 == 1))
 
@@ -596,14 +605,9 @@ def test_w4a8_decode_shapes(M, N, K):
     gemm8_case(M, N, K, seed=M * 13 + N + K, bias=(M % 2 == 1))
 
 
-@pytest.mark.parametrize("variant", ["default", "tile"])
-def test_w4a8_prefill_kernels(variant, monkeypatch):
-    # the ring kernel with 8-bit A blocks (default) and the register-staged tile kernel it
-    # falls back to for operands beyond 31-bit offsets: ragged M and N, K not a multiple of
-    # a 128-k stage, both tile widths of the fallback
-    say(f"w4a8_linear prefill kernel {variant}")
-    if variant != "default":
-        monkeypatch.setenv("SQ_W4A8_VARIANT", variant)
+def test_w4a8_prefill_kernels():
+    # the ring kernel with 8-bit A blocks: ragged M and N, K not a multiple of a 128-k stage
+    say("w4a8_linear prefill ring kernel")
     for (M, N, K) in [(300, 390, 448), (257, 600, 320), (129, 1000, 2112), (640, 520, 1024), (2048, 300, 256),
                       (4096, 4096, 128)]:
         gemm8_case(M, N, K, seed=M + N + K + 7)
@@ -853,35 +857,160 @@ def test_kv_full_sampled():
     check_kv(q, k, v, sample)
 
 
-@pytest.mark.parametrize("variant", ["0", "1", "2", "3", "4", "5", "9", "10", "11", "12", "13", "14", "15", "16"])
-def test_gemm_tile_variants(variant, monkeypatch):
-    say(f"w4a4_linear tile variant {variant}: ragged shapes, vector and element-wise stores")
-    monkeypatch.setenv("SQ_GEMM_VARIANT", variant)
-    for (M, N, K) in [(300, 390, 448), (64, 130, 192), (257, 257, 128), (520, 600, 320), (384, 264, 2112)]:
-        rng = workloads.rng_for(M + N + K)
-        qa = rng.integers(0, 16, size=(M, K))
-        qw = rng.integers(-7, 8, size=(N, K))
-        xa = rng.uniform(0.05, 3.0, M).astype(np.float32)
-        xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
-        wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
-        rs = qw.sum(1).astype(np.int32)
-        bi = (rng.standard_normal(N) * 0.1).astype(np.float16)
-        args = (dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs), dev(bi))
-        oy, oacc = olin.w4a4_linear(qa, xa, xb, qw, wa, rs, bi)
-        y_dbg, acc = sq.w4a4_linear(*args, dbg=True)
-        np.testing.assert_array_equal(host(acc), oacc)
-        parity.assert_out_close(host(y_dbg), oy)
-        y_fast, _ = sq.w4a4_linear(*args)                      # vector stores inside N
-        np.testing.assert_array_equal(host(y_fast), host(y_dbg))
-        wide = torch.zeros((M, N + 3), dtype=torch.float16, device=DEV)
-        sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: element-wise stores
-        np.testing.assert_array_equal(host(wide[:, :N]), host(y_dbg))
-        assert not host(wide[:, N:]).any()
-        w8 = (N + 1 + 7) // 8 * 8                              # ldy % 8 == 0: vector stores,
-        wide8 = torch.zeros((M, w8), dtype=torch.float16, device=DEV)   # edge tiles element-wise
-        sq.w4a4_linear(*args, out=wide8[:, :N])
-        np.testing.assert_array_equal(host(wide8[:, :N]), host(y_dbg))
-        assert not host(wide8[:, N:]).any()
+# Each size class of the dispatch: 16 < M <= 128 (128 x 128 tiles, two K groups), fewer
+# than 256 tiles of 256 x 256 (256 x 128 tiles, two workgroups per CU), at least 256 such
+# tiles (8-wave 256 x 256); ragged M, N and K (K % 128 == 64: a half stage)
+GEMM_CLASS_SHAPES = [(64, 130, 192), (100, 1000, 2112), (300, 390, 448), (257, 257, 128), (520, 600, 320),
+                     (384, 264, 2112), (4096, 4096, 192), (4000, 4100, 320)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_CLASS_SHAPES)
+def test_gemm_size_classes(M, N, K):
+    say(f"w4a4_linear M={M} N={N} K={K}: vector and element-wise stores")
+    rng = workloads.rng_for(M + N + K)
+    qa = rng.integers(0, 16, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    xa = rng.uniform(0.05, 3.0, M).astype(np.float32)
+    xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+    wa = rng.uniform(1e-3, 2e-2, N).astype(np.float32)
+    rs = qw.sum(1).astype(np.int32)
+    bi = (rng.standard_normal(N) * 0.1).astype(np.float16)
+    args = (dev(oq.pack_nibbles(qa)), dev(xa), dev(xb), dev(oq.pack_nibbles(qw)), dev(wa), dev(rs), dev(bi))
+    oy, oacc = olin.w4a4_linear(qa, xa, xb, qw, wa, rs, bi)
+    y_dbg, acc = sq.w4a4_linear(*args, dbg=True)
+    np.testing.assert_array_equal(host(acc), oacc)
+    parity.assert_out_close(host(y_dbg), oy)
+    y_fast, _ = sq.w4a4_linear(*args)                      # vector stores inside N
+    np.testing.assert_array_equal(host(y_fast), host(y_dbg))
+    wide = torch.zeros((M, N + 3), dtype=torch.float16, device=DEV)
+    sq.w4a4_linear(*args, out=wide[:, :N])                 # odd ldy: element-wise stores
+    np.testing.assert_array_equal(host(wide[:, :N]), host(y_dbg))
+    assert not host(wide[:, N:]).any()
+    w8 = (N + 1 + 7) // 8 * 8                              # ldy % 8 == 0: vector stores,
+    wide8 = torch.zeros((M, w8), dtype=torch.float16, device=DEV)   # edge tiles element-wise
+    sq.w4a4_linear(*args, out=wide8[:, :N])
+    np.testing.assert_array_equal(host(wide8[:, :N]), host(y_dbg))
+    assert not host(wide8[:, N:]).any()
+
+
+# Operands of 2 GB and more do not fit the 31-bit buffer offsets of the ring and decode
+# kernels, and take the register-staged kernels.  The big operand repeats a few seeded rows
+# (built on the device), so the oracle computes the sampled outputs from those rows.  K % 128
+# == 64 takes the half stage at the end of K.
+def big_gemm_case(M, N, K, big, seed, a8=False, rows=None):
+    rng = workloads.rng_for(seed)
+    base = 4
+    hi = 256 if a8 else 16
+    rows = np.array([0, 1, 2, 3, M // 2, M - 1]) if rows is None else rows
+    xa = rng.uniform(0.003 if a8 else 0.05, 0.2 if a8 else 3.0, M).astype(np.float32)
+    xb = rng.uniform(-20.0, 0.0, M).astype(np.float32)
+    codes = lambda q: dev(q.astype(np.uint8) if a8 else oq.pack_nibbles(q))
+    if big == "a":  # activation row m = base row m % 4
+        qa_b = rng.integers(0, hi, size=(base, K), dtype=np.int64)
+        qw = rng.integers(-7, 8, size=(N, K), dtype=np.int64)
+        wa = (rng.uniform(1e-3, 2e-2, N) / np.sqrt(K / 4096)).astype(np.float32)
+        qa_d = codes(qa_b).repeat((M + base - 1) // base, 1)[:M]
+        qw_d = dev(oq.pack_nibbles(qw))
+        qa_r, qw_o, wa_o, cols = qa_b[rows % base], qw, wa, np.arange(N)
+    else:  # weight row n = base row n % 4 (codes, scale and row sum)
+        qa_r = rng.integers(0, hi, size=(len(rows), K), dtype=np.int64)
+        qa = np.zeros((M, K), dtype=np.int8 if not a8 else np.uint8)
+        qa[rows] = qa_r
+        qw_o = rng.integers(-7, 8, size=(base, K), dtype=np.int64)
+        wa_o = (rng.uniform(1e-3, 2e-2, base) / np.sqrt(K / 4096)).astype(np.float32)
+        wa = wa_o[np.arange(N) % base]
+        qa_d = codes(qa)
+        del qa
+        qw_d = dev(oq.pack_nibbles(qw_o)).repeat((N + base - 1) // base, 1)[:N]
+        cols = np.arange(N) % base
+    assert qa_d.is_contiguous() and qw_d.is_contiguous()
+    assert max(qa_d.numel(), qw_d.numel()) >= 1 << 31
+    rs_o = qw_o.sum(1).astype(np.int32)
+    rs = rs_o[cols] if big != "a" else rs_o
+    fn = sq.w4a8_linear if a8 else sq.w4a4_linear
+    args = (qa_d, dev(xa), dev(xb), qw_d, dev(wa), dev(rs), None)
+    y, acc = fn(*args, dbg=True)
+    y2, _ = fn(*args)
+    gy, gacc, gy2 = host(y), host(acc), host(y2)
+    oy, oacc = olin.w4a4_linear(qa_r, xa[rows], xb[rows], qw_o, wa_o, rs_o)
+    np.testing.assert_array_equal(gacc[rows], oacc[:, cols])
+    parity.assert_out_close(gy[rows], oy[:, cols])
+    np.testing.assert_array_equal(gy2, gy)
+    del qa_d, qw_d, args
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("M,N,K,big", [(4100, 64, (1 << 20) - 64, "a"),    # 256 x 256 register-staged tiles
+                                       (100, 4100, (1 << 20) - 64, "w"),   # 128 x 128 (M <= 128)
+                                       (8, 4100, (1 << 20) - 64, "w")])    # decode-sized M
+def test_gemm_beyond_31bit_offsets(M, N, K, big):
+    say(f"w4a4_linear M={M} N={N} K={K}: {big} operand >= 2 GB, register-staged kernel")
+    big_gemm_case(M, N, K, big, seed=M + N)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("M,N,K", [(16400, 64, (1 << 17) - 64),   # 128 x 64-deep tiles (K % 128 == 64)
+                                   (16400, 64, 1 << 17),          # 128 x 128
+                                   (16400, 1024, 1 << 17)])       # 256 x 128 (>= 512 wide tiles)
+def test_w4a8_beyond_31bit_offsets(M, N, K):
+    say(f"w4a8_linear M={M} N={N} K={K}: 8-bit codes >= 2 GB, register-staged kernel")
+    big_gemm_case(M, N, K, "a", seed=M + N + 1, a8=True)
+
+
+def tile_rows(M, tile=256):
+    """Two rows of every `tile`-row block of M (its first and one inside), plus the last."""
+    r = [t + o for t in range(0, M, tile) for o in (0, (37 * (t // tile + 1)) % tile) if t + o < M]
+    return np.unique(np.array(r + [M - 1]))
+
+
+def test_gemm_llama2_7b_down_full():
+    # the launch the bench times: [2048 x 11008] x [4096 x 11008], every output column of
+    # sampled rows in every M tile
+    say("w4a4_linear LLaMA-2-7B down [2048x11008]x[4096x11008], rows of every M tile")
+    gemm_case(2048, 4096, 11008, seed=23, bias=False, sample_rows=tile_rows(2048))
+
+
+def test_gemm_llama2_7b_gate_up_stacked_full():
+    say("w4a4_linear LLaMA-2-7B gate+up stacked [2048x4096]x[22016x4096], rows of every M tile")
+    gemm_case(2048, 22016, 4096, seed=24, bias=False, sample_rows=tile_rows(2048))
+
+
+def test_swiglu_llama2_7b_full_tiles():
+    # the gate/up launch of the bench's layer step, rows in every M tile
+    say("w4a4_linear_swiglu LLaMA-2-7B [2048x4096]x[2x11008x4096], rows of every M tile")
+    swiglu_case(2048, 11008, 4096, seed=44, bias=False, sample_rows=tile_rows(2048))
+
+
+@pytest.mark.parametrize("M,N,K", [(8, 4096, 11008), (100, 1000, 2112), (2048, 4096, 11008), (4096, 4096, 192)])
+def test_gemm_deterministic(M, N, K):
+    # decode kernel (8 waves' partial sums in LDS), two K groups (partial sums exchanged in
+    # LDS), 256 x 128 and 256 x 256 ring tiles: two launches give the same bytes
+    say(f"w4a4_linear determinism M={M} N={N} K={K}")
+    rng = workloads.rng_for(M + N + K + 3)
+    qa = rng.integers(0, 16, size=(M, K))
+    qw = rng.integers(-7, 8, size=(N, K))
+    args = (dev(oq.pack_nibbles(qa)), dev(rng.uniform(0.05, 3.0, M).astype(np.float32)),
+            dev(rng.uniform(-20.0, 0.0, M).astype(np.float32)), dev(oq.pack_nibbles(qw)),
+            dev(rng.uniform(1e-3, 2e-2, N).astype(np.float32)), dev(qw.sum(1).astype(np.int32)))
+    r = [host(sq.w4a4_linear(*args)[0]).view(np.uint16) for _ in range(2)]
+    np.testing.assert_array_equal(r[0], r[1])
+    a = [host(sq.w4a4_linear(*args, dbg=True)[1]) for _ in range(2)]
+    np.testing.assert_array_equal(a[0], a[1])
+
+
+def test_kv_and_attention_deterministic():
+    say("qk_had_kvquant and attn_decode_kv4 determinism [2,512,32,128]")
+    q, k, v = (dev(t) for t in workloads.kv_inputs(B=2, S=512, H=32, D=128))
+    outs = [sq.qk_had_kvquant(q, k, v) for _ in range(2)]
+    for name in (n for n in outs[0] if outs[0][n] is not None):
+        np.testing.assert_array_equal(host(outs[0][name]).view(np.uint8), host(outs[1][name]).view(np.uint8),
+                                      err_msg=name)
+    o = outs[0]
+    qr = o["q_rot"][:, -1].contiguous()
+    cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+    att = [host(sq.attn_decode_kv4(qr, *cache)).view(np.uint16) for _ in range(2)]
+    np.testing.assert_array_equal(att[0], att[1])
 
 
 def test_time_next_call_events():
