@@ -1,4 +1,5 @@
-"""Builds libsq.so (HIP kernels for gfx950 + the C-ABI host code) in-tree with hipcc.
+"""Builds libsq.so (HIP kernels for gfx950 + the C-ABI host code) and libsq_probe.so (the
+roofline probes of include/sq_probe.h, used by the benchmark) in-tree with hipcc.
 
     python -m paper_2405_16406_amd.build        # compiles every source, always
     python -m paper_2405_16406_amd.build asan   # also the sanitizer build (below)
@@ -31,6 +32,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsq.so")
+PROBE_SRC = os.path.join(PKG, "probe", "roofline_probe.hip")
+PROBE_LIB = os.path.join(PKG, "libsq_probe.so")
 ASAN_DIR = os.path.join(BUILD_DIR, "asan")
 ASAN_LIB = os.path.join(ASAN_DIR, "libsq_asan.so")
 
@@ -63,21 +66,26 @@ def _compile(src: str, out_dir: str = BUILD_DIR, extra=()) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libsq.so; returns the library path."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    srcs = sources()
-    workers = min(len(srcs), max(1, min(8, os.cpu_count() or 1)))
-    with cf.ThreadPoolExecutor(workers) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp"
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source, link libsq.so and libsq_probe.so; returns libsq.so's path."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = sources() + [PROBE_SRC]
+    workers = min(len(srcs), max(1, min(8, os.cpu_count() or 1)))
+    with cf.ThreadPoolExecutor(workers) as ex:
+        objs = list(ex.map(_compile, srcs))
+    _link(objs[:-1], LIB)
+    _link(objs[-1:], PROBE_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 

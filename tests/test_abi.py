@@ -42,6 +42,21 @@ def test_header_symbols_exported(L):
         assert hasattr(L, name), name
 
 
+def test_probe_header_symbols_exported():
+    # the roofline probes of the benchmark: every function of include/sq_probe.h is exported
+    text = open(os.path.join(ROOT, "include", "sq_probe.h")).read()
+    declared = set(re.findall(r"^\s*(?:int32_t|const char\*)\s+(sq_probe_\w+)\s*\(", text, re.M))
+    assert declared == {"sq_probe_last_error", "sq_probe_mfma_i8", "sq_probe_copy", "sq_probe_read", "sq_probe_sleep"}
+    P = ctypes.CDLL(os.path.join(ROOT, "paper_2405_16406_amd", "libsq_probe.so"))
+    for name in declared:
+        assert hasattr(P, name), name
+    # host checks only (no launch)
+    P.sq_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    P.sq_probe_last_error.restype = ctypes.c_char_p
+    assert P.sq_probe_copy(fake(0), fake(0), 64, 1, None) == 1
+    assert b"overlap" in P.sq_probe_last_error()
+
+
 def test_abi_version(L):
     assert sq.abi_version() == 1
 
