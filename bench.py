@@ -485,14 +485,20 @@ def kv_config(torch, sq, workloads, dev, variants=False):
             fns.append(lambda qc=qc, kc=kc, vc=vc, o=o: sq.qk_had_kvquant(qc, kc, vc, out=o, **kw))
         return fns
 
-    def attn_fns(nbytes, **kw):
+    def attn_fns(nbytes, split=False, **kw):
+        # split: sq_attn_decode_kv4_split with one workspace (the calls are ordered on the stream)
+        ws = torch.empty(max(sq.attn_decode_workspace_bytes(B, S, H, D), 1), dtype=torch.uint8, device=dev)
         fns = []
         for _ in range(n_copies(nbytes)):
             o = sq.qk_had_kvquant(q, k, v, **kw)
             qr = o["q_rot"][:, -1].contiguous()
             oa = torch.empty_like(qr)
             cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
-            fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4(qr, *cache, out=oa))
+            if split:
+                fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4_split(qr, *cache, out=oa,
+                                                                                       workspace=ws))
+            else:
+                fns.append(lambda qr=qr, cache=cache, oa=oa: sq.attn_decode_kv4(qr, *cache, out=oa))
         return fns
 
     kk = {}
@@ -500,6 +506,8 @@ def kv_config(torch, sq, workloads, dev, variants=False):
     kk["kv_quant"] = entry(timed_calls(torch, sq, kv_fns(b)), b, "bytes")
     b = attn_bytes(B, S, H)
     kk["attn_decode"] = entry(timed_calls(torch, sq, attn_fns(b)), b, "bytes")
+    kk["attn_decode_split"] = entry(timed_calls(torch, sq, attn_fns(b, split=True)), b, "bytes")
+    kk["attn_decode_split"]["workspace_bytes"] = sq.attn_decode_workspace_bytes(B, S, H, D)
     if variants:
         b = kv_bytes(E, bits=8)
         kk["kv_quant_8bit"] = entry(timed_calls(torch, sq, kv_fns(b, bits=8)), b, "bytes")

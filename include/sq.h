@@ -318,6 +318,36 @@ sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const voi
                                 int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
                                 void* out, void* stream);
 
+/*
+ * sq_attn_decode_workspace -- device bytes of the workspace sq_attn_decode_kv4_split needs
+ * for B, S, H and D on the CURRENT device (the split depends on its compute-unit count):
+ * B * H * chunks * 528, where chunks is the number of pieces the S tokens are split into
+ * (0 bytes when they are not split).  Shape rules and errors of sq_attn_decode_kv4;
+ * SQ_ERR_NULL for a NULL bytes; SQ_ERR_HIP when the device cannot be queried.
+ */
+sq_status sq_attn_decode_workspace(int64_t B, int64_t S, int64_t H, int64_t D, uint64_t* bytes);
+
+/*
+ * sq_attn_decode_kv4_split -- the attention of sq_attn_decode_kv4_ex (same formula, Sec. 3.1
+ * R3 with eq. 1 dequantisation), split over the sequence as in flash-decoding: each
+ * workgroup reads one chunk of tokens for 16 heads at once, so the cache streams in whole
+ * token lines; a second kernel merges the chunks' partial softmax states (maximum, sum,
+ * 128 weighted dims, in fp32) in chunk order.  The result equals sq_attn_decode_kv4_ex's
+ * up to the order of fp32 additions, and is deterministic.
+ *   workspace        device memory, 16-byte aligned, at least the bytes
+ *                    sq_attn_decode_workspace gives (NULL allowed when that is 0); the
+ *                    caller owns it; its contents need no initialisation and are scratch
+ *                    after the call; it must not overlap any argument
+ *   workspace_bytes  its size in bytes
+ * Every other argument, layout and error as sq_attn_decode_kv4_ex; SQ_ERR_SHAPE when the
+ * workspace is too small, SQ_ERR_ALIGN / SQ_ERR_ALIAS for its alignment and overlaps.
+ * Calls that share a workspace must be ordered (same stream, or synchronised).
+ */
+sq_status sq_attn_decode_kv4_split(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                                   const uint8_t* v_q, const void* v_alpha, const void* v_beta,
+                                   int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
+                                   void* out, void* workspace, uint64_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -46,10 +46,12 @@ __device__ __forceinline__ float quad_xor(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, false));
 }
 
-// allreduce over the lanes with the same lane % 4 (the 16 token slots of a wave)
-template <typename Op>
+// allreduce over the token slots of a wave: the lanes with the same lane % 4 (HPW = 1, 16
+// slots) or lane % 8 (HPW = 2, 8 slots)
+template <int HPW = 1, typename Op>
 __device__ __forceinline__ float slots_reduce(float v, Op op) {
-  v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror:4
+  if constexpr (HPW == 1)
+    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror:4
   v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false)));  // row_ror:8
   const bool odd_row = (threadIdx.x >> 4) & 1, upper = (threadIdx.x >> 5) & 1;
   const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -70,21 +72,31 @@ __device__ __forceinline__ float rescale(float a, float b) {
   return a == -INFINITY ? 0.0f : exp2f(__fsub_rn(a, b));
 }
 
-template <bool P16>
-__global__ void __launch_bounds__(kThreads)
-attn_decode_kv4(AttnArgs a) {
-  __shared__ float red_ml[kWaves][2];
-  __shared__ float red_acc[kWaves][128];
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  const int tok = lane >> 2;
-  const int qd = lane & 3;
-  const int64_t G = a.B * a.H;
-  const int64_t i = blockIdx.x;
-  const int64_t x = (G % 8 == 0) ? (i % 8) * (G / 8) + i / 8 : i;
-  const int64_t b = x / a.H, h = x % a.H;
-  const int64_t S = a.S;
+// Partial attention state of one wave: running maximum m (base 2), and per lane the sums
+// over the tokens it has seen: l = sum p, acc_d = sum p alpha (1024 + c_d), pa = sum p alpha,
+// bsum = sum p beta.
+struct WaveAttn {
+  float m = -INFINITY, l = 0.0f, bsum = 0.0f, pa_sum = 0.0f;
+  float acc[32];
+};
 
+// One wave's pass over the batches first, first + step, ... (count of them) of 16 / HPW
+// tokens.  HPW = 1: every lane serves head (b, h); lane l = 4 tok + qd.  HPW = 2: the wave
+// serves heads h and h + 1 (one 128-byte piece of a token's line), lane l = 8 tok + 4 hp + qd
+// serves head h + hp; when h + 1 is past the heads, its lanes see no tokens.
+template <bool P16, int HPW = 1>
+__device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0, int first, int step, int count,
+                                       WaveAttn& st) {
+  static_assert(HPW == 1 || HPW == 2, "one or two heads per wave");
+  constexpr int TS = 16 / HPW;  // tokens per batch
+  const int lane = threadIdx.x & 63;
+  const int tok = lane >> (HPW == 2 ? 3 : 2);
+  const int hp = HPW == 2 ? (lane >> 2) & 1 : 0;
+  const int qd = lane & 3;
+  const int64_t S = a.S;
+  const int nh = HPW == 2 && h0 + 1 < a.H ? 2 : 1;  // heads of this wave
+  const bool hok = hp < nh;
+  const int64_t h = h0 + (hok ? hp : 0);             // this lane's head
   // ---- query: the lane's 32 dims as fp16 pairs (8w+e, 8w+e+4) matching the code pairs
   v2h qp[4][4];
   float qsum_lane = 0.0f;
@@ -110,8 +122,8 @@ attn_decode_kv4(AttnArgs a) {
   const float bias1024 = __fmul_rn(1024.0f, qsum_lane);
 
   // ---- cache of this (batch, head): token t at byte t * H * 64 (codes) / t * H * 4 (scales)
-  const int64_t row0 = b * S * a.H + h;
-  const int64_t cspan = ((S - 1) * a.H + 1) * 64;
+  const int64_t row0 = b * S * a.H + h0;
+  const int64_t cspan = ((S - 1) * a.H + nh) * 64;
   const __amdgpu_buffer_rsrc_t rk = rsrc(a.kq + row0 * 64, cspan);
   const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, cspan);
   const void* pb = qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb;  // this lane's scale array
@@ -119,27 +131,25 @@ attn_decode_kv4(AttnArgs a) {
   const uint32_t H32 = static_cast<uint32_t>(a.H), S32 = static_cast<uint32_t>(S);
   const uint32_t cstride = H32 * 64;
 
-  const int nb = static_cast<int>((S + 15) / 16);  // batches of 16 tokens
-  const int mine = nb > w ? (nb - w + kWaves - 1) / kWaves : 0;
   v4u kc[kDepth], vc[kDepth];
   float pv[kDepth];
   auto load = [&](int slot, int it) {
-    const uint32_t t = static_cast<uint32_t>(w + kWaves * it) * 16 + tok;
-    const bool ok = it < mine && t < S32;  // past the end: codes out of range (zeros), scale of token 0
-    const uint32_t co = ok ? t * cstride + 16 * qd : 0x80000000u;
+    const uint32_t t = static_cast<uint32_t>(first + step * it) * TS + tok;
+    const bool ok = hok && it < count && t < S32;  // else codes out of range (zeros), scale of token 0
+    const uint32_t co = ok ? t * cstride + 64 * hp + 16 * qd : 0x80000000u;
     kc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rk, co, 0, 0));
     vc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rv, co, 0, 0));
-    const int64_t pi = row0 + (ok ? t * H32 : 0u);
+    const int64_t pi = row0 + (ok ? t * H32 + hp : 0u);
     if constexpr (P16)
       pv[slot] = h2f(static_cast<const uint16_t*>(pb)[pi]);
     else
       pv[slot] = static_cast<const float*>(pb)[pi];
   };
 
-  float m = -INFINITY, l = 0.0f, bsum = 0.0f, pa_sum = 0.0f;
+  float m = st.m, l = st.l, bsum = st.bsum, pa_sum = st.pa_sum;
   float acc[32];
 #pragma unroll
-  for (int d = 0; d < 32; ++d) acc[d] = 0.0f;
+  for (int d = 0; d < 32; ++d) acc[d] = st.acc[d];
   const float cs = a.scale_log2e;
   // code pair masks kept in registers (a VOP3 and-or takes no literal operands)
   uint32_t kMask = 0x000F000Fu, kBase = 0x64006400u;
@@ -152,12 +162,12 @@ attn_decode_kv4(AttnArgs a) {
 
 #pragma unroll
   for (int d = 0; d < kDepth; ++d) load(d, d);
-  for (int it0 = 0; it0 < mine; it0 += kDepth) {
+  for (int it0 = 0; it0 < count; it0 += kDepth) {
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
       const int it = it0 + d;
-      const uint32_t t = static_cast<uint32_t>(w + kWaves * it) * 16 + tok;
-      const bool ok = it < mine && t < S32;  // uniform over the quad of a token
+      const uint32_t t = static_cast<uint32_t>(first + step * it) * TS + tok;
+      const bool ok = hok && it < count && t < S32;  // uniform over the quad of a token
       // q . c_t over the lane's 32 dims, then over the quad
       float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
@@ -175,8 +185,8 @@ attn_decode_kv4(AttnArgs a) {
       const float ka = quad_bcast<0>(pv[d]), kb = quad_bcast<1>(pv[d]);
       const float va = quad_bcast<2>(pv[d]), vb = quad_bcast<3>(pv[d]);
       const float s = ok ? __fmul_rn(cs, __fmaf_rn(ka, dot, __fmul_rn(kb, qsum))) : -INFINITY;
-      const float mb = slots_reduce(s, [](float u, float v) { return fmaxf(u, v); });
-      if (mb > m) {  // (wave-uniform) new running maximum: rescale what has been summed
+      const float mb = slots_reduce<HPW>(s, [](float u, float v) { return fmaxf(u, v); });
+      if (mb > m) {  // (uniform over a head's lanes) new running maximum: rescale the sums
         const float f = rescale(m, mb);
         l = __fmul_rn(l, f);
         bsum = __fmul_rn(bsum, f);
@@ -205,14 +215,48 @@ attn_decode_kv4(AttnArgs a) {
       load(d, it + kDepth);
     }
   }
-
-  // ---- the 16 token slots of the wave share m: their sums add up
-  auto add = [](float u, float v) { return __fadd_rn(u, v); };
-  l = slots_reduce(l, add);
-  bsum = slots_reduce(bsum, add);
-  pa_sum = slots_reduce(pa_sum, add);
+  st.m = m;
+  st.l = l;
+  st.bsum = bsum;
+  st.pa_sum = pa_sum;
 #pragma unroll
-  for (int e = 0; e < 32; ++e) acc[e] = slots_reduce(acc[e], add);
+  for (int d = 0; d < 32; ++d) st.acc[d] = acc[d];
+}
+
+// The token slots of a head share m: their sums add up (every lane ends with its head's
+// totals of its 32 dims).
+template <int HPW = 1>
+__device__ __forceinline__ void wave_total(WaveAttn& st) {
+  auto add = [](float u, float v) { return __fadd_rn(u, v); };
+  st.l = slots_reduce<HPW>(st.l, add);
+  st.bsum = slots_reduce<HPW>(st.bsum, add);
+  st.pa_sum = slots_reduce<HPW>(st.pa_sum, add);
+#pragma unroll
+  for (int e = 0; e < 32; ++e) st.acc[e] = slots_reduce<HPW>(st.acc[e], add);
+}
+
+template <bool P16>
+__global__ void __launch_bounds__(kThreads)
+attn_decode_kv4(AttnArgs a) {
+  __shared__ float red_ml[kWaves][2];
+  __shared__ float red_acc[kWaves][128];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int qd = lane & 3;
+  const int64_t G = a.B * a.H;
+  const int64_t i = blockIdx.x;
+  const int64_t x = (G % 8 == 0) ? (i % 8) * (G / 8) + i / 8 : i;
+  const int64_t b = x / a.H, h = x % a.H;
+  const int nb = static_cast<int>((a.S + 15) / 16);  // batches of 16 tokens
+  const int mine = nb > w ? (nb - w + kWaves - 1) / kWaves : 0;
+  WaveAttn st;
+#pragma unroll
+  for (int d = 0; d < 32; ++d) st.acc[d] = 0.0f;
+  attend<P16>(a, b, h, w, kWaves, mine, st);
+  wave_total(st);
+  const float m = st.m, l = st.l, bsum = st.bsum, pa_sum = st.pa_sum;
+  const float* acc = st.acc;
+
   // remove the 1024 offset of the code pairs and add the betas: the wave's dims
   const float off = __fmul_rn(1024.0f, pa_sum);
   if (lane < 4) {
@@ -242,7 +286,113 @@ attn_decode_kv4(AttnArgs a) {
       static_cast<uint32_t>(f2h(o0)) | (static_cast<uint32_t>(f2h(o1)) << 16);
 }
 
+// ---- split over the sequence (flash-decoding): workgroup (b, chunk c, group g of 16
+// heads) of 8 waves; wave w serves heads 16 g + 2 w and 16 g + 2 w + 1 over the chunk's
+// batches of 8 tokens, so each of its loads brings whole 128-byte lines (8 tokens x 128
+// bytes), where one wave per head uses half of every line it touches.  Two workgroups
+// share a CU.  Each head leaves its partial state (m, l, the 128 dims with the code offset
+// removed and the betas added) in part; the combine kernel merges the chunks of a head.
+// FINAL (a single chunk): the lanes divide and store the output themselves.
+constexpr int kSplitWaves = 8;
+
+template <bool P16, bool FINAL>
+__global__ void __launch_bounds__(64 * kSplitWaves, 4)
+attn_decode_part(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int qd = lane & 3;
+  const int hp = (lane >> 2) & 1;
+  // the workgroup count (B * chunks * NG, at most B * NG or about four times the CUs) fits 32 bits
+  const int NG = static_cast<int>((a.H + 15) / 16), NC = static_cast<int>(a.chunks);
+  const int g = static_cast<int>(blockIdx.x) % NG;
+  const int c = (static_cast<int>(blockIdx.x) / NG) % NC;
+  const int b = static_cast<int>(blockIdx.x) / NG / NC;
+  const int h0 = 16 * g + 2 * w;
+  if (h0 >= a.H) return;  // no workgroup barrier follows
+  const int nb = static_cast<int>((a.S + 7) / 8);  // batches of 8 tokens
+  const int first = 2 * c * static_cast<int>(a.chunk_batches);
+  const int count = min(2 * static_cast<int>(a.chunk_batches), nb - first);
+  WaveAttn st;
+#pragma unroll
+  for (int d = 0; d < 32; ++d) st.acc[d] = 0.0f;
+  attend<P16, 2>(a, b, h0, first, 1, count, st);
+  wave_total<2>(st);
+  const int h = h0 + hp;
+  if (lane >= 8 || h >= a.H) return;  // lanes 4 hp + qd of token slot 0 write
+  const float off = __fmul_rn(1024.0f, st.pa_sum);
+  float* dims = st.acc;  // in place: the lane's 32 dims
+#pragma unroll
+  for (int e = 0; e < 32; ++e) dims[e] = __fadd_rn(__fsub_rn(st.acc[e], off), st.bsum);
+  if constexpr (FINAL) {  // a chunk holds every token (l > 0: S >= 1)
+    uint32_t* o = reinterpret_cast<uint32_t*>(a.out + (static_cast<int64_t>(b) * a.H + h) * 128 + 32 * qd);
+#pragma unroll
+    for (int e = 0; e < 32; e += 2)
+      o[e / 2] = static_cast<uint32_t>(f2h(__fdiv_rn(dims[e], st.l))) |
+                 (static_cast<uint32_t>(f2h(__fdiv_rn(dims[e + 1], st.l))) << 16);
+  } else {
+    float* pr = a.part + ((static_cast<int64_t>(b) * a.H + h) * NC + c) * kAttnPart;
+    if (qd == 0) {
+      pr[0] = st.m;
+      pr[1] = st.l;
+    }
+    float4* pd = reinterpret_cast<float4*>(pr + 4 + 32 * qd);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pd[e] = make_float4(dims[4 * e], dims[4 * e + 1], dims[4 * e + 2], dims[4 * e + 3]);
+  }
+}
+
+// One wave per head: the chunks' states (at most 64) rescaled to their common maximum and
+// summed.  Lane c holds chunk c's maximum and sum; the dims (lane l finishes 2 l and 2 l + 1)
+// are loaded eight chunks at a time, all eight loads in flight together, and added in chunk
+// order.
+__global__ void __launch_bounds__(256)
+attn_decode_combine(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t x = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (x >= a.B * a.H) return;
+  const int NC = static_cast<int>(a.chunks);
+  const float* pr = a.part + x * NC * kAttnPart;
+  const float mc = lane < NC ? pr[lane * kAttnPart] : -INFINITY;
+  const float lc = lane < NC ? pr[lane * kAttnPart + 1] : 0.0f;
+  float M = mc;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  const float fc = rescale(mc, M);  // 0 for lanes past the chunks
+  float L = __fmul_rn(lc, fc);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) L = __fadd_rn(L, __shfl_xor(L, o));
+  float A0 = 0.0f, A1 = 0.0f;
+  for (int c0 = 0; c0 < NC; c0 += 8) {
+    float2 d[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      d[j] = c0 + j < NC ? reinterpret_cast<const float2*>(pr + (c0 + j) * kAttnPart + 4)[lane] : float2{0.0f, 0.0f};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fc), min(c0 + j, 63)));
+      A0 = __fmaf_rn(d[j].x, f, A0);
+      A1 = __fmaf_rn(d[j].y, f, A1);
+    }
+  }
+  reinterpret_cast<uint32_t*>(a.out + x * 128)[lane] =
+      static_cast<uint32_t>(f2h(__fdiv_rn(A0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(A1, L))) << 16);
+}
+
 }  // namespace
+
+hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream) {
+  const int64_t NG = (a.H + 15) / 16;
+  const unsigned parts = static_cast<unsigned>(a.B * a.chunks * NG);
+  const dim3 block(64 * kSplitWaves);
+  if (a.chunks == 1)
+    return a.param16 ? launch(attn_decode_part<true, true>, dim3(parts), block, 0, stream, a)
+                     : launch(attn_decode_part<false, true>, dim3(parts), block, 0, stream, a);
+  hipError_t e = a.param16 ? launch(attn_decode_part<true, false>, dim3(parts), block, 0, stream, a)
+                           : launch(attn_decode_part<false, false>, dim3(parts), block, 0, stream, a);
+  if (e != hipSuccess) return e;
+  const unsigned heads = static_cast<unsigned>((a.B * a.H + 3) / 4);
+  return launch(attn_decode_combine, dim3(heads), dim3(256), 0, stream, a);
+}
 
 hipError_t launch_attn_decode_kv4(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = static_cast<unsigned>(a.B * a.H);

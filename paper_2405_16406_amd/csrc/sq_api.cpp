@@ -408,11 +408,13 @@ sq_status sq_qk_had_kvquant(const void* q, const void* k, const void* v,
                               v_alpha, v_beta, dbg_k_rot, stream);
 }
 
-sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
-                                const uint8_t* v_q, const void* v_alpha, const void* v_beta,
-                                int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
-                                void* out, void* stream) {
-  TimingScope timing_scope;
+namespace {
+
+// Validation shared by the decode-attention entry points; fills a (apart from the split).
+sq_status attn_args(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                    const uint8_t* v_q, const void* v_alpha, const void* v_beta, int64_t B, int64_t S, int64_t H,
+                    int64_t D, float scale, int32_t param_bits, void* out, const void* workspace,
+                    uint64_t workspace_bytes, sq::AttnArgs& a) {
   if (!q_rot || !k_q || !k_alpha || !k_beta || !v_q || !v_alpha || !v_beta || !out)
     return fail(SQ_ERR_NULL, "q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta and out are required");
   if (B < 0 || S < 1 || H < 1) return fail(SQ_ERR_SHAPE, "need B >= 0, S >= 1, H >= 1");
@@ -425,17 +427,19 @@ sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const voi
                 param_bits);
   const uint64_t pb = static_cast<uint64_t>(param_bits / 8);
   if (!aligned(q_rot, 16) || !aligned(k_q, 16) || !aligned(v_q, 16) || !aligned(out, 16) || !aligned(k_alpha, pb) ||
-      !aligned(k_beta, pb) || !aligned(v_alpha, pb) || !aligned(v_beta, pb))
-    return fail(SQ_ERR_ALIGN, "q_rot, k_q, v_q and out need 16-byte alignment, group parameters their own size");
+      !aligned(k_beta, pb) || !aligned(v_alpha, pb) || !aligned(v_beta, pb) || !aligned(workspace, 16))
+    return fail(SQ_ERR_ALIGN,
+                "q_rot, k_q, v_q, out and the workspace need 16-byte alignment, group parameters their own size");
   const uint64_t heads = static_cast<uint64_t>(B) * static_cast<uint64_t>(H);
   const uint64_t cache = heads * static_cast<uint64_t>(S);
+  std::vector<Range> outs = {{out, heads * 256, "out"}};
+  if (workspace && workspace_bytes) outs.push_back({workspace, workspace_bytes, "workspace"});
   sq_status s = check_alias({{q_rot, heads * 256, "q_rot"}, {k_q, cache * 64, "k_q"}, {v_q, cache * 64, "v_q"},
                              {k_alpha, cache * pb, "k_alpha"}, {k_beta, cache * pb, "k_beta"},
                              {v_alpha, cache * pb, "v_alpha"}, {v_beta, cache * pb, "v_beta"}},
-                            {{out, heads * 256, "out"}});
+                            outs);
   if (s != SQ_OK) return s;
-  if (B == 0) return ok();
-  sq::AttnArgs a{};
+  a = sq::AttnArgs{};
   a.q = static_cast<const uint16_t*>(q_rot);
   a.kq = k_q;
   a.ka = k_alpha;
@@ -449,7 +453,69 @@ sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const voi
   a.scale_log2e = static_cast<float>(static_cast<double>(scale) * 1.4426950408889634);
   a.param16 = param_bits == 16;
   a.out = static_cast<uint16_t*>(out);
+  return SQ_OK;
+}
+
+// The sequence split on the current device, and the workspace bytes it needs.
+sq_status attn_split_here(int64_t B, int64_t S, int64_t H, int64_t& chunks, int64_t& chunk_batches,
+                          uint64_t& bytes) {
+  int cus = 0;
+  const hipError_t e = sq::device_cus(&cus);
+  if (e != hipSuccess) return hip_status(e, "compute-unit count of the current device");
+  sq::attn_split(B, S, H, cus, chunks, chunk_batches);
+  bytes = chunks > 1 ? static_cast<uint64_t>(B) * static_cast<uint64_t>(H) * static_cast<uint64_t>(chunks) *
+                           (sq::kAttnPart * 4)
+                     : 0;
+  return SQ_OK;
+}
+
+}  // namespace
+
+sq_status sq_attn_decode_kv4_ex(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                                const uint8_t* v_q, const void* v_alpha, const void* v_beta,
+                                int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
+                                void* out, void* stream) {
+  TimingScope timing_scope;
+  sq::AttnArgs a;
+  const sq_status s = attn_args(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, B, S, H, D, scale, param_bits,
+                                out, nullptr, 0, a);
+  if (s != SQ_OK) return s;
+  if (B == 0) return ok();
   return hip_status(sq::launch_attn_decode_kv4(a, static_cast<hipStream_t>(stream)), "attn_decode_kv4 launch");
+}
+
+sq_status sq_attn_decode_workspace(int64_t B, int64_t S, int64_t H, int64_t D, uint64_t* bytes) {
+  if (!bytes) return fail(SQ_ERR_NULL, "bytes is required");
+  if (B < 0 || S < 1 || H < 1) return fail(SQ_ERR_SHAPE, "need B >= 0, S >= 1, H >= 1");
+  if (D != 128) return fail(SQ_ERR_UNSUPPORTED, "D=%lld: only head_dim 128 is implemented", (long long)D);
+  if (B * H >= (int64_t{1} << 31) || S >= (int64_t{1} << 31) / (H * 64))
+    return fail(SQ_ERR_SHAPE, "B*H=%lld or S*H*64 beyond 2^31", (long long)(B * H));
+  int64_t chunks = 1, cb = 0;
+  uint64_t need = 0;
+  const sq_status s = attn_split_here(B, S, H, chunks, cb, need);
+  if (s != SQ_OK) return s;
+  *bytes = need;
+  return ok();
+}
+
+sq_status sq_attn_decode_kv4_split(const void* q_rot, const uint8_t* k_q, const void* k_alpha, const void* k_beta,
+                                   const uint8_t* v_q, const void* v_alpha, const void* v_beta,
+                                   int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
+                                   void* out, void* workspace, uint64_t workspace_bytes, void* stream) {
+  TimingScope timing_scope;
+  sq::AttnArgs a;
+  sq_status s = attn_args(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, B, S, H, D, scale, param_bits, out,
+                          workspace, workspace_bytes, a);
+  if (s != SQ_OK) return s;
+  if (B == 0) return ok();
+  uint64_t need = 0;
+  s = attn_split_here(B, S, H, a.chunks, a.chunk_batches, need);
+  if (s != SQ_OK) return s;
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(SQ_ERR_SHAPE, "workspace of %llu bytes, %llu needed", (unsigned long long)workspace_bytes,
+                (unsigned long long)need);
+  a.part = static_cast<float*>(workspace);
+  return hip_status(sq::launch_attn_decode_split(a, static_cast<hipStream_t>(stream)), "attn_decode_split launch");
 }
 
 sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,

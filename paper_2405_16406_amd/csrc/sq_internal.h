@@ -83,9 +83,32 @@ struct AttnArgs {
   int64_t B, S, H;       // S * H * 64 < 2^31 (32-bit buffer offsets per head)
   float scale_log2e;     // score scale times log2(e)
   uint16_t* out;         // fp16 [B, H, 128]
+  // split over the sequence: chunks of chunk_batches batches of 16 tokens, partial softmax
+  // states in part (float [B, H, chunks, kAttnPart]); chunks == 1 needs no part
+  int64_t chunks = 1;
+  int64_t chunk_batches = 0;
+  float* part = nullptr;
 };
 
+constexpr int kAttnPart = 132;  // floats per partial state: m, l, 2 unused, 128 dims
+
+// Chunks of the sequence split for a device with `cus` compute units: enough (batch,
+// chunk, 16-head group) workgroups to give every CU two; at least 4 batches of 16 tokens a
+// chunk, at most 64 chunks (one per lane of the combine).
+inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks, int64_t& chunk_batches) {
+  const int64_t nb = (S + 15) / 16;
+  const int64_t groups = B * ((H + 15) / 16);
+  const int64_t slots = 2 * static_cast<int64_t>(cus);
+  int64_t want = groups < slots ? (slots + groups - 1) / groups : 1;
+  const int64_t most = (nb + 3) / 4 < 64 ? (nb + 3) / 4 : 64;
+  if (want > most) want = most;
+  if (want < 1) want = 1;
+  chunk_batches = (nb + want - 1) / want;
+  chunks = (nb + chunk_batches - 1) / chunk_batches;
+}
+
 hipError_t launch_attn_decode_kv4(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream);
 
 struct KvArgs {
   const uint16_t* q;
@@ -143,6 +166,29 @@ hipError_t blocks_per_cu(int threads, int lds, int* out) {
     cached.store(v, std::memory_order_release);
   }
   *out = v;
+  return hipSuccess;
+}
+
+// Compute units of the current device (queried per device and cached; a failed query is
+// not remembered).
+inline hipError_t device_cus(int* out) {
+  static std::atomic<int> cached[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) {
+    const int v = cached[dev].load(std::memory_order_acquire);
+    if (v > 0) {
+      *out = v;
+      return hipSuccess;
+    }
+  }
+  int n = 0;
+  e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (n < 1) n = 1;
+  if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_release);
+  *out = n;
   return hipSuccess;
 }
 

@@ -22,7 +22,7 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
            "sq_had_quant_act_ex", "sq_pack_w4", "sq_pack_w4_ex", "sq_w4a4_linear", "sq_w4a8_linear",
            "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_qk_had_kvquant_ex", "sq_attn_decode_kv4",
-           "sq_attn_decode_kv4_ex")
+           "sq_attn_decode_kv4_ex", "sq_attn_decode_workspace", "sq_attn_decode_kv4_split")
 
 
 class SqError(RuntimeError):
@@ -85,6 +85,11 @@ def load(path: str) -> ctypes.CDLL:
     L.sq_attn_decode_kv4.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _P, _P]
     L.sq_attn_decode_kv4_ex.restype = _I32
     L.sq_attn_decode_kv4_ex.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32, _P, _P]
+    L.sq_attn_decode_workspace.restype = _I32
+    L.sq_attn_decode_workspace.argtypes = [_I64, _I64, _I64, _I64, _P]
+    L.sq_attn_decode_kv4_split.restype = _I32
+    L.sq_attn_decode_kv4_split.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32, _P, _P,
+                                           ctypes.c_uint64, _P]
     return L
 
 
@@ -295,6 +300,40 @@ def qk_had_kvquant(q, k, v, dbg: bool = False, out=None, bits: int = 4, k_clip: 
                                           float(v_clip), pbits, *outs), "sq_qk_had_kvquant_ex")
     out = dict(out)
     out["k_rot"] = kr
+    return out
+
+
+def attn_decode_workspace_bytes(B, S, H, D=128):
+    """Device bytes of the workspace attn_decode_kv4_split needs on the current device."""
+    n = ctypes.c_uint64(0)
+    _check(lib().sq_attn_decode_workspace(B, S, H, D, ctypes.byref(n)), "sq_attn_decode_workspace")
+    return n.value
+
+
+def attn_decode_kv4_split(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None, out=None, workspace=None):
+    """attn_decode_kv4 split over the sequence (sq_attn_decode_kv4_split).  workspace: a
+    uint8 device tensor of at least attn_decode_workspace_bytes() bytes, allocated here
+    when None.  Returns out fp16 [B, H, 128]."""
+    _need(q_rot, torch.float16, "q_rot")
+    for t, nme in ((q_rot, "q_rot"), (k_q, "k_q"), (v_q, "v_q"), (k_alpha, "k_alpha"), (k_beta, "k_beta"),
+                   (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        if not t.is_contiguous():
+            raise ValueError(f"{nme} must be contiguous")
+    B, H, D = q_rot.shape
+    S = k_q.shape[1]
+    scale = 1.0 / D ** 0.5 if scale is None else scale
+    out = torch.empty_like(q_rot) if out is None else out
+    pdt = k_alpha.dtype
+    for t, nme in ((k_alpha, "k_alpha"), (k_beta, "k_beta"), (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        _need(t, pdt, nme)
+    if workspace is None:
+        workspace = torch.empty(max(attn_decode_workspace_bytes(B, S, H, D), 1), dtype=torch.uint8,
+                                device=q_rot.device)
+    _need(workspace, torch.uint8, "workspace")
+    _check(lib().sq_attn_decode_kv4_split(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q),
+                                          _ptr(v_alpha), _ptr(v_beta), B, S, H, D, float(scale),
+                                          {torch.float32: 32, torch.float16: 16}[pdt], _ptr(out), _ptr(workspace),
+                                          workspace.numel(), _stream(q_rot)), "sq_attn_decode_kv4_split")
     return out
 
 

@@ -316,6 +316,34 @@ def test_attn_decode_ex_validation(L):
     assert call(out=ctypes.c_void_p(fake(2).value)) == sq.SQ_ERR_ALIAS
 
 
+def attn_split(L, B=2, S=4, H=2, D=128, scale=0.1, pbits=32, ws_bytes=1 << 20, **kw):
+    ptrs = [fake(i) for i in range(9)]
+    for i, nm in enumerate(("q", "kq", "ka", "kb", "vq", "va", "vb", "out", "ws")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_attn_decode_kv4_split(*ptrs[:7], B, S, H, D, ctypes.c_float(scale), pbits, ptrs[7], ptrs[8],
+                                      ws_bytes, None)
+
+
+def test_attn_decode_split_validation(L):
+    # the argument checks that come before the device is asked for its compute units
+    assert attn_split(L, out=None) == sq.SQ_ERR_NULL
+    assert attn_split(L, S=0) == sq.SQ_ERR_SHAPE
+    assert attn_split(L, D=64) == sq.SQ_ERR_UNSUPPORTED
+    assert attn_split(L, pbits=8) == sq.SQ_ERR_UNSUPPORTED
+    assert attn_split(L, ws=ctypes.c_void_p(fake(8).value + 4)) == sq.SQ_ERR_ALIGN
+    assert attn_split(L, ws=ctypes.c_void_p(fake(1).value)) == sq.SQ_ERR_ALIAS       # over k_q
+    assert attn_split(L, ws=ctypes.c_void_p(fake(7).value + 256)) == sq.SQ_ERR_ALIAS  # over out
+    assert attn_split(L, B=0) == sq.SQ_OK
+    assert attn_split(L, B=0, ws=None, ws_bytes=0) == sq.SQ_OK
+    n = ctypes.c_uint64(7)
+    assert L.sq_attn_decode_workspace(2, 4, 2, 128, None) == sq.SQ_ERR_NULL
+    assert L.sq_attn_decode_workspace(2, 0, 2, 128, ctypes.byref(n)) == sq.SQ_ERR_SHAPE
+    assert L.sq_attn_decode_workspace(2, 4, 2, 64, ctypes.byref(n)) == sq.SQ_ERR_UNSUPPORTED
+    assert L.sq_attn_decode_workspace(1, 1 << 24, 4, 128, ctypes.byref(n)) == sq.SQ_ERR_SHAPE
+    assert n.value == 7
+
+
 @pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU driver is present: the calls below would "
                     "launch kernels on fake pointers")
 def test_no_device_is_a_hip_error(L):
@@ -329,6 +357,9 @@ def test_no_device_is_a_hip_error(L):
     assert lin_sw(L) == sq.SQ_ERR_HIP
     assert kvq(L) == sq.SQ_ERR_HIP
     assert attn(L) == sq.SQ_ERR_HIP
+    assert attn_split(L) == sq.SQ_ERR_HIP  # the split asks the device for its compute units
+    n = ctypes.c_uint64(0)
+    assert L.sq_attn_decode_workspace(8, 2048, 32, 128, ctypes.byref(n)) == sq.SQ_ERR_HIP
     assert L.sq_pack_w4(fake(0), 8, 256, 256, 1, None, 1, fake(1), fake(2), fake(3), None) == sq.SQ_ERR_HIP
     # a later failing check still reports its own status and message
     assert hqa(L, x=None) == sq.SQ_ERR_NULL

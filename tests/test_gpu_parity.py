@@ -662,15 +662,17 @@ def test_w4a8_rotated_chain():
 
 # ---------------------------------------------------------------- decode attention
 
-def attn_case(B, S, H, seed, scale=None, qscale=2.0):
-    """GPU sq_attn_decode_kv4 vs oracle.attn_decode on a random 4-bit cache."""
+def attn_case(B, S, H, seed, scale=None, qscale=2.0, split=False):
+    """GPU sq_attn_decode_kv4 (split: sq_attn_decode_kv4_split) vs oracle.attn_decode on a
+    random 4-bit cache."""
     rng = workloads.rng_for(seed)
     kc, vc = rng.integers(0, 16, (B, S, H, 128)), rng.integers(0, 16, (B, S, H, 128))
     ka, va = (rng.uniform(0.01, 0.2, (B, S, H)).astype(np.float32) for _ in range(2))
     kb, vb = (rng.uniform(-1.5, 0.0, (B, S, H)).astype(np.float32) for _ in range(2))
     q = (rng.standard_normal((B, H, 128)) * qscale).astype(np.float16)
     kq, vq = oq.pack_nibbles(kc), oq.pack_nibbles(vc)
-    out = sq.attn_decode_kv4(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb), scale=scale)
+    fn = sq.attn_decode_kv4_split if split else sq.attn_decode_kv4
+    out = fn(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb), scale=scale)
     ref = okv.attn_decode(q, kq, ka, kb, vq, va, vb, scale)
     got = host(out)
     assert np.isfinite(got).all()
@@ -687,29 +689,85 @@ def test_attn_decode_shapes(B, S, H):
     attn_case(B, S, H, seed=600 + B + S + H)
 
 
-def test_attn_decode_degenerate_scores():
-    say("attn_decode_kv4: scale 0 (mean of V), a sharp softmax, a single token")
-    got, ref, V = attn_case(2, 37, 3, seed=7, scale=0.0)
+@pytest.mark.parametrize("split", [False, True])
+def test_attn_decode_degenerate_scores(split):
+    say(f"attn_decode_kv4 (split={split}): scale 0 (mean of V), a sharp softmax, a single token")
+    got, ref, V = attn_case(2, 37, 3, seed=7, scale=0.0, split=split)
     parity.assert_out_close(got, V.mean(axis=1).astype(np.float16))
-    attn_case(2, 200, 2, seed=8, scale=1.0, qscale=8.0)
-    got, ref, V = attn_case(1, 1, 4, seed=9)
+    attn_case(2, 200, 2, seed=8, scale=1.0, qscale=8.0, split=split)
+    attn_case(1, 3000, 2, seed=10, scale=1.0, qscale=8.0, split=split)  # sharp, over many chunks
+    got, ref, V = attn_case(1, 1, 4, seed=9, split=split)
     parity.assert_out_close(got, V[:, 0].astype(np.float16))
+
+
+@pytest.mark.parametrize("B,S,H", [(1, 1, 1), (1, 5, 3), (2, 17, 2), (1, 129, 4), (1, 300, 5), (2, 4099, 4),
+                                   (1, 1000, 33), (3, 777, 17), (1, 4096, 2), (1, 20000, 3), (8, 2048, 32)])
+def test_attn_decode_split_shapes(B, S, H):
+    # one chunk (the output written by the partial kernel) and many, up to the 64 the
+    # combine takes; ragged chunks and batches; odd head counts (a wave's second head
+    # missing) and counts below, at and past a 16-head group; the full [8, 2048, 32] cache
+    nbytes = sq.attn_decode_workspace_bytes(B, S, H)
+    say(f"attn_decode_kv4_split B={B} S={S} H={H} workspace {nbytes} bytes")
+    attn_case(B, S, H, seed=640 + B + S + H, split=True)
+
+
+def test_attn_decode_split_matches_unsplit():
+    # the two kernels sum in different orders: their outputs agree to fp16 rounding
+    say("attn_decode_kv4_split vs attn_decode_kv4 on the chain cache [2,1500,32,128]")
+    q, k, v = (dev(t) for t in workloads.kv_inputs(B=2, S=1500, H=32, D=128))
+    o = sq.qk_had_kvquant(q, k, v)
+    qr = o["q_rot"][:, -1].contiguous()
+    cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+    a = host(sq.attn_decode_kv4(qr, *cache)).astype(np.float32)
+    b = host(sq.attn_decode_kv4_split(qr, *cache)).astype(np.float32)
+    np.testing.assert_allclose(b, a, rtol=4e-3, atol=2e-3 * np.abs(a).max())
+
+
+def test_attn_decode_split_workspace_checks():
+    say("attn_decode_kv4_split: workspace too small, misaligned, overlapping, NULL")
+    B, S, H = 1, 1000, 8
+    rng = workloads.rng_for(650)
+    kq, vq = (dev(rng.integers(0, 256, (B, S, H, 64), dtype=np.uint8)) for _ in range(2))
+    ka, kb, va, vb = (dev(rng.uniform(0.01, 0.2, (B, S, H)).astype(np.float32)) for _ in range(4))
+    q = dev(rng.standard_normal((B, H, 128)).astype(np.float16))
+    need = sq.attn_decode_workspace_bytes(B, S, H)
+    assert need > 0 and need % 528 == 0
+    args = (q, kq, ka, kb, vq, va, vb)
+    with pytest.raises(sq.SqError, match="SQ_ERR_SHAPE"):
+        sq.attn_decode_kv4_split(*args, workspace=torch.empty(need - 16, dtype=torch.uint8, device="cuda"))
+    big = torch.empty(need + 64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sq.SqError, match="SQ_ERR_ALIGN"):
+        sq.attn_decode_kv4_split(*args, workspace=big[4:need + 4])
+    with pytest.raises(sq.SqError, match="SQ_ERR_ALIAS"):
+        sq.attn_decode_kv4_split(*args, out=big[:B * H * 256].view(torch.float16).view(B, H, 128), workspace=big)
+    L = sq.lib()
+    st = L.sq_attn_decode_kv4_split(q.data_ptr(), kq.data_ptr(), ka.data_ptr(), kb.data_ptr(), vq.data_ptr(),
+                                    va.data_ptr(), vb.data_ptr(), B, S, H, 128, 0.1, 32,
+                                    torch.empty_like(q).data_ptr(), None, 0, None)
+    assert st == sq.SQ_ERR_SHAPE
+    # exactly the bytes asked for, and a B == 0 no-op with no workspace
+    out = sq.attn_decode_kv4_split(*args, workspace=torch.empty(need, dtype=torch.uint8, device="cuda"))
+    parity.assert_out_close(host(out), okv.attn_decode(*(host(t) for t in args)))
+    e = torch.empty_like(q)
+    assert L.sq_attn_decode_kv4_split(q.data_ptr(), kq.data_ptr(), ka.data_ptr(), kb.data_ptr(), vq.data_ptr(),
+                                      va.data_ptr(), vb.data_ptr(), 0, S, H, 128, 0.1, 32, e.data_ptr(), None, 0,
+                                      None) == sq.SQ_OK
 
 
 def test_attn_decode_after_kv_quant_full():
     # the whole consumer chain at [8, 2048, 32, 128]: R3 + KV4 on the GPU, then the last
     # token's rotated query attends over the cache the GPU wrote; oracle on two batches
-    say("qk_had_kvquant -> attn_decode_kv4 [8, 2048, 32, 128], last token's query")
+    say("qk_had_kvquant -> attn_decode_kv4 and _split [8, 2048, 32, 128], last token's query")
     q, k, v = workloads.kv_inputs()
     o = sq.qk_had_kvquant(dev(q), dev(k), dev(v))
     qr = o["q_rot"][:, -1].contiguous()
-    out = sq.attn_decode_kv4(qr, o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
-    got = host(out)
-    for b in (0, 7):
-        sl = slice(b, b + 1)
-        ref = okv.attn_decode(host(qr)[sl], host(o["k_q"])[sl], host(o["k_alpha"])[sl], host(o["k_beta"])[sl],
-                              host(o["v_q"])[sl], host(o["v_alpha"])[sl], host(o["v_beta"])[sl])
-        parity.assert_out_close(got[sl], ref)
+    cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
+    for fn in (sq.attn_decode_kv4, sq.attn_decode_kv4_split):
+        got = host(fn(qr, *cache))
+        for b in (0, 7):
+            sl = slice(b, b + 1)
+            ref = okv.attn_decode(host(qr)[sl], *(host(t)[sl] for t in cache))
+            parity.assert_out_close(got[sl], ref)
 
 
 # ---------------------------------------------------------------- chain
@@ -827,14 +885,16 @@ def test_attn_decode_fp16_params():
     kb, vb = (rng.uniform(-1.5, 0.0, (B, S, H)).astype(np.float16) for _ in range(2))
     q = (rng.standard_normal((B, H, 128)) * 2).astype(np.float16)
     kq, vq = oq.pack_nibbles(kc), oq.pack_nibbles(vc)
-    out = sq.attn_decode_kv4(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb))
-    parity.assert_out_close(host(out), okv.attn_decode(q, kq, ka, kb, vq, va, vb))
+    for fn in (sq.attn_decode_kv4, sq.attn_decode_kv4_split):
+        out = fn(dev(q), dev(kq), dev(ka), dev(kb), dev(vq), dev(va), dev(vb))
+        parity.assert_out_close(host(out), okv.attn_decode(q, kq, ka, kb, vq, va, vb))
     qh, kh, vh = workloads.kv_inputs(1, 257, 4, 128)
     o = sq.qk_had_kvquant(dev(qh), dev(kh), dev(vh), param_dtype=torch.float16)
     qr = o["q_rot"][:, -1].contiguous()
     cache = [o[n] for n in ("k_q", "k_alpha", "k_beta", "v_q", "v_alpha", "v_beta")]
-    got = host(sq.attn_decode_kv4(qr, *cache))
-    parity.assert_out_close(got, okv.attn_decode(host(qr), *[host(t) for t in cache]))
+    for fn in (sq.attn_decode_kv4, sq.attn_decode_kv4_split):
+        got = host(fn(qr, *cache))
+        parity.assert_out_close(got, okv.attn_decode(host(qr), *[host(t) for t in cache]))
 
 
 def test_kv8_small_and_sampled():
@@ -1009,8 +1069,9 @@ def test_kv_and_attention_deterministic():
     o = outs[0]
     qr = o["q_rot"][:, -1].contiguous()
     cache = (o["k_q"], o["k_alpha"], o["k_beta"], o["v_q"], o["v_alpha"], o["v_beta"])
-    att = [host(sq.attn_decode_kv4(qr, *cache)).view(np.uint16) for _ in range(2)]
-    np.testing.assert_array_equal(att[0], att[1])
+    for fn in (sq.attn_decode_kv4, sq.attn_decode_kv4_split):
+        att = [host(fn(qr, *cache)).view(np.uint16) for _ in range(2)]
+        np.testing.assert_array_equal(att[0], att[1])
 
 
 def test_time_next_call_events():
