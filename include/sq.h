@@ -348,6 +348,24 @@ sq_status sq_attn_decode_kv4_split(const void* q_rot, const uint8_t* k_q, const 
                                    int64_t B, int64_t S, int64_t H, int64_t D, float scale, int32_t param_bits,
                                    void* out, void* workspace, uint64_t workspace_bytes, void* stream);
 
+/*
+ * sq_attn_decode_kv4_split_noalloc -- sq_attn_decode_kv4_split for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid it): the same kernels, with the partial states in the library's own scratch, a
+ * file-scope device array of 8 MiB per GPU, held from its first use until the process
+ * ends.  The call allocates nothing and frees nothing.
+ * The scratch is shared by every call on the same GPU and keeps the last call's contents
+ * (no part of it needs clearing: a call writes every state it reads).  Calls that overlap
+ * on one GPU race: order them (same stream, or synchronised).
+ * Arguments, layouts and errors as sq_attn_decode_kv4_split without the workspace;
+ * SQ_ERR_SHAPE when the split needs more than the 8 MiB (sq_attn_decode_workspace gives
+ * the bytes; on MI355X no valid shape needs more than about 4.3 MiB).
+ */
+sq_status sq_attn_decode_kv4_split_noalloc(const void* q_rot, const uint8_t* k_q, const void* k_alpha,
+                                           const void* k_beta, const uint8_t* v_q, const void* v_alpha,
+                                           const void* v_beta, int64_t B, int64_t S, int64_t H, int64_t D,
+                                           float scale, int32_t param_bits, void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,6 +23,8 @@
 // Workgroup i serves head index x(i) = (i % 8) * (G / 8) + i / 8 when the G = B * H heads
 // are a multiple of 8: workgroups go round-robin over the 8 XCDs, so heads h and h + 1 (the
 // two 64-byte halves of a 128-byte line of a token) are read through the same L2.
+#include <mutex>
+
 #include "sq_device.h"
 #include "sq_internal.h"
 
@@ -378,7 +380,30 @@ attn_decode_combine(AttnArgs a) {
       static_cast<uint32_t>(f2h(__fdiv_rn(A0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(A1, L))) << 16);
 }
 
+// Partial states of the allocation-free split attention: one array per device, kept until
+// the process ends.  Host code uses its device address from hipGetSymbolAddress, never
+// the array's name.
+static __device__ __align__(256) unsigned char scratch[kAttnScratchBytes];
+
 }  // namespace
+
+hipError_t attn_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {  // once per device, with that device current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream) {
   const int64_t NG = (a.H + 15) / 16;

@@ -518,6 +518,29 @@ sq_status sq_attn_decode_kv4_split(const void* q_rot, const uint8_t* k_q, const 
   return hip_status(sq::launch_attn_decode_split(a, static_cast<hipStream_t>(stream)), "attn_decode_split launch");
 }
 
+sq_status sq_attn_decode_kv4_split_noalloc(const void* q_rot, const uint8_t* k_q, const void* k_alpha,
+                                           const void* k_beta, const uint8_t* v_q, const void* v_alpha,
+                                           const void* v_beta, int64_t B, int64_t S, int64_t H, int64_t D,
+                                           float scale, int32_t param_bits, void* out, void* stream) {
+  TimingScope timing_scope;
+  sq::AttnArgs a;
+  sq_status s = attn_args(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, B, S, H, D, scale, param_bits, out,
+                          nullptr, 0, a);
+  if (s != SQ_OK) return s;
+  if (B == 0) return ok();
+  uint64_t need = 0;
+  s = attn_split_here(B, S, H, a.chunks, a.chunk_batches, need);
+  if (s != SQ_OK) return s;
+  if (need > sq::kAttnScratchBytes)
+    return fail(SQ_ERR_SHAPE, "the split needs %llu bytes of scratch; this entry point has %llu",
+                (unsigned long long)need, (unsigned long long)sq::kAttnScratchBytes);
+  void* scratch = nullptr;
+  const hipError_t e = sq::attn_scratch(&scratch);
+  if (e != hipSuccess) return hip_status(e, "address of the attention scratch");
+  a.part = static_cast<float*>(scratch);
+  return hip_status(sq::launch_attn_decode_split(a, static_cast<hipStream_t>(stream)), "attn_decode_split launch");
+}
+
 sq_status sq_attn_decode_kv4(const void* q_rot, const uint8_t* k_q, const float* k_alpha, const float* k_beta,
                              const uint8_t* v_q, const float* v_alpha, const float* v_beta,
                              int64_t B, int64_t S, int64_t H, int64_t D, float scale, void* out, void* stream) {

@@ -110,6 +110,12 @@ inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks
 hipError_t launch_attn_decode_kv4(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream);
 
+// The library's own scratch for the allocation-free split attention: 8 MiB per device (the
+// split of any shape on a device of up to 1000 CUs needs less).
+constexpr uint64_t kAttnScratchBytes = uint64_t{8} << 20;
+// Device address of that scratch on the current device (looked up once per device).
+hipError_t attn_scratch(void** ptr);
+
 struct KvArgs {
   const uint16_t* q;
   const uint16_t* k;

@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_UNSU
 EXPORTS = ("sq_abi_version", "sq_last_error", "sq_time_next_call", "sq_hadamard_factor", "sq_had_quant_act",
            "sq_had_quant_act_ex", "sq_pack_w4", "sq_pack_w4_ex", "sq_w4a4_linear", "sq_w4a8_linear",
            "sq_w4a4_linear_swiglu", "sq_qk_had_kvquant", "sq_qk_had_kvquant_ex", "sq_attn_decode_kv4",
-           "sq_attn_decode_kv4_ex", "sq_attn_decode_workspace", "sq_attn_decode_kv4_split")
+           "sq_attn_decode_kv4_ex", "sq_attn_decode_workspace", "sq_attn_decode_kv4_split",
+           "sq_attn_decode_kv4_split_noalloc")
 
 
 class SqError(RuntimeError):
@@ -90,6 +91,9 @@ def load(path: str) -> ctypes.CDLL:
     L.sq_attn_decode_kv4_split.restype = _I32
     L.sq_attn_decode_kv4_split.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32, _P, _P,
                                            ctypes.c_uint64, _P]
+    L.sq_attn_decode_kv4_split_noalloc.restype = _I32
+    L.sq_attn_decode_kv4_split_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _I64, _F32, _I32,
+                                                   _P, _P]
     return L
 
 
@@ -334,6 +338,28 @@ def attn_decode_kv4_split(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, sca
                                           _ptr(v_alpha), _ptr(v_beta), B, S, H, D, float(scale),
                                           {torch.float32: 32, torch.float16: 16}[pdt], _ptr(out), _ptr(workspace),
                                           workspace.numel(), _stream(q_rot)), "sq_attn_decode_kv4_split")
+    return out
+
+
+def attn_decode_kv4_split_noalloc(q_rot, k_q, k_alpha, k_beta, v_q, v_alpha, v_beta, scale=None, out=None):
+    """attn_decode_kv4_split with the library's own scratch (sq_attn_decode_kv4_split_noalloc):
+    the call allocates no device memory (out must then be given).  Returns out."""
+    _need(q_rot, torch.float16, "q_rot")
+    for t, nme in ((q_rot, "q_rot"), (k_q, "k_q"), (v_q, "v_q"), (k_alpha, "k_alpha"), (k_beta, "k_beta"),
+                   (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        if not t.is_contiguous():
+            raise ValueError(f"{nme} must be contiguous")
+    B, H, D = q_rot.shape
+    S = k_q.shape[1]
+    scale = 1.0 / D ** 0.5 if scale is None else scale
+    out = torch.empty_like(q_rot) if out is None else out
+    pdt = k_alpha.dtype
+    for t, nme in ((k_alpha, "k_alpha"), (k_beta, "k_beta"), (v_alpha, "v_alpha"), (v_beta, "v_beta")):
+        _need(t, pdt, nme)
+    _check(lib().sq_attn_decode_kv4_split_noalloc(_ptr(q_rot), _ptr(k_q), _ptr(k_alpha), _ptr(k_beta), _ptr(v_q),
+                                                  _ptr(v_alpha), _ptr(v_beta), B, S, H, D, float(scale),
+                                                  {torch.float32: 32, torch.float16: 16}[pdt], _ptr(out),
+                                                  _stream(q_rot)), "sq_attn_decode_kv4_split_noalloc")
     return out
 
 

@@ -325,6 +325,23 @@ def attn_split(L, B=2, S=4, H=2, D=128, scale=0.1, pbits=32, ws_bytes=1 << 20, *
                                       ws_bytes, None)
 
 
+def attn_noalloc(L, B=2, S=4, H=2, D=128, scale=0.1, pbits=32, **kw):
+    ptrs = [fake(i) for i in range(8)]
+    for i, nm in enumerate(("q", "kq", "ka", "kb", "vq", "va", "vb", "out")):
+        if nm in kw:
+            ptrs[i] = kw[nm]
+    return L.sq_attn_decode_kv4_split_noalloc(*ptrs[:7], B, S, H, D, ctypes.c_float(scale), pbits, ptrs[7], None)
+
+
+def test_attn_decode_noalloc_validation(L):
+    assert attn_noalloc(L, out=None) == sq.SQ_ERR_NULL
+    assert attn_noalloc(L, H=0) == sq.SQ_ERR_SHAPE
+    assert attn_noalloc(L, D=64) == sq.SQ_ERR_UNSUPPORTED
+    assert attn_noalloc(L, out=ctypes.c_void_p(fake(7).value + 8)) == sq.SQ_ERR_ALIGN
+    assert attn_noalloc(L, out=ctypes.c_void_p(fake(0).value)) == sq.SQ_ERR_ALIAS
+    assert attn_noalloc(L, B=0) == sq.SQ_OK
+
+
 def test_attn_decode_split_validation(L):
     # the argument checks that come before the device is asked for its compute units
     assert attn_split(L, out=None) == sq.SQ_ERR_NULL
@@ -358,6 +375,7 @@ def test_no_device_is_a_hip_error(L):
     assert kvq(L) == sq.SQ_ERR_HIP
     assert attn(L) == sq.SQ_ERR_HIP
     assert attn_split(L) == sq.SQ_ERR_HIP  # the split asks the device for its compute units
+    assert attn_noalloc(L) == sq.SQ_ERR_HIP
     n = ctypes.c_uint64(0)
     assert L.sq_attn_decode_workspace(8, 2048, 32, 128, ctypes.byref(n)) == sq.SQ_ERR_HIP
     assert L.sq_pack_w4(fake(0), 8, 256, 256, 1, None, 1, fake(1), fake(2), fake(3), None) == sq.SQ_ERR_HIP
