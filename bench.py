@@ -133,6 +133,9 @@ TRAFFIC_MAP = {
     "c3/down_gemm": ("c3", "w4a4_gemm_ring<2, 4, 4, 2, 4, 1, 1, false>", 131072),
     "c4/kv_quant": ("c4", "qk_had_kvquant_v2<true, 4, false>", 2097152),
     "c4/attn_decode": ("c4", "attn_decode_kv4<false>", 262144),
+    # two kernels (on 256 CUs: 32 chunks x 2 head groups x 8 batches, then one wave per head)
+    "c4/attn_decode_split": [("c4", "attn_decode_part<false, false>", 262144),
+                             ("c4", "attn_decode_combine", 16384)],
 }
 for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the GEMM launch shapes
     TRAFFIC_MAP[f"c5m{_m}/act_quant"] = ("c5", "quant_rows_identity<4, 4>", _g)
@@ -146,14 +149,19 @@ def measured_traffic(key):
     committed rocprofv3 FETCH_SIZE/WRITE_SIZE runs, if they were taken on the current source."""
     if key not in TRAFFIC_MAP:
         return None
+    launches = TRAFFIC_MAP[key] if isinstance(TRAFFIC_MAP[key], list) else [TRAFFIC_MAP[key]]
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)["by_grid"].get("|".join(str(v) for v in TRAFFIC_MAP[key]))
+            by_grid = json.load(f)["by_grid"]
     except (OSError, ValueError, KeyError):
         return None
-    if not t or t.get("source_sha256_16") != source_hash(os.path.join(CSRC, t["source"])):
-        return None
-    return {"read": t["read_bytes"], "write": t["write_bytes"], "total": t["read_bytes"] + t["write_bytes"]}
+    rd = wr = 0
+    for launch in launches:  # a call of several kernels: their bytes add up
+        t = by_grid.get("|".join(str(v) for v in launch))
+        if not t or t.get("source_sha256_16") != source_hash(os.path.join(CSRC, t["source"])):
+            return None
+        rd, wr = rd + t["read_bytes"], wr + t["write_bytes"]
+    return {"read": rd, "write": wr, "total": rd + wr}
 
 
 # ---------------------------------------------------------------- roofline probes
@@ -240,10 +248,26 @@ def measure_peaks(torch, dev):
         out[f"read_{wg}_workgroups"] = {"GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 1)}
     del src, dst, sink
     torch.cuda.empty_cache()
+    # the ROCm library's int8 GEMM (torch._int_mm -> hipBLASLt) on int8 operands of the MLP
+    # shapes, codes in [-8, 8): what a vendor kernel sustains on the same matrix cores
+    # (twice the operand bytes of the packed 4-bit kernels, no nibble expansion)
+    vendor = {}
+    for (M, N, K) in ((2048, 22016, 4096), (2048, 4096, 11008), (4096, 28672, 4096), (4096, 4096, 14336)):
+        try:
+            g = torch.Generator(device=dev).manual_seed(M + N + K)
+            a = torch.randint(-8, 8, (M, K), dtype=torch.int8, device=dev, generator=g)
+            bt = torch.randint(-8, 8, (N, K), dtype=torch.int8, device=dev, generator=g).t()
+            ms = timed(lambda: torch._int_mm(a, bt), 10)
+            vendor[f"{M}x{N}x{K}"] = {"TOPs": round(2 * M * N * K / (ms * 1e-3) / 1e12, 1), "us": round(ms * 1e3, 1)}
+            del a, bt
+        except (RuntimeError, AttributeError) as e:  # an operator missing from this torch build
+            vendor[f"{M}x{N}x{K}"] = {"error": str(e)[:120]}
+    torch.cuda.empty_cache()
     best = lambda pre, f: max(v[f] for k, v in out.items() if k.startswith(pre))
     return {"int8_mfma_TOPs": best("mfma", "TOPs"), "copy_GBps": best("copy", "GBps"), "read_GBps": best("read", "GBps"),
             "datasheet": {"int8_mfma_TOPs": INT8_PEAK_TOPS, "hbm_GBps": HBM_PEAK_GBS},
             "runs": out,
+            "vendor_int8_gemm": vendor,
             "note": "int8 loop: back-to-back v_mfma_i32_32x32x32_i8 on registers with int4-code operand bytes, "
                     "8 accumulators per wave; copy GB/s counts bytes read + written; median of 5 launches"}
 
