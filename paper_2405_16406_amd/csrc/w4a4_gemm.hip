@@ -35,9 +35,12 @@ typedef float v2f __attribute__((ext_vector_type(2)));
 
 // The epilogue rounds twice, fp32 then fp16 (round to nearest even), in both of its paths.
 // fp32_result pins a value as a rounded fp32 register so that the compiler cannot fuse the
-// final fma with the fp16 conversion into one single-rounding v_fma_mix.
+// final fma with the fp16 conversion into one single-rounding v_fma_mix.  The asm is not
+// volatile: it only hides the value, and the scheduler stays free to interleave the
+// independent outputs (volatile asm statements keep their program order, which serialised
+// the epilogue's long-latency exp and reciprocal steps).
 __device__ __forceinline__ float fp32_result(float v) {
-  asm volatile("" : "+v"(v));
+  asm("" : "+v"(v));
   return v;
 }
 // two fp32 -> two fp16 (round to nearest even), packed low | high << 16
@@ -207,6 +210,33 @@ __device__ __forceinline__ float load_scale(const GemmArgs& g, int idx, int64_t 
 
 // Fast path: the wave's columns lie inside N, rows past M are dropped by the buffer range,
 // output rows are 8-byte aligned and the output fits a 31-bit byte range.
+// Byte address in a staged output tile (rows of RB bytes, 16-byte chunks of row r XOR-ed
+// with r % (RB / 16) so that the 32 rows one store instruction spans fall on different banks).
+template <int RB>
+__device__ __forceinline__ uint32_t stage_addr(int r, int b) {
+  constexpr int CH = RB / 16;
+  return static_cast<uint32_t>(r * RB + (((b >> 4) ^ (r & (CH - 1))) << 4) + (b & 15));
+}
+
+// Stores a staged BM x BNO fp16 output tile (rows m0.., columns n0o..) with whole-row 16-byte
+// pieces: one store instruction covers 64 / (BNO / 8) full rows.  Rows past M are dropped by
+// the buffer range.  Needs ldy % 8 == 0, a 16-byte aligned y and n0o % 8 == 0.
+template <int BM, int BNO>
+__device__ __forceinline__ void store_staged(const GemmArgs& g, const uint8_t* stg, int64_t m0, int64_t n0o, int wave,
+                                             int waves, int lane) {
+  constexpr int RB = BNO * 2, CH = RB / 16, RPI = 64 / CH;
+  static_assert(CH <= 64 && 64 % CH == 0, "rows of at most 1 KB");
+  const __amdgpu_buffer_rsrc_t ry = buf_rsrc(g.y, g.M * g.ldy * 2);
+  const int k = lane % CH;
+  for (int r0 = wave * RPI; r0 < BM; r0 += waves * RPI) {
+    const int rr = r0 + lane / CH;
+    const v4u v = *reinterpret_cast<const v4u*>(stg + stage_addr<RB>(rr, 16 * k));
+    const int64_t m = m0 + rr;
+    const uint32_t off = m < g.M ? static_cast<uint32_t>((m * g.ldy + n0o) * 2 + 16 * k) : 0x80000000u;
+    __builtin_amdgcn_raw_buffer_store_b128(v, ry, static_cast<int>(off), 0, 0);
+  }
+}
+
 template <int TM, int TN, int BM, int BN>
 __device__ __forceinline__ void ring_epilogue_fast(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
                                                    int tm, int tn, int lane, const float* __restrict__ sc) {
@@ -306,9 +336,11 @@ __device__ __forceinline__ void ring_epilogue_checked(const GemmArgs& g, const v
 }
 
 // SiLU(gate) * up of two dequantised fp32 outputs, as the fp16 input of down_proj:
-// g u / (1 + e^-g); for g -> -inf the denominator is +inf and the product 0.
+// g u / (1 + e^-g), the quotient as a product with v_rcp_f32 (1 ulp; the result is rounded
+// to fp16) instead of the IEEE division sequence, which took most of the gate/up epilogue's
+// instructions; for g -> -inf the denominator is +inf, its reciprocal 0 and the product 0.
 __device__ __forceinline__ float swiglu_value(float gv, float uv) {
-  return __fdividef(__fmul_rn(gv, uv), __fadd_rn(1.0f, __expf(-gv)));
+  return __fmul_rn(__fmul_rn(gv, uv), __builtin_amdgcn_rcpf(__fadd_rn(1.0f, __expf(-gv))));
 }
 
 // Gate/up epilogues: wq interleaves gate and up rows in blocks of 32, so the wave's block
@@ -418,6 +450,102 @@ __device__ __forceinline__ void ring_epilogue_swiglu_checked(const GemmArgs& g, 
 }
 
 // Epilogue of a ring-kernel block: plain or gate/up, vector (fast) or element-wise stores.
+// The fast epilogue through a staged tile in LDS (stg: BM x BN fp16, or BM x BN/2 for
+// gate/up, in the ring's bytes, which the caller has drained): every wave writes its block
+// (same arithmetic as the other epilogues), a workgroup barrier, then the whole tile goes
+// out in whole-row pieces.  Column groups q run outermost so that only one group's column
+// scales are live.  Needs what store_staged needs.
+template <int TM, int TN, int BM, int BN>
+__device__ __forceinline__ void ring_epilogue_staged(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t m0,
+                                                     int64_t n0, int tm, int tn, int lane, const float* __restrict__ sc,
+                                                     uint8_t* stg, int wave, int waves) {
+  const int c = lane & 31;
+  const int h = lane >> 5;
+  const float* rowA = sc;
+  const float* rowB = sc + BM;
+  const float* colS = sc + 2 * BM;
+  const float* colR = colS + BN;
+  const float* colB = colR + BN;
+  float ra[TM], rb[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    ra[i] = rowA[(tm + i) * 32 + c];
+    rb[i] = rowB[(tm + i) * 32 + c];
+  }
+  const bool sw = g.swiglu;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float s[TN][4], w[TN][4], bv[TN][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int cb = (tn + j) * 32 + 8 * q + 4 * h;
+      const float4 sv = *reinterpret_cast<const float4*>(colS + cb);
+      const float4 rv = *reinterpret_cast<const float4*>(colR + cb);
+      const float4 bb = *reinterpret_cast<const float4*>(colB + cb);
+      const float s4[4] = {sv.x, sv.y, sv.z, sv.w}, r4[4] = {rv.x, rv.y, rv.z, rv.w}, b4[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[j][e] = s4[e];
+        w[j][e] = __fmul_rn(s4[e], r4[e]);
+        bv[j][e] = b4[e];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r0 = 4 * q;
+      const int row = (tm + i) * 32 + c;
+      if (sw) {
+        if constexpr (TN % 2 == 0) {
+#pragma unroll
+          for (int p = 0; p < TN / 2; ++p) {
+            uint32_t pk[2];
+#pragma unroll
+            for (int e2 = 0; e2 < 2; ++e2) {
+              float hv[2];
+#pragma unroll
+              for (int u = 0; u < 2; ++u) {
+                const int e = 2 * e2 + u;
+                const int jg = 2 * p, ju = 2 * p + 1;
+                const float tg = __fmul_rn(s[jg][e], static_cast<float>(acc[i][jg][r0 + e]));
+                const float tu = __fmul_rn(s[ju][e], static_cast<float>(acc[i][ju][r0 + e]));
+                const float gv = fp32_result(__fmaf_rn(ra[i], tg, __fmaf_rn(rb[i], w[jg][e], bv[jg][e])));
+                const float uv = fp32_result(__fmaf_rn(ra[i], tu, __fmaf_rn(rb[i], w[ju][e], bv[ju][e])));
+                hv[u] = fp32_result(swiglu_value(gv, uv));
+              }
+              pk[e2] = f2h2(hv[0], hv[1]);
+            }
+            *reinterpret_cast<v2u*>(stg + stage_addr<BN>(row, ((tn / 2 + p) * 32 + 8 * q + 4 * h) * 2)) =
+                v2u{pk[0], pk[1]};
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          uint32_t pk[2];
+#pragma unroll
+          for (int e2 = 0; e2 < 2; ++e2) {
+            float yv[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int e = 2 * e2 + u;
+              const float t = __fmul_rn(s[j][e], static_cast<float>(acc[i][j][r0 + e]));
+              yv[u] = fp32_result(__fmaf_rn(ra[i], t, __fmaf_rn(rb[i], w[j][e], bv[j][e])));
+            }
+            pk[e2] = f2h2(yv[0], yv[1]);
+          }
+          *reinterpret_cast<v2u*>(stg + stage_addr<BN * 2>(row, ((tn + j) * 32 + 8 * q + 4 * h) * 2)) =
+              v2u{pk[0], pk[1]};
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (sw)
+    store_staged<BM, BN / 2>(g, stg, m0, n0 / 2, wave, waves, lane);
+  else
+    store_staged<BM, BN>(g, stg, m0, n0, wave, waves, lane);
+}
+
 template <int TM, int TN, int BM, int BN>
 __device__ __forceinline__ void ring_epilogue(const GemmArgs& g, const v16i (&acc)[TM][TN], int64_t mw, int64_t nw,
                                               int tm, int tn, int lane, const float* __restrict__ sc, bool fast) {
@@ -857,7 +985,15 @@ w4a4_gemm_ring(GemmArgs g) {
   const bool fast = g.dbg_acc == nullptr && (g.ldy & 3) == 0 && (reinterpret_cast<uintptr_t>(g.y) & 7) == 0 &&
                     g.M * g.ldy * 2 < (int64_t{1} << 31) && n0 + R::BN <= g.N;
   if constexpr (KS == 1) {
-    ring_epilogue<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales, fast);
+    // whole-row stores through the drained ring when rows are 16-byte aligned (uniform over
+    // the workgroup, as is the barrier inside)
+    static_assert(R::BM * R::BN * 2 <= L::RINGS, "the output tile fits the ring");
+    if (fast && (g.ldy & 7) == 0 && (reinterpret_cast<uintptr_t>(g.y) & 15) == 0) {
+      __syncthreads();  // every wave's copies have landed and its last fragments are read
+      ring_epilogue_staged<TM, TN, R::BM, R::BN>(g, acc, m0, n0, wm, wn, lane, scales, lds, wave, R::WAVES);
+    } else {  // element-wise stores (a third, direct-store path would cost the kernel spills)
+      ring_epilogue<TM, TN, R::BM, R::BN>(g, acc, m0 + wm * 32, n0 + wn * 32, wm, wn, lane, scales, false);
+    }
   } else {
     // group h finishes row blocks [h*HT, h*HT + HT) of the wave's block
     constexpr int HT = TM / 2;
