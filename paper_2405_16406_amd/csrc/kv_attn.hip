@@ -288,14 +288,15 @@ attn_decode_kv4(AttnArgs a) {
       static_cast<uint32_t>(f2h(o0)) | (static_cast<uint32_t>(f2h(o1)) << 16);
 }
 
-// ---- split over the sequence (flash-decoding): workgroup (b, chunk c, group g of 16
-// heads) of 8 waves; wave w serves heads 16 g + 2 w and 16 g + 2 w + 1 over the chunk's
+// ---- split over the sequence (flash-decoding): workgroup (b, chunk c, group g of 32
+// heads) of 16 waves; wave w serves heads 32 g + 2 w and 32 g + 2 w + 1 over the chunk's
 // batches of 8 tokens, so each of its loads brings whole 128-byte lines (8 tokens x 128
-// bytes), where one wave per head uses half of every line it touches.  Two workgroups
-// share a CU.  Each head leaves its partial state (m, l, the 128 dims with the code offset
-// removed and the betas added) in part; the combine kernel merges the chunks of a head.
+// bytes), where one wave per head uses half of every line it touches, and the workgroup
+// reads whole 2 KB token lines of a 32-head cache.  Each head leaves its partial state (m,
+// l, the 128 dims with the code offset removed and the betas added) in part; the combine
+// kernel merges the chunks of a head.
 // FINAL (a single chunk): the lanes divide and store the output themselves.
-constexpr int kSplitWaves = 8;
+constexpr int kSplitWaves = kAttnGroupHeads / 2;
 
 template <bool P16, bool FINAL>
 __global__ void __launch_bounds__(64 * kSplitWaves, 4)
@@ -305,11 +306,11 @@ attn_decode_part(AttnArgs a) {
   const int qd = lane & 3;
   const int hp = (lane >> 2) & 1;
   // the workgroup count (B * chunks * NG, at most B * NG or about four times the CUs) fits 32 bits
-  const int NG = static_cast<int>((a.H + 15) / 16), NC = static_cast<int>(a.chunks);
+  const int NG = static_cast<int>((a.H + kAttnGroupHeads - 1) / kAttnGroupHeads), NC = static_cast<int>(a.chunks);
   const int g = static_cast<int>(blockIdx.x) % NG;
   const int c = (static_cast<int>(blockIdx.x) / NG) % NC;
   const int b = static_cast<int>(blockIdx.x) / NG / NC;
-  const int h0 = 16 * g + 2 * w;
+  const int h0 = kAttnGroupHeads * g + 2 * w;
   if (h0 >= a.H) return;  // no workgroup barrier follows
   const int nb = static_cast<int>((a.S + 7) / 8);  // batches of 8 tokens
   const int first = 2 * c * static_cast<int>(a.chunk_batches);
@@ -345,7 +346,7 @@ attn_decode_part(AttnArgs a) {
 
 // One wave per head: the chunks' states (at most 64) rescaled to their common maximum and
 // summed.  Lane c holds chunk c's maximum and sum; the dims (lane l finishes 2 l and 2 l + 1)
-// are loaded eight chunks at a time, all eight loads in flight together, and added in chunk
+// are loaded 32 chunks at a time, all 32 loads in flight together, and added in chunk
 // order.
 __global__ void __launch_bounds__(256)
 attn_decode_combine(AttnArgs a) {
@@ -364,13 +365,13 @@ attn_decode_combine(AttnArgs a) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) L = __fadd_rn(L, __shfl_xor(L, o));
   float A0 = 0.0f, A1 = 0.0f;
-  for (int c0 = 0; c0 < NC; c0 += 8) {
-    float2 d[8];
+  for (int c0 = 0; c0 < NC; c0 += 32) {
+    float2 d[32];
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 32; ++j)
       d[j] = c0 + j < NC ? reinterpret_cast<const float2*>(pr + (c0 + j) * kAttnPart + 4)[lane] : float2{0.0f, 0.0f};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < 32; ++j) {
       const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fc), min(c0 + j, 63)));
       A0 = __fmaf_rn(d[j].x, f, A0);
       A1 = __fmaf_rn(d[j].y, f, A1);
@@ -406,7 +407,7 @@ hipError_t attn_scratch(void** ptr) {
 }
 
 hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream) {
-  const int64_t NG = (a.H + 15) / 16;
+  const int64_t NG = (a.H + kAttnGroupHeads - 1) / kAttnGroupHeads;
   const unsigned parts = static_cast<unsigned>(a.B * a.chunks * NG);
   const dim3 block(64 * kSplitWaves);
   if (a.chunks == 1)

@@ -93,12 +93,13 @@ struct AttnArgs {
 constexpr int kAttnPart = 132;  // floats per partial state: m, l, 2 unused, 128 dims
 
 // Chunks of the sequence split for a device with `cus` compute units: enough (batch,
-// chunk, 16-head group) workgroups to give every CU two; at least 4 batches of 16 tokens a
-// chunk, at most 64 chunks (one per lane of the combine).
+// chunk, 32-head group) workgroups of 16 waves to give every CU one; at least 4 batches of
+// 16 tokens a chunk, at most 64 chunks (one per lane of the combine).
+constexpr int kAttnGroupHeads = 32;  // heads of one workgroup of the split attention (a wave per pair)
 inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks, int64_t& chunk_batches) {
   const int64_t nb = (S + 15) / 16;
-  const int64_t groups = B * ((H + 15) / 16);
-  const int64_t slots = 2 * static_cast<int64_t>(cus);
+  const int64_t groups = B * ((H + kAttnGroupHeads - 1) / kAttnGroupHeads);
+  const int64_t slots = static_cast<int64_t>(cus) * (32 / kAttnGroupHeads);  // 16 waves per CU
   int64_t want = groups < slots ? (slots + groups - 1) / groups : 1;
   const int64_t most = (nb + 3) / 4 < 64 ? (nb + 3) / 4 : 64;
   if (want > most) want = most;
