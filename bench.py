@@ -182,6 +182,10 @@ class Probe:
         L.sq_probe_copy.argtypes = [P, P, I64, I32, P]
         L.sq_probe_read.restype = I32
         L.sq_probe_read.argtypes = [P, I64, I32, P, P]
+        L.sq_probe_copy_blocks.restype = I32
+        L.sq_probe_copy_blocks.argtypes = [P, P, I64, I32, P]
+        L.sq_probe_read_blocks.restype = I32
+        L.sq_probe_read_blocks.argtypes = [P, I64, I32, P, P]
         L.sq_probe_sleep.restype = I32
         L.sq_probe_sleep.argtypes = [I64, P]
         self.L = L
@@ -238,14 +242,18 @@ def measure_peaks(torch, dev):
     src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(3)
     dst = torch.empty_like(src)
     sink = torch.empty(2048 * 256, dtype=torch.int32, device=dev)
-    for wg in (2048, 8192):
-        ms = timed(lambda: pr.check(pr.L.sq_probe_copy(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
-                                                       nbytes, wg, stream), "copy probe"), 5)
-        out[f"copy_{wg}_workgroups"] = {"GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 1)}
+    sp, dp = ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr())
+    for wg in (1024, 2048, 8192):
         sk = torch.empty(wg * 256, dtype=torch.int32, device=dev)
-        ms = timed(lambda: pr.check(pr.L.sq_probe_read(ctypes.c_void_p(src.data_ptr()), nbytes, wg,
-                                                       ctypes.c_void_p(sk.data_ptr()), stream), "read probe"), 5)
-        out[f"read_{wg}_workgroups"] = {"GBps": round(nbytes / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 1)}
+        skp = ctypes.c_void_p(sk.data_ptr())
+        for kind, fn in (("", pr.L.sq_probe_copy), ("blocks_", pr.L.sq_probe_copy_blocks)):
+            ms = timed(lambda: pr.check(fn(sp, dp, nbytes, wg, stream), "copy probe"), 5)
+            out[f"copy_{kind}{wg}_workgroups"] = {"GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1),
+                                                  "us": round(ms * 1e3, 1)}
+        for kind, fn in (("", pr.L.sq_probe_read), ("blocks_", pr.L.sq_probe_read_blocks)):
+            ms = timed(lambda: pr.check(fn(sp, nbytes, wg, skp, stream), "read probe"), 5)
+            out[f"read_{kind}{wg}_workgroups"] = {"GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                                                  "us": round(ms * 1e3, 1)}
     del src, dst, sink
     torch.cuda.empty_cache()
     # the ROCm library's int8 GEMM (torch._int_mm -> hipBLASLt) on int8 operands of the MLP
@@ -269,7 +277,8 @@ def measure_peaks(torch, dev):
             "runs": out,
             "vendor_int8_gemm": vendor,
             "note": "int8 loop: back-to-back v_mfma_i32_32x32x32_i8 on registers with int4-code operand bytes, "
-                    "8 accumulators per wave; copy GB/s counts bytes read + written; median of 5 launches"}
+                    "8 accumulators per wave; copy GB/s counts bytes read + written; copy/read: grid-stride 16-byte "
+                    "accesses, blocks_: each workgroup streams its own contiguous region; median of 5 launches"}
 
 
 # ---------------------------------------------------------------- the chained layer step

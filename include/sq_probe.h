@@ -51,6 +51,16 @@ int32_t sq_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgro
 int32_t sq_probe_read(const void* src, int64_t bytes, int32_t workgroups, uint32_t* sink, void* stream);
 
 /*
+ * sq_probe_copy_blocks, sq_probe_read_blocks -- the copy and read above, but workgroup b
+ * owns one contiguous block of ceil(bytes / 16 / workgroups) 16-byte items and walks it
+ * 4 KB at a time (8 copies or 16 reads in flight per thread): each workgroup streams its
+ * own region, the access pattern HBM serves fastest.  Arguments, checks and traffic as
+ * sq_probe_copy and sq_probe_read.
+ */
+int32_t sq_probe_copy_blocks(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
+int32_t sq_probe_read_blocks(const void* src, int64_t bytes, int32_t workgroups, uint32_t* sink, void* stream);
+
+/*
  * sq_probe_sleep -- one wave that sleeps (s_sleep) until `microseconds` have passed on the
  * GPU's constant-rate wall clock (hipDeviceAttributeWallClockRate of the current device),
  * and in any case after at most as many sleep steps as wall-clock ticks.  Holds the stream,

@@ -88,6 +88,38 @@ __global__ void __launch_bounds__(256) probe_read(const v4u* __restrict__ src, i
   sink[blockIdx.x * blockDim.x + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
 }
 
+// Streams: workgroup b owns the contiguous items [b * per, min((b + 1) * per, n)) and walks
+// them 256 items (4 KB) at a time, 16 loads in flight per thread.
+__global__ void __launch_bounds__(256) probe_read_blocks(const v4u* __restrict__ src, int64_t n, int64_t per,
+                                                         uint32_t* sink) {
+  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per;
+  const int64_t b1 = b0 + per < n ? b0 + per : n;
+  v4u acc = {0u, 0u, 0u, 0u};
+  int64_t i = b0 + threadIdx.x;
+  for (; i + 15 * 256 < b1; i += 16 * 256) {
+    v4u x[16];
+#pragma unroll
+    for (int d = 0; d < 16; ++d) x[d] = src[i + d * 256];
+#pragma unroll
+    for (int d = 0; d < 16; ++d) acc ^= x[d];
+  }
+  for (; i < b1; i += 256) acc ^= src[i];
+  sink[blockIdx.x * blockDim.x + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+}
+__global__ void __launch_bounds__(256) probe_copy_blocks(const v4u* __restrict__ src, v4u* __restrict__ dst,
+                                                         int64_t n, int64_t per) {
+  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per;
+  const int64_t b1 = b0 + per < n ? b0 + per : n;
+  int64_t i = b0 + threadIdx.x;
+  for (; i + 7 * 256 < b1; i += 8 * 256) {
+    v4u x[8];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) x[d] = src[i + d * 256];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) dst[i + d * 256] = x[d];
+  }
+  for (; i < b1; i += 256) dst[i] = src[i];
+}
 // bounded wait: ends when the wall clock has advanced `ticks` or after `ticks` sleeps of
 // about 64 cycles each, whichever comes first
 __global__ void __launch_bounds__(64) probe_sleep(int64_t ticks) {
@@ -145,6 +177,25 @@ int32_t sq_probe_read(const void* src, int64_t bytes, int32_t workgroups, uint32
   return hip_result(hipGetLastError(), "probe_read launch");
 }
 
+int32_t sq_probe_read_blocks(const void* src, int64_t bytes, int32_t workgroups, uint32_t* sink, void* stream) {
+  if (!src || !sink || bytes <= 0 || bytes % 16 || workgroups <= 0 || reinterpret_cast<uintptr_t>(src) % 16)
+    return bad("16-byte aligned src, bytes > 0 and a multiple of 16, workgroups > 0, a sink");
+  const int64_t n = bytes / 16, per = (n + workgroups - 1) / workgroups;
+  hipLaunchKernelGGL(probe_read_blocks, dim3(workgroups), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const v4u*>(src), n, per, sink);
+  return hip_result(hipGetLastError(), "probe_read_blocks launch");
+}
+int32_t sq_probe_copy_blocks(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {
+  if (!src || !dst || bytes <= 0 || bytes % 16 || workgroups <= 0 ||
+      (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16)
+    return bad("16-byte aligned src and dst, bytes > 0 and a multiple of 16, workgroups > 0");
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + static_cast<uint64_t>(bytes) && d0 < s0 + static_cast<uint64_t>(bytes)) return bad("src and dst overlap");
+  const int64_t n = bytes / 16, per = (n + workgroups - 1) / workgroups;
+  hipLaunchKernelGGL(probe_copy_blocks, dim3(workgroups), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const v4u*>(src), static_cast<v4u*>(dst), n, per);
+  return hip_result(hipGetLastError(), "probe_copy_blocks launch");
+}
 int32_t sq_probe_sleep(int64_t microseconds, void* stream) {
   if (microseconds <= 0) return bad("microseconds > 0");
   int dev = 0, khz = 0;

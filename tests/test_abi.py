@@ -46,7 +46,8 @@ def test_probe_header_symbols_exported():
     # the roofline probes of the benchmark: every function of include/sq_probe.h is exported
     text = open(os.path.join(ROOT, "include", "sq_probe.h")).read()
     declared = set(re.findall(r"^\s*(?:int32_t|const char\*)\s+(sq_probe_\w+)\s*\(", text, re.M))
-    assert declared == {"sq_probe_last_error", "sq_probe_mfma_i8", "sq_probe_copy", "sq_probe_read", "sq_probe_sleep"}
+    assert declared == {"sq_probe_last_error", "sq_probe_mfma_i8", "sq_probe_copy", "sq_probe_read",
+                        "sq_probe_copy_blocks", "sq_probe_read_blocks", "sq_probe_sleep"}
     P = ctypes.CDLL(os.path.join(ROOT, "paper_2405_16406_amd", "libsq_probe.so"))
     for name in declared:
         assert hasattr(P, name), name
