@@ -29,7 +29,6 @@
 #include "sq_device.h"
 #include "sq_internal.h"
 
-#include <mutex>
 #include <utility>
 
 namespace sq {
@@ -1130,17 +1129,11 @@ had_quant_lines(RotQuantArgs args) {
   }
 }
 
-int g_num_cu = 0;
-std::once_flag g_cu_once;
-
+// Compute units of the current device (the persistent grids' size); if the query fails,
+// 256 (MI355X): the grid then only runs in fewer or more rounds.
 int num_cus() {
-  std::call_once(g_cu_once, [] {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&g_num_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      g_num_cu = 256;
-  });
-  return g_num_cu;
+  int n = 0;
+  return device_cus(&n) == hipSuccess ? n : 256;
 }
 
 template <int A, int APAD, int NT, int B, int MW, int NW, bool STAGE, bool DBG>
