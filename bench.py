@@ -499,8 +499,55 @@ def mlp_config(tag, shape, torch, sq, workloads, dev, variants=False, inp=None, 
                                              "bytes")
     for n, e in k.items():
         e["traffic"] = measured_traffic(f"{tag}/{n}")
+    res = {"workload": shape.name if tokens is None else f"{shape.name.split(',')[0]}, M={M}", "kernels": k}
+    if decode:
+        res["chained_step"] = decode_chain(torch, sq, xin, had, shape.had_pow2, wsw, wd)
     torch.cuda.empty_cache()
-    return {"workload": shape.name if tokens is None else f"{shape.name.split(',')[0]}, M={M}", "kernels": k}
+    return res
+
+
+def decode_chain(torch, sq, x, had, pow2, wsw, wd, reps=50):
+    """The decode MLP step chained (act quant -> gate/up with SiLU -> R4 + quant -> down) on
+    preallocated buffers: mean time per step over `reps` back-to-back steps, launched
+    eagerly and as the replay of one captured HIP graph."""
+    M, H = x.shape
+    I = wd[0].shape[1] * 2
+    dev = x.device
+    xq = (torch.empty((M, H // 2), dtype=torch.uint8, device=dev), torch.empty((M, 1), dtype=torch.float32, device=dev),
+          torch.empty((M, 1), dtype=torch.float32, device=dev))
+    hq = (torch.empty((M, I // 2), dtype=torch.uint8, device=dev), torch.empty((M, 1), dtype=torch.float32, device=dev),
+          torch.empty((M, 1), dtype=torch.float32, device=dev))
+    h = torch.empty((M, I), dtype=torch.float16, device=dev)
+    y = torch.empty((M, H), dtype=torch.float16, device=dev)
+
+    def step():
+        sq.had_quant_act(x, out=xq)
+        sq.w4a4_linear_swiglu(*xq, *wsw, out=h)
+        sq.had_quant_act(h, had, pow2, out=hq)
+        sq.w4a4_linear(*hq, *wd, out=y)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        probe().hold(torch, 2.0 + 0.05 * reps)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3
+
+    eager_us = timed(step)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    graph_us = timed(g.replay)
+    del g
+    return {"eager_us": round(eager_us, 2), "graph_us": round(graph_us, 2), "steps": reps,
+            "note": "four library calls per step; weights are read from HBM each step (352 MB > the 256 MB "
+                    "Infinity Cache)"}
 
 
 def kv_config(torch, sq, workloads, dev, variants=False):
