@@ -776,13 +776,16 @@ def summarize(d):
         lines = [f"# Kernel durations: {names[part]}", "",
                  "rocprofv3 kernel trace of `bench.py --only " + part + "`; every launch of a kernel counts in",
                  "its row (warm-up, timed and per-kernel event passes).  Commands (from /tmp, TMPDIR=/tmp):", "",
-                 cmds, "", "| kernel | grid (threads) | calls | avg us | min us | max us |",
-                 "|---|---:|---:|---:|---:|---:|"]
+                 cmds, "",
+                 "The first launches of each kernel run on a cold chip (clock, caches); the median is the",
+                 "steady state that bench.py's second, event-timed pass reports.", "",
+                 "| kernel | grid (threads) | calls | avg us | median us | min us | max us |",
+                 "|---|---:|---:|---:|---:|---:|---:|"]
         for (name, grid), v in sorted(dur.items(), key=lambda kv: -np.mean(kv[1]) * len(kv[1])):
             if "sq::" not in name:  # the library's kernels only (not torch's set-up copies)
                 continue
-            lines.append(f"| `{_short(name)}` | {grid} | {len(v)} | {np.mean(v):.1f} | {np.min(v):.1f} | "
-                         f"{np.max(v):.1f} |")
+            lines.append(f"| `{_short(name)}` | {grid} | {len(v)} | {np.mean(v):.1f} | {np.median(v):.1f} | "
+                         f"{np.min(v):.1f} | {np.max(v):.1f} |")
         with open(os.path.join(PROFILE_DIR, f"kernel_stats_{part}.md"), "w") as f:
             f.write("\n".join(lines) + "\n")
         fetch = _pmc_per_kernel(_csv_rows(d, f"pmc_FETCH_SIZE_{part}/*counter_collection.csv"), "FETCH_SIZE")
