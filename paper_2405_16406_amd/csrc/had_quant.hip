@@ -217,11 +217,19 @@ quant_rows_identity(RotQuantArgs args) {
   const uint16_t* __restrict__ xr = args.x + row * args.ldx;
   float v[CHMAX][8];
   float mn = INFINITY, mx = -INFINITY;
+  // every chunk load is issued before any is used (clamped index; the duplicates are not
+  // counted), so a row costs one memory round trip
+  uint4 dch[CHMAX];
+#pragma unroll
+  for (int j = 0; j < CHMAX; ++j) {
+    const int ch = threadIdx.x + j * T;
+    dch[j] = reinterpret_cast<const uint4*>(xr)[ch < nchunk ? ch : nchunk - 1];
+  }
 #pragma unroll
   for (int j = 0; j < CHMAX; ++j) {
     const int ch = threadIdx.x + j * T;
     if (ch < nchunk) {
-      const uint4 d = reinterpret_cast<const uint4*>(xr)[ch];
+      const uint4 d = dch[j];
       const uint32_t w[4] = {d.x, d.y, d.z, d.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {

@@ -191,21 +191,38 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, int64_
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, static_cast<int>(bytes), 0x00020000);
 }
 
-// Loads scale value `idx` of a tile (RingScales layout); out-of-range rows/columns read 0.
+// Scale value `idx` of a tile (RingScales layout), in two steps: fetch() reads every
+// candidate source at a clamped index, unconditionally, and value() selects and converts.
+// The caller issues the fetches before the tile's first copies and calls value() after the
+// first stage has landed: the loads are then all in flight at once and off the copies'
+// path (loads in branches made the compiler wait for each before the copies went out).
+// Out-of-range rows/columns give 0.
+struct ScaleFetch {
+  float xa, xb, wa;
+  int32_t rs;
+  uint16_t bias;
+};
 template <int BM, int BN>
-__device__ __forceinline__ float load_scale(const GemmArgs& g, int idx, int64_t m0, int64_t n0) {
+__device__ __forceinline__ ScaleFetch scale_fetch(const GemmArgs& g, int idx, int64_t m0, int64_t n0) {
+  const int t = idx < 2 * BM ? 0 : idx - 2 * BM;
+  const int64_t m = m0 + (idx % BM), n = n0 + (t % BN);
+  const int64_t mc = m < g.M ? m : g.M - 1, nc = n < g.N ? n : g.N - 1;
+  // without a bias the fetch reads (and discards) the first bytes of the scales
+  const uint16_t* bp = g.bias ? g.bias : reinterpret_cast<const uint16_t*>(g.wa);
+  return ScaleFetch{g.xa[mc], g.xb[mc], g.wa[nc], g.rs[nc], bp[nc]};
+}
+template <int BM, int BN>
+__device__ __forceinline__ float scale_value(const GemmArgs& g, const ScaleFetch& f, int idx, int64_t m0, int64_t n0) {
   if (idx < 2 * BM) {
-    const int64_t m = m0 + (idx % BM);
-    if (m >= g.M) return 0.0f;
-    if (idx < BM) return __fmul_rn(g.xa[m], 0.0625f);
-    return g.a8 ? __fmaf_rn(128.0f, g.xa[m], g.xb[m]) : g.xb[m];  // 8-bit codes enter as qa - 128
+    if (m0 + (idx % BM) >= g.M) return 0.0f;
+    if (idx < BM) return __fmul_rn(f.xa, 0.0625f);
+    return g.a8 ? __fmaf_rn(128.0f, f.xa, f.xb) : f.xb;  // 8-bit codes enter as qa - 128
   }
   const int t = idx - 2 * BM;
-  const int64_t n = n0 + (t % BN);
-  if (n >= g.N) return 0.0f;
-  if (t < BN) return g.wa[n];
-  if (t < 2 * BN) return static_cast<float>(g.rs[n]);
-  return g.bias ? h2f(g.bias[n]) : 0.0f;
+  if (n0 + (t % BN) >= g.N) return 0.0f;
+  if (t < BN) return f.wa;
+  if (t < 2 * BN) return static_cast<float>(f.rs);
+  return g.bias ? h2f(f.bias) : 0.0f;
 }
 
 // Fast path: the wave's columns lie inside N, rows past M are dropped by the buffer range,
@@ -935,18 +952,18 @@ w4a4_gemm_ring(GemmArgs g) {
   // landed (the main loop's barriers publish them)
   constexpr int TT = R::THREADS * KS;
   constexpr int SPT = (SC::COUNT + TT - 1) / TT;
-  float sv[SPT];
+  ScaleFetch sf[SPT];
 #pragma unroll
   for (int u = 0; u < SPT; ++u) {
     const int idx = static_cast<int>(threadIdx.x) + u * TT;
-    sv[u] = idx < SC::COUNT ? load_scale<R::BM, R::BN>(g, idx, m0, n0) : 0.0f;
+    sf[u] = scale_fetch<R::BM, R::BN>(g, idx < SC::COUNT ? idx : 0, m0, n0);
   }
   for (int s = 0; s < NS - 1; ++s) issue(s);
   sync();
 #pragma unroll
   for (int u = 0; u < SPT; ++u) {
     const int idx = static_cast<int>(threadIdx.x) + u * TT;
-    if (idx < SC::COUNT) scales[idx] = sv[u];
+    if (idx < SC::COUNT) scales[idx] = scale_value<R::BM, R::BN>(g, sf[u], idx, m0, n0);
   }
   issue(NS - 1);
   RingPacked<TM, TN, A8> P0, P1;
