@@ -126,7 +126,7 @@ TRAFFIC_MAP = {
     "c2/act_quant": ("step", "quant_rows_identity<4, 2>", 524288),
     "c2/gate_up_swiglu": ("step", "w4a4_gemm_ring<2, 4, 4, 2, 4, 1, 1, false>", 352256),
     "c2/r4_had_quant": ("step", "had_quant_pair<172, 176, 6, false, 4, false>", 131072),
-    "c2/down_gemm": ("step", "w4a4_gemm_ring<2, 2, 4, 2, 3, 2, 1, false>", 65536),
+    "c2/down_gemm": ("step", "w4a4_gemm_ring<2, 4, 2, 2, 3, 1, 1, false>", 131072),
     "c3/act_quant": ("c3", "quant_rows_identity<4, 2>", 1048576),
     "c3/gate_up_swiglu": ("c3", "w4a4_gemm_ring<2, 4, 4, 2, 4, 1, 1, false>", 917504),
     "c3/r4_had_quant": ("c3", "had_quant_lines<28, 8, 7, false, 4, false>", 229376),

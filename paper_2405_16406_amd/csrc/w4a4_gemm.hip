@@ -1338,7 +1338,9 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
   // Measured on MI355X (LLaMA-2-7B / LLaMA-3-8B MLP shapes, same data, interleaved runs):
   // the 8-wave 256 x 256 ring tile is fastest once there are at least as many of its tiles
   // as CUs (7B gate+up 169 vs 191 us, 8B gate 427 vs 477 us, 8B down 186 vs 212 us); with
-  // fewer, 256 x 128 tiles keep every CU busy (7B down 96 vs 123 us).  Decode-sized M
+  // fewer, 128 x 256 tiles of 8 waves (64 x 64 each) keep every CU busy with two waves per
+  // SIMD (7B down 83.5 vs 93.1 us for 256 x 128 tiles of 4 waves, M = 1024: 67.6 vs 77.2
+  // us; the gate/up product keeps the 4-wave tiles, 59 vs 61 us at M = 512).  Decode-sized M
   // (<= 16) streams the weights with the skinny kernel (LLaMA-2-70B, M = 16: down
   // [16x28672]x[8192x28672] 31 vs 98 us, gate [16x8192]x[28672x8192] 36 vs 41 us against
   // the tile kernels); 16 < M <= 128 runs 128 x 128 tiles with two K groups per workgroup.
@@ -1354,7 +1356,7 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     if (fits_ring<2, 4, 4, 2, 4>(g)) return launch_ring<2, 4, 4, 2, 4>(g, stream);
     return launch_tile<2, 4, 4, 2>(g, stream);
   }
-  if (fits_ring<2, 2, 4, 2, 3>(g)) return launch_ring<2, 2, 4, 2, 3, 2>(g, stream);
+  if (fits_ring<2, 4, 2, 2, 3>(g)) return launch_ring<2, 4, 2, 2, 3>(g, stream);
   return launch_tile<2, 4, 4, 2>(g, stream);
 }
 

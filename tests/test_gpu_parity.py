@@ -924,8 +924,8 @@ def test_kv_full_sampled():
 
 
 # Each size class of the dispatch: 16 < M <= 128 (128 x 128 tiles, two K groups), fewer
-# than 256 tiles of 256 x 256 (256 x 128 tiles, two workgroups per CU), at least 256 such
-# tiles (8-wave 256 x 256); ragged M, N and K (K % 128 == 64: a half stage)
+# than 256 tiles of 256 x 256 (128 x 256 tiles of 8 waves), at least 256 such tiles
+# (8-wave 256 x 256); ragged M, N and K (K % 128 == 64: a half stage)
 GEMM_CLASS_SHAPES = [(64, 130, 192), (100, 1000, 2112), (300, 390, 448), (257, 257, 128), (520, 600, 320),
                      (384, 264, 2112), (4096, 4096, 192), (4000, 4100, 320)]
 
@@ -1051,7 +1051,7 @@ def test_swiglu_llama2_7b_full_tiles():
 @pytest.mark.parametrize("M,N,K", [(8, 4096, 11008), (100, 1000, 2112), (2048, 4096, 11008), (4096, 4096, 192)])
 def test_gemm_deterministic(M, N, K):
     # decode kernel (8 waves' partial sums in LDS), two K groups (partial sums exchanged in
-    # LDS), 256 x 128 and 256 x 256 ring tiles: two launches give the same bytes
+    # LDS), 128 x 256 and 256 x 256 ring tiles: two launches give the same bytes
     say(f"w4a4_linear determinism M={M} N={N} K={K}")
     rng = workloads.rng_for(M + N + K + 3)
     qa = rng.integers(0, 16, size=(M, K))
