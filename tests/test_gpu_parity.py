@@ -612,10 +612,11 @@ def test_w4a8_decode_shapes(M, N, K):
 
 
 def test_w4a8_prefill_kernels():
-    # the ring kernel with 8-bit A blocks: ragged M and N, K not a multiple of a 128-k stage
+    # the ring kernels with 8-bit A blocks (128 x 256 tiles; 256 x 256 tiles from 256 such
+    # tiles on): ragged M and N, K not a multiple of a 128-k stage
     say("w4a8_linear prefill ring kernel")
     for (M, N, K) in [(300, 390, 448), (257, 600, 320), (129, 1000, 2112), (640, 520, 1024), (2048, 300, 256),
-                      (4096, 4096, 128)]:
+                      (4096, 4096, 128), (4000, 4100, 320)]:
         gemm8_case(M, N, K, seed=M + N + K + 7)
 
 
