@@ -1255,6 +1255,259 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g);
 }
 
+// ------------------------------------------------------------------ dot-product decode kernel
+// M <= 4: one to four activation rows against the whole weight matrix, a matrix-vector
+// product whose cost is reading the packed weights once.  Each wave owns a contiguous run of
+// at most 64 output units (a weight row n, or with SiLU a gate/up row pair of one output
+// column) and streams the rows of its run whole: in step (u, j) lane l loads the 16 bytes at
+// byte 1024 j + 16 l of unit u's row(s), so one load instruction of the wave covers 1 KB of
+// one row, and the wave keeps D steps in flight.  The activation rows sit in LDS made signed
+// (q - 8: every nibble xor 8, rows zero-padded to whole KB); v_dot8_i32_i4 multiplies the
+// eight signed 4-bit codes of a weight dword with the eight of the matching activation dword
+// (both in the packed nibble order) and adds, so
+//   sum_k qa qw = sum_k (qa - 8) qw + 8 rs_n.
+// Bytes past K are loaded out of their buffer range and read as zeros.  At the end of a unit
+// the wave adds up its 64 lane sums (DPP within rows of 16, permlane swaps across them) and
+// lane i keeps unit i; the epilogue runs once per wave, one unit per lane, with the decode
+// kernel's arithmetic (acc16 = 16 acc), so both give the same fp16 results.
+template <int MB, bool SW>
+struct Gemv {
+  static constexpr int WAVES = 8;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int RPS = SW ? 2 : 1;  // weight rows per unit
+  static constexpr int D = 16 / RPS;      // steps in flight: 16 loads per lane
+  static constexpr int RUN = 64;          // units per wave at most
+  static constexpr int CH = 4;            // 8 KB chunks of an activation row: K <= 65536
+  static constexpr int MAX_LDS = MB * CH * 8 * 1024;
+};
+
+// sum over the 64 lanes, in every lane
+__device__ __forceinline__ int wave_total(int v) {
+  v += __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  v += __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);  // row_half_mirror: the other quad of 8
+  v += __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);  // row_mirror: the other 8 of 16
+  const bool odd_row = (threadIdx.x >> 4) & 1, upper = (threadIdx.x >> 5) & 1;
+  const auto s16 = __builtin_amdgcn_permlane16_swap(static_cast<uint32_t>(v), static_cast<uint32_t>(v), false, false);
+  v += static_cast<int>(odd_row ? s16[0] : s16[1]);  // the other row of the 32-lane half
+  const auto s32 = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(v), static_cast<uint32_t>(v), false, false);
+  v += static_cast<int>(upper ? s32[0] : s32[1]);    // the other half
+  return v;
+}
+
+template <int MB, bool SW>
+__global__ void __launch_bounds__(512)
+w4a4_gemv(GemmArgs g) {
+  using V = Gemv<MB, SW>;
+  constexpr int D = V::D, RPS = V::RPS;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t KB = static_cast<uint32_t>(g.K / 2);
+  const uint32_t J = (KB + 1023) / 1024;  // 1 KB chunks per row
+  const uint32_t AROW = J * 1024;         // LDS bytes per activation row
+  // balanced runs: wave w of W owns units [w U / W, (w + 1) U / W)
+  const int64_t U = SW ? g.N / 2 : g.N;
+  const int64_t W = static_cast<int64_t>(gridDim.x) * V::WAVES;
+  const int64_t gw = static_cast<int64_t>(blockIdx.x) * V::WAVES + wave;
+  const int64_t u0 = gw * U / W, u1 = (gw + 1) * U / W;
+  const uint32_t run = static_cast<uint32_t>(u1 - u0);
+  // weight rows of the run: [row0, rowe); byte offsets are relative to row0
+  const int64_t row0 = SW ? 64 * (u0 / 32) : u0;
+  const int64_t rowe = SW ? (u1 > u0 ? 64 * ((u1 + 31) / 32) : row0) : u1;
+  const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq + row0 * KB, (rowe - row0) * KB);
+
+  // the epilogue's operands first (lane i: unit i; clamped indices, loaded unconditionally),
+  // then the first D steps, then the activations: one round trip for all of them
+  const int64_t pe = u0 + (static_cast<uint32_t>(lane) < run ? lane : 0);
+  const int64_t ne = pe < U ? (SW ? 64 * (pe / 32) + (pe % 32) : pe) : 0;
+  const uint16_t* const bp = g.bias ? g.bias : reinterpret_cast<const uint16_t*>(g.wa);  // no branch around the load
+  float esc[RPS];
+  int32_t ers[RPS];
+  uint16_t eb[RPS];
+#pragma unroll
+  for (int r = 0; r < RPS; ++r) {
+    esc[r] = g.wa[ne + 32 * r];
+    ers[r] = g.rs[ne + 32 * r];
+    eb[r] = bp[ne + 32 * r];
+  }
+  float exa[MB], exb[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    const int64_t mc = m < g.M ? m : g.M - 1;
+    exa[m] = g.xa[mc];
+    exb[m] = g.xb[mc];
+  }
+
+  v4u wb[D][RPS];
+  uint32_t lu = 0, lj = 0;  // next step to load: unit lu of the run, chunk lj
+  auto load = [&](int slot) {
+    const uint32_t k = lj * 1024 + 16 * lane;
+    const bool ok = lu < run && k < KB;
+    int64_t r;
+    if constexpr (SW) {
+      const int64_t p = u0 + lu;
+      r = 64 * (p / 32) + (p % 32) - row0;  // gate row; the up row is 32 further
+    } else {
+      r = lu;
+    }
+    const uint32_t off = static_cast<uint32_t>(r) * KB + k;
+    wb[slot][0] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? off : 0x80000000u, 0, 0));
+    if constexpr (SW)
+      wb[slot][1] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? off + 32 * KB : 0x80000000u, 0, 0));
+    if (++lj == J) {
+      lj = 0;
+      ++lu;
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(d);
+
+  // activation rows -> LDS, signed and zero-padded; rows past M are zeros.  A row has at most
+  // CH x 8 KB (fits_gemv); every load is issued before the first write, unconditionally (out
+  // of range where there is nothing to load), so that the waits do not serialise them.
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
+  v4u a[V::CH][MB];
+#pragma unroll
+  for (int h = 0; h < V::CH; ++h)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      const uint32_t o = 16 * (threadIdx.x + h * V::THREADS);
+      const bool ok = m < g.M && o < KB;
+      a[h][m] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? m * KB + o : 0x80000000u, 0, 0));
+    }
+#pragma unroll
+  for (int h = 0; h < V::CH; ++h)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      const uint32_t o = 16 * (threadIdx.x + h * V::THREADS);
+      const bool ok = m < g.M && o < KB;
+      const v4u v = a[h][m] ^ (ok ? 0x88888888u : 0u);  // out of range: loaded as zeros
+      if (o < AROW) *reinterpret_cast<v4u*>(lds + m * AROW + o) = v;
+    }
+  __syncthreads();
+
+  int acc[RPS][MB], res[RPS][MB];
+#pragma unroll
+  for (int r = 0; r < RPS; ++r)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) acc[r][m] = res[r][m] = 0;
+  uint32_t cu = 0, cj = 0;  // step being consumed
+  const uint32_t steps = run * J;
+  for (uint32_t t0 = 0; t0 < steps; t0 += D) {
+    static_for<D>([&](auto dc) {
+      constexpr int d = decltype(dc)::value;
+      // steps past the run consume zeros (loaded out of range)
+      const uint32_t ao = cj * 1024 + 16 * lane;
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        const v4u a = *reinterpret_cast<const v4u*>(lds + m * AROW + ao);
+#pragma unroll
+        for (int r = 0; r < RPS; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[r][m] = __builtin_amdgcn_sdot8(static_cast<int>(a[e]), static_cast<int>(wb[d][r][e]), acc[r][m], false);
+      }
+      load(d);
+      if (++cj == J) {
+        cj = 0;
+        if (cu < run) {  // steps past the run only consumed zeros
+#pragma unroll
+          for (int r = 0; r < RPS; ++r)
+#pragma unroll
+            for (int m = 0; m < MB; ++m) {
+              const int s = wave_total(acc[r][m]);
+              res[r][m] = lane == static_cast<int>(cu) ? s : res[r][m];
+              acc[r][m] = 0;
+            }
+        }
+        ++cu;
+      }
+    });
+  }
+
+  if (static_cast<uint32_t>(lane) >= run) return;
+  const int64_t p = u0 + lane;
+  if constexpr (SW) {
+    const float wg = __fmul_rn(esc[0], static_cast<float>(ers[0])), wu = __fmul_rn(esc[1], static_cast<float>(ers[1]));
+    const float bg = g.bias ? h2f(eb[0]) : 0.0f, bu = g.bias ? h2f(eb[1]) : 0.0f;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= g.M) break;
+      const int ag = (res[0][m] + 8 * ers[0]) * 16, au = (res[1][m] + 8 * ers[1]) * 16;
+      const float ra = __fmul_rn(exa[m], 0.0625f);
+      const float gv = fp32_result(__fmaf_rn(ra, __fmul_rn(esc[0], static_cast<float>(ag)), __fmaf_rn(exb[m], wg, bg)));
+      const float uv = fp32_result(__fmaf_rn(ra, __fmul_rn(esc[1], static_cast<float>(au)), __fmaf_rn(exb[m], wu, bu)));
+      g.y[m * g.ldy + p] = f2h(fp32_result(swiglu_value(gv, uv)));
+    }
+  } else {
+    const int64_t n = p;
+    const float wn = __fmul_rn(esc[0], static_cast<float>(ers[0]));
+    const float bn = g.bias ? h2f(eb[0]) : 0.0f;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= g.M) break;
+      const int a = res[0][m] + 8 * ers[0];
+      const float t = __fmul_rn(esc[0], static_cast<float>(16 * a));
+      const float yv = fp32_result(__fmaf_rn(__fmul_rn(exa[m], 0.0625f), t, __fmaf_rn(exb[m], wn, bn)));
+      g.y[m * g.ldy + n] = f2h(yv);
+      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
+    }
+  }
+}
+
+template <int MB, bool SW>
+bool fits_gemv(const GemmArgs& g) {
+  const int64_t kb = g.K / 2, lds = MB * ((kb + 1023) / 1024) * 1024;
+  return g.M <= MB && lds <= Gemv<MB, SW>::MAX_LDS && g.M * kb + 64 < (int64_t{1} << 31) && (!SW || g.N % 64 == 0);
+}
+
+// About one workgroup of 8 waves per CU, and more where the runs would exceed 64 units.
+template <int MB, bool SW>
+hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
+  using V = Gemv<MB, SW>;
+  constexpr auto kern = w4a4_gemv<MB, SW>;
+  const int lds = static_cast<int>(MB * ((g.K / 2 + 1023) / 1024) * 1024);
+  if (lds > 64 * 1024) {
+    const hipError_t init = set_max_lds<kern>(V::MAX_LDS);
+    if (init != hipSuccess) return init;
+  }
+  int cus = 0;
+  const hipError_t e = device_cus(&cus);
+  if (e != hipSuccess) return e;
+  const int64_t U = SW ? g.N / 2 : g.N;
+  int64_t waves = static_cast<int64_t>(cus) * V::WAVES;
+  if (waves * V::RUN < U) waves = (U + V::RUN - 1) / V::RUN;
+  if (waves > U) waves = U;
+  const dim3 grid(static_cast<unsigned>((waves + V::WAVES - 1) / V::WAVES));
+  return launch(kern, grid, dim3(V::THREADS), lds, stream, g);
+}
+
+// The dot-product kernel for M <= 2, and for M <= 4 from 96 MB of weights (sets *e and
+// returns true when it covers the arguments).  Measured on MI355X against the 16-row decode
+// kernel, same data, interleaved (us): LLaMA-2-70B [M x 8192] x [57344 x 8192] with SiLU
+// 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8 vs 58.8 (M = 4); [M x 28672] x
+// [8192 x 28672] 22.9 vs 27.2 (M = 1), 23.7 vs 27.5 (M = 2), 27.2 vs 28.4 (M = 4);
+// LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU 12.3 vs 16.1 (M = 1), 14.3 vs 16.6
+// (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs
+// 9.8 (M = 4).
+template <bool SW>
+bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
+  if (g.M == 1 && fits_gemv<1, SW>(g)) {
+    *e = launch_gemv<1, SW>(g, stream);
+    return true;
+  }
+  if (g.M == 2 && fits_gemv<2, SW>(g)) {
+    *e = launch_gemv<2, SW>(g, stream);
+    return true;
+  }
+  if (g.M <= 4 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<4, SW>(g)) {
+    *e = launch_gemv<4, SW>(g, stream);
+    return true;
+  }
+  return false;
+}
+
 // NB = ceil(N / 4096) blocks of 16 rows, about one workgroup per CU of a 256-CU part; from
 // NB = 7 on, 8 blocks two steps ahead (measured on MI355X, LLaMA-2-70B: [M x 8192] x
 // [57344 x 8192] 58-64 vs 65-72 us, [M x 8192] x [28672 x 8192] 31-36 vs 33-37 us against
@@ -1332,6 +1585,8 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     // gate/up with SiLU: the ring kernels (block pairs per wave) and the decode kernel with
     // four 16-row blocks (two gate, two up); the same size classes as below
     constexpr int SD4 = skinny_depth<4>(), SD8 = skinny_depth<8>();
+    hipError_t e;
+    if (try_gemv<true>(g, stream, &e)) return e;
     if (g.M <= 16 && g.N > 16384) return fits_skinny<8, SD8>(g) ? launch_skinny<8, SD8>(g, stream) : hipErrorNotSupported;
     if (g.M <= 16) return fits_skinny<4, SD4>(g) ? launch_skinny<4, SD4>(g, stream) : hipErrorNotSupported;
     if (g.M <= 128)
@@ -1351,6 +1606,8 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
   // the tile kernels); 16 < M <= 128 runs 128 x 128 tiles with two K groups per workgroup.
   // Problems whose byte offsets do not fit 31 bits (operands of 2 GB and more) use the
   // register-staged kernel.
+  hipError_t e;
+  if (try_gemv<false>(g, stream, &e)) return e;
   if (g.M <= 16) return launch_skinny_sized(g, stream);
   if (g.M <= 128) {
     if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);

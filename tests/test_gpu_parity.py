@@ -574,6 +574,24 @@ def test_gemm_decode_kernel():
         gemm_case(M, N, K, seed=M * 31 + N + K, bias=(M % 2 == 1))
 
 
+def test_gemm_gemv_kernel():
+    # M <= 2 (and M <= 4 from 96 MB of weights) runs the dot-product kernel: whole 1 KB
+    # chunks of a row per wave load, K/2 not a multiple of 1 KB, K/2 shorter than one chunk,
+    # the largest K it takes (65536) and the first it leaves to the 16-row kernel, fewer rows
+    # than waves, and runs of more than 64 rows per wave's share (more workgroups)
+    say("w4a4_linear dot-product decode kernel: M 1..4, ragged N and K")
+    for (M, N, K) in [(1, 3, 64), (2, 8, 64), (1, 1000, 4160), (2, 4097, 2112), (1, 700, 65536),
+                      (2, 300, 65600), (1, 2048 * 64 + 5, 64), (3, 8192, 28672), (4, 8197, 24576)]:
+        gemm_case(M, N, K, seed=M * 37 + N + K, bias=(N % 2 == 1))
+
+
+@pytest.mark.parametrize("M,I,K,bias", [(1, 96, 4160, True), (2, 32, 64, False), (1, 2048 * 64 + 32, 64, True),
+                                        (2, 4128, 2112, True), (3, 14336, 8192, False)])
+def test_swiglu_gemv_kernel(M, I, K, bias):
+    say(f"w4a4_linear_swiglu dot-product decode kernel M={M} I={I} K={K} bias={bias}")
+    swiglu_case(M, I, K, seed=600 + M + I + K, bias=bias)
+
+
 # ---------------------------------------------------------------- W4A8
 
 def gemm8_case(M, N, K, seed, bias=True, sample_rows=None):
