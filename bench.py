@@ -140,12 +140,11 @@ TRAFFIC_MAP = {
 for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the GEMM launch shapes
     TRAFFIC_MAP[f"c5m{_m}/act_quant"] = ("c5", "quant_rows_identity<4, 4>", _g)
     TRAFFIC_MAP[f"c5m{_m}/r4_had_quant"] = ("c5", "had_quant_lines<28, 16, 14, false, 4, false>", 896 * _m)
-    if _m == 1:  # one token: the dot-product kernel, 8 waves on each of the 256 CUs
-        TRAFFIC_MAP["c5m1/gate_up_swiglu"] = ("c5", "w4a4_gemv<1, true>", 131072)
-        TRAFFIC_MAP["c5m1/down_gemm"] = ("c5", "w4a4_gemv<1, false>", 131072)
-    else:
-        TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = ("c5", "w4a4_gemm_skinny<8, 2, false>", 229376)
-        TRAFFIC_MAP[f"c5m{_m}/down_gemm"] = ("c5", "w4a4_gemm_skinny<2, 10, false>", 131072)
+    # M = 1 (and gate/up at M = 8): the dot-product kernel, 8 waves on each of the 256 CUs
+    TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = (("c5", f"w4a4_gemv<{_m}, true>", 131072) if _m < 16 else
+                                              ("c5", "w4a4_gemm_skinny<8, 2, false>", 229376))
+    TRAFFIC_MAP[f"c5m{_m}/down_gemm"] = (("c5", "w4a4_gemv<1, false>", 131072) if _m == 1 else
+                                         ("c5", "w4a4_gemm_skinny<2, 10, false>", 131072))
 
 
 def measured_traffic(key):

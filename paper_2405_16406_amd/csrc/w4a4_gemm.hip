@@ -1256,12 +1256,13 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 }
 
 // ------------------------------------------------------------------ dot-product decode kernel
-// M <= 4: one to four activation rows against the whole weight matrix, a matrix-vector
+// Decode sizes (M <= 8): a few activation rows against the whole weight matrix, a matrix-vector
 // product whose cost is reading the packed weights once.  Each wave owns a contiguous run of
-// at most 64 output units (a weight row n, or with SiLU a gate/up row pair of one output
-// column) and streams the rows of its run whole: in step (u, j) lane l loads the 16 bytes at
-// byte 1024 j + 16 l of unit u's row(s), so one load instruction of the wave covers 1 KB of
-// one row, and the wave keeps D steps in flight.  The activation rows sit in LDS made signed
+// at most 64 output units (a weight row; with SiLU the gate/up row pair of one output column;
+// from four activation rows on two neighbouring rows, which then share each activation read)
+// and streams the rows of its run whole: in step (u, j) lane l loads the 16 bytes at byte
+// 1024 j + 16 l of unit u's row(s), so one load instruction of the wave covers 1 KB of one
+// row, and the wave keeps 16 loads in flight.  The activation rows sit in LDS made signed
 // (q - 8: every nibble xor 8, rows zero-padded to whole KB); v_dot8_i32_i4 multiplies the
 // eight signed 4-bit codes of a weight dword with the eight of the matching activation dword
 // (both in the packed nibble order) and adds, so
@@ -1274,10 +1275,13 @@ template <int MB, bool SW>
 struct Gemv {
   static constexpr int WAVES = 8;
   static constexpr int THREADS = 64 * WAVES;
-  static constexpr int RPS = SW ? 2 : 1;  // weight rows per unit
-  static constexpr int D = 16 / RPS;      // steps in flight: 16 loads per lane
+  // weight rows per unit: the gate and up rows of an output column (32 rows apart), or with
+  // four and more activation rows two neighbouring rows, which share the activation reads
+  static constexpr int RPS = SW || MB >= 4 ? 2 : 1;
+  static constexpr int RSTEP = SW ? 32 : 1;  // rows between the rows of a unit
+  static constexpr int D = 16 / RPS;         // steps in flight: 16 loads per lane
   static constexpr int RUN = 64;          // units per wave at most
-  static constexpr int CH = 4;            // 8 KB chunks of an activation row: K <= 65536
+  static constexpr int CH = MB <= 4 ? 4 : 2;  // 8 KB chunks of an activation row: K <= 65536 (32768)
   static constexpr int MAX_LDS = MB * CH * 8 * 1024;
 };
 
@@ -1299,7 +1303,7 @@ template <int MB, bool SW>
 __global__ void __launch_bounds__(512)
 w4a4_gemv(GemmArgs g) {
   using V = Gemv<MB, SW>;
-  constexpr int D = V::D, RPS = V::RPS;
+  constexpr int D = V::D, RPS = V::RPS, RSTEP = V::RSTEP;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1307,29 +1311,30 @@ w4a4_gemv(GemmArgs g) {
   const uint32_t J = (KB + 1023) / 1024;  // 1 KB chunks per row
   const uint32_t AROW = J * 1024;         // LDS bytes per activation row
   // balanced runs: wave w of W owns units [w U / W, (w + 1) U / W)
-  const int64_t U = SW ? g.N / 2 : g.N;
+  const int64_t U = SW ? g.N / 2 : (g.N + RPS - 1) / RPS;
   const int64_t W = static_cast<int64_t>(gridDim.x) * V::WAVES;
   const int64_t gw = static_cast<int64_t>(blockIdx.x) * V::WAVES + wave;
   const int64_t u0 = gw * U / W, u1 = (gw + 1) * U / W;
   const uint32_t run = static_cast<uint32_t>(u1 - u0);
   // weight rows of the run: [row0, rowe); byte offsets are relative to row0
-  const int64_t row0 = SW ? 64 * (u0 / 32) : u0;
-  const int64_t rowe = SW ? (u1 > u0 ? 64 * ((u1 + 31) / 32) : row0) : u1;
+  const int64_t row0 = SW ? 64 * (u0 / 32) : RPS * u0;
+  const int64_t rowe = SW ? (u1 > u0 ? 64 * ((u1 + 31) / 32) : row0) : (RPS * u1 < g.N ? RPS * u1 : g.N);
   const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq + row0 * KB, (rowe - row0) * KB);
 
   // the epilogue's operands first (lane i: unit i; clamped indices, loaded unconditionally),
   // then the first D steps, then the activations: one round trip for all of them
   const int64_t pe = u0 + (static_cast<uint32_t>(lane) < run ? lane : 0);
-  const int64_t ne = pe < U ? (SW ? 64 * (pe / 32) + (pe % 32) : pe) : 0;
+  const int64_t ne = pe < U ? (SW ? 64 * (pe / 32) + (pe % 32) : RPS * pe) : 0;  // first row of the unit
   const uint16_t* const bp = g.bias ? g.bias : reinterpret_cast<const uint16_t*>(g.wa);  // no branch around the load
   float esc[RPS];
   int32_t ers[RPS];
   uint16_t eb[RPS];
 #pragma unroll
   for (int r = 0; r < RPS; ++r) {
-    esc[r] = g.wa[ne + 32 * r];
-    ers[r] = g.rs[ne + 32 * r];
-    eb[r] = bp[ne + 32 * r];
+    const int64_t n = ne + RSTEP * r < g.N ? ne + RSTEP * r : g.N - 1;
+    esc[r] = g.wa[n];
+    ers[r] = g.rs[n];
+    eb[r] = bp[n];
   }
   float exa[MB], exb[MB];
 #pragma unroll
@@ -1349,12 +1354,12 @@ w4a4_gemv(GemmArgs g) {
       const int64_t p = u0 + lu;
       r = 64 * (p / 32) + (p % 32) - row0;  // gate row; the up row is 32 further
     } else {
-      r = lu;
+      r = RPS * lu;  // a second row past N is past the buffer range: zeros
     }
     const uint32_t off = static_cast<uint32_t>(r) * KB + k;
-    wb[slot][0] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? off : 0x80000000u, 0, 0));
-    if constexpr (SW)
-      wb[slot][1] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? off + 32 * KB : 0x80000000u, 0, 0));
+#pragma unroll
+    for (int q = 0; q < RPS; ++q)
+      wb[slot][q] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsb, ok ? off + q * RSTEP * KB : 0x80000000u, 0, 0));
     if (++lj == J) {
       lj = 0;
       ++lu;
@@ -1441,17 +1446,21 @@ w4a4_gemv(GemmArgs g) {
       g.y[m * g.ldy + p] = f2h(fp32_result(swiglu_value(gv, uv)));
     }
   } else {
-    const int64_t n = p;
-    const float wn = __fmul_rn(esc[0], static_cast<float>(ers[0]));
-    const float bn = g.bias ? h2f(eb[0]) : 0.0f;
 #pragma unroll
-    for (int m = 0; m < MB; ++m) {
-      if (m >= g.M) break;
-      const int a = res[0][m] + 8 * ers[0];
-      const float t = __fmul_rn(esc[0], static_cast<float>(16 * a));
-      const float yv = fp32_result(__fmaf_rn(__fmul_rn(exa[m], 0.0625f), t, __fmaf_rn(exb[m], wn, bn)));
-      g.y[m * g.ldy + n] = f2h(yv);
-      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
+    for (int r = 0; r < RPS; ++r) {
+      const int64_t n = RPS * p + r;
+      if (n >= g.N) break;
+      const float wn = __fmul_rn(esc[r], static_cast<float>(ers[r]));
+      const float bn = g.bias ? h2f(eb[r]) : 0.0f;
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        if (m >= g.M) break;
+        const int a = res[r][m] + 8 * ers[r];
+        const float t = __fmul_rn(esc[r], static_cast<float>(16 * a));
+        const float yv = fp32_result(__fmaf_rn(__fmul_rn(exa[m], 0.0625f), t, __fmaf_rn(exb[m], wn, bn)));
+        g.y[m * g.ldy + n] = f2h(yv);
+        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
+      }
     }
   }
 }
@@ -1475,7 +1484,7 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
   int cus = 0;
   const hipError_t e = device_cus(&cus);
   if (e != hipSuccess) return e;
-  const int64_t U = SW ? g.N / 2 : g.N;
+  const int64_t U = SW ? g.N / 2 : (g.N + V::RPS - 1) / V::RPS;
   int64_t waves = static_cast<int64_t>(cus) * V::WAVES;
   if (waves * V::RUN < U) waves = (U + V::RUN - 1) / V::RUN;
   if (waves > U) waves = U;
@@ -1483,14 +1492,16 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(V::THREADS), lds, stream, g);
 }
 
-// The dot-product kernel for M <= 2, and for M <= 4 from 96 MB of weights (sets *e and
-// returns true when it covers the arguments).  Measured on MI355X against the 16-row decode
-// kernel, same data, interleaved (us): LLaMA-2-70B [M x 8192] x [57344 x 8192] with SiLU
-// 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8 vs 58.8 (M = 4); [M x 28672] x
-// [8192 x 28672] 22.9 vs 27.2 (M = 1), 23.7 vs 27.5 (M = 2), 27.2 vs 28.4 (M = 4);
-// LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU 12.3 vs 16.1 (M = 1), 14.3 vs 16.6
-// (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs
-// 9.8 (M = 4).
+// The dot-product kernel for M <= 2, for M <= 4 from 96 MB of weights, and with SiLU for
+// M <= 8 from 96 MB (sets *e and returns true when it covers the arguments).  Measured on
+// MI355X against the 16-row decode kernel, same data, interleaved (us): LLaMA-2-70B
+// [M x 8192] x [57344 x 8192] with SiLU 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8
+// vs 58.8 (M = 4), 54.5 vs 61.0 (M = 8); [M x 28672] x [8192 x 28672] 22.9 vs 27.2
+// (M = 1), 23.7 vs 27.5 (M = 2), 25.0 vs 28.4 (M = 4), 30.7 vs 29.2 (M = 8: eight
+// activation rows of 14 KB per workgroup); LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU
+// 12.3 vs 16.1 (M = 1), 14.3 vs 16.6 (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x
+// [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs 9.8 (M = 4).  With eight rows the kernel is
+// bound by its v_dot8 issue rather than by HBM.
 template <bool SW>
 bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   if (g.M == 1 && fits_gemv<1, SW>(g)) {
@@ -1503,6 +1514,10 @@ bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   }
   if (g.M <= 4 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<4, SW>(g)) {
     *e = launch_gemv<4, SW>(g, stream);
+    return true;
+  }
+  if (SW && g.M <= 8 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<8, SW>(g)) {
+    *e = launch_gemv<8, SW>(g, stream);
     return true;
   }
   return false;

@@ -550,7 +550,7 @@ def test_swiglu_linear_llama3_8b_sampled():
     swiglu_case(4096, 14336, 4096, seed=42, bias=True, sample_rows=np.array([0, 4095]))
 
 
-@pytest.mark.parametrize("M", [1, 16])
+@pytest.mark.parametrize("M", [1, 8, 16])
 def test_swiglu_linear_llama2_70b_decode(M):
     say(f"w4a4_linear_swiglu LLaMA-2-70B decode M={M}: [M,8192]x[2x28672,8192]")
     swiglu_case(M, 28672, 8192, seed=43 + M, bias=False)
@@ -586,7 +586,7 @@ def test_gemm_gemv_kernel():
 
 
 @pytest.mark.parametrize("M,I,K,bias", [(1, 96, 4160, True), (2, 32, 64, False), (1, 2048 * 64 + 32, 64, True),
-                                        (2, 4128, 2112, True), (3, 14336, 8192, False)])
+                                        (2, 4128, 2112, True), (3, 14336, 8192, False), (5, 14368, 8192, True)])
 def test_swiglu_gemv_kernel(M, I, K, bias):
     say(f"w4a4_linear_swiglu dot-product decode kernel M={M} I={I} K={K} bias={bias}")
     swiglu_case(M, I, K, seed=600 + M + I + K, bias=bias)
