@@ -706,7 +706,7 @@ PROFILE_COMMANDS["summary"] = "python3 bench.py --summarize DIR"
 
 SOURCE_OF = {"qk_had_kvquant": "kv_quant.hip", "quant_rows_identity": "had_quant.hip",
              "had_quant_act_generic": "had_quant.hip", "had_quant_": "had_quant_kron.hip",
-             "w4a4_gemm": "w4a4_gemm.hip", "attn_decode": "kv_attn.hip"}
+             "w4a4_gemm": "w4a4_gemm.hip", "w4a4_gemv": "w4a4_gemm.hip", "attn_decode": "kv_attn.hip"}
 
 
 def _csv_rows(d, pattern):

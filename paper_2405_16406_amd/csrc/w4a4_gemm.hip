@@ -18,6 +18,9 @@
 // two workgroups per CU) and 256 x 256 (8 waves of 128 x 64).
 // Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
 // used where 32-bit buffer offsets do not cover the operands.
+// Decode sizes: w4a4_gemv (a few activation rows, whole weight rows streamed through
+// v_dot8_i32_i4) and w4a4_gemm_skinny (M <= 16, weight rows straight into registers and
+// v_mfma_i32_16x16x64_i8).
 #include <utility>
 
 #include "sq_device.h"
