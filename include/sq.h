@@ -330,8 +330,8 @@ sq_status sq_attn_decode_workspace(int64_t B, int64_t S, int64_t H, int64_t D, u
 /*
  * sq_attn_decode_kv4_split -- the attention of sq_attn_decode_kv4_ex (same formula, Sec. 3.1
  * R3 with eq. 1 dequantisation), split over the sequence as in flash-decoding: each
- * workgroup reads one chunk of tokens for 32 heads at once, so the cache streams in whole
- * token lines; a second kernel merges the chunks' partial softmax states (maximum, sum,
+ * workgroup reads one chunk of tokens for 16 heads at once, 1 KB of one token per wave
+ * load; a second kernel merges the chunks' partial softmax states (maximum, sum,
  * 128 weighted dims, in fp32) in chunk order.  The result equals sq_attn_decode_kv4_ex's
  * up to the order of fp32 additions, and is deterministic.
  *   workspace        device memory, 16-byte aligned, at least the bytes

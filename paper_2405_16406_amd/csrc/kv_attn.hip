@@ -10,13 +10,16 @@
 // the batch and head dims 32 qd .. 32 qd + 31, i.e. one 16-byte load of K codes and one of
 // V codes (a batch reads 16 x 64 contiguous bytes of each); lane qd of the token loads its
 // scale number qd (k_alpha, k_beta, v_alpha, v_beta) and the quad shares them by DPP.
-//   * q . c_t: v_dot2_f32_f16 on code pairs made fp16 as 1024 + c (exact), minus 1024 times
-//     the lane's query sum; the four lanes of a token add their parts (DPP quad permutes).
+//   * q . c_t: v_dot2_f32_f16 on code pairs made fp16 (exact): nibbles 0, 2, 4 and 6 of a
+//     code word as 1024 + c, nibbles 1, 3, 5 and 7 in place as 1024 + 16 c (five VALU per
+//     word: one shift, four and-or), minus 1024 times the lane's query sums, the second part
+//     divided by 16; the four lanes of a token add their parts (DPP quad permutes).
 //   * Online softmax in base 2 (log2 e is folded into the scale) with one running maximum m
 //     per wave (the batch maximum by DPP row rotations and permlane swaps; a rescale only
 //     when it grows).  Each lane sums, over the tokens it sees, l = sum_t p_t,
-//     acc_d = sum_t p_t alpha_t (1024 + c_td) (v_fma_mix_f32 on the same fp16 code pairs),
-//     pa = sum_t p_t alpha_t and bsum = sum_t p_t beta_t; dim d is acc_d - 1024 pa + bsum.
+//     acc_d = sum_t p_t alpha_t (1024 + c_td), or (1024 + 16 c_td) for the odd dims
+//     (v_fma_mix_f32 on the same fp16 code pairs), pa = sum_t p_t alpha_t and
+//     bsum = sum_t p_t beta_t; dim d is acc_d - 1024 pa (divided by 16 for odd d) + bsum.
 //   * At the end the 16 token slots of a wave add up in registers (same maximum), and the 16
 //     waves merge in LDS; out_d = (sum of the waves' rescaled dims) / (their rescaled l).
 // The group parameters are fp32, or fp16 (P16: half the parameter bytes of the cache).
@@ -48,12 +51,10 @@ __device__ __forceinline__ float quad_xor(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, false));
 }
 
-// allreduce over the token slots of a wave: the lanes with the same lane % 4 (HPW = 1, 16
-// slots) or lane % 8 (HPW = 2, 8 slots)
-template <int HPW = 1, typename Op>
+// allreduce over the 16 token slots of a wave: the lanes with the same lane % 4
+template <typename Op>
 __device__ __forceinline__ float slots_reduce(float v, Op op) {
-  if constexpr (HPW == 1)
-    v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror:4
+  v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror:4
   v = op(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false)));  // row_ror:8
   const bool odd_row = (threadIdx.x >> 4) & 1, upper = (threadIdx.x >> 5) & 1;
   const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -74,6 +75,82 @@ __device__ __forceinline__ float rescale(float a, float b) {
   return a == -INFINITY ? 0.0f : exp2f(__fsub_rn(a, b));
 }
 
+// The lane's 32 query dims (32 qd .. 32 qd + 31 of the head whose query row is qrow) as fp16
+// pairs (8c + k, 8c + k + 4) matching the code pairs, the head's query sum (over the quad of
+// lanes) and the code offsets of the lane's even and odd pairs (1024 times their query sums).
+struct QueryPairs {
+  v2h qp[4][4];
+  float qsum, bias_even, bias_odd;
+};
+__device__ __forceinline__ void load_query(const uint16_t* qrow, int qd, QueryPairs& qq) {
+  float qsum_lane = 0.0f, qodd_lane = 0.0f;  // all 32 dims; the odd dims
+  const v4u* qv = reinterpret_cast<const v4u*>(qrow + 32 * qd);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const v4u v = qv[c];  // dims 32 qd + 8 c .. + 7: words [q0|q1] [q2|q3] [q4|q5] [q6|q7]
+    _Float16 e[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      e[2 * k] = __builtin_bit_cast(_Float16, static_cast<uint16_t>(v[k] & 0xFFFFu));
+      e[2 * k + 1] = __builtin_bit_cast(_Float16, static_cast<uint16_t>(v[k] >> 16));
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) qq.qp[c][k] = v2h{e[k], e[k + 4]};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) qsum_lane = __fadd_rn(qsum_lane, static_cast<float>(e[k]));
+#pragma unroll
+    for (int k = 1; k < 8; k += 2) qodd_lane = __fadd_rn(qodd_lane, static_cast<float>(e[k]));
+  }
+  float qsum = __fadd_rn(qsum_lane, quad_xor<1>(qsum_lane));
+  qq.qsum = __fadd_rn(qsum, quad_xor<2>(qsum));
+  qq.bias_even = __fmul_rn(1024.0f, __fsub_rn(qsum_lane, qodd_lane));
+  qq.bias_odd = __fmul_rn(1024.0f, qodd_lane);
+}
+
+// Code-word to fp16 pairs: (e0,e4) and (e2,e6) as 1024 + c, (e1,e5) and (e3,e7) as
+// 1024 + 16 c (those nibbles stay in place, in mantissa bits 4-7): one shift and four and-or.
+// The masks are kept in registers (a VOP3 and-or takes no literal operands).
+struct PairMasks {
+  uint32_t lo = 0x000F000Fu, hi = 0x00F000F0u, base = 0x64006400u;
+  __device__ __forceinline__ PairMasks() { asm volatile("" : "+v"(lo), "+v"(hi), "+v"(base)); }
+  __device__ __forceinline__ void pairs(uint32_t cw, v2h (&pr)[4]) const {
+    const uint32_t sh = cw >> 8;
+    pr[0] = __builtin_bit_cast(v2h, (cw & lo) | base);
+    pr[1] = __builtin_bit_cast(v2h, (cw & hi) | base);
+    pr[2] = __builtin_bit_cast(v2h, (sh & lo) | base);
+    pr[3] = __builtin_bit_cast(v2h, (sh & hi) | base);
+  }
+};
+
+// q . c over the lane's 32 dims of one token (code words cw), before the quad sum
+__device__ __forceinline__ float lane_dot(const QueryPairs& qq, const PairMasks& pm, const v4u& cw) {
+  float s0 = 0.0f, s1 = 0.0f;  // pairs 0 and 2 (1024 + c), pairs 1 and 3 (1024 + 16 c)
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    v2h pr[4];
+    pm.pairs(cw[c], pr);  // dims 8c .. 8c+7 of the lane
+    s0 = __builtin_amdgcn_fdot2(qq.qp[c][0], pr[0], s0, false);
+    s1 = __builtin_amdgcn_fdot2(qq.qp[c][1], pr[1], s1, false);
+    s0 = __builtin_amdgcn_fdot2(qq.qp[c][2], pr[2], s0, false);
+    s1 = __builtin_amdgcn_fdot2(qq.qp[c][3], pr[3], s1, false);
+  }
+  return __fmaf_rn(__fsub_rn(s1, qq.bias_odd), 0.0625f, __fsub_rn(s0, qq.bias_even));
+}
+
+// acc_d += pa (1024 + c_d) (odd d: 1024 + 16 c_d) over the lane's 32 dims of one token
+__device__ __forceinline__ void lane_accumulate(float (&acc)[32], float pa, const PairMasks& pm, const v4u& cw) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    v2h pr[4];
+    pm.pairs(cw[c], pr);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {  // pair k holds dims 8c + k and 8c + k + 4
+      acc[8 * c + k] = __fmaf_rn(pa, static_cast<float>(pr[k][0]), acc[8 * c + k]);
+      acc[8 * c + k + 4] = __fmaf_rn(pa, static_cast<float>(pr[k][1]), acc[8 * c + k + 4]);
+    }
+  }
+}
+
 // Partial attention state of one wave: running maximum m (base 2), and per lane the sums
 // over the tokens it has seen: l = sum p, acc_d = sum p alpha (1024 + c_d), pa = sum p alpha,
 // bsum = sum p beta.
@@ -82,50 +159,22 @@ struct WaveAttn {
   float acc[32];
 };
 
-// One wave's pass over the batches first, first + step, ... (count of them) of 16 / HPW
-// tokens.  HPW = 1: every lane serves head (b, h); lane l = 4 tok + qd.  HPW = 2: the wave
-// serves heads h and h + 1 (one 128-byte piece of a token's line), lane l = 8 tok + 4 hp + qd
-// serves head h + hp; when h + 1 is past the heads, its lanes see no tokens.
-template <bool P16, int HPW = 1>
-__device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0, int first, int step, int count,
+// One wave's pass over the batches first, first + step, ... (count of them) of 16 tokens of
+// head (b, h); lane l = 4 tok + qd.
+template <bool P16>
+__device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h, int first, int step, int count,
                                        WaveAttn& st) {
-  static_assert(HPW == 1 || HPW == 2, "one or two heads per wave");
-  constexpr int TS = 16 / HPW;  // tokens per batch
   const int lane = threadIdx.x & 63;
-  const int tok = lane >> (HPW == 2 ? 3 : 2);
-  const int hp = HPW == 2 ? (lane >> 2) & 1 : 0;
+  const int tok = lane >> 2;
   const int qd = lane & 3;
   const int64_t S = a.S;
-  const int nh = HPW == 2 && h0 + 1 < a.H ? 2 : 1;  // heads of this wave
-  const bool hok = hp < nh;
-  const int64_t h = h0 + (hok ? hp : 0);             // this lane's head
-  // ---- query: the lane's 32 dims as fp16 pairs (8w+e, 8w+e+4) matching the code pairs
-  v2h qp[4][4];
-  float qsum_lane = 0.0f;
-  {
-    const v4u* qv = reinterpret_cast<const v4u*>(a.q + (b * a.H + h) * 128 + 32 * qd);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const v4u v = qv[c];  // dims 32 qd + 8 c .. + 7: words [q0|q1] [q2|q3] [q4|q5] [q6|q7]
-      _Float16 e[8];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        e[2 * k] = __builtin_bit_cast(_Float16, static_cast<uint16_t>(v[k] & 0xFFFFu));
-        e[2 * k + 1] = __builtin_bit_cast(_Float16, static_cast<uint16_t>(v[k] >> 16));
-      }
-#pragma unroll
-      for (int k = 0; k < 4; ++k) qp[c][k] = v2h{e[k], e[k + 4]};
-#pragma unroll
-      for (int k = 0; k < 8; ++k) qsum_lane = __fadd_rn(qsum_lane, static_cast<float>(e[k]));
-    }
-  }
-  float qsum = __fadd_rn(qsum_lane, quad_xor<1>(qsum_lane));
-  qsum = __fadd_rn(qsum, quad_xor<2>(qsum));
-  const float bias1024 = __fmul_rn(1024.0f, qsum_lane);
+  QueryPairs qq;
+  load_query(a.q + (b * a.H + h) * 128, qd, qq);
+  const PairMasks pm;
 
   // ---- cache of this (batch, head): token t at byte t * H * 64 (codes) / t * H * 4 (scales)
-  const int64_t row0 = b * S * a.H + h0;
-  const int64_t cspan = ((S - 1) * a.H + nh) * 64;
+  const int64_t row0 = b * S * a.H + h;
+  const int64_t cspan = ((S - 1) * a.H + 1) * 64;
   const __amdgpu_buffer_rsrc_t rk = rsrc(a.kq + row0 * 64, cspan);
   const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, cspan);
   const void* pb = qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb;  // this lane's scale array
@@ -136,12 +185,12 @@ __device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0,
   v4u kc[kDepth], vc[kDepth];
   float pv[kDepth];
   auto load = [&](int slot, int it) {
-    const uint32_t t = static_cast<uint32_t>(first + step * it) * TS + tok;
-    const bool ok = hok && it < count && t < S32;  // else codes out of range (zeros), scale of token 0
-    const uint32_t co = ok ? t * cstride + 64 * hp + 16 * qd : 0x80000000u;
+    const uint32_t t = static_cast<uint32_t>(first + step * it) * 16 + tok;
+    const bool ok = it < count && t < S32;  // else codes out of range (zeros), scale of token 0
+    const uint32_t co = ok ? t * cstride + 16 * qd : 0x80000000u;
     kc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rk, co, 0, 0));
     vc[slot] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rv, co, 0, 0));
-    const int64_t pi = row0 + (ok ? t * H32 + hp : 0u);
+    const int64_t pi = row0 + (ok ? t * H32 : 0u);
     if constexpr (P16)
       pv[slot] = h2f(static_cast<const uint16_t*>(pb)[pi]);
     else
@@ -153,14 +202,6 @@ __device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0,
 #pragma unroll
   for (int d = 0; d < 32; ++d) acc[d] = st.acc[d];
   const float cs = a.scale_log2e;
-  // code pair masks kept in registers (a VOP3 and-or takes no literal operands)
-  uint32_t kMask = 0x000F000Fu, kBase = 0x64006400u;
-  asm volatile("" : "+v"(kMask), "+v"(kBase));
-  // the four fp16 pairs (1024 + c) of a code word: (e0,e4) (e1,e5) (e2,e6) (e3,e7)
-  auto pairs = [&](uint32_t cw, v2h (&pr)[4]) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) pr[k] = __builtin_bit_cast(v2h, ((cw >> (4 * k)) & kMask) | kBase);
-  };
 
 #pragma unroll
   for (int d = 0; d < kDepth; ++d) load(d, d);
@@ -168,27 +209,17 @@ __device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0,
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
       const int it = it0 + d;
-      const uint32_t t = static_cast<uint32_t>(first + step * it) * TS + tok;
-      const bool ok = hok && it < count && t < S32;  // uniform over the quad of a token
+      const uint32_t t = static_cast<uint32_t>(first + step * it) * 16 + tok;
+      const bool ok = it < count && t < S32;  // uniform over the quad of a token
       // q . c_t over the lane's 32 dims, then over the quad
-      float s0 = 0.0f, s1 = 0.0f;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        v2h pr[4];
-        pairs(kc[d][c], pr);  // dims 8c .. 8c+7 of the lane
-        s0 = __builtin_amdgcn_fdot2(qp[c][0], pr[0], s0, false);
-        s1 = __builtin_amdgcn_fdot2(qp[c][1], pr[1], s1, false);
-        s0 = __builtin_amdgcn_fdot2(qp[c][2], pr[2], s0, false);
-        s1 = __builtin_amdgcn_fdot2(qp[c][3], pr[3], s1, false);
-      }
-      float dot = __fsub_rn(__fadd_rn(s0, s1), bias1024);
+      float dot = lane_dot(qq, pm, kc[d]);
       dot = __fadd_rn(dot, quad_xor<1>(dot));
       dot = __fadd_rn(dot, quad_xor<2>(dot));
       const float ka = quad_bcast<0>(pv[d]), kb = quad_bcast<1>(pv[d]);
       const float va = quad_bcast<2>(pv[d]), vb = quad_bcast<3>(pv[d]);
-      const float s = ok ? __fmul_rn(cs, __fmaf_rn(ka, dot, __fmul_rn(kb, qsum))) : -INFINITY;
-      const float mb = slots_reduce<HPW>(s, [](float u, float v) { return fmaxf(u, v); });
-      if (mb > m) {  // (uniform over a head's lanes) new running maximum: rescale the sums
+      const float s = ok ? __fmul_rn(cs, __fmaf_rn(ka, dot, __fmul_rn(kb, qq.qsum))) : -INFINITY;
+      const float mb = slots_reduce(s, [](float u, float v) { return fmaxf(u, v); });
+      if (mb > m) {  // (uniform) new running maximum: rescale the sums
         const float f = rescale(m, mb);
         l = __fmul_rn(l, f);
         bsum = __fmul_rn(bsum, f);
@@ -203,16 +234,7 @@ __device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0,
         bsum = __fmaf_rn(p, vb, bsum);
         const float pa = __fmul_rn(p, va);
         pa_sum = __fadd_rn(pa_sum, pa);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          v2h pr[4];
-          pairs(vc[d][c], pr);
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {  // pair k holds dims 8c + k and 8c + k + 4
-            acc[8 * c + k] = __fmaf_rn(pa, static_cast<float>(pr[k][0]), acc[8 * c + k]);
-            acc[8 * c + k + 4] = __fmaf_rn(pa, static_cast<float>(pr[k][1]), acc[8 * c + k + 4]);
-          }
-        }
+        lane_accumulate(acc, pa, pm, vc[d]);
       }
       load(d, it + kDepth);
     }
@@ -225,16 +247,22 @@ __device__ __forceinline__ void attend(const AttnArgs& a, int64_t b, int64_t h0,
   for (int d = 0; d < 32; ++d) st.acc[d] = acc[d];
 }
 
+// Dim e of a lane's 32 from its sum acc_e: the code offset (1024 pa) removed, the odd
+// dims' codes (1024 + 16 c) scaled back by 1/16 (exact), the betas added.
+__device__ __forceinline__ float dim_value(float acc, float off, float bsum, int e) {
+  const float v = __fsub_rn(acc, off);
+  return __fadd_rn(e & 1 ? __fmul_rn(v, 0.0625f) : v, bsum);
+}
+
 // The token slots of a head share m: their sums add up (every lane ends with its head's
 // totals of its 32 dims).
-template <int HPW = 1>
 __device__ __forceinline__ void wave_total(WaveAttn& st) {
   auto add = [](float u, float v) { return __fadd_rn(u, v); };
-  st.l = slots_reduce<HPW>(st.l, add);
-  st.bsum = slots_reduce<HPW>(st.bsum, add);
-  st.pa_sum = slots_reduce<HPW>(st.pa_sum, add);
+  st.l = slots_reduce(st.l, add);
+  st.bsum = slots_reduce(st.bsum, add);
+  st.pa_sum = slots_reduce(st.pa_sum, add);
 #pragma unroll
-  for (int e = 0; e < 32; ++e) st.acc[e] = slots_reduce<HPW>(st.acc[e], add);
+  for (int e = 0; e < 32; ++e) st.acc[e] = slots_reduce(st.acc[e], add);
 }
 
 template <bool P16>
@@ -263,7 +291,7 @@ attn_decode_kv4(AttnArgs a) {
   const float off = __fmul_rn(1024.0f, pa_sum);
   if (lane < 4) {
 #pragma unroll
-    for (int e = 0; e < 32; ++e) red_acc[w][32 * qd + e] = __fadd_rn(__fsub_rn(acc[e], off), bsum);
+    for (int e = 0; e < 32; ++e) red_acc[w][32 * qd + e] = dim_value(acc[e], off, bsum, e);
     if (lane == 0) {
       red_ml[w][0] = m;
       red_ml[w][1] = l;
@@ -288,59 +316,164 @@ attn_decode_kv4(AttnArgs a) {
       static_cast<uint32_t>(f2h(o0)) | (static_cast<uint32_t>(f2h(o1)) << 16);
 }
 
-// ---- split over the sequence (flash-decoding): workgroup (b, chunk c, group g of 32
-// heads) of 16 waves; wave w serves heads 32 g + 2 w and 32 g + 2 w + 1 over the chunk's
-// batches of 8 tokens, so each of its loads brings whole 128-byte lines (8 tokens x 128
-// bytes), where one wave per head uses half of every line it touches, and the workgroup
-// reads whole 2 KB token lines of a 32-head cache.  Each head leaves its partial state (m,
-// l, the 128 dims with the code offset removed and the betas added) in part; the combine
-// kernel merges the chunks of a head.
-// FINAL (a single chunk): the lanes divide and store the output themselves.
-constexpr int kSplitWaves = kAttnGroupHeads / 2;
+// ---- split over the sequence (flash-decoding): workgroup (b, 16-head group g, chunk c) of 8
+// waves.  Lane l = 4 hh + qd serves head 16 g + hh, dims 32 qd .. 32 qd + 31, so one load of
+// the wave brings the 1 KB of codes of one token for the group's 16 heads (half of a 32-head
+// token line), and the four parameter loads 64 contiguous bytes each.  The chunk's tokens go
+// in batches of 8 per wave (wave w takes tokens 64 i + 8 w .. + 7 of the chunk, so the 8 waves
+// walk the chunk's lines together), two batches in flight.  Each lane keeps its head's state;
+// a batch's 8 scores are in the lane, so its maximum (and the rare rescale) is taken once per
+// batch without crossing lanes.  The 8 waves merge in LDS; each head leaves its partial state
+// (m, l, the 128 dims with the code offset removed and the betas added) in part, and the
+// combine kernel merges the chunks of a head.
+// FINAL (a single chunk): the workgroup divides and stores the output itself.
+constexpr int kSplitWaves = kAttnSplitWaves;
+constexpr int kBatch = 8;  // tokens per wave batch
+constexpr int kSplitLds = kSplitWaves * kAttnGroupHeads * (128 + 2) * 4;
 
 template <bool P16, bool FINAL>
-__global__ void __launch_bounds__(64 * kSplitWaves, 4)
+__global__ void __launch_bounds__(64 * kSplitWaves, 2)
 attn_decode_part(AttnArgs a) {
+  // dynamic LDS (kSplitLds bytes): the waves' dims [wave][head][128], then (m, l) [wave][head]
+  extern __shared__ __attribute__((aligned(16))) float split_lds[];
+  auto red_d = reinterpret_cast<float (*)[kAttnGroupHeads][128]>(split_lds);
+  auto red_ml = reinterpret_cast<float (*)[kAttnGroupHeads][2]>(split_lds + kSplitWaves * kAttnGroupHeads * 128);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int qd = lane & 3;
-  const int hp = (lane >> 2) & 1;
-  // the workgroup count (B * chunks * NG, at most B * NG or about four times the CUs) fits 32 bits
+  const int hh = lane >> 2, qd = lane & 3;
+  // the workgroup count (B * chunks * NG, at most B * NG or about the CUs) fits 32 bits
   const int NG = static_cast<int>((a.H + kAttnGroupHeads - 1) / kAttnGroupHeads), NC = static_cast<int>(a.chunks);
   const int g = static_cast<int>(blockIdx.x) % NG;
   const int c = (static_cast<int>(blockIdx.x) / NG) % NC;
-  const int b = static_cast<int>(blockIdx.x) / NG / NC;
-  const int h0 = kAttnGroupHeads * g + 2 * w;
-  if (h0 >= a.H) return;  // no workgroup barrier follows
-  const int nb = static_cast<int>((a.S + 7) / 8);  // batches of 8 tokens
-  const int first = 2 * c * static_cast<int>(a.chunk_batches);
-  const int count = min(2 * static_cast<int>(a.chunk_batches), nb - first);
-  WaveAttn st;
+  const int64_t b = static_cast<int>(blockIdx.x) / NG / NC;
+  const int64_t h = kAttnGroupHeads * g + hh;
+  const bool hok = h < a.H;
+  const int64_t hq = hok ? h : a.H - 1;  // lanes past the heads run on the last head and store nothing
+  QueryPairs qq;
+  load_query(a.q + (b * a.H + hq) * 128, qd, qq);
+  const PairMasks pm;
+
+  // tokens of the chunk: 64-token batches first .. first + count - 1; wave w, batch i: tokens
+  // 64 (first + i) + 8 w + j, j < 8
+  const int nb = static_cast<int>((a.S + 63) / 64);
+  const int first = c * static_cast<int>(a.chunk_batches);
+  const int count = min(static_cast<int>(a.chunk_batches), nb - first);
+  const uint32_t H32 = static_cast<uint32_t>(a.H), S32 = static_cast<uint32_t>(a.S);
+  // token offsets fit 32 bits: S * H * 64 < 2^31 is checked on the host
+  const int64_t row0 = b * a.S * a.H;
+  const __amdgpu_buffer_rsrc_t rk = rsrc(a.kq + row0 * 64, a.S * a.H * 64);
+  const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, a.S * a.H * 64);
+  const void* pb = qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb;  // this lane's scale array
+
+  v4u kc[2][kBatch], vc[2][kBatch];
+  float pv[2][kBatch];
+  auto token = [&](int i, int j) { return static_cast<uint32_t>(64 * (first + i) + 8 * w + j); };
+  auto load = [&](int buf, int i) {
 #pragma unroll
-  for (int d = 0; d < 32; ++d) st.acc[d] = 0.0f;
-  attend<P16, 2>(a, b, h0, first, 1, count, st);
-  wave_total<2>(st);
-  const int h = h0 + hp;
-  if (lane >= 8 || h >= a.H) return;  // lanes 4 hp + qd of token slot 0 write
-  const float off = __fmul_rn(1024.0f, st.pa_sum);
-  float* dims = st.acc;  // in place: the lane's 32 dims
-#pragma unroll
-  for (int e = 0; e < 32; ++e) dims[e] = __fadd_rn(__fsub_rn(st.acc[e], off), st.bsum);
-  if constexpr (FINAL) {  // a chunk holds every token (l > 0: S >= 1)
-    uint32_t* o = reinterpret_cast<uint32_t*>(a.out + (static_cast<int64_t>(b) * a.H + h) * 128 + 32 * qd);
-#pragma unroll
-    for (int e = 0; e < 32; e += 2)
-      o[e / 2] = static_cast<uint32_t>(f2h(__fdiv_rn(dims[e], st.l))) |
-                 (static_cast<uint32_t>(f2h(__fdiv_rn(dims[e + 1], st.l))) << 16);
-  } else {
-    float* pr = a.part + ((static_cast<int64_t>(b) * a.H + h) * NC + c) * kAttnPart;
-    if (qd == 0) {
-      pr[0] = st.m;
-      pr[1] = st.l;
+    for (int j = 0; j < kBatch; ++j) {
+      const uint32_t t = token(i, j);
+      const bool ok = hok && i < count && t < S32;  // else codes out of range (zeros), scale of token 0
+      const uint32_t co = ok ? (t * H32 + static_cast<uint32_t>(h)) * 64 + 16 * qd : 0x80000000u;
+      kc[buf][j] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rk, co, 0, 0));
+      vc[buf][j] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rv, co, 0, 0));
+      const int64_t pi = row0 + (ok ? t * H32 + static_cast<uint32_t>(h) : 0u);
+      if constexpr (P16)
+        pv[buf][j] = h2f(static_cast<const uint16_t*>(pb)[pi]);
+      else
+        pv[buf][j] = static_cast<const float*>(pb)[pi];
     }
-    float4* pd = reinterpret_cast<float4*>(pr + 4 + 32 * qd);
+  };
+
+  float m = -INFINITY, l = 0.0f, bsum = 0.0f, pa_sum = 0.0f;
+  float acc[32];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pd[e] = make_float4(dims[4 * e], dims[4 * e + 1], dims[4 * e + 2], dims[4 * e + 3]);
+  for (int e = 0; e < 32; ++e) acc[e] = 0.0f;
+  const float cs = a.scale_log2e;
+  auto process = [&](int buf, int i) {
+    float sc[kBatch];
+    float mb = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const bool ok = hok && i < count && token(i, j) < S32;  // uniform over the quad
+      float dot = lane_dot(qq, pm, kc[buf][j]);
+      dot = __fadd_rn(dot, quad_xor<1>(dot));
+      dot = __fadd_rn(dot, quad_xor<2>(dot));
+      const float ka = quad_bcast<0>(pv[buf][j]), kb = quad_bcast<1>(pv[buf][j]);
+      sc[j] = ok ? __fmul_rn(cs, __fmaf_rn(ka, dot, __fmul_rn(kb, qq.qsum))) : -INFINITY;
+      mb = fmaxf(mb, sc[j]);
+    }
+    if (mb > m) {  // new running maximum of this lane's head: rescale the sums
+      const float f = rescale(m, mb);
+      l = __fmul_rn(l, f);
+      bsum = __fmul_rn(bsum, f);
+      pa_sum = __fmul_rn(pa_sum, f);
+#pragma unroll
+      for (int e = 0; e < 32; ++e) acc[e] = __fmul_rn(acc[e], f);
+      m = mb;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (sc[j] != -INFINITY) {
+        const float va = quad_bcast<2>(pv[buf][j]), vb = quad_bcast<3>(pv[buf][j]);
+        const float p = exp2f(__fsub_rn(sc[j], m));
+        l = __fadd_rn(l, p);
+        bsum = __fmaf_rn(p, vb, bsum);
+        const float pa = __fmul_rn(p, va);
+        pa_sum = __fadd_rn(pa_sum, pa);
+        lane_accumulate(acc, pa, pm, vc[buf][j]);
+      }
+    }
+  };
+  load(0, 0);
+  load(1, 1);
+  for (int i = 0; i < count; i += 2) {
+    process(0, i);
+    load(0, i + 2);
+    process(1, i + 1);
+    load(1, i + 3);
+  }
+
+  // the 8 waves' states of each head meet in LDS
+  const float off = __fmul_rn(1024.0f, pa_sum);
+  if (qd == 0) {
+    red_ml[w][hh][0] = m;
+    red_ml[w][hh][1] = l;
+  }
+  float4* rd = reinterpret_cast<float4*>(&red_d[w][hh][32 * qd]);
+#pragma unroll
+  for (int e = 0; e < 32; e += 4)
+    rd[e / 4] = make_float4(dim_value(acc[e], off, bsum, e), dim_value(acc[e + 1], off, bsum, e + 1),
+                            dim_value(acc[e + 2], off, bsum, e + 2), dim_value(acc[e + 3], off, bsum, e + 3));
+  __syncthreads();
+  // thread x: head x / 32 of the group, dims 4 (x % 32) .. + 3
+  const int mh = threadIdx.x >> 5, md = 4 * (threadIdx.x & 31);
+  const int64_t oh = kAttnGroupHeads * g + mh;
+  if (oh >= a.H) return;  // no barrier follows
+  float M = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < kSplitWaves; ++v) M = fmaxf(M, red_ml[v][mh][0]);
+  float L = 0.0f, D0 = 0.0f, D1 = 0.0f, D2 = 0.0f, D3 = 0.0f;
+#pragma unroll
+  for (int v = 0; v < kSplitWaves; ++v) {
+    const float f = rescale(red_ml[v][mh][0], M);  // 0 for a wave that saw no token
+    const float4 d = *reinterpret_cast<const float4*>(&red_d[v][mh][md]);
+    L = __fmaf_rn(red_ml[v][mh][1], f, L);
+    D0 = __fmaf_rn(d.x, f, D0);
+    D1 = __fmaf_rn(d.y, f, D1);
+    D2 = __fmaf_rn(d.z, f, D2);
+    D3 = __fmaf_rn(d.w, f, D3);
+  }
+  if constexpr (FINAL) {  // a chunk holds every token (L > 0: S >= 1)
+    uint32_t* o = reinterpret_cast<uint32_t*>(a.out + (b * a.H + oh) * 128 + md);
+    o[0] = static_cast<uint32_t>(f2h(__fdiv_rn(D0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D1, L))) << 16);
+    o[1] = static_cast<uint32_t>(f2h(__fdiv_rn(D2, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D3, L))) << 16);
+  } else {
+    float* pr = a.part + ((b * a.H + oh) * NC + c) * kAttnPart;
+    if (md == 0) {
+      pr[0] = M;
+      pr[1] = L;
+    }
+    *reinterpret_cast<float4*>(pr + 4 + md) = make_float4(D0, D1, D2, D3);
   }
 }
 
@@ -406,15 +539,22 @@ hipError_t attn_scratch(void** ptr) {
   return hipSuccess;
 }
 
+namespace {
+template <bool P16, bool FINAL>
+hipError_t launch_part(const AttnArgs& a, unsigned parts, hipStream_t stream) {
+  constexpr auto kern = attn_decode_part<P16, FINAL>;
+  const hipError_t init = set_max_lds<kern>(kSplitLds);  // above the 64 KB default
+  if (init != hipSuccess) return init;
+  return launch(kern, dim3(parts), dim3(64 * kSplitWaves), kSplitLds, stream, a);
+}
+}  // namespace
+
 hipError_t launch_attn_decode_split(const AttnArgs& a, hipStream_t stream) {
   const int64_t NG = (a.H + kAttnGroupHeads - 1) / kAttnGroupHeads;
   const unsigned parts = static_cast<unsigned>(a.B * a.chunks * NG);
-  const dim3 block(64 * kSplitWaves);
   if (a.chunks == 1)
-    return a.param16 ? launch(attn_decode_part<true, true>, dim3(parts), block, 0, stream, a)
-                     : launch(attn_decode_part<false, true>, dim3(parts), block, 0, stream, a);
-  hipError_t e = a.param16 ? launch(attn_decode_part<true, false>, dim3(parts), block, 0, stream, a)
-                           : launch(attn_decode_part<false, false>, dim3(parts), block, 0, stream, a);
+    return a.param16 ? launch_part<true, true>(a, parts, stream) : launch_part<false, true>(a, parts, stream);
+  hipError_t e = a.param16 ? launch_part<true, false>(a, parts, stream) : launch_part<false, false>(a, parts, stream);
   if (e != hipSuccess) return e;
   const unsigned heads = static_cast<unsigned>((a.B * a.H + 3) / 4);
   return launch(attn_decode_combine, dim3(heads), dim3(256), 0, stream, a);

@@ -83,7 +83,7 @@ struct AttnArgs {
   int64_t B, S, H;       // S * H * 64 < 2^31 (32-bit buffer offsets per head)
   float scale_log2e;     // score scale times log2(e)
   uint16_t* out;         // fp16 [B, H, 128]
-  // split over the sequence: chunks of chunk_batches batches of 16 tokens, partial softmax
+  // split over the sequence: chunks of chunk_batches batches of 64 tokens, partial softmax
   // states in part (float [B, H, chunks, kAttnPart]); chunks == 1 needs no part
   int64_t chunks = 1;
   int64_t chunk_batches = 0;
@@ -92,16 +92,16 @@ struct AttnArgs {
 
 constexpr int kAttnPart = 132;  // floats per partial state: m, l, 2 unused, 128 dims
 
-// Chunks of the sequence split for a device with `cus` compute units: enough (batch,
-// chunk, 32-head group) workgroups of 16 waves to give every CU one; at least 4 batches of
-// 16 tokens a chunk, at most 64 chunks (one per lane of the combine).
-constexpr int kAttnGroupHeads = 32;  // heads of one workgroup of the split attention (a wave per pair)
+// Chunks of the sequence split for a device with `cus` compute units: enough (batch, chunk,
+// 16-head group) workgroups of 8 waves to give every CU one, a chunk being whole batches of
+// 64 tokens (8 per wave), at most 64 chunks (one per lane of the combine).
+constexpr int kAttnGroupHeads = 16;  // heads of one workgroup of the split attention (4 lanes each)
+constexpr int kAttnSplitWaves = 8;   // its waves, which split the chunk's tokens
 inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks, int64_t& chunk_batches) {
-  const int64_t nb = (S + 15) / 16;
+  const int64_t nb = (S + 63) / 64;
   const int64_t groups = B * ((H + kAttnGroupHeads - 1) / kAttnGroupHeads);
-  const int64_t slots = static_cast<int64_t>(cus) * (32 / kAttnGroupHeads);  // 16 waves per CU
-  int64_t want = groups < slots ? (slots + groups - 1) / groups : 1;
-  const int64_t most = (nb + 3) / 4 < 64 ? (nb + 3) / 4 : 64;
+  int64_t want = groups < cus ? (cus + groups - 1) / groups : 1;
+  const int64_t most = nb < 64 ? nb : 64;
   if (want > most) want = most;
   if (want < 1) want = 1;
   chunk_batches = (nb + want - 1) / want;
