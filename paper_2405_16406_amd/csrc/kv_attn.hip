@@ -479,8 +479,9 @@ attn_decode_part(AttnArgs a) {
 
 // One wave per head: the chunks' states (at most 64) rescaled to their common maximum and
 // summed.  Lane c holds chunk c's maximum and sum; the dims (lane l finishes 2 l and 2 l + 1)
-// are loaded 32 chunks at a time, all 32 loads in flight together, and added in chunk
-// order.
+// come 32 chunks at a time, added in chunk order.  Every load of a pass is issued before the
+// first is used, at clamped chunk indices (a chunk past NC gets weight 0), so the maxima,
+// the sums and the first 32 chunks' dims take one round trip together.
 __global__ void __launch_bounds__(256)
 attn_decode_combine(AttnArgs a) {
   const int lane = threadIdx.x & 63;
@@ -488,8 +489,13 @@ attn_decode_combine(AttnArgs a) {
   if (x >= a.B * a.H) return;
   const int NC = static_cast<int>(a.chunks);
   const float* pr = a.part + x * NC * kAttnPart;
-  const float mc = lane < NC ? pr[lane * kAttnPart] : -INFINITY;
-  const float lc = lane < NC ? pr[lane * kAttnPart + 1] : 0.0f;
+  const int cl = lane < NC ? lane : NC - 1;
+  const float2 ml = *reinterpret_cast<const float2*>(pr + cl * kAttnPart);
+  float2 d[32];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) d[j] = reinterpret_cast<const float2*>(pr + min(j, NC - 1) * kAttnPart + 4)[lane];
+  const float mc = lane < NC ? ml.x : -INFINITY;
+  const float lc = lane < NC ? ml.y : 0.0f;
   float M = mc;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
@@ -498,17 +504,20 @@ attn_decode_combine(AttnArgs a) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) L = __fadd_rn(L, __shfl_xor(L, o));
   float A0 = 0.0f, A1 = 0.0f;
-  for (int c0 = 0; c0 < NC; c0 += 32) {
-    float2 d[32];
-#pragma unroll
-    for (int j = 0; j < 32; ++j)
-      d[j] = c0 + j < NC ? reinterpret_cast<const float2*>(pr + (c0 + j) * kAttnPart + 4)[lane] : float2{0.0f, 0.0f};
+  auto add32 = [&](int c0) {
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
-      const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fc), min(c0 + j, 63)));
+      const float f = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(fc), c0 + j));
       A0 = __fmaf_rn(d[j].x, f, A0);
       A1 = __fmaf_rn(d[j].y, f, A1);
     }
+  };
+  add32(0);
+  if (NC > 32) {  // chunks 32 .. 63
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      d[j] = reinterpret_cast<const float2*>(pr + min(32 + j, NC - 1) * kAttnPart + 4)[lane];
+    add32(32);
   }
   reinterpret_cast<uint32_t*>(a.out + x * 128)[lane] =
       static_cast<uint32_t>(f2h(__fdiv_rn(A0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(A1, L))) << 16);
