@@ -320,21 +320,26 @@ attn_decode_kv4(AttnArgs a) {
 // waves.  Lane l = 4 hh + qd serves head 16 g + hh, dims 32 qd .. 32 qd + 31, so one load of
 // the wave brings the 1 KB of codes of one token for the group's 16 heads (half of a 32-head
 // token line), and the four parameter loads 64 contiguous bytes each.  The chunk's tokens go
-// in batches of 8 per wave (wave w takes tokens 64 i + 8 w .. + 7 of the chunk, so the 8 waves
-// walk the chunk's lines together), two batches in flight.  Each lane keeps its head's state;
-// a batch's 8 scores are in the lane, so its maximum (and the rare rescale) is taken once per
-// batch without crossing lanes.  The 8 waves merge in LDS; each head leaves its partial state
-// (m, l, the 128 dims with the code offset removed and the betas added) in part, and the
-// combine kernel merges the chunks of a head.
+// in batches of 4 per wave (wave w takes tokens 32 i + 4 w .. + 3 of the chunk, so the 8 waves
+// walk the chunk's lines together), two batches in flight (154 VGPRs; batches of 8 with 236
+// VGPRs measured 24.9 against 22.6 us on [8, 2048, 32, 128]).  Each lane keeps its head's
+// state; a batch's scores are in the lane, so its maximum (and the rare rescale) is taken
+// once per batch without crossing lanes.  The 8 waves merge in LDS; each head leaves its
+// partial state (m, l, the 128 dims with the code offset removed and the betas added) in
+// part, and the combine kernel merges the chunks of a head.
 // FINAL (a single chunk): the workgroup divides and stores the output itself.
-constexpr int kSplitWaves = kAttnSplitWaves;
-constexpr int kBatch = 8;  // tokens per wave batch
-constexpr int kSplitLds = kSplitWaves * kAttnGroupHeads * (128 + 2) * 4;
+template <int WAVES>
+constexpr int part_lds_bytes() {
+  return WAVES * kAttnGroupHeads * (128 + 2) * 4;
+}
 
-template <bool P16, bool FINAL>
-__global__ void __launch_bounds__(64 * kSplitWaves, 2)
+// WAVES waves of batches of TB tokens (a chunk is made of WAVES x TB-token batches), at
+// least WPE waves per SIMD.
+template <bool P16, bool FINAL, int kSplitWaves = kAttnSplitWaves, int kBatch = kAttnBatch, int WPE = 2>
+__global__ void __launch_bounds__(64 * kSplitWaves, WPE)
 attn_decode_part(AttnArgs a) {
-  // dynamic LDS (kSplitLds bytes): the waves' dims [wave][head][128], then (m, l) [wave][head]
+  constexpr int kChunkUnit = kSplitWaves * kBatch;
+  // dynamic LDS (part_lds_bytes bytes): the waves' dims [wave][head][128], then (m, l) [wave][head]
   extern __shared__ __attribute__((aligned(16))) float split_lds[];
   auto red_d = reinterpret_cast<float (*)[kAttnGroupHeads][128]>(split_lds);
   auto red_ml = reinterpret_cast<float (*)[kAttnGroupHeads][2]>(split_lds + kSplitWaves * kAttnGroupHeads * 128);
@@ -353,9 +358,9 @@ attn_decode_part(AttnArgs a) {
   load_query(a.q + (b * a.H + hq) * 128, qd, qq);
   const PairMasks pm;
 
-  // tokens of the chunk: 64-token batches first .. first + count - 1; wave w, batch i: tokens
-  // 64 (first + i) + 8 w + j, j < 8
-  const int nb = static_cast<int>((a.S + 63) / 64);
+  // tokens of the chunk: units of kChunkUnit tokens first .. first + count - 1; wave w,
+  // batch i: tokens kChunkUnit (first + i) + kBatch w + j, j < kBatch
+  const int nb = static_cast<int>((a.S + kChunkUnit - 1) / kChunkUnit);
   const int first = c * static_cast<int>(a.chunk_batches);
   const int count = min(static_cast<int>(a.chunk_batches), nb - first);
   const uint32_t H32 = static_cast<uint32_t>(a.H), S32 = static_cast<uint32_t>(a.S);
@@ -367,7 +372,7 @@ attn_decode_part(AttnArgs a) {
 
   v4u kc[2][kBatch], vc[2][kBatch];
   float pv[2][kBatch];
-  auto token = [&](int i, int j) { return static_cast<uint32_t>(64 * (first + i) + 8 * w + j); };
+  auto token = [&](int i, int j) { return static_cast<uint32_t>(kChunkUnit * (first + i) + kBatch * w + j); };
   auto load = [&](int buf, int i) {
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
@@ -433,7 +438,7 @@ attn_decode_part(AttnArgs a) {
     load(1, i + 3);
   }
 
-  // the 8 waves' states of each head meet in LDS
+  // the waves' states of each head meet in LDS
   const float off = __fmul_rn(1024.0f, pa_sum);
   if (qd == 0) {
     red_ml[w][hh][0] = m;
@@ -445,35 +450,37 @@ attn_decode_part(AttnArgs a) {
     rd[e / 4] = make_float4(dim_value(acc[e], off, bsum, e), dim_value(acc[e + 1], off, bsum, e + 1),
                             dim_value(acc[e + 2], off, bsum, e + 2), dim_value(acc[e + 3], off, bsum, e + 3));
   __syncthreads();
-  // thread x: head x / 32 of the group, dims 4 (x % 32) .. + 3
-  const int mh = threadIdx.x >> 5, md = 4 * (threadIdx.x & 31);
-  const int64_t oh = kAttnGroupHeads * g + mh;
-  if (oh >= a.H) return;  // no barrier follows
-  float M = -INFINITY;
+  // item x of 512: head x / 32 of the group, dims 4 (x % 32) .. + 3
+  for (int x = threadIdx.x; x < 32 * kAttnGroupHeads; x += 64 * kSplitWaves) {
+    const int mh = x >> 5, md = 4 * (x & 31);
+    const int64_t oh = kAttnGroupHeads * g + mh;
+    if (oh >= a.H) break;  // the heads past H come last; no barrier follows
+    float M = -INFINITY;
 #pragma unroll
-  for (int v = 0; v < kSplitWaves; ++v) M = fmaxf(M, red_ml[v][mh][0]);
-  float L = 0.0f, D0 = 0.0f, D1 = 0.0f, D2 = 0.0f, D3 = 0.0f;
+    for (int v = 0; v < kSplitWaves; ++v) M = fmaxf(M, red_ml[v][mh][0]);
+    float L = 0.0f, D0 = 0.0f, D1 = 0.0f, D2 = 0.0f, D3 = 0.0f;
 #pragma unroll
-  for (int v = 0; v < kSplitWaves; ++v) {
-    const float f = rescale(red_ml[v][mh][0], M);  // 0 for a wave that saw no token
-    const float4 d = *reinterpret_cast<const float4*>(&red_d[v][mh][md]);
-    L = __fmaf_rn(red_ml[v][mh][1], f, L);
-    D0 = __fmaf_rn(d.x, f, D0);
-    D1 = __fmaf_rn(d.y, f, D1);
-    D2 = __fmaf_rn(d.z, f, D2);
-    D3 = __fmaf_rn(d.w, f, D3);
-  }
-  if constexpr (FINAL) {  // a chunk holds every token (L > 0: S >= 1)
-    uint32_t* o = reinterpret_cast<uint32_t*>(a.out + (b * a.H + oh) * 128 + md);
-    o[0] = static_cast<uint32_t>(f2h(__fdiv_rn(D0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D1, L))) << 16);
-    o[1] = static_cast<uint32_t>(f2h(__fdiv_rn(D2, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D3, L))) << 16);
-  } else {
-    float* pr = a.part + ((b * a.H + oh) * NC + c) * kAttnPart;
-    if (md == 0) {
-      pr[0] = M;
-      pr[1] = L;
+    for (int v = 0; v < kSplitWaves; ++v) {
+      const float f = rescale(red_ml[v][mh][0], M);  // 0 for a wave that saw no token
+      const float4 d = *reinterpret_cast<const float4*>(&red_d[v][mh][md]);
+      L = __fmaf_rn(red_ml[v][mh][1], f, L);
+      D0 = __fmaf_rn(d.x, f, D0);
+      D1 = __fmaf_rn(d.y, f, D1);
+      D2 = __fmaf_rn(d.z, f, D2);
+      D3 = __fmaf_rn(d.w, f, D3);
     }
-    *reinterpret_cast<float4*>(pr + 4 + md) = make_float4(D0, D1, D2, D3);
+    if constexpr (FINAL) {  // a chunk holds every token (L > 0: S >= 1)
+      uint32_t* o = reinterpret_cast<uint32_t*>(a.out + (b * a.H + oh) * 128 + md);
+      o[0] = static_cast<uint32_t>(f2h(__fdiv_rn(D0, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D1, L))) << 16);
+      o[1] = static_cast<uint32_t>(f2h(__fdiv_rn(D2, L))) | (static_cast<uint32_t>(f2h(__fdiv_rn(D3, L))) << 16);
+    } else {
+      float* pr = a.part + ((b * a.H + oh) * NC + c) * kAttnPart;
+      if (md == 0) {
+        pr[0] = M;
+        pr[1] = L;
+      }
+      *reinterpret_cast<float4*>(pr + 4 + md) = make_float4(D0, D1, D2, D3);
+    }
   }
 }
 
@@ -552,9 +559,10 @@ namespace {
 template <bool P16, bool FINAL>
 hipError_t launch_part(const AttnArgs& a, unsigned parts, hipStream_t stream) {
   constexpr auto kern = attn_decode_part<P16, FINAL>;
-  const hipError_t init = set_max_lds<kern>(kSplitLds);  // above the 64 KB default
+  constexpr int lds = part_lds_bytes<kAttnSplitWaves>();
+  const hipError_t init = set_max_lds<kern>(lds);  // above the 64 KB default
   if (init != hipSuccess) return init;
-  return launch(kern, dim3(parts), dim3(64 * kSplitWaves), kSplitLds, stream, a);
+  return launch(kern, dim3(parts), dim3(64 * kAttnSplitWaves), lds, stream, a);
 }
 }  // namespace
 

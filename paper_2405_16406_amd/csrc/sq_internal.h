@@ -94,11 +94,13 @@ constexpr int kAttnPart = 132;  // floats per partial state: m, l, 2 unused, 128
 
 // Chunks of the sequence split for a device with `cus` compute units: enough (batch, chunk,
 // 16-head group) workgroups of 8 waves to give every CU one, a chunk being whole batches of
-// 64 tokens (8 per wave), at most 64 chunks (one per lane of the combine).
+// 32 tokens (4 per wave), at most 64 chunks (one per lane of the combine).
 constexpr int kAttnGroupHeads = 16;  // heads of one workgroup of the split attention (4 lanes each)
 constexpr int kAttnSplitWaves = 8;   // its waves, which split the chunk's tokens
+constexpr int kAttnBatch = 4;        // tokens of a wave's batch
 inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks, int64_t& chunk_batches) {
-  const int64_t nb = (S + 63) / 64;
+  constexpr int unit = kAttnSplitWaves * kAttnBatch;  // tokens of one batch of the workgroup
+  const int64_t nb = (S + unit - 1) / unit;
   const int64_t groups = B * ((H + kAttnGroupHeads - 1) / kAttnGroupHeads);
   int64_t want = groups < cus ? (cus + groups - 1) / groups : 1;
   const int64_t most = nb < 64 ? nb : 64;

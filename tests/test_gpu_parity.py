@@ -1067,10 +1067,12 @@ def test_swiglu_llama2_7b_full_tiles():
     swiglu_case(2048, 11008, 4096, seed=44, bias=False, sample_rows=tile_rows(2048))
 
 
-@pytest.mark.parametrize("M,N,K", [(8, 4096, 11008), (100, 1000, 2112), (2048, 4096, 11008), (4096, 4096, 192)])
+@pytest.mark.parametrize("M,N,K", [(1, 8192, 28672), (4, 8192, 28672), (8, 4096, 11008), (100, 1000, 2112),
+                                   (2048, 4096, 11008), (4096, 4096, 192)])
 def test_gemm_deterministic(M, N, K):
-    # decode kernel (8 waves' partial sums in LDS), two K groups (partial sums exchanged in
-    # LDS), 128 x 256 and 256 x 256 ring tiles: two launches give the same bytes
+    # dot-product decode kernel (lane sums added by DPP), 16-row decode kernel (8 waves'
+    # partial sums in LDS), two K groups (partial sums exchanged in LDS), 128 x 256 and
+    # 256 x 256 ring tiles: two launches give the same bytes
     say(f"w4a4_linear determinism M={M} N={N} K={K}")
     rng = workloads.rng_for(M + N + K + 3)
     qa = rng.integers(0, 16, size=(M, K))
