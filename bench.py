@@ -133,8 +133,9 @@ TRAFFIC_MAP = {
     "c3/down_gemm": ("c3", "w4a4_gemm_ring<2, 4, 4, 2, 4, 1, 1, false>", 131072),
     "c4/kv_quant": ("c4", "qk_had_kvquant_v2<true, 4, false>", 2097152),
     "c4/attn_decode": ("c4", "attn_decode_kv4<false>", 262144),
-    # two kernels (on 256 CUs: 32 chunks x 2 head groups x 8 batches, then one wave per head)
-    "c4/attn_decode_split": [("c4", "attn_decode_part<false, false>", 262144),
+    # two kernels (on 256 CUs: 16 chunks x 2 groups of 16 heads x 8 batches of 8 waves,
+    # then one wave per head)
+    "c4/attn_decode_split": [("c4", "attn_decode_part<false, false, 8, 4, 2>", 131072),
                              ("c4", "attn_decode_combine", 16384)],
 }
 for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the GEMM launch shapes

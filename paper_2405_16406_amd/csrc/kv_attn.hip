@@ -348,9 +348,20 @@ attn_decode_part(AttnArgs a) {
   const int hh = lane >> 2, qd = lane & 3;
   // the workgroup count (B * chunks * NG, at most B * NG or about the CUs) fits 32 bits
   const int NG = static_cast<int>((a.H + kAttnGroupHeads - 1) / kAttnGroupHeads), NC = static_cast<int>(a.chunks);
-  const int g = static_cast<int>(blockIdx.x) % NG;
-  const int c = (static_cast<int>(blockIdx.x) / NG) % NC;
-  const int64_t b = static_cast<int>(blockIdx.x) / NG / NC;
+  // Workgroups go round-robin over the 8 XCDs.  When the count allows, the NG head groups of
+  // one (batch, chunk) get ids equal mod 8, so they run on one XCD and the two halves of a
+  // token's parameter lines (64 bytes each of a 128-byte line) come through one L2.
+  const int id = static_cast<int>(blockIdx.x), total = static_cast<int>(gridDim.x);
+  int g, bc;
+  if (NG > 1 && total % (8 * NG) == 0) {
+    g = (id / 8) % NG;
+    bc = (id / (8 * NG)) * 8 + id % 8;
+  } else {
+    g = id % NG;
+    bc = id / NG;
+  }
+  const int c = bc % NC;
+  const int64_t b = bc / NC;
   const int64_t h = kAttnGroupHeads * g + hh;
   const bool hok = h < a.H;
   const int64_t hq = hok ? h : a.H - 1;  // lanes past the heads run on the last head and store nothing
