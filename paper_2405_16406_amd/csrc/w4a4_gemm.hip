@@ -1272,8 +1272,8 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 //   sum_k qa qw = sum_k (qa - 8) qw + 8 rs_n.
 // Bytes past K are loaded out of their buffer range and read as zeros.  At the end of a unit
 // the wave adds up its 64 lane sums (DPP within rows of 16, permlane swaps across them) and
-// lane i keeps unit i; the epilogue runs once per wave, one unit per lane, with the decode
-// kernel's arithmetic (acc16 = 16 acc), so both give the same fp16 results.
+// lane i keeps unit i; the epilogue runs once per wave, one unit per lane, with the 16-row
+// decode kernel's arithmetic (acc16 = 16 acc), so both give the same fp16 results.
 template <int MB, bool SW>
 struct Gemv {
   static constexpr int WAVES = 8;
@@ -1283,7 +1283,7 @@ struct Gemv {
   static constexpr int RPS = SW || MB >= 4 ? 2 : 1;
   static constexpr int RSTEP = SW ? 32 : 1;  // rows between the rows of a unit
   static constexpr int D = 16 / RPS;         // steps in flight: 16 loads per lane
-  static constexpr int RUN = 64;          // units per wave at most
+  static constexpr int RUN = 64;             // units per wave at most
   static constexpr int CH = MB <= 4 ? 4 : 2;  // 8 KB chunks of an activation row: K <= 65536 (32768)
   static constexpr int MAX_LDS = MB * CH * 8 * 1024;
 };
