@@ -831,7 +831,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the rotated W4A4 path is not "
+        print(json.dumps({"error": "one GPU only: the rotated W4A4 path is not "
                                    "sharded across GPUs", "n_gpus": args.gpus}))
         sys.exit(2)
 

@@ -53,7 +53,7 @@ typedef enum {
   SQ_OK = 0,
   SQ_ERR_NULL = 1,        /* a required pointer is NULL */
   SQ_ERR_SHAPE = 2,       /* sizes inconsistent or out of range */
-  SQ_ERR_UNSUPPORTED = 3, /* a valid request this build does not implement (e.g. bits = 6) */
+  SQ_ERR_UNSUPPORTED = 3, /* a valid request the library does not implement (e.g. bits = 6) */
   SQ_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
   SQ_ERR_ALIAS = 5,       /* an output overlaps an input or another output */
   SQ_ERR_HIP = 6          /* the HIP runtime reported an error (no device, launch failure) */
