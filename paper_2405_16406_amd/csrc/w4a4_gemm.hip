@@ -1572,9 +1572,13 @@ hipError_t try_skinny8(const GemmArgs& g, hipStream_t stream) {
 }  // namespace
 
 // 8-bit activations on the ring, with the W4A4 size classes: at least as many 256 x 256
-// tiles as CUs -> 256 x 256 tiles of 8 waves of 128 x 64, three stages (3 x 48 KB of LDS);
-// fewer -> 128 x 256 tiles of 8 waves of 64 x 64, four stages.  Measured on MI355X (us,
-// one process, interleaved; 256 x 256 vs 128 x 256 tiles):
+// tiles as CUs -> 256 x 256 tiles of 8 waves of 64 x 128, three stages (3 x 48 KB of LDS);
+// fewer -> 128 x 256 tiles of 8 waves of 64 x 64, four stages.  A wave tile of 64 rows by
+// 128 columns reads 8 KB of 8-bit A and 8 KB of packed B from LDS per stage, against 16 and
+// 4 KB for 128 x 64 (the W4A4 kernel, whose A is half the bytes, gains nothing from it).
+// Measured on MI355X (us, one process, interleaved; 256 x 256 tiles of 64 x 128 vs 128 x 64
+// wave tiles): [2048 x 22016 x 4096] 210 vs 229, [4096 x 28672 x 4096] 504 vs 525,
+// [4096 x 4096 x 14336] 247 vs 254; and 256 x 256 (128 x 64) vs 128 x 256 tiles:
 //   [2048 x 22016 x 4096]   211 vs 255      [4096 x 28672 x 4096]   505 vs 611
 //   [4096 x 4096 x 14336]   241 vs 290      [2048 x 4096 x 11008]   150 vs 104 (128 tiles)
 // and earlier, 128 x 256 against 128 x 128 (2 per CU, 3 stages) / 256 x 128 (8 waves,
@@ -1585,7 +1589,7 @@ hipError_t launch_w4a8_ring(const GemmArgs& g0, hipStream_t stream) {
   GemmArgs g = g0;
   g.a8 = 1;
   const int64_t tiles256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (tiles256 >= 256 && fits_ring<2, 4, 4, 2, 3, true>(g)) return launch_ring<2, 4, 4, 2, 3, 1, 1, true>(g, stream);
+  if (tiles256 >= 256 && fits_ring<4, 2, 2, 4, 3, true>(g)) return launch_ring<4, 2, 2, 4, 3, 1, 1, true>(g, stream);
   if (!fits_ring<2, 4, 2, 2, 4, true>(g)) return hipErrorNotSupported;
   return launch_ring<2, 4, 2, 2, 4, 1, 1, true>(g, stream);
 }
