@@ -1274,7 +1274,12 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 // the wave adds up its 64 lane sums (DPP within rows of 16, permlane swaps across them) and
 // lane i keeps unit i; the epilogue runs once per wave, one unit per lane, with the 16-row
 // decode kernel's arithmetic (acc16 = 16 acc), so both give the same fp16 results.
-template <int MB, bool SW>
+// A8 (8-bit activation codes, the W4A8 setting, M <= 2): the LDS rows hold the codes made
+// signed (xor 0x80: q - 128) and, in every 8-code group, in the order the weight expansion
+// gives (even codes, then odd: v_perm_b32); the weight dword expands to two dwords of 16 x
+// code bytes and v_dot4_i32_i8 takes four products at a time, so the unit sums are the 16-row
+// kernel's 16 sum (qa - 128) qw and its 8-bit epilogue applies (beta + 128 alpha).
+template <int MB, bool SW, bool A8 = false>
 struct Gemv {
   static constexpr int WAVES = 8;
   static constexpr int THREADS = 64 * WAVES;
@@ -1284,8 +1289,10 @@ struct Gemv {
   static constexpr int RSTEP = SW ? 32 : 1;  // rows between the rows of a unit
   static constexpr int D = 16 / RPS;         // steps in flight: 16 loads per lane
   static constexpr int RUN = 64;             // units per wave at most
-  static constexpr int CH = MB <= 4 ? 4 : 2;  // 8 KB chunks of an activation row: K <= 65536 (32768)
-  static constexpr int MAX_LDS = MB * CH * 8 * 1024;
+  static constexpr int CH = MB <= 4 ? 4 : 2;  // 8 KB chunks of a 4-bit row: K <= 65536 (32768)
+  static constexpr int AB = A8 ? 2 : 1;       // activation bytes per packed weight byte
+  static constexpr int MAX_LDS = MB * CH * 8 * 1024 * AB;
+  static_assert(!A8 || (!SW && MB <= 2), "8-bit activations: plain products, one or two rows");
 };
 
 // sum over the 64 lanes, in every lane
@@ -1302,17 +1309,17 @@ __device__ __forceinline__ int wave_total(int v) {
   return v;
 }
 
-template <int MB, bool SW>
+template <int MB, bool SW, bool A8 = false>
 __global__ void __launch_bounds__(512)
 w4a4_gemv(GemmArgs g) {
-  using V = Gemv<MB, SW>;
+  using V = Gemv<MB, SW, A8>;
   constexpr int D = V::D, RPS = V::RPS, RSTEP = V::RSTEP;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t KB = static_cast<uint32_t>(g.K / 2);
   const uint32_t J = (KB + 1023) / 1024;  // 1 KB chunks per row
-  const uint32_t AROW = J * 1024;         // LDS bytes per activation row
+  const uint32_t AROW = J * 1024 * V::AB;  // LDS bytes per activation row
   // balanced runs: wave w of W owns units [w U / W, (w + 1) U / W)
   const int64_t U = SW ? g.N / 2 : (g.N + RPS - 1) / RPS;
   const int64_t W = static_cast<int64_t>(gridDim.x) * V::WAVES;
@@ -1372,25 +1379,36 @@ w4a4_gemv(GemmArgs g) {
   for (int d = 0; d < D; ++d) load(d);
 
   // activation rows -> LDS, signed and zero-padded; rows past M are zeros.  A row has at most
-  // CH x 8 KB (fits_gemv); every load is issued before the first write, unconditionally (out
-  // of range where there is nothing to load), so that the waits do not serialise them.
-  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
-  v4u a[V::CH][MB];
+  // CH x 8 KB (x 2 with 8-bit codes; fits_gemv); every load is issued before the first
+  // write, unconditionally (out of range where there is nothing to load), so that the waits
+  // do not serialise them.
+  const uint32_t XR = KB * V::AB;  // activation bytes per row in global memory
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * XR);
+  v4u a[V::CH * V::AB][MB];
 #pragma unroll
-  for (int h = 0; h < V::CH; ++h)
+  for (int h = 0; h < V::CH * V::AB; ++h)
 #pragma unroll
     for (int m = 0; m < MB; ++m) {
       const uint32_t o = 16 * (threadIdx.x + h * V::THREADS);
-      const bool ok = m < g.M && o < KB;
-      a[h][m] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? m * KB + o : 0x80000000u, 0, 0));
+      const bool ok = m < g.M && o < XR;
+      a[h][m] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rsa, ok ? m * XR + o : 0x80000000u, 0, 0));
     }
 #pragma unroll
-  for (int h = 0; h < V::CH; ++h)
+  for (int h = 0; h < V::CH * V::AB; ++h)
 #pragma unroll
     for (int m = 0; m < MB; ++m) {
       const uint32_t o = 16 * (threadIdx.x + h * V::THREADS);
-      const bool ok = m < g.M && o < KB;
-      const v4u v = a[h][m] ^ (ok ? 0x88888888u : 0u);  // out of range: loaded as zeros
+      const bool ok = m < g.M && o < XR;
+      v4u v;
+      if constexpr (A8) {  // q - 128, each 8-code group as (even codes | odd codes); bytes past K
+                           // meet zero weights
+        const v4u d = a[h][m];
+        v = v4u{__builtin_amdgcn_perm(d[1], d[0], 0x06040200u), __builtin_amdgcn_perm(d[1], d[0], 0x07050301u),
+                __builtin_amdgcn_perm(d[3], d[2], 0x06040200u), __builtin_amdgcn_perm(d[3], d[2], 0x07050301u)} ^
+            0x80808080u;
+      } else {
+        v = a[h][m] ^ (ok ? 0x88888888u : 0u);  // out of range: loaded as zeros
+      }
       if (o < AROW) *reinterpret_cast<v4u*>(lds + m * AROW + o) = v;
     }
   __syncthreads();
@@ -1406,15 +1424,29 @@ w4a4_gemv(GemmArgs g) {
     static_for<D>([&](auto dc) {
       constexpr int d = decltype(dc)::value;
       // steps past the run consume zeros (loaded out of range)
-      const uint32_t ao = cj * 1024 + 16 * lane;
+      const uint32_t ao = (cj * 1024 + 16 * lane) * V::AB;
 #pragma unroll
       for (int m = 0; m < MB; ++m) {
-        const v4u a = *reinterpret_cast<const v4u*>(lds + m * AROW + ao);
+        if constexpr (A8) {  // the lane's 32 codes: 8 dwords, (even | odd) per 8-code group
+          const v4u a0 = *reinterpret_cast<const v4u*>(lds + m * AROW + ao);
+          const v4u a1 = *reinterpret_cast<const v4u*>(lds + m * AROW + ao + 16);
+          const uint32_t av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
 #pragma unroll
-        for (int r = 0; r < RPS; ++r)
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t w = wb[d][0][e];
+            acc[0][m] = __builtin_amdgcn_sdot4(static_cast<int>(av[2 * e]), static_cast<int>((w << 4) & 0xF0F0F0F0u),
+                                               acc[0][m], false);
+            acc[0][m] = __builtin_amdgcn_sdot4(static_cast<int>(av[2 * e + 1]), static_cast<int>(w & 0xF0F0F0F0u),
+                                               acc[0][m], false);
+          }
+        } else {
+          const v4u a = *reinterpret_cast<const v4u*>(lds + m * AROW + ao);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc[r][m] = __builtin_amdgcn_sdot8(static_cast<int>(a[e]), static_cast<int>(wb[d][r][e]), acc[r][m], false);
+          for (int r = 0; r < RPS; ++r)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc[r][m] = __builtin_amdgcn_sdot8(static_cast<int>(a[e]), static_cast<int>(wb[d][r][e]), acc[r][m], false);
+        }
       }
       load(d);
       if (++cj == J) {
@@ -1458,28 +1490,31 @@ w4a4_gemv(GemmArgs g) {
 #pragma unroll
       for (int m = 0; m < MB; ++m) {
         if (m >= g.M) break;
-        const int a = res[r][m] + 8 * ers[r];
-        const float t = __fmul_rn(esc[r], static_cast<float>(16 * a));
-        const float yv = fp32_result(__fmaf_rn(__fmul_rn(exa[m], 0.0625f), t, __fmaf_rn(exb[m], wn, bn)));
+        // 16 x the sum (A8: 16 x the sum of (qa - 128) qw, with beta + 128 alpha below)
+        const int a16 = A8 ? res[r][m] : 16 * (res[r][m] + 8 * ers[r]);
+        const float t = __fmul_rn(esc[r], static_cast<float>(a16));
+        const float xb = A8 ? __fmaf_rn(128.0f, exa[m], exb[m]) : exb[m];
+        const float yv = fp32_result(__fmaf_rn(__fmul_rn(exa[m], 0.0625f), t, __fmaf_rn(xb, wn, bn)));
         g.y[m * g.ldy + n] = f2h(yv);
-        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = a;
+        if (g.dbg_acc) g.dbg_acc[m * g.N + n] = (a16 >> 4) + (A8 ? 128 * ers[r] : 0);
       }
     }
   }
 }
 
-template <int MB, bool SW>
+template <int MB, bool SW, bool A8 = false>
 bool fits_gemv(const GemmArgs& g) {
-  const int64_t kb = g.K / 2, lds = MB * ((kb + 1023) / 1024) * 1024;
-  return g.M <= MB && lds <= Gemv<MB, SW>::MAX_LDS && g.M * kb + 64 < (int64_t{1} << 31) && (!SW || g.N % 64 == 0);
+  using V = Gemv<MB, SW, A8>;
+  const int64_t kb = g.K / 2, lds = MB * ((kb + 1023) / 1024) * 1024 * V::AB;
+  return g.M <= MB && lds <= V::MAX_LDS && g.M * kb * V::AB + 64 < (int64_t{1} << 31) && (!SW || g.N % 64 == 0);
 }
 
 // About one workgroup of 8 waves per CU, and more where the runs would exceed 64 units.
-template <int MB, bool SW>
+template <int MB, bool SW, bool A8 = false>
 hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
-  using V = Gemv<MB, SW>;
-  constexpr auto kern = w4a4_gemv<MB, SW>;
-  const int lds = static_cast<int>(MB * ((g.K / 2 + 1023) / 1024) * 1024);
+  using V = Gemv<MB, SW, A8>;
+  constexpr auto kern = w4a4_gemv<MB, SW, A8>;
+  const int lds = static_cast<int>(MB * ((g.K / 2 + 1023) / 1024) * 1024 * V::AB);
   if (lds > 64 * 1024) {
     const hipError_t init = set_max_lds<kern>(V::MAX_LDS);
     if (init != hipSuccess) return init;
@@ -1596,6 +1631,14 @@ hipError_t launch_w4a8_ring(const GemmArgs& g0, hipStream_t stream) {
 
 hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream) {
   if (g.M > 16) return hipErrorNotSupported;
+  // one row, or two from 32 MB of weights: the dot-product kernel in its 8-bit mode.
+  // Measured on MI355X against the 16-row kernel (us, same data, interleaved): LLaMA-2-70B
+  // [M x 8192] x [57344 x 8192] 43.4 vs 71.3 (M = 1), 46.3 vs 73.5 (M = 2); [M x 28672] x
+  // [8192 x 28672] 24.3 vs 27.7, 26.8 vs 28.3; LLaMA-2-7B [M x 4096] x [22016 x 4096] 14.9
+  // vs 20.2, 17.0 vs 21.1; [M x 11008] x [4096 x 11008] 9.6 vs 9.6, 11.0 vs 9.8.
+  if (g.M == 1 && fits_gemv<1, false, true>(g)) return launch_gemv<1, false, true>(g, stream);
+  if (g.M == 2 && g.N * (g.K / 2) >= (int64_t{32} << 20) && fits_gemv<2, false, true>(g))
+    return launch_gemv<2, false, true>(g, stream);
   const int64_t nb = (g.N + 4095) / 4096;  // the rows-per-workgroup rule of the W4A4 decode kernel
   if (nb <= 1) return try_skinny8<1>(g, stream);
   if (nb <= 3) return try_skinny8<2>(g, stream);
