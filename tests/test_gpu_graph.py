@@ -19,9 +19,11 @@ def up(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def test_decode_step_graph_replays_match_eager():
+@pytest.mark.parametrize("M", [1, 4])
+def test_decode_step_graph_replays_match_eager(M):
+    # M = 1: the dot-product decode kernels; M = 4: the 16-row decode kernels
     shape = workloads.LLAMA2_7B_MLP
-    M, H, I = 4, shape.hidden, shape.inter
+    H, I = shape.hidden, shape.inter
     print(f"[gpu case] graph of a decode step M={M}, LLaMA-2-7B MLP", flush=True)
     inp = workloads.mlp_inputs(shape, rows=3 * M)
     had = up(sq.hadamard_factor(shape.had_dense))
