@@ -328,9 +328,16 @@ attn_decode_kv4(AttnArgs a) {
 // partial state (m, l, the 128 dims with the code offset removed and the betas added) in
 // part, and the combine kernel merges the chunks of a head.
 // FINAL (a single chunk): the workgroup divides and stores the output itself.
+// LDS row of a head's 128 dims in the merge: four quarters of 32, each padded to 36 floats,
+// so that the 16-byte stores of lanes 4 hh + qd (16 of them at a time) and the merge's reads
+// meet no bank conflicts (with rows of 128 floats all 16 heads' lanes of one quarter hit the
+// same banks: 9e5 conflict cycles per launch)
+constexpr int kQuarter = 36;
+constexpr int kDimRow = 4 * kQuarter;
+
 template <int WAVES>
 constexpr int part_lds_bytes() {
-  return WAVES * kAttnGroupHeads * (128 + 2) * 4;
+  return WAVES * kAttnGroupHeads * (kDimRow + 2) * 4;
 }
 
 // WAVES waves of batches of TB tokens (a chunk is made of WAVES x TB-token batches), at
@@ -339,10 +346,10 @@ template <bool P16, bool FINAL, int kSplitWaves = kAttnSplitWaves, int kBatch = 
 __global__ void __launch_bounds__(64 * kSplitWaves, WPE)
 attn_decode_part(AttnArgs a) {
   constexpr int kChunkUnit = kSplitWaves * kBatch;
-  // dynamic LDS (part_lds_bytes bytes): the waves' dims [wave][head][128], then (m, l) [wave][head]
+  // dynamic LDS (part_lds_bytes bytes): the waves' dims [wave][head][kDimRow], then (m, l) [wave][head]
   extern __shared__ __attribute__((aligned(16))) float split_lds[];
-  auto red_d = reinterpret_cast<float (*)[kAttnGroupHeads][128]>(split_lds);
-  auto red_ml = reinterpret_cast<float (*)[kAttnGroupHeads][2]>(split_lds + kSplitWaves * kAttnGroupHeads * 128);
+  auto red_d = reinterpret_cast<float (*)[kAttnGroupHeads][kDimRow]>(split_lds);
+  auto red_ml = reinterpret_cast<float (*)[kAttnGroupHeads][2]>(split_lds + kSplitWaves * kAttnGroupHeads * kDimRow);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 2, qd = lane & 3;
@@ -455,7 +462,7 @@ attn_decode_part(AttnArgs a) {
     red_ml[w][hh][0] = m;
     red_ml[w][hh][1] = l;
   }
-  float4* rd = reinterpret_cast<float4*>(&red_d[w][hh][32 * qd]);
+  float4* rd = reinterpret_cast<float4*>(&red_d[w][hh][kQuarter * qd]);
 #pragma unroll
   for (int e = 0; e < 32; e += 4)
     rd[e / 4] = make_float4(dim_value(acc[e], off, bsum, e), dim_value(acc[e + 1], off, bsum, e + 1),
@@ -473,7 +480,7 @@ attn_decode_part(AttnArgs a) {
 #pragma unroll
     for (int v = 0; v < kSplitWaves; ++v) {
       const float f = rescale(red_ml[v][mh][0], M);  // 0 for a wave that saw no token
-      const float4 d = *reinterpret_cast<const float4*>(&red_d[v][mh][md]);
+      const float4 d = *reinterpret_cast<const float4*>(&red_d[v][mh][kQuarter * (md / 32) + md % 32]);
       L = __fmaf_rn(red_ml[v][mh][1], f, L);
       D0 = __fmaf_rn(d.x, f, D0);
       D1 = __fmaf_rn(d.y, f, D1);
