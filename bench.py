@@ -135,7 +135,7 @@ TRAFFIC_MAP = {
     "c4/attn_decode": ("c4", "attn_decode_kv4<false>", 262144),
     # two kernels (on 256 CUs: 16 chunks x 2 groups of 16 heads x 8 batches of 8 waves,
     # then one wave per head)
-    "c4/attn_decode_split": [("c4", "attn_decode_part<false, false, 8, 4, 2>", 131072),
+    "c4/attn_decode_split": [("c4", "attn_decode_part<false, false, 8, 1, 2, 2>", 131072),
                              ("c4", "attn_decode_combine", 16384)],
 }
 for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the GEMM launch shapes

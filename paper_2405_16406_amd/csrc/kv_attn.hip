@@ -320,11 +320,11 @@ attn_decode_kv4(AttnArgs a) {
 // waves.  Lane l = 4 hh + qd serves head 16 g + hh, dims 32 qd .. 32 qd + 31, so one load of
 // the wave brings the 1 KB of codes of one token for the group's 16 heads (half of a 32-head
 // token line), and the four parameter loads 64 contiguous bytes each.  The chunk's tokens go
-// in batches of 4 per wave (wave w takes tokens 32 i + 4 w .. + 3 of the chunk, so the 8 waves
-// walk the chunk's lines together), two batches in flight (154 VGPRs; batches of 8 with 236
-// VGPRs measured 24.9 against 22.6 us on [8, 2048, 32, 128]).  Each lane keeps its head's
-// state; a batch's scores are in the lane, so its maximum (and the rare rescale) is taken
-// once per batch without crossing lanes.  The 8 waves merge in LDS; each head leaves its
+// one per wave and step (wave w takes token 8 i + w of the chunk, so the 8 waves walk the
+// chunk's lines together), two tokens in flight (94 VGPRs).  On [8, 2048, 32, 128] this
+// measured 20.4 us against 22.8 us for batches of 4 tokens (154 VGPRs) and 21.0-21.3 us
+// with 3 or 4 in flight.  Each lane keeps its head's state; a batch's scores are in the
+// lane, so its maximum (and the rare rescale) needs no cross-lane step.  The 8 waves merge in LDS; each head leaves its
 // partial state (m, l, the 128 dims with the code offset removed and the betas added) in
 // part, and the combine kernel merges the chunks of a head.
 // FINAL (a single chunk): the workgroup divides and stores the output itself.
@@ -340,9 +340,10 @@ constexpr int part_lds_bytes() {
   return WAVES * kAttnGroupHeads * (kDimRow + 2) * 4;
 }
 
-// WAVES waves of batches of TB tokens (a chunk is made of WAVES x TB-token batches), at
-// least WPE waves per SIMD.
-template <bool P16, bool FINAL, int kSplitWaves = kAttnSplitWaves, int kBatch = kAttnBatch, int WPE = 2>
+// WAVES waves of batches of TB tokens (a chunk is made of WAVES x TB-token batches), DEPTH
+// batches in flight per wave, at least WPE waves per SIMD.
+template <bool P16, bool FINAL, int kSplitWaves = kAttnSplitWaves, int kBatch = kAttnBatch, int WPE = 2,
+          int kDepth = kAttnDepth>
 __global__ void __launch_bounds__(64 * kSplitWaves, WPE)
 attn_decode_part(AttnArgs a) {
   constexpr int kChunkUnit = kSplitWaves * kBatch;
@@ -388,8 +389,8 @@ attn_decode_part(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rv = rsrc(a.vq + row0 * 64, a.S * a.H * 64);
   const void* pb = qd == 0 ? a.ka : qd == 1 ? a.kb : qd == 2 ? a.va : a.vb;  // this lane's scale array
 
-  v4u kc[2][kBatch], vc[2][kBatch];
-  float pv[2][kBatch];
+  v4u kc[kDepth][kBatch], vc[kDepth][kBatch];
+  float pv[kDepth][kBatch];
   auto token = [&](int i, int j) { return static_cast<uint32_t>(kChunkUnit * (first + i) + kBatch * w + j); };
   auto load = [&](int buf, int i) {
 #pragma unroll
@@ -447,13 +448,14 @@ attn_decode_part(AttnArgs a) {
       }
     }
   };
-  load(0, 0);
-  load(1, 1);
-  for (int i = 0; i < count; i += 2) {
-    process(0, i);
-    load(0, i + 2);
-    process(1, i + 1);
-    load(1, i + 3);
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) load(d, d);
+  for (int i = 0; i < count; i += kDepth) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      process(d, i + d);
+      load(d, i + d + kDepth);
+    }
   }
 
   // the waves' states of each head meet in LDS

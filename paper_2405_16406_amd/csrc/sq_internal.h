@@ -84,7 +84,7 @@ struct AttnArgs {
   int64_t B, S, H;       // S * H * 64 < 2^31 (32-bit buffer offsets per head)
   float scale_log2e;     // score scale times log2(e)
   uint16_t* out;         // fp16 [B, H, 128]
-  // split over the sequence: chunks of chunk_batches batches of 64 tokens, partial softmax
+  // split over the sequence: chunks of chunk_batches batches of 8 tokens, partial softmax
   // states in part (float [B, H, chunks, kAttnPart]); chunks == 1 needs no part
   int64_t chunks = 1;
   int64_t chunk_batches = 0;
@@ -95,10 +95,11 @@ constexpr int kAttnPart = 132;  // floats per partial state: m, l, 2 unused, 128
 
 // Chunks of the sequence split for a device with `cus` compute units: enough (batch, chunk,
 // 16-head group) workgroups of 8 waves to give every CU one, a chunk being whole batches of
-// 32 tokens (4 per wave), at most 64 chunks (one per lane of the combine).
+// 8 tokens (one per wave), at most 64 chunks (one per lane of the combine).
 constexpr int kAttnGroupHeads = 16;  // heads of one workgroup of the split attention (4 lanes each)
 constexpr int kAttnSplitWaves = 8;   // its waves, which split the chunk's tokens
-constexpr int kAttnBatch = 4;        // tokens of a wave's batch
+constexpr int kAttnBatch = 1;        // tokens of a wave's batch
+constexpr int kAttnDepth = 2;        // batches in flight per wave
 inline void attn_split(int64_t B, int64_t S, int64_t H, int cus, int64_t& chunks, int64_t& chunk_batches) {
   constexpr int unit = kAttnSplitWaves * kAttnBatch;  // tokens of one batch of the workgroup
   const int64_t nb = (S + unit - 1) / unit;
