@@ -134,18 +134,19 @@ TRAFFIC_MAP = {
     "c4/kv_quant": ("c4", "qk_had_kvquant_v2<true, 4, false>", 2097152),
     "c4/attn_decode": ("c4", "attn_decode_kv4<false>", 262144),
     # two kernels (on 256 CUs: 16 chunks x 2 groups of 16 heads x 8 batches of 8 waves,
-    # then one wave per head)
+    # then one workgroup of one wave per head)
     "c4/attn_decode_split": [("c4", "attn_decode_part<false, false, 8, 1, 2, 2>", 131072),
                              ("c4", "attn_decode_combine", 16384)],
 }
 for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the GEMM launch shapes
     TRAFFIC_MAP[f"c5m{_m}/act_quant"] = ("c5", "quant_rows_identity<4, 4>", _g)
     TRAFFIC_MAP[f"c5m{_m}/r4_had_quant"] = ("c5", "had_quant_lines<28, 16, 14, false, 4, false>", 896 * _m)
-    # M = 1 (and gate/up at M = 8): the dot-product kernel, 8 waves on each of the 256 CUs
-    TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = (("c5", f"w4a4_gemv<{_m}, true>", 131072) if _m < 16 else
-                                              ("c5", "w4a4_gemm_skinny<8, 2, false>", 229376))
+    # M = 1: the dot-product kernel, 8 waves on each of the 256 CUs; M = 8 and 16: the
+    # LDS-streaming kernel (gate/up: 224 workgroups of 16 row blocks; down: 256 of 2)
+    TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = (("c5", "w4a4_gemv<1, true>", 131072) if _m == 1 else
+                                              ("c5", "w4a4_gemm_stream<256, 2, true>", 114688))
     TRAFFIC_MAP[f"c5m{_m}/down_gemm"] = (("c5", "w4a4_gemv<1, false>", 131072) if _m == 1 else
-                                         ("c5", "w4a4_gemm_skinny<2, 10, false>", 131072))
+                                         ("c5", "w4a4_gemm_stream<256, 2, false>", 131072))
 
 
 def measured_traffic(key):

@@ -18,9 +18,10 @@
 // two workgroups per CU) and 256 x 256 (8 waves of 128 x 64).
 // Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
 // used where 32-bit buffer offsets do not cover the operands.
-// Decode sizes: w4a4_gemv (a few activation rows, whole weight rows streamed through
-// v_dot8_i32_i4) and w4a4_gemm_skinny (M <= 16, weight rows straight into registers and
-// v_mfma_i32_16x16x64_i8).
+// Decode sizes: w4a4_gemv (M <= 2, or 4 on large weights: whole weight rows streamed through
+// v_dot8_i32_i4), w4a4_gemm_stream (M <= 16: weight and activation row segments copied
+// into LDS, v_mfma_i32_16x16x64_i8) and w4a4_gemm_skinny (the remaining M <= 16 cases and
+// the 8-bit activations: weight rows straight into registers).
 #include <utility>
 
 #include "sq_device.h"
@@ -1082,6 +1083,47 @@ hipError_t launch_ring(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(R::THREADS * KS), LDS, stream, g);
 }
 
+// Epilogue of one 16 x 16 block of a decode product (v_mfma_i32_16x16x64_i8 layout: lane
+// r + 16 sg, register i holds D[4 sg + i][r]) for weight row n: the ring kernel's arithmetic
+// (acc holds 16 x the sum; A8: of qa - 128, whose shift the zero-point term takes back).
+template <bool A8>
+__device__ __forceinline__ void decode_store(const GemmArgs& g, const v4i& acc, int64_t n, int sg) {
+  if (n >= g.N) return;
+  const float sn = g.wa[n];
+  const float wn = __fmul_rn(sn, static_cast<float>(g.rs[n]));
+  const float bn = g.bias ? h2f(g.bias[n]) : 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = 4 * sg + i;
+    if (m >= g.M) continue;
+    const float t = __fmul_rn(sn, static_cast<float>(acc[i]));
+    const float xb = A8 ? __fmaf_rn(128.0f, g.xa[m], g.xb[m]) : g.xb[m];
+    const float yv = fp32_result(__fmaf_rn(__fmul_rn(g.xa[m], 0.0625f), t, __fmaf_rn(xb, wn, bn)));
+    g.y[m * g.ldy + n] = f2h(yv);
+    if (g.dbg_acc) g.dbg_acc[m * g.N + n] = (acc[i] >> 4) + (A8 ? 128 * g.rs[n] : 0);
+  }
+}
+
+// The same for a gate block (rows ng) and its up block (rows ng + 32): SiLU(g) u to output
+// column col.
+__device__ __forceinline__ void decode_store_swiglu(const GemmArgs& g, const v4i& accg, const v4i& accu, int64_t ng,
+                                                    int64_t col, int sg) {
+  if (ng >= g.N) return;
+  const int64_t nu = ng + 32;
+  const float scg = g.wa[ng], scu = g.wa[nu];
+  const float wg = __fmul_rn(scg, static_cast<float>(g.rs[ng])), wu = __fmul_rn(scu, static_cast<float>(g.rs[nu]));
+  const float bg = g.bias ? h2f(g.bias[ng]) : 0.0f, bu = g.bias ? h2f(g.bias[nu]) : 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = 4 * sg + i;
+    if (m >= g.M) continue;
+    const float ra = __fmul_rn(g.xa[m], 0.0625f);
+    const float gv = fp32_result(__fmaf_rn(ra, __fmul_rn(scg, static_cast<float>(accg[i])), __fmaf_rn(g.xb[m], wg, bg)));
+    const float uv = fp32_result(__fmaf_rn(ra, __fmul_rn(scu, static_cast<float>(accu[i])), __fmaf_rn(g.xb[m], wu, bu)));
+    g.y[m * g.ldy + col] = f2h(fp32_result(swiglu_value(gv, uv)));
+  }
+}
+
 // ------------------------------------------------------------------ decode-sized kernel
 // M <= 16 (token-at-a-time decoding): the GEMM streams the packed weights once from HBM and
 // the activations (M x K/2 bytes) stay in L2.  A workgroup owns 16 * NB weight rows (NB
@@ -1196,45 +1238,15 @@ w4a4_gemm_skinny(GemmArgs g) {
     if constexpr (NB % 4 == 0) {
 #pragma unroll
       for (int jj = 0; jj < NB / 2; ++jj) {
+        // gate block j = 4t + s (s = 0, 1) holds output columns n0/2 + 32t + 16s + r
         const int j = 4 * (jj / 2) + (jj % 2);
-        const int64_t ng = n0 + 16 * j + r, nu = ng + 32;
-        if (ng >= g.N) continue;
-        const float scg = g.wa[ng], scu = g.wa[nu];
-        const float wg = __fmul_rn(scg, static_cast<float>(g.rs[ng])), wu = __fmul_rn(scu, static_cast<float>(g.rs[nu]));
-        const float bg = g.bias ? h2f(g.bias[ng]) : 0.0f, bu = g.bias ? h2f(g.bias[nu]) : 0.0f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int64_t m = 4 * sg + i;
-          if (m >= g.M) continue;
-          const float ra = __fmul_rn(g.xa[m], 0.0625f);
-          const float gv = fp32_result(__fmaf_rn(ra, __fmul_rn(scg, static_cast<float>(acc[j][i])), __fmaf_rn(g.xb[m], wg, bg)));
-          const float uv = fp32_result(__fmaf_rn(ra, __fmul_rn(scu, static_cast<float>(acc[j + 2][i])), __fmaf_rn(g.xb[m], wu, bu)));
-          // gate block j = 4t + s (s = 0, 1) holds output columns n0/2 + 32t + 16s + r
-          g.y[m * g.ldy + n0 / 2 + 32 * (j / 4) + 16 * (j % 4) + r] = f2h(fp32_result(swiglu_value(gv, uv)));
-        }
+        decode_store_swiglu(g, acc[j], acc[j + 2], n0 + 16 * j + r, n0 / 2 + 32 * (j / 4) + 16 * (j % 4) + r, sg);
       }
     }
     return;
   }
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int64_t n = n0 + 16 * j + r;
-    if (n >= g.N) continue;
-    const float sn = g.wa[n];
-    const float wn = __fmul_rn(sn, static_cast<float>(g.rs[n]));
-    const float bn = g.bias ? h2f(g.bias[n]) : 0.0f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t m = 4 * sg + i;
-      if (m >= g.M) continue;
-      // same arithmetic as the ring kernel's epilogue (acc holds 16 * sum; A8: of qa - 128)
-      const float t = __fmul_rn(sn, static_cast<float>(acc[j][i]));
-      const float xb = A8 ? __fmaf_rn(128.0f, g.xa[m], g.xb[m]) : g.xb[m];
-      const float yv = fp32_result(__fmaf_rn(__fmul_rn(g.xa[m], 0.0625f), t, __fmaf_rn(xb, wn, bn)));
-      g.y[m * g.ldy + n] = f2h(yv);
-      if (g.dbg_acc) g.dbg_acc[m * g.N + n] = (acc[j][i] >> 4) + (A8 ? 128 * g.rs[n] : 0);
-    }
-  }
+  for (int j = 0; j < NB; ++j) decode_store<A8>(g, acc[j], n0 + 16 * j + r, sg);
 }
 
 // Prefetch steps: (NB + 1) 16-byte loads per step.
@@ -1258,8 +1270,218 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g);
 }
 
+// ------------------------------------------------------------------ streaming decode kernel
+// 2 < M <= 16 (the dot-product kernel's v_dot8 issue grows with M): the packed weight rows
+// stream through LDS by direct copies (buffer_load ... lds) of SEG-byte row segments,
+// SEG / 16 lanes per row, so one copy instruction reads 64 / (SEG / 16) rows of SEG
+// contiguous bytes (the 16-row kernel's loads take 64 bytes of each of 16 rows).
+//   * A workgroup owns nb blocks of 16 weight rows.  Its (block, stage) pairs, a stage being
+//     SEG bytes of the block's 16 rows, are split evenly over its 8 waves, so where the
+//     counts do not divide a wave runs from the end of one block into the next.
+//   * Each wave has NS ring slots of its own.  A slot holds the stage's 16 weight rows and
+//     the same SEG bytes of activation rows 0-15 (L2-resident), both copied the same way, so
+//     the loop's only vector memory operations are copies into LDS: it waits on the wave's
+//     own load counter, never on a barrier.  (With the activations loaded into registers
+//     the compiler's waits for them held back the copies: 58 against 53 us below.)
+//   * In a slot, chunk c (16 bytes) of row r sits at position c ^ r: the copying lane loads
+//     the chunk that belongs at its landing position.  The 16 lanes of one LDS read (16 rows,
+//     one chunk) then fall on 16 different bank groups.
+//   * Lane r + 16 s reads chunk 4 t + s (t < SEG / 64) of weight row r and of activation row
+//     r.  Both expand as in the 16-row kernel into two v_mfma_i32_16x16x64_i8 k-steps, so D
+//     has that kernel's layout.
+//   * A wave leaves its sums of every block it touched in LDS; after the loop the waves add
+//     the partial sums of a block and apply the 16-row kernel's epilogue (SW: gate blocks
+//     4 q, 4 q + 1 with up blocks 4 q + 2, 4 q + 3), so both kernels give the same bits.
+// Measured on MI355X (same data, one process, interleaved, us; against the 16-row kernel):
+// LLaMA-2-70B [M x 28672] x [8192 x 28672] 26.2 vs 32.1 (M = 16), 24.3 vs 29.4 (M = 8);
+// [M x 8192] x [57344 x 8192] with SiLU 53.1 vs 60.9 (M = 16), 51.4 vs 59.2 (M = 8);
+// LLaMA-2-7B M = 16: [16 x 11008] x [4096 x 11008] 9.2 vs 11.0, [16 x 4096] x [22016 x 4096]
+// with SiLU 15.1 vs 18.1.  The weights' two stages per wave are all the LDS allows.
+template <int SEG, int NS>
+struct Stream {
+  static constexpr int WAVES = 8;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int LPR = SEG / 16;   // lanes per row in a copy
+  static constexpr int RPI = 64 / LPR;   // rows per copy instruction (1 KB)
+  static constexpr int CPS = 16 / RPI;   // copies per stage
+  static constexpr int XPS = SEG / 64;   // chunks of a row a lane reads per stage
+  static constexpr int OPS = 2 * CPS;    // copies per stage: weight rows, then activation rows
+  static constexpr int WSTAGE = 16 * SEG;  // the 16 weight rows of a stage
+  static constexpr int STAGE = 2 * WSTAGE;  // then activation rows 0-15 of the same bytes of K
+  static constexpr int MAXP = 4;         // blocks one wave's run may touch
+  static constexpr int RING = WAVES * NS * STAGE;
+  static constexpr int LDS = RING + WAVES * MAXP * 1024;
+  static_assert(SEG == 256 || SEG == 512, "row segments of 16 or 32 lanes");
+  static_assert((NS - 1) * OPS <= 63, "outstanding loads fit the vmcnt counter");
+  static_assert(LDS <= 160 * 1024, "LDS of one CU");
+};
+
+template <int SEG, int NS, bool SW>
+__global__ void __launch_bounds__(512)
+w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
+  using S = Stream<SEG, NS>;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, sg = lane >> 4;
+  const uint32_t KB = static_cast<uint32_t>(g.K / 2);
+  const int64_t blk0 = static_cast<int64_t>(blockIdx.x) * nb;  // first block of the workgroup
+  // offsets are 32-bit: (N + 16 nb) K / 2 < 2^31 is checked on the host; rows past M or N
+  // and bytes past K are out of range and read as zeros
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
+  const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq, g.N * KB);
+  uint8_t* const ring = lds + w * NS * S::STAGE;
+  int* const part = reinterpret_cast<int*>(lds + S::RING);  // [wave][MAXP][4][64]
+  const int T = nb * spb;
+  const int u0 = w * T / S::WAVES, u1 = (w + 1) * T / S::WAVES;  // this wave's (block, stage) run
+
+  // copies: lane i brings row q RPI + i / LPR of the stage, landing at chunk position i % LPR;
+  // per lane the row offset and the chunk's byte within the segment are fixed
+  const int crow = lane / S::LPR, cpos = lane % S::LPR;
+  uint32_t crowk[S::CPS], ccol[S::CPS];
+#pragma unroll
+  for (int q = 0; q < S::CPS; ++q) {
+    const int rr = q * S::RPI + crow;
+    crowk[q] = static_cast<uint32_t>(rr) * KB;
+    ccol[q] = 16 * static_cast<uint32_t>(cpos ^ rr);
+  }
+  int ib = u0 / spb, is = u0 - ib * spb, iu = u0;  // the next stage to copy
+  // Branch-free: a stage past the run is copied with every byte out of range (zeros).
+  auto issue = [&](auto slot_c) {
+    constexpr int slot = decltype(slot_c)::value;
+    // The slot was read by the previous step: those LDS reads must have returned before the
+    // copy is issued (a copy of out-of-range zeros lands almost at once, and the compiler
+    // may place the copy right behind the reads).
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt not waited on
+    asm volatile("" ::: "memory");
+    const uint32_t lim = iu < u1 ? KB : 0u;  // bytes of the row in range
+    const uint32_t rbase = static_cast<uint32_t>((blk0 + ib) * 16) * KB;
+    const uint32_t kst = static_cast<uint32_t>(is) * SEG;
+#pragma unroll
+    for (int q = 0; q < S::CPS; ++q) {
+      const uint32_t k = kst + ccol[q];
+      const uint32_t off = k < lim ? rbase + crowk[q] + k : 0x80000000u;
+      auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<uintptr_t>(ring + slot * S::STAGE + q * 1024));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, dst, 16, static_cast<int>(off), 0, 0, 0);
+    }
+    // activation rows 0-15 of the same bytes, laid out like the weight rows (rows past M
+    // are out of range: zeros)
+#pragma unroll
+    for (int q = 0; q < S::CPS; ++q) {
+      const uint32_t k = kst + ccol[q];
+      const uint32_t off = k < lim ? crowk[q] + k : 0x80000000u;
+      auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<uintptr_t>(ring + slot * S::STAGE + S::WSTAGE + q * 1024));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, dst, 16, static_cast<int>(off), 0, 0, 0);
+    }
+    ++iu;
+    if (++is == spb) {
+      is = 0;
+      ++ib;
+    }
+  };
+  auto flush = [&](const v4i& a, int k) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[((w * S::MAXP + k) * 4 + i) * 64 + lane] = a[i];
+  };
+
+  static_for<NS - 1>([&](auto pc) { issue(pc); });
+  v4i acc = {0, 0, 0, 0};
+  int cs = u0 - (u0 / spb) * spb;  // stage within its block of the next stage to consume
+  int kp = 0;                      // partial-sum slot of the current block
+  for (int u = u0; u < u1; u += NS) {
+    static_for<NS>([&](auto pc) {
+      constexpr int p = decltype(pc)::value;
+      issue(std::integral_constant<int, (p + NS - 1) % NS>{});  // stage u + p + NS - 1 (that slot was read last step)
+      wait_vm_lgkm0<(NS - 1) * S::OPS>();                         // stage u + p has landed
+      asm volatile("" ::: "memory");
+      if (u + p < u1) {  // uniform over the wave
+        if (cs == spb) {  // the run enters its next block
+          flush(acc, kp);
+          ++kp;
+          acc = v4i{0, 0, 0, 0};
+          cs = 0;
+        }
+        const uint8_t* sb = ring + p * S::STAGE + r * SEG;
+#pragma unroll
+        for (int t = 0; t < S::XPS; ++t) {
+          const v4u wv = *reinterpret_cast<const v4u*>(sb + 16 * ((4 * t + sg) ^ r));
+          const v4u av = *reinterpret_cast<const v4u*>(sb + S::WSTAGE + 16 * ((4 * t + sg) ^ r));
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const uint32_t a0 = av[2 * hh], a1 = av[2 * hh + 1];
+            const v4i ea = {static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
+                            static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+            const uint32_t b0 = wv[2 * hh], b1 = wv[2 * hh + 1];
+            const v4i eb = {static_cast<int>((b0 << 4) & 0xF0F0F0F0u), static_cast<int>(b0 & 0xF0F0F0F0u),
+                            static_cast<int>((b1 << 4) & 0xF0F0F0F0u), static_cast<int>(b1 & 0xF0F0F0F0u)};
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(ea, eb, acc, 0, 0, 0);
+          }
+        }
+        ++cs;
+      }
+    });
+  }
+  if (u0 < u1) flush(acc, kp);
+  wait_vm_lgkm0<0>();  // copies past the run (zeros) land before the workgroup's LDS is released
+  __syncthreads();
+
+  // block b: the partial sums of the waves whose runs meet it, in wave order
+  auto block_sum = [&](int b) {
+    v4i sum = {0, 0, 0, 0};
+#pragma unroll
+    for (int v = 0; v < S::WAVES; ++v) {
+      const int a0 = v * T / S::WAVES, a1 = (v + 1) * T / S::WAVES;
+      if (a0 < a1 && a0 < (b + 1) * spb && a1 > b * spb) {
+        const int k = b - a0 / spb;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sum[i] += part[((v * S::MAXP + k) * 4 + i) * 64 + lane];
+      }
+    }
+    return sum;
+  };
+  if constexpr (SW) {  // nb % 4 == 0: group q = gate blocks 4q, 4q + 1, up blocks 4q + 2, 4q + 3
+    for (int q = w; q < nb / 4; q += S::WAVES) {
+      const v4i g0 = block_sum(4 * q), g1 = block_sum(4 * q + 1), up0 = block_sum(4 * q + 2), up1 = block_sum(4 * q + 3);
+      const int64_t n0 = (blk0 + 4 * q) * 16;  // a multiple of 64
+      decode_store_swiglu(g, g0, up0, n0 + r, n0 / 2 + r, sg);
+      decode_store_swiglu(g, g1, up1, n0 + 16 + r, n0 / 2 + 16 + r, sg);
+    }
+  } else {
+    for (int b = w; b < nb; b += S::WAVES) decode_store<false>(g, block_sum(b), (blk0 + b) * 16 + r, sg);
+  }
+}
+
+// Plans the streaming kernel: about one workgroup per CU (nb blocks of 16 rows each, a
+// multiple of 4 with SiLU), each wave's run touching at most MAXP blocks.  Returns false
+// where it does not apply.
+template <int SEG, int NS, bool SW>
+bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
+  using S = Stream<SEG, NS>;
+  if (g.M > 16 || g.a8 || (SW && g.N % 64 != 0)) return false;
+  int cus = 0;
+  *err = device_cus(&cus);
+  if (*err != hipSuccess) return true;
+  const int64_t kb = g.K / 2, blocks = (g.N + 15) / 16;
+  int64_t nb = (blocks + cus - 1) / cus;
+  if (SW) nb = (nb + 3) / 4 * 4;
+  const int64_t spb = (kb + SEG - 1) / SEG, T = nb * spb;
+  if (nb > 16 || T < S::WAVES || T * S::WAVES >= (int64_t{1} << 31)) return false;
+  const int64_t L = (T + S::WAVES - 1) / S::WAVES;  // longest run
+  if ((L - 1 + spb - 1) / spb + 1 > S::MAXP) return false;
+  if ((g.N + 16 * nb) * kb + 64 >= (int64_t{1} << 31) || g.M * kb + 64 >= (int64_t{1} << 31)) return false;
+  constexpr auto kern = w4a4_gemm_stream<SEG, NS, SW>;
+  *err = set_max_lds<kern>(S::LDS);
+  if (*err != hipSuccess) return true;
+  const dim3 grid(static_cast<unsigned>((blocks + nb - 1) / nb));
+  *err = launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g, static_cast<int>(nb), static_cast<int>(spb));
+  return true;
+}
+
 // ------------------------------------------------------------------ dot-product decode kernel
-// Decode sizes (M <= 8): a few activation rows against the whole weight matrix, a matrix-vector
+// Decode sizes (M <= 4): a few activation rows against the whole weight matrix, a matrix-vector
 // product whose cost is reading the packed weights once.  Each wave owns a contiguous run of
 // at most 64 output units (a weight row; with SiLU the gate/up row pair of one output column;
 // from four activation rows on two neighbouring rows, which then share each activation read)
@@ -1530,16 +1752,15 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(V::THREADS), lds, stream, g);
 }
 
-// The dot-product kernel for M <= 2, for M <= 4 from 96 MB of weights, and with SiLU for
-// M <= 8 from 96 MB (sets *e and returns true when it covers the arguments).  Measured on
-// MI355X against the 16-row decode kernel, same data, interleaved (us): LLaMA-2-70B
-// [M x 8192] x [57344 x 8192] with SiLU 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8
-// vs 58.8 (M = 4), 54.5 vs 61.0 (M = 8); [M x 28672] x [8192 x 28672] 22.9 vs 27.2
-// (M = 1), 23.7 vs 27.5 (M = 2), 25.0 vs 28.4 (M = 4), 30.7 vs 29.2 (M = 8: eight
-// activation rows of 14 KB per workgroup); LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU
-// 12.3 vs 16.1 (M = 1), 14.3 vs 16.6 (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x
-// [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs 9.8 (M = 4).  With eight rows the kernel is
-// bound by its v_dot8 issue rather than by HBM.
+// The dot-product kernel for M <= 2, and for M <= 4 from 96 MB of weights (sets *e and
+// returns true when it covers the arguments).  Measured on MI355X against the 16-row
+// decode kernel, same data, interleaved (us): LLaMA-2-70B [M x 8192] x [57344 x 8192] with
+// SiLU 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8 vs 58.8 (M = 4); [M x 28672] x
+// [8192 x 28672] 22.9 vs 27.2 (M = 1), 23.7 vs 27.5 (M = 2), 25.0 vs 28.4 (M = 4);
+// LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU 12.3 vs 16.1 (M = 1), 14.3 vs 16.6
+// (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs
+// 9.8 (M = 4).  With eight rows it is bound by its v_dot8 issue (70B gate/up with SiLU
+// 53.2 us), and the streaming kernel takes those sizes (51.4 us).
 template <bool SW>
 bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   if (g.M == 1 && fits_gemv<1, SW>(g)) {
@@ -1552,10 +1773,6 @@ bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   }
   if (g.M <= 4 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<4, SW>(g)) {
     *e = launch_gemv<4, SW>(g, stream);
-    return true;
-  }
-  if (SW && g.M <= 8 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<8, SW>(g)) {
-    *e = launch_gemv<8, SW>(g, stream);
     return true;
   }
   return false;
@@ -1652,6 +1869,7 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
     constexpr int SD4 = skinny_depth<4>(), SD8 = skinny_depth<8>();
     hipError_t e;
     if (try_gemv<true>(g, stream, &e)) return e;
+    if (g.M <= 16 && try_stream<256, 2, true>(g, stream, &e)) return e;
     if (g.M <= 16 && g.N > 16384) return fits_skinny<8, SD8>(g) ? launch_skinny<8, SD8>(g, stream) : hipErrorNotSupported;
     if (g.M <= 16) return fits_skinny<4, SD4>(g) ? launch_skinny<4, SD4>(g, stream) : hipErrorNotSupported;
     if (g.M <= 128)
@@ -1673,6 +1891,7 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream) {
   // register-staged kernel.
   hipError_t e;
   if (try_gemv<false>(g, stream, &e)) return e;
+  if (g.M <= 16 && try_stream<256, 2, false>(g, stream, &e)) return e;
   if (g.M <= 16) return launch_skinny_sized(g, stream);
   if (g.M <= 128) {
     if (fits_ring<2, 2, 2, 2, 4>(g)) return launch_ring<2, 2, 2, 2, 4, 2, 2>(g, stream);

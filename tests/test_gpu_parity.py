@@ -585,8 +585,29 @@ def test_gemm_gemv_kernel():
         gemm_case(M, N, K, seed=M * 37 + N + K, bias=(N % 2 == 1))
 
 
+def test_gemm_stream_kernel():
+    # 2 < M <= 16 on larger weights runs the LDS-streaming kernel (on a 256-CU part): ragged
+    # N (a partial last block of 16 rows), K/2 not a multiple of the 256-byte stage, 1 to 16
+    # blocks per workgroup, a single block, and runs of the 8 waves that cross one or two
+    # block boundaries (16 blocks of 2 stages); rows past M of the 16-row blocks
+    say("w4a4_linear LDS-streaming decode kernel: M 3..16, ragged N and K, runs across blocks")
+    for (M, N, K) in [(16, 4096 * 3 + 40, 2112), (5, 16 * 256 * 16 - 16 * 7, 576), (3, 300, 65536),
+                      (12, 8208, 2048), (8, 17, 16384), (16, 16, 8192), (7, 4096, 11008)]:
+        gemm_case(M, N, K, seed=M * 41 + N + K, bias=(K % 3 == 0))
+
+
+@pytest.mark.parametrize("M,I,K,bias", [(6, 4128, 2112, True), (9, 32, 4096, False), (11, 28672, 8256, True),
+                                        (16, 11008, 4096, True)])
+def test_swiglu_stream_kernel(M, I, K, bias):
+    # the LDS-streaming kernel with SiLU: groups of four 16-row blocks (two gate, two up) per
+    # output column range, one group in all, and runs crossing block boundaries (17 stages a
+    # block)
+    say(f"w4a4_linear_swiglu LDS-streaming decode kernel M={M} I={I} K={K} bias={bias}")
+    swiglu_case(M, I, K, seed=700 + M + I + K, bias=bias)
+
+
 @pytest.mark.parametrize("M,I,K,bias", [(1, 96, 4160, True), (2, 32, 64, False), (1, 2048 * 64 + 32, 64, True),
-                                        (2, 4128, 2112, True), (3, 14336, 8192, False), (5, 14368, 8192, True)])
+                                        (2, 4128, 2112, True), (3, 14336, 8192, False)])
 def test_swiglu_gemv_kernel(M, I, K, bias):
     say(f"w4a4_linear_swiglu dot-product decode kernel M={M} I={I} K={K} bias={bias}")
     swiglu_case(M, I, K, seed=600 + M + I + K, bias=bias)
@@ -1071,12 +1092,13 @@ def test_swiglu_llama2_7b_full_tiles():
     swiglu_case(2048, 11008, 4096, seed=44, bias=False, sample_rows=tile_rows(2048))
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 8192, 28672), (4, 8192, 28672), (8, 4096, 11008), (100, 1000, 2112),
+@pytest.mark.parametrize("M,N,K", [(1, 8192, 28672), (4, 8192, 28672), (8, 4096, 11008), (16, 8192, 28672),
+                                   (5, 16 * 256 * 16 - 16 * 7, 576), (100, 1000, 2112),
                                    (2048, 4096, 11008), (4096, 4096, 192)])
 def test_gemm_deterministic(M, N, K):
-    # dot-product decode kernel (lane sums added by DPP), 16-row decode kernel (8 waves'
-    # partial sums in LDS), two K groups (partial sums exchanged in LDS), 128 x 256 and
-    # 256 x 256 ring tiles: two launches give the same bytes
+    # dot-product decode kernel (lane sums added by DPP), LDS-streaming decode kernel (the
+    # waves' partial sums of a block added in LDS), two K groups (partial sums exchanged in
+    # LDS), 128 x 256 and 256 x 256 ring tiles: two launches give the same bytes
     say(f"w4a4_linear determinism M={M} N={N} K={K}")
     rng = workloads.rng_for(M + N + K + 3)
     qa = rng.integers(0, 16, size=(M, K))
