@@ -1275,9 +1275,12 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 // stream through LDS by direct copies (buffer_load ... lds) of SEG-byte row segments,
 // SEG / 16 lanes per row, so one copy instruction reads 64 / (SEG / 16) rows of SEG
 // contiguous bytes (the 16-row kernel's loads take 64 bytes of each of 16 rows).
-//   * A workgroup owns nb blocks of 16 weight rows.  Its (block, stage) pairs, a stage being
-//     SEG bytes of the block's 16 rows, are split evenly over its 8 waves, so where the
-//     counts do not divide a wave runs from the end of one block into the next.
+//   * A workgroup owns nb blocks of 16 weight rows: consecutive ones, or with SW nb / 2 pairs
+//     of a gate block and its up block (a finer unit than the groups of four that hold 32
+//     output columns: LLaMA-2-70B gate/up has 1792 pairs, 7 per CU, against 896 groups).
+//     Its (block, stage) pairs, a stage being SEG bytes of the block's 16 rows, are split
+//     evenly over its 8 waves, so where the counts do not divide a wave runs from the end
+//     of one block into the next.
 //   * Each wave has NS ring slots of its own.  A slot holds the stage's 16 weight rows and
 //     the same SEG bytes of activation rows 0-15 (L2-resident), both copied the same way, so
 //     the loop's only vector memory operations are copies into LDS: it waits on the wave's
@@ -1290,13 +1293,14 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 //     r.  Both expand as in the 16-row kernel into two v_mfma_i32_16x16x64_i8 k-steps, so D
 //     has that kernel's layout.
 //   * A wave leaves its sums of every block it touched in LDS; after the loop the waves add
-//     the partial sums of a block and apply the 16-row kernel's epilogue (SW: gate blocks
-//     4 q, 4 q + 1 with up blocks 4 q + 2, 4 q + 3), so both kernels give the same bits.
+//     the partial sums of a block and apply the 16-row kernel's epilogue (SW: each gate
+//     block with its up block), so both kernels give the same bits.
 // Measured on MI355X (same data, one process, interleaved, us; against the 16-row kernel):
 // LLaMA-2-70B [M x 28672] x [8192 x 28672] 26.2 vs 32.1 (M = 16), 24.3 vs 29.4 (M = 8);
-// [M x 8192] x [57344 x 8192] with SiLU 53.1 vs 60.9 (M = 16), 51.4 vs 59.2 (M = 8);
+// [M x 8192] x [57344 x 8192] with SiLU 53.1 vs 60.9 (M = 16), 51.4 vs 59.2 (M = 8), in
+// groups of four blocks; in pairs 48.2 (M = 16) and 45.8 (M = 8) against 52.5 and 50.9;
 // LLaMA-2-7B M = 16: [16 x 11008] x [4096 x 11008] 9.2 vs 11.0, [16 x 4096] x [22016 x 4096]
-// with SiLU 15.1 vs 18.1.  The weights' two stages per wave are all the LDS allows.
+// with SiLU 15.1 vs 18.1 (pairs: 13.9).
 template <int SEG, int NS>
 struct Stream {
   static constexpr int WAVES = 8;
@@ -1325,7 +1329,23 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, sg = lane >> 4;
   const uint32_t KB = static_cast<uint32_t>(g.K / 2);
-  const int64_t blk0 = static_cast<int64_t>(blockIdx.x) * nb;  // first block of the workgroup
+  // Plain: blocks blk0 .. blk0 + nb - 1.  SW: nb / 2 gate/up pairs from pair bx nb / 2 on (the
+  // last workgroup may have fewer); pair p is gate block 4 (p / 2) + p % 2 with its up block
+  // two further, local blocks 2 i (gate) and 2 i + 1 (up) of pair i.
+  const int64_t blk0 = static_cast<int64_t>(blockIdx.x) * nb;
+  const int64_t pair0 = static_cast<int64_t>(blockIdx.x) * (nb / 2);
+  if constexpr (SW) {
+    const int64_t pairs = g.N / 32;
+    if (pair0 + nb / 2 > pairs) nb = static_cast<int>(2 * (pairs - pair0));
+  }
+  auto block_of = [&](int lb) -> int64_t {
+    if constexpr (SW) {
+      const int64_t pr = pair0 + lb / 2;
+      return 4 * (pr / 2) + pr % 2 + 2 * (lb % 2);
+    } else {
+      return blk0 + lb;
+    }
+  };
   // offsets are 32-bit: (N + 16 nb) K / 2 < 2^31 is checked on the host; rows past M or N
   // and bytes past K are out of range and read as zeros
   const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
@@ -1356,7 +1376,7 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt not waited on
     asm volatile("" ::: "memory");
     const uint32_t lim = iu < u1 ? KB : 0u;  // bytes of the row in range
-    const uint32_t rbase = static_cast<uint32_t>((blk0 + ib) * 16) * KB;
+    const uint32_t rbase = static_cast<uint32_t>(block_of(ib) * 16) * KB;
     const uint32_t kst = static_cast<uint32_t>(is) * SEG;
 #pragma unroll
     for (int q = 0; q < S::CPS; ++q) {
@@ -1442,20 +1462,19 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
     }
     return sum;
   };
-  if constexpr (SW) {  // nb % 4 == 0: group q = gate blocks 4q, 4q + 1, up blocks 4q + 2, 4q + 3
-    for (int q = w; q < nb / 4; q += S::WAVES) {
-      const v4i g0 = block_sum(4 * q), g1 = block_sum(4 * q + 1), up0 = block_sum(4 * q + 2), up1 = block_sum(4 * q + 3);
-      const int64_t n0 = (blk0 + 4 * q) * 16;  // a multiple of 64
-      decode_store_swiglu(g, g0, up0, n0 + r, n0 / 2 + r, sg);
-      decode_store_swiglu(g, g1, up1, n0 + 16 + r, n0 / 2 + 16 + r, sg);
+  if constexpr (SW) {  // pair i: gate rows 16 gb + r, output columns 32 (p / 2) + 16 (p % 2) + r
+    for (int i = w; i < nb / 2; i += S::WAVES) {
+      const int64_t pr = pair0 + i;
+      decode_store_swiglu(g, block_sum(2 * i), block_sum(2 * i + 1), block_of(2 * i) * 16 + r,
+                          32 * (pr / 2) + 16 * (pr % 2) + r, sg);
     }
   } else {
     for (int b = w; b < nb; b += S::WAVES) decode_store<false>(g, block_sum(b), (blk0 + b) * 16 + r, sg);
   }
 }
 
-// Plans the streaming kernel: about one workgroup per CU (nb blocks of 16 rows each, a
-// multiple of 4 with SiLU), each wave's run touching at most MAXP blocks.  Returns false
+// Plans the streaming kernel: about one workgroup per CU (nb blocks of 16 rows each; with
+// SiLU nb / 2 gate/up pairs), each wave's run touching at most MAXP blocks.  Returns false
 // where it does not apply.
 template <int SEG, int NS, bool SW>
 bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
@@ -1465,8 +1484,9 @@ bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
   *err = device_cus(&cus);
   if (*err != hipSuccess) return true;
   const int64_t kb = g.K / 2, blocks = (g.N + 15) / 16;
-  int64_t nb = (blocks + cus - 1) / cus;
-  if (SW) nb = (nb + 3) / 4 * 4;
+  // plain: blocks in order; SW: gate/up pairs of blocks (N / 32 of them), an even count
+  const int64_t units = SW ? g.N / 32 : blocks, per = (units + cus - 1) / cus;
+  const int64_t nb = SW ? 2 * per : per;
   const int64_t spb = (kb + SEG - 1) / SEG, T = nb * spb;
   if (nb > 16 || T < S::WAVES || T * S::WAVES >= (int64_t{1} << 31)) return false;
   const int64_t L = (T + S::WAVES - 1) / S::WAVES;  // longest run
@@ -1475,7 +1495,7 @@ bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
   constexpr auto kern = w4a4_gemm_stream<SEG, NS, SW>;
   *err = set_max_lds<kern>(S::LDS);
   if (*err != hipSuccess) return true;
-  const dim3 grid(static_cast<unsigned>((blocks + nb - 1) / nb));
+  const dim3 grid(static_cast<unsigned>((units + per - 1) / per));
   *err = launch(kern, grid, dim3(S::THREADS), S::LDS, stream, g, static_cast<int>(nb), static_cast<int>(spb));
   return true;
 }

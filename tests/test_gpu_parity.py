@@ -599,9 +599,9 @@ def test_gemm_stream_kernel():
 @pytest.mark.parametrize("M,I,K,bias", [(6, 4128, 2112, True), (9, 32, 4096, False), (11, 28672, 8256, True),
                                         (16, 11008, 4096, True)])
 def test_swiglu_stream_kernel(M, I, K, bias):
-    # the LDS-streaming kernel with SiLU: groups of four 16-row blocks (two gate, two up) per
-    # output column range, one group in all, and runs crossing block boundaries (17 stages a
-    # block)
+    # the LDS-streaming kernel with SiLU: pairs of a gate and an up block of 16 rows, a
+    # single group of four blocks in all, a last workgroup with fewer pairs (LLaMA-2-7B:
+    # 688 pairs, 3 per workgroup), and runs crossing block boundaries (17 stages a block)
     say(f"w4a4_linear_swiglu LDS-streaming decode kernel M={M} I={I} K={K} bias={bias}")
     swiglu_case(M, I, K, seed=700 + M + I + K, bias=bias)
 
