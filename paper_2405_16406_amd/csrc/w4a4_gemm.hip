@@ -19,9 +19,9 @@
 // Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
 // used where 32-bit buffer offsets do not cover the operands.
 // Decode sizes: w4a4_gemv (M <= 2, or 4 on large weights: whole weight rows streamed through
-// v_dot8_i32_i4), w4a4_gemm_stream (M <= 16: weight and activation row segments copied
-// into LDS, v_mfma_i32_16x16x64_i8) and w4a4_gemm_skinny (the remaining M <= 16 cases and
-// the 8-bit activations: weight rows straight into registers).
+// v_dot8_i32_i4), w4a4_gemm_stream (M <= 16, 8-bit activations M <= 8: weight and
+// activation row segments copied into LDS, v_mfma_i32_16x16x64_i8) and w4a4_gemm_skinny
+// (the remaining M <= 16 cases: weight rows straight into registers).
 #include <utility>
 
 #include "sq_device.h"
@@ -1292,6 +1292,11 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 //   * Lane r + 16 s reads chunk 4 t + s (t < SEG / 64) of weight row r and of activation row
 //     r.  Both expand as in the 16-row kernel into two v_mfma_i32_16x16x64_i8 k-steps, so D
 //     has that kernel's layout.
+//   * A8 (8-bit activation codes, the W4A8 setting, M <= 8): the slot holds activation rows
+//     0-7 with the 2 SEG code bytes of the stage's k (32 lanes per row, chunk c of row r at
+//     position c ^ r); a lane takes the 32 codes of its weight chunk as two 16-byte reads,
+//     made signed and reordered as in the ring kernel (act8_operand), and the epilogue adds
+//     the shift back (the 16-row kernel's 8-bit arithmetic).
 //   * A wave leaves its sums of every block it touched in LDS; after the loop the waves add
 //     the partial sums of a block and apply the 16-row kernel's epilogue (SW: each gate
 //     block with its up block), so both kernels give the same bits.
@@ -1301,7 +1306,7 @@ hipError_t launch_skinny(const GemmArgs& g, hipStream_t stream) {
 // groups of four blocks; in pairs 48.2 (M = 16) and 45.8 (M = 8) against 52.5 and 50.9;
 // LLaMA-2-7B M = 16: [16 x 11008] x [4096 x 11008] 9.2 vs 11.0, [16 x 4096] x [22016 x 4096]
 // with SiLU 15.1 vs 18.1 (pairs: 13.9).
-template <int SEG, int NS>
+template <int SEG, int NS, bool A8 = false>
 struct Stream {
   static constexpr int WAVES = 8;
   static constexpr int THREADS = 64 * WAVES;
@@ -1311,7 +1316,8 @@ struct Stream {
   static constexpr int XPS = SEG / 64;   // chunks of a row a lane reads per stage
   static constexpr int OPS = 2 * CPS;    // copies per stage: weight rows, then activation rows
   static constexpr int WSTAGE = 16 * SEG;  // the 16 weight rows of a stage
-  static constexpr int STAGE = 2 * WSTAGE;  // then activation rows 0-15 of the same bytes of K
+  // then activation rows 0-15 of the same bytes of K; A8: rows 0-7 of 8-bit codes (2 SEG bytes)
+  static constexpr int STAGE = 2 * WSTAGE;
   static constexpr int MAXP = 4;         // blocks one wave's run may touch
   static constexpr int RING = WAVES * NS * STAGE;
   static constexpr int LDS = RING + WAVES * MAXP * 1024;
@@ -1320,10 +1326,11 @@ struct Stream {
   static_assert(LDS <= 160 * 1024, "LDS of one CU");
 };
 
-template <int SEG, int NS, bool SW>
+template <int SEG, int NS, bool SW, bool A8 = false>
 __global__ void __launch_bounds__(512)
 w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
-  using S = Stream<SEG, NS>;
+  using S = Stream<SEG, NS, A8>;
+  static_assert(!A8 || (!SW && SEG == 256), "8-bit activations: plain products, 256-byte stages");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1348,7 +1355,8 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
   };
   // offsets are 32-bit: (N + 16 nb) K / 2 < 2^31 is checked on the host; rows past M or N
   // and bytes past K are out of range and read as zeros
-  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * KB);
+  const uint32_t XB = A8 ? 2 * KB : KB;  // activation bytes per row
+  const __amdgpu_buffer_rsrc_t rsa = buf_rsrc(g.xq, g.M * XB);
   const __amdgpu_buffer_rsrc_t rsb = buf_rsrc(g.wq, g.N * KB);
   uint8_t* const ring = lds + w * NS * S::STAGE;
   int* const part = reinterpret_cast<int*>(lds + S::RING);  // [wave][MAXP][4][64]
@@ -1365,6 +1373,18 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
     crowk[q] = static_cast<uint32_t>(rr) * KB;
     ccol[q] = 16 * static_cast<uint32_t>(cpos ^ rr);
   }
+  // A8: an activation copy brings rows 2 q + i / 32 (512 bytes each), landing at chunk
+  // position i % 32, which holds chunk (i % 32) ^ row
+  const int xrow = lane / 32, xpos = lane % 32;
+  uint32_t xrowk[S::CPS], xcol[S::CPS];
+#pragma unroll
+  for (int q = 0; q < S::CPS; ++q) {
+    const int rr = 2 * q + xrow;
+    xrowk[q] = static_cast<uint32_t>(rr) * XB;
+    xcol[q] = 16 * static_cast<uint32_t>(xpos ^ rr);
+  }
+  (void)xrowk;
+  (void)xcol;
   int ib = u0 / spb, is = u0 - ib * spb, iu = u0;  // the next stage to copy
   // Branch-free: a stage past the run is copied with every byte out of range (zeros).
   auto issue = [&](auto slot_c) {
@@ -1387,11 +1407,17 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, dst, 16, static_cast<int>(off), 0, 0, 0);
     }
     // activation rows 0-15 of the same bytes, laid out like the weight rows (rows past M
-    // are out of range: zeros)
+    // are out of range: zeros); A8: rows 0-7, the 2 SEG code bytes of the same k
 #pragma unroll
     for (int q = 0; q < S::CPS; ++q) {
-      const uint32_t k = kst + ccol[q];
-      const uint32_t off = k < lim ? crowk[q] + k : 0x80000000u;
+      uint32_t off;
+      if constexpr (A8) {
+        const uint32_t k = 2 * kst + xcol[q];
+        off = k < 2 * lim ? xrowk[q] + k : 0x80000000u;
+      } else {
+        const uint32_t k = kst + ccol[q];
+        off = k < lim ? crowk[q] + k : 0x80000000u;
+      }
       auto* dst = reinterpret_cast<__attribute__((address_space(3))) void*>(
           reinterpret_cast<uintptr_t>(ring + slot * S::STAGE + S::WSTAGE + q * 1024));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, dst, 16, static_cast<int>(off), 0, 0, 0);
@@ -1427,13 +1453,28 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
         const uint8_t* sb = ring + p * S::STAGE + r * SEG;
 #pragma unroll
         for (int t = 0; t < S::XPS; ++t) {
-          const v4u wv = *reinterpret_cast<const v4u*>(sb + 16 * ((4 * t + sg) ^ r));
-          const v4u av = *reinterpret_cast<const v4u*>(sb + S::WSTAGE + 16 * ((4 * t + sg) ^ r));
+          const int c = 4 * t + sg;  // the lane's chunk of the stage
+          const v4u wv = *reinterpret_cast<const v4u*>(sb + 16 * (c ^ r));
+          v4u av, av2;
+          if constexpr (A8) {  // codes 32 c .. 32 c + 31 of row r (rows past 7: row 0, never stored)
+            const int xr = r < 8 ? r : 0;
+            const uint8_t* xb = ring + p * S::STAGE + S::WSTAGE + xr * (2 * SEG);
+            av = *reinterpret_cast<const v4u*>(xb + 16 * ((2 * c) ^ xr));
+            av2 = *reinterpret_cast<const v4u*>(xb + 16 * ((2 * c + 1) ^ xr));
+          } else {
+            av = *reinterpret_cast<const v4u*>(sb + S::WSTAGE + 16 * (c ^ r));
+            av2 = av;
+          }
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            const uint32_t a0 = av[2 * hh], a1 = av[2 * hh + 1];
-            const v4i ea = {static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
-                            static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+            v4i ea;
+            if constexpr (A8) {
+              ea = act8_operand(hh == 0 ? av : av2);
+            } else {
+              const uint32_t a0 = av[2 * hh], a1 = av[2 * hh + 1];
+              ea = v4i{static_cast<int>(a0 & 0x0F0F0F0Fu), static_cast<int>((a0 >> 4) & 0x0F0F0F0Fu),
+                       static_cast<int>(a1 & 0x0F0F0F0Fu), static_cast<int>((a1 >> 4) & 0x0F0F0F0Fu)};
+            }
             const uint32_t b0 = wv[2 * hh], b1 = wv[2 * hh + 1];
             const v4i eb = {static_cast<int>((b0 << 4) & 0xF0F0F0F0u), static_cast<int>(b0 & 0xF0F0F0F0u),
                             static_cast<int>((b1 << 4) & 0xF0F0F0F0u), static_cast<int>(b1 & 0xF0F0F0F0u)};
@@ -1469,17 +1510,17 @@ w4a4_gemm_stream(GemmArgs g, int nb, int spb) {
                           32 * (pr / 2) + 16 * (pr % 2) + r, sg);
     }
   } else {
-    for (int b = w; b < nb; b += S::WAVES) decode_store<false>(g, block_sum(b), (blk0 + b) * 16 + r, sg);
+    for (int b = w; b < nb; b += S::WAVES) decode_store<A8>(g, block_sum(b), (blk0 + b) * 16 + r, sg);
   }
 }
 
 // Plans the streaming kernel: about one workgroup per CU (nb blocks of 16 rows each; with
 // SiLU nb / 2 gate/up pairs), each wave's run touching at most MAXP blocks.  Returns false
 // where it does not apply.
-template <int SEG, int NS, bool SW>
+template <int SEG, int NS, bool SW, bool A8 = false>
 bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
-  using S = Stream<SEG, NS>;
-  if (g.M > 16 || g.a8 || (SW && g.N % 64 != 0)) return false;
+  using S = Stream<SEG, NS, A8>;
+  if (g.M > (A8 ? 8 : 16) || (g.a8 != 0) != A8 || (SW && g.N % 64 != 0)) return false;
   int cus = 0;
   *err = device_cus(&cus);
   if (*err != hipSuccess) return true;
@@ -1491,8 +1532,9 @@ bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
   if (nb > 16 || T < S::WAVES || T * S::WAVES >= (int64_t{1} << 31)) return false;
   const int64_t L = (T + S::WAVES - 1) / S::WAVES;  // longest run
   if ((L - 1 + spb - 1) / spb + 1 > S::MAXP) return false;
-  if ((g.N + 16 * nb) * kb + 64 >= (int64_t{1} << 31) || g.M * kb + 64 >= (int64_t{1} << 31)) return false;
-  constexpr auto kern = w4a4_gemm_stream<SEG, NS, SW>;
+  if ((g.N + 16 * nb) * kb + 64 >= (int64_t{1} << 31) || g.M * kb * (A8 ? 2 : 1) + 64 >= (int64_t{1} << 31))
+    return false;
+  constexpr auto kern = w4a4_gemm_stream<SEG, NS, SW, A8>;
   *err = set_max_lds<kern>(S::LDS);
   if (*err != hipSuccess) return true;
   const dim3 grid(static_cast<unsigned>((units + per - 1) / per));
@@ -1876,6 +1918,11 @@ hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream) {
   if (g.M == 1 && fits_gemv<1, false, true>(g)) return launch_gemv<1, false, true>(g, stream);
   if (g.M == 2 && g.N * (g.K / 2) >= (int64_t{32} << 20) && fits_gemv<2, false, true>(g))
     return launch_gemv<2, false, true>(g, stream);
+  // Up to 8 rows: the streaming kernel with 8-bit activation rows, bit-identical to the
+  // 16-row kernel (us): LLaMA-2-70B gate+up 47.4 vs 79.5 (M = 8), 44.8 vs 75.8 (M = 3); down
+  // 25.9 vs 32.8, 23.9 vs 28.7; LLaMA-2-7B gate+up 13.7 vs 23.8, down 9.6 vs 11.5 (M = 8).
+  hipError_t e;
+  if (g.M <= 8 && try_stream<256, 2, false, true>(g, stream, &e)) return e;
   const int64_t nb = (g.N + 4095) / 4096;  // the rows-per-workgroup rule of the W4A4 decode kernel
   if (nb <= 1) return try_skinny8<1>(g, stream);
   if (nb <= 3) return try_skinny8<2>(g, stream);

@@ -645,11 +645,14 @@ def test_w4a8_gemm_small_shapes(M, N, K):
 @pytest.mark.parametrize("M,N,K", [(1, 8, 64), (2, 40, 128), (7, 1000, 4160), (16, 130, 3136), (11, 4097, 640),
                                    (16, 28672, 8192), (1, 8192, 28672), (13, 96, 28672),
                                    (1, 1001, 4160), (1, 2048 * 64 + 5, 64), (2, 8192, 8192), (1, 700, 65536),
-                                   (1, 64, 65600)])
+                                   (1, 64, 65600), (8, 8192, 28672), (3, 4096 * 3 + 40, 2112),
+                                   (5, 16 * 256 * 16 - 16 * 7, 576), (8, 17, 16384), (4, 4096, 11008)])
 def test_w4a8_decode_shapes(M, N, K):
     # M <= 16 with 8-bit activations: the dot-product kernel for one row (two from 32 MB of
     # weights; ragged N and K, K/2 shorter than 1 KB, long runs, the largest K it takes and
-    # the first it leaves) and the 16-row kernel (1, 2 or 4 blocks of 16 rows) otherwise
+    # the first it leaves), the LDS-streaming kernel up to 8 rows (ragged N, K/2 not a
+    # multiple of its 256-byte stage, 1 to 16 blocks per workgroup, runs across block
+    # boundaries) and the 16-row kernel (1, 2 or 4 blocks of 16 rows) otherwise
     say(f"w4a8_linear decode M={M} N={N} K={K}")
     gemm8_case(M, N, K, seed=M * 13 + N + K, bias=(M % 2 == 1))
 
