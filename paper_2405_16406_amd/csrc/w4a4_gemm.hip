@@ -18,8 +18,8 @@
 // two workgroups per CU) and 256 x 256 (8 waves of 128 x 64).
 // Register-staged kernel (w4a4_gemm_tile): global -> registers -> LDS, double-buffered;
 // used where 32-bit buffer offsets do not cover the operands.
-// Decode sizes: w4a4_gemv (M <= 2, or 4 on large weights: whole weight rows streamed through
-// v_dot8_i32_i4), w4a4_gemm_stream (M <= 16, 8-bit activations M <= 8: weight and
+// Decode sizes: w4a4_gemv (M <= 2: whole weight rows streamed through v_dot8_i32_i4),
+// w4a4_gemm_stream (M <= 16, 8-bit activations M <= 8: weight and
 // activation row segments copied into LDS, v_mfma_i32_16x16x64_i8) and w4a4_gemm_skinny
 // (the remaining M <= 16 cases: weight rows straight into registers).
 #include <utility>
@@ -1543,7 +1543,7 @@ bool try_stream(const GemmArgs& g, hipStream_t stream, hipError_t* err) {
 }
 
 // ------------------------------------------------------------------ dot-product decode kernel
-// Decode sizes (M <= 4): a few activation rows against the whole weight matrix, a matrix-vector
+// Decode sizes (M <= 2): a few activation rows against the whole weight matrix, a matrix-vector
 // product whose cost is reading the packed weights once.  Each wave owns a contiguous run of
 // at most 64 output units (a weight row; with SiLU the gate/up row pair of one output column;
 // from four activation rows on two neighbouring rows, which then share each activation read)
@@ -1814,15 +1814,15 @@ hipError_t launch_gemv(const GemmArgs& g, hipStream_t stream) {
   return launch(kern, grid, dim3(V::THREADS), lds, stream, g);
 }
 
-// The dot-product kernel for M <= 2, and for M <= 4 from 96 MB of weights (sets *e and
-// returns true when it covers the arguments).  Measured on MI355X against the 16-row
-// decode kernel, same data, interleaved (us): LLaMA-2-70B [M x 8192] x [57344 x 8192] with
-// SiLU 41.0 vs 56.6 (M = 1), 42.2 vs 56.9 (M = 2), 44.8 vs 58.8 (M = 4); [M x 28672] x
-// [8192 x 28672] 22.9 vs 27.2 (M = 1), 23.7 vs 27.5 (M = 2), 25.0 vs 28.4 (M = 4);
+// The dot-product kernel for M <= 2 (sets *e and returns true when it covers the
+// arguments).  Measured on MI355X against the 16-row decode kernel, same data, interleaved
+// (us): LLaMA-2-70B [M x 8192] x [57344 x 8192] with SiLU 41.0 vs 56.6 (M = 1), 42.2 vs
+// 56.9 (M = 2); [M x 28672] x [8192 x 28672] 22.9 vs 27.2 (M = 1), 23.7 vs 27.5 (M = 2);
 // LLaMA-2-7B [M x 4096] x [22016 x 4096] with SiLU 12.3 vs 16.1 (M = 1), 14.3 vs 16.6
-// (M = 2), 18.3 vs 17.6 (M = 4); [M x 11008] x [4096 x 11008] 8.2 vs 8.9 (M = 1), 11.2 vs
-// 9.8 (M = 4).  With eight rows it is bound by its v_dot8 issue (70B gate/up with SiLU
-// 53.2 us), and the streaming kernel takes those sizes (51.4 us).
+// (M = 2); [M x 11008] x [4096 x 11008] 8.2 vs 8.9 (M = 1).  From three rows the streaming
+// kernel is as fast or faster (70B gate/up with SiLU at M = 4 45.1 vs 45.5, down 24.1 vs
+// 25.0; [4 x 4096] x [57344 x 4096] with SiLU 25.2 vs 27.2), and with eight rows this
+// kernel is bound by its v_dot8 issue.
 template <bool SW>
 bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   if (g.M == 1 && fits_gemv<1, SW>(g)) {
@@ -1831,10 +1831,6 @@ bool try_gemv(const GemmArgs& g, hipStream_t stream, hipError_t* e) {
   }
   if (g.M == 2 && fits_gemv<2, SW>(g)) {
     *e = launch_gemv<2, SW>(g, stream);
-    return true;
-  }
-  if (g.M <= 4 && g.N * (g.K / 2) >= (int64_t{96} << 20) && fits_gemv<4, SW>(g)) {
-    *e = launch_gemv<4, SW>(g, stream);
     return true;
   }
   return false;

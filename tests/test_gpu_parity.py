@@ -575,10 +575,11 @@ def test_gemm_decode_kernel():
 
 
 def test_gemm_gemv_kernel():
-    # M <= 2 (and M <= 4 from 96 MB of weights) runs the dot-product kernel: whole 1 KB
-    # chunks of a row per wave load, K/2 not a multiple of 1 KB, K/2 shorter than one chunk,
-    # the largest K it takes (65536) and the first it leaves to the 16-row kernel, fewer rows
-    # than waves, and runs of more than 64 rows per wave's share (more workgroups)
+    # M <= 2 runs the dot-product kernel: whole 1 KB chunks of a row per wave load, K/2 not
+    # a multiple of 1 KB, K/2 shorter than one chunk, the largest K it takes (65536) and the
+    # first it leaves to the 16-row kernel, fewer rows than waves, and runs of more than 64
+    # rows per wave's share (more workgroups); M = 3 and 4 on 117 MB of weights, which it
+    # also took before the streaming kernel did
     say("w4a4_linear dot-product decode kernel: M 1..4, ragged N and K")
     for (M, N, K) in [(1, 3, 64), (2, 8, 64), (1, 1000, 4160), (2, 4097, 2112), (1, 700, 65536),
                       (2, 300, 65600), (1, 2048 * 64 + 5, 64), (3, 8192, 28672), (4, 8197, 24576)]:
