@@ -66,7 +66,8 @@ hipError_t launch_w4a4_gemm(const GemmArgs& g, hipStream_t stream);
 // The same product with 8-bit activation codes (xq [M, K], one code per byte).
 hipError_t launch_w4a8_gemm(const GemmArgs& g, hipStream_t stream);
 // Its decode-sized (M <= 16) weight-streaming kernels (the dot-product kernel for one or two
-// rows, the 16-row kernel otherwise); hipErrorNotSupported otherwise.
+// rows, the LDS-streaming kernel up to 8, the 16-row kernel otherwise); hipErrorNotSupported
+// otherwise.
 hipError_t launch_w4a8_skinny(const GemmArgs& g, hipStream_t stream);
 // Its prefill kernel on the LDS ring of the W4A4 GEMM; hipErrorNotSupported where the 32-bit
 // buffer offsets do not cover the operands.
