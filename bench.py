@@ -144,10 +144,10 @@ for _m, _g in ((1, 256), (8, 2048), (16, 4096)):  # the decode sizes share the G
     # M = 1: the dot-product kernel, 8 waves on each of the 256 CUs; M = 8 and 16: the
     # LDS-streaming kernel (gate/up: 256 workgroups of 7 gate/up block pairs; down: 256 of 2
     # blocks)
-    TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = (("c5", "w4a4_gemv<1, true>", 131072) if _m == 1 else
-                                              ("c5", "w4a4_gemm_stream<256, 2, true>", 131072))
-    TRAFFIC_MAP[f"c5m{_m}/down_gemm"] = (("c5", "w4a4_gemv<1, false>", 131072) if _m == 1 else
-                                         ("c5", "w4a4_gemm_stream<256, 2, false>", 131072))
+    TRAFFIC_MAP[f"c5m{_m}/gate_up_swiglu"] = (("c5", "w4a4_gemv<1, true, false>", 131072) if _m == 1 else
+                                              ("c5", "w4a4_gemm_stream<256, 2, true, false>", 131072))
+    TRAFFIC_MAP[f"c5m{_m}/down_gemm"] = (("c5", "w4a4_gemv<1, false, false>", 131072) if _m == 1 else
+                                         ("c5", "w4a4_gemm_stream<256, 2, false, false>", 131072))
 
 
 def measured_traffic(key):
